@@ -1,0 +1,275 @@
+/*
+ * rkc.h -- C ABI of the MI355X (gfx950) batched replay of resident-KV-claim arbitration.
+ *
+ * What is replayed.  Many independent paged-KV block pools, each driven by its own event trace,
+ * through the resident-claim contract of "Resident KV Claims: A Conformance Contract for Future
+ * Reuse under Active KV Pressure" (Stepanek, 2026):
+ *   - the active/resident feasibility check  protected_resident + active_live <= usable  (§3.4);
+ *   - ordinary (LRU) eviction, soft priority, write no-admit and hard protected claims as pool
+ *     policies (§3.1 protection-mode table; §3.5 mechanism table; §5.2; §5.3);
+ *   - the leading-prefix materialization predicate (§3.1 "useful resident value"; §4.1 ledger);
+ *   - claim decisions, lifecycle, demotion, expiry and harm (§3.1 schema table; §3.2 harm table);
+ *   - scheduler-visible active refusal with blocking-claim attribution and its capacity proof
+ *     (§5.4 refusal record: protected 60, required 70, sum 130, usable 80, shortfall 50).
+ *
+ * Everything on this path is integer.  Conflicts are contract outcomes, not errors (§3.2, §7):
+ * a refusal, a materialization failure or a harm is reported in the outcome stream; only bad calls
+ * return a negative status.
+ *
+ * Ownership.  The caller owns every buffer (in practice torch tensors in device memory).  The
+ * library allocates no device memory, keeps no mutable global state and is re-entrant for disjoint
+ * buffers on different streams.  Every output buffer is fully overwritten by a replay, so callers
+ * need not clear them.  Buffers must stay alive until the stream has finished the replay.
+ *
+ * All integers are little-endian.  Device pointers are HIP device addresses of the current device.
+ */
+#ifndef RKC_H
+#define RKC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define RKC_ABI_VERSION 1
+
+/* Hard limits of this implementation (checked on the host and per pool on the device). */
+#define RKC_MAX_USABLE_BLOCKS   (1 << 22) /* U per pool                                        */
+#define RKC_MAX_EVENTS_PER_POOL (1 << 24) /* events per pool; request/claim ids are < this     */
+#define RKC_MAX_FIELD_BLOCKS    (1 << 24) /* S, k, L, P, T above this make an event malformed  */
+
+/* ----------------------------------------------------------------------------------------------
+ * Event: 16 bytes = 4 x int32, pool-major (CSR by rkc_pool_desc.event_offset).
+ *
+ * w0 = type[0:4] | hard[4] | prio[5:7] | reserved[7:16] | duration[16:32] (u16, 0 = no expiry)
+ *
+ *   PREFILL (0)  active request r = the event's step index.  w1 = S blocks, w2 = shared chain c
+ *                (ignored when P = 0), w3 = shared prefix P (0 <= P <= S).  Positions [0,P) are
+ *                content of shared chain c and can hit the prefix cache; positions [P,S) are
+ *                private to r.  (§2.1 prefix caching; §4.1 leading-prefix ledger.)
+ *   EXTEND  (1)  decode/chunk growth of a live request.  w1 = k blocks, w2 = selector (u32).  The
+ *                request is the (selector mod #live)-th live request in ascending id order.
+ *                (§3.1 "active live KV" grows across chunks; §5.2 chunked-prefill table.)
+ *   CLAIM   (2)  resident claim q = the event's step index.  w1 = footprint L blocks, w2 = chain c,
+ *                w3 = materialization threshold T (0 <= T <= L), hard/prio/duration from w0.
+ *                (§3.1 ResidentClaimInput: footprint, protection mode, optional duration_steps,
+ *                materialization predicate "leading contiguous survival >= T".)
+ *   FINISH  (3)  w1 = selector: the request finishes and releases its live KV.
+ *   RELEASE (4)  w1 = selector over live claims (ascending id): the claim is released.
+ *   DEMOTE  (5)  w1 = selector over materialized hard-requested claims: hard -> soft (§3.1, §3.2).
+ *   NOP     (6)  no operation.
+ * Any other type, or out-of-range fields, makes the event malformed: outcome INVALID.
+ * -------------------------------------------------------------------------------------------- */
+typedef struct rkc_event {
+  int32_t w[4];
+} rkc_event;
+
+enum rkc_event_type {
+  RKC_EV_PREFILL = 0,
+  RKC_EV_EXTEND = 1,
+  RKC_EV_CLAIM = 2,
+  RKC_EV_FINISH = 3,
+  RKC_EV_RELEASE = 4,
+  RKC_EV_DEMOTE = 5,
+  RKC_EV_NOP = 6
+};
+
+/* Pool policy: how the runtime lowers claims (§3.5 mechanism table rows "native eviction",
+ * "write no-admit only", "resident victim exclusion"; §5.4 check C1 for soft lowering). */
+enum rkc_pool_mode {
+  RKC_MODE_LRU = 0,     /* native eviction: claims are only observed (shadow)                  */
+  RKC_MODE_SOFT = 1,    /* soft priority: claims accepted, hard requests lowered (approximate)  */
+  RKC_MODE_NOADMIT = 2, /* write no-admit: request KV never becomes reusable; claims observed   */
+  RKC_MODE_HARD = 3     /* hard protected-resident exclusion with scheduler-visible refusal     */
+};
+
+/* ----------------------------------------------------------------------------------------------
+ * Pool descriptor: 48 bytes.
+ * -------------------------------------------------------------------------------------------- */
+typedef struct rkc_pool_desc {
+  int32_t usable_blocks;     /* U, 1..RKC_MAX_USABLE_BLOCKS; block size is 16 tokens (§4.1)     */
+  int32_t mode;              /* enum rkc_pool_mode                                               */
+  int32_t n_events;          /* events of this pool                                              */
+  int32_t n_chains;          /* valid shared chain ids are [0, n_chains)                         */
+  int32_t max_live_claims;   /* live-claim table capacity; a CLAIM beyond it is INVALID          */
+  int32_t max_live_requests; /* live-request table capacity; a PREFILL beyond it is INVALID      */
+  int32_t n_claim_slots;     /* telemetry slots; the k-th CLAIM event uses slot k                */
+  int32_t reserved;          /* must be 0                                                        */
+  int64_t event_offset;      /* index of the pool's first event in the event (and outcome) array */
+  int64_t claim_slot_offset; /* index of the pool's first slot in the claim telemetry array      */
+} rkc_pool_desc;
+
+/* ----------------------------------------------------------------------------------------------
+ * Outcome: 16 bytes, one per event, at the event's index.   (§3.1 ClaimEvent; §5.4 refusal record)
+ *
+ * w0 = code[0:8] | flags[8:16] | n16[16:32]
+ *   n16 = number of blocking claims for REFUSED_CLAIM, 0 for REFUSED_CAPACITY, otherwise the
+ *         number of claims that expired at the start of this step; saturates at 65535.
+ * w1 = id, w2 = a, w3 = b:
+ *   ADMIT / EVICT_RESIDENT  after PREFILL: id = request, a = resident victims, b = leading hits h
+ *                           after EXTEND : id = request, a = resident victims, b = active blocks after
+ *                           after CLAIM  : id = claim,   a = resident victims, b = blocks allocated
+ *   REFUSED_CLAIM/CAPACITY  id = smallest blocking claim id (or -1), a = protected resident Pr,
+ *                           b = active live required (A + cached hits + need); shortfall = a + b - U
+ *   MATFAIL                 id = claim, a = blocks needed, b = FREE + evictable blocks available
+ *   DEMOTED / RELEASED      id = claim, a = min(leading registered length, L), b = T
+ *   FINISHED                id = request, a = blocks turned cached, b = blocks dropped (no-admit)
+ *   NOOP / INVALID          id = -1, a = 0, b = 0
+ * -------------------------------------------------------------------------------------------- */
+typedef struct rkc_outcome {
+  int32_t w[4];
+} rkc_outcome;
+
+enum rkc_outcome_code {
+  RKC_OC_ADMIT = 0,
+  RKC_OC_EVICT_RESIDENT = 1,
+  RKC_OC_REFUSED_CLAIM = 2,
+  RKC_OC_REFUSED_CAPACITY = 3,
+  RKC_OC_MATFAIL = 4,
+  RKC_OC_DEMOTED = 5,
+  RKC_OC_RELEASED = 6,
+  RKC_OC_FINISHED = 7,
+  RKC_OC_NOOP = 8,
+  RKC_OC_INVALID = 9
+};
+
+enum rkc_outcome_flag {
+  RKC_FL_EXPIRED = 1,           /* >= 1 claim expired at the start of this step                  */
+  RKC_FL_PRED_FAIL = 2,         /* >= 1 claim first failed its materialization predicate         */
+  RKC_FL_HARM = 4,              /* >= 1 accepted claim was harmed (§3.2)                          */
+  RKC_FL_POST_RELEASE_LOSS = 8, /* a victim was covered only by demoted/expired claims (§3.2)     */
+  RKC_FL_EVICT_UNCLAIMED = 16,  /* a victim was covered by no live claim                          */
+  RKC_FL_NOADMIT_DROP = 32,     /* FINISH dropped non-admitted blocks                              */
+  RKC_FL_LOWERED = 64,          /* hard request lowered to soft priority (check C1, §5.4)          */
+  RKC_FL_SHADOW = 128           /* claim materialized as ordinary cache, not accepted              */
+};
+
+/* ----------------------------------------------------------------------------------------------
+ * Claim telemetry: 40 bytes = 10 x int32, one slot per CLAIM event in step order.
+ *   [0] claim_id (step index; -1 for an unused slot)
+ *   [1] packed = decision[0:4] | state[4:8] | hard_req[8] | prio[9:11] | eff_prot[11:13]
+ *   [2] accept_step [3] demote_step [4] expire_step [5] release_step [6] pred_fail_step
+ *   [7] harm_step   (every step field is -1 when the transition never happened)
+ *   [8] blocked_count: active refusals this claim was attributed to
+ *   [9] lead_end = min(leading registered length of the chain, L) at the end of the replay
+ * A malformed or table-rejected CLAIM keeps its slot with packed = 0 and lead_end = 0.
+ * -------------------------------------------------------------------------------------------- */
+typedef struct rkc_claim_telemetry {
+  int32_t w[10];
+} rkc_claim_telemetry;
+
+enum rkc_decision { /* §3.1 ResidentClaimDecision */
+  RKC_DEC_NONE = 0,
+  RKC_DEC_ACCEPTED = 1,
+  RKC_DEC_ACCEPTED_APPROX = 2,
+  RKC_DEC_SHADOW = 3,
+  RKC_DEC_REJECTED = 4
+};
+
+enum rkc_claim_state { /* §3.1 ResidentClaimState */
+  RKC_ST_SUBMITTED = 0,
+  RKC_ST_OBSERVED = 1,
+  RKC_ST_MATERIALIZED = 2,
+  RKC_ST_DEMOTED = 3,
+  RKC_ST_EXPIRED = 4,
+  RKC_ST_RELEASED = 5,
+  RKC_ST_HARMED = 6,
+  RKC_ST_REJECTED = 7
+};
+
+enum rkc_protection { RKC_PROT_NONE = 0, RKC_PROT_SOFT = 1, RKC_PROT_HARD = 2 };
+
+/* ----------------------------------------------------------------------------------------------
+ * Pool telemetry: 128 bytes = 32 x int32.
+ *   [0..9]  outcomes per code          [10] victims  [11] resident victims  [12] post-release victims
+ *   [13] blocks dropped by no-admit    [14] sum of leading hits of served prefills
+ *   [15] accepted [16] accepted-approx [17] shadow [18] rejected                  (claim decisions)
+ *   [19] harmed [20] predicate failures [21] expired [22] demoted [23] released   (lifecycle)
+ *   [24] peak active blocks [25] final active blocks
+ *   [26] final cached blocks [27] final free blocks [28] final protected blocks
+ *   [29] final live requests [30] final live claims
+ *   [31] status: 0, or RKC_PS_* bits
+ * -------------------------------------------------------------------------------------------- */
+typedef struct rkc_pool_telemetry {
+  int32_t w[32];
+} rkc_pool_telemetry;
+
+enum rkc_pool_status {
+  RKC_PS_REQUEST_TABLE = 1, /* a PREFILL found the live-request table full                   */
+  RKC_PS_CLAIM_TABLE = 2,   /* a CLAIM found the live-claim table full                         */
+  RKC_PS_SLOT_TABLE = 4,    /* more CLAIM events than n_claim_slots                            */
+  RKC_PS_DESCRIPTOR = 256   /* descriptor outside the batch limits; the pool was not replayed,
+                               every outcome is INVALID (an ABI fault, not a contract outcome) */
+};
+
+/* ----------------------------------------------------------------------------------------------
+ * Batch: host struct describing one replay launch.
+ * -------------------------------------------------------------------------------------------- */
+typedef struct rkc_batch {
+  int32_t n_pools;           /* >= 0                                                             */
+  int32_t max_usable_blocks; /* >= every pool's U                                                */
+  int32_t max_events;        /* >= every pool's n_events                                         */
+  int32_t max_chains;        /* >= every pool's n_chains                                         */
+  int32_t max_live_requests; /* >= every pool's max_live_requests                                */
+  int32_t max_live_claims;   /* >= every pool's max_live_claims                                  */
+  int32_t max_claim_slots;   /* >= every pool's n_claim_slots                                    */
+  int32_t flags;             /* must be 0                                                        */
+  int64_t n_events_total;    /* length of the event and outcome arrays                           */
+  int64_t n_claim_slots_total; /* length of the claim telemetry array                            */
+  const rkc_pool_desc* d_pools;     /* [n_pools], 16-byte aligned                               */
+  const rkc_event* d_events;        /* [n_events_total], 16-byte aligned                        */
+  rkc_outcome* d_outcomes;          /* [n_events_total], 16-byte aligned, written               */
+  rkc_pool_telemetry* d_pool_tel;   /* [n_pools], 16-byte aligned, written                      */
+  rkc_claim_telemetry* d_claim_tel; /* [n_claim_slots_total], 8-byte aligned, written           */
+  void* d_scratch;                  /* >= rkc_scratch_bytes(b) bytes, 256-byte aligned          */
+  size_t scratch_bytes;
+} rkc_batch;
+
+typedef enum rkc_status {
+  RKC_OK = 0,
+  RKC_E_NULL = -1,        /* a required pointer is NULL                                       */
+  RKC_E_ALIGN = -2,       /* a pointer is misaligned                                           */
+  RKC_E_RANGE = -3,       /* a count, index or limit is out of range                           */
+  RKC_E_UNSUPPORTED = -4, /* a limit beyond what this implementation supports                  */
+  RKC_E_SCRATCH = -5,     /* scratch buffer missing or too small                               */
+  RKC_E_HIP = -6,         /* a HIP runtime call failed (launch, copy, synchronize)             */
+  RKC_E_POOL_STATUS = -7  /* query succeeded, but the pool's status word is non-zero           */
+} rkc_status;
+
+/* ABI version (RKC_ABI_VERSION). */
+int32_t rkc_abi_version(void);
+
+/* Device scratch bytes rkc_replay_batch needs for this batch (0 when pool state fits on chip).
+ * Reads only the host-side limits of b; never fails (returns 0 for a NULL b). */
+size_t rkc_scratch_bytes(const rkc_batch* b);
+
+/* Replay every pool of the batch from empty pools (all U blocks FREE, no claims, no requests).
+ * Asynchronous: validates the host struct, then only enqueues kernels on stream s (NULL = the
+ * default stream).  Pool i is replayed by its own wavefront or workgroup; pools are independent,
+ * so results do not depend on batch composition or order.  Returns RKC_OK or a negative status;
+ * on a negative status nothing was enqueued. */
+rkc_status rkc_replay_batch(const rkc_batch* b, void* s /* hipStream_t */);
+
+/* Copy outcomes [first, first + count) of pool `pool` into host_dst after synchronizing s.
+ * Also reads the pool descriptor back to locate the events.  Returns RKC_E_RANGE when the range
+ * leaves the pool, RKC_E_POOL_STATUS (data still copied) when the pool's status is non-zero. */
+rkc_status rkc_query_outcomes(const rkc_batch* b, int32_t pool, int32_t first, int32_t count,
+                              rkc_outcome* host_dst, void* s);
+
+/* Copy pool telemetry of `pool` (if host_pool != NULL) and up to max_claims of its claim
+ * telemetry slots (if host_claims != NULL; *n_claims receives the pool's slot count) after
+ * synchronizing s.  Returns RKC_E_POOL_STATUS (data still copied) for a non-zero pool status. */
+rkc_status rkc_query_telemetry(const rkc_batch* b, int32_t pool, rkc_pool_telemetry* host_pool,
+                               rkc_claim_telemetry* host_claims, int32_t max_claims,
+                               int32_t* n_claims, void* s);
+
+/* Static, human-readable name of a status. */
+const char* rkc_status_string(rkc_status st);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RKC_H */

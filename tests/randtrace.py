@@ -1,0 +1,75 @@
+"""Seeded random pools for invariant, brute-force and parity tests (input generation only)."""
+from __future__ import annotations
+
+import numpy as np
+
+
+def random_pool(rng: np.random.Generator, U: int, mode: int, n_events: int, n_chains: int = 3,
+                p_malformed: float = 0.03, tight_tables: bool = False) -> dict:
+    """One pool of arbitrary events, including malformed ones and table overflows."""
+    from paper_2605_24259_amd import tracegen as tg
+    evs = []
+    for _ in range(n_events):
+        r = rng.random()
+        sel = int(rng.integers(0, 1 << 32))
+        if r < 0.26:
+            S = int(rng.integers(1, U + 3))
+            if rng.random() < 0.3:
+                c, P = -1, 0
+            else:
+                c = int(rng.integers(0, n_chains))
+                P = int(rng.integers(0, S + 1))
+            e = tg.prefill(S, c, P)
+        elif r < 0.40:
+            e = tg.extend(int(rng.integers(1, 4)), sel)
+        elif r < 0.62:
+            L = int(rng.integers(1, U + 2))
+            c = int(rng.integers(0, n_chains))
+            T = int(rng.integers(0, L + 1))
+            dur = 0 if rng.random() < 0.5 else int(rng.integers(1, 8))
+            e = tg.claim(L, c, T, hard=int(rng.integers(0, 2)), prio=int(rng.integers(0, 4)),
+                         dur=dur)
+        elif r < 0.76:
+            e = tg.finish(sel)
+        elif r < 0.85:
+            e = tg.release(sel)
+        elif r < 0.96:
+            e = tg.demote(sel)
+        else:
+            e = tg.nop()
+        if rng.random() < p_malformed:
+            kind = int(rng.integers(0, 6))
+            e = list(e)
+            if kind == 0:
+                e[0] = (e[0] & ~15) | int(rng.integers(7, 16))    # unknown type
+            elif kind == 1:
+                e[1] = 0                                           # empty size / footprint
+            elif kind == 2 and (e[0] & 15) == 0:
+                e[3] = e[1] + 1                                    # P > S
+            elif kind == 3 and (e[0] & 15) in (0, 2):
+                e[2] = n_chains + 1                                # chain out of range
+            elif kind == 4 and (e[0] & 15) == 2:
+                e[3] = e[1] + 1                                    # T > L
+            elif kind == 5:
+                e[1] = -5
+        evs.append([int(x) for x in e])
+    pool = dict(usable_blocks=U, mode=mode, n_chains=n_chains, events=evs)
+    if tight_tables:
+        pool["max_live_requests"] = int(rng.integers(1, 4))
+        pool["max_live_claims"] = int(rng.integers(1, 4))
+        n_claims = sum(1 for e in evs if (e[0] & 15) == 2)
+        pool["n_claim_slots"] = int(rng.integers(0, n_claims + 2))
+    return pool
+
+
+def random_batch(seed: int, n_pools: int, U_range=(2, 9), n_events=(1, 14), n_chains=3,
+                 tight_every: int = 5, p_malformed: float = 0.03):
+    from paper_2605_24259_amd import tracegen as tg
+    rng = np.random.default_rng(seed)
+    pools = []
+    for i in range(n_pools):
+        U = int(rng.integers(U_range[0], U_range[1]))
+        ne = int(rng.integers(n_events[0], n_events[1] + 1))
+        pools.append(random_pool(rng, U, i % 4, ne, n_chains=n_chains, p_malformed=p_malformed,
+                                 tight_tables=(tight_every > 0 and i % tight_every == tight_every - 1)))
+    return tg.from_pools(pools, f"random{seed}")

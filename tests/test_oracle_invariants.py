@@ -1,0 +1,141 @@
+"""Oracle against invariants, metamorphic relations and a brute-force model (no GPU needed).
+
+Invariants (checked by the oracle after every step, reported in its check word):
+I1 block counts; I2 no hard-protected victim; I3 no harm of a hard claim under hard protection;
+I4 no acceptance or harm in LRU / no-admit pools; I6 refusal identity Pr + req > U and attribution
+preconditions; I7 one block per (chain, pos); I8 lifecycle transitions; I9 strict eviction order;
+registered positions of a chain always form a leading run; refcounts match live requests.
+"""
+import numpy as np
+import pytest
+
+from tests import randtrace
+
+
+def _check_clean(oracle_mod, trace, **kw):
+    out, ptel, ctel, chk = oracle_mod.replay(trace.desc, trace.events, trace.n_claim_slots, **kw)
+    bad = np.nonzero(chk)[0]
+    assert bad.size == 0, [(int(i), oracle_mod.check_names(int(chk[i]))) for i in bad[:5]]
+    return out, ptel, ctel
+
+
+@pytest.mark.parametrize("seed", [1, 2, 3])
+def test_invariants_random_small(oracle_mod, seed):
+    trace = randtrace.random_batch(seed, 600, U_range=(1, 12), n_events=(1, 40), n_chains=3)
+    _check_clean(oracle_mod, trace)
+
+
+@pytest.mark.parametrize("seed", [11, 12])
+def test_invariants_random_medium(oracle_mod, seed):
+    trace = randtrace.random_batch(seed, 120, U_range=(16, 160), n_events=(50, 200), n_chains=5,
+                                   p_malformed=0.01)
+    _check_clean(oracle_mod, trace)
+
+
+def test_invariants_generated_workloads(oracle_mod, tg):
+    for name, n in (("small", 64), ("zipf", 8)):
+        trace = tg.generate(name, n_pools=n)
+        _, ptel, _ = _check_clean(oracle_mod, trace, threads=8)
+        assert (ptel[:, 31] == 0).all()
+
+
+def test_invariant_accounting(oracle_mod):
+    """Telemetry identities that hold for every pool: final FREE + ACTIVE + CACHED = U, outcome
+    counts sum to the event count, resident >= post-release victims, harm <= predicate failures."""
+    trace = randtrace.random_batch(7, 400, U_range=(1, 40), n_events=(1, 60), n_chains=4)
+    out, ptel, ctel = _check_clean(oracle_mod, trace)
+    U = trace.field("usable_blocks")
+    ne = trace.field("n_events")
+    assert (ptel[:, 25] + ptel[:, 26] + ptel[:, 27] == U).all()
+    assert (ptel[:, :10].sum(1) == ne).all()
+    assert (ptel[:, 11] >= ptel[:, 12]).all() and (ptel[:, 10] >= ptel[:, 11]).all()
+    assert (ptel[:, 19] <= ptel[:, 20]).all()
+    assert (ptel[:, 24] >= ptel[:, 25]).all() and (ptel[:, 24] <= U).all()
+    # every refusal satisfies the infeasibility identity a + b > U (§3.4)
+    eo = trace.field("event_offset")
+    for i in range(trace.n_pools):
+        o = out[eo[i]: eo[i] + ne[i]]
+        code = o[:, 0] & 255
+        ref = (code == 2) | (code == 3)
+        assert (o[ref, 2].astype(np.int64) + o[ref, 3] > U[i]).all()
+        # attributed refusals only in hard pools, with the active side alone fitting
+        att = code == 2
+        if att.any():
+            assert trace.field("mode")[i] == 3
+            assert (o[att, 3] <= U[i]).all() and (o[att, 2] > 0).all()
+            assert ((o[att, 0].view(np.uint32) >> 16) >= 1).all()
+
+
+def test_no_claims_policy_independent(oracle_mod, tg):
+    """I11: with no CLAIM events, LRU, soft and hard pools give identical outputs."""
+    rng = np.random.default_rng(5)
+    pools = []
+    for k in range(60):
+        base = randtrace.random_pool(rng, int(rng.integers(4, 50)), 0, 60, n_chains=3)
+        evs = [e for e in base["events"] if (e[0] & 15) != 2]
+        for mode in (0, 1, 3):
+            pools.append(dict(base, mode=mode, events=evs))
+    trace = tg.from_pools(pools)
+    out, ptel, ctel = _check_clean(oracle_mod, trace)
+    eo = trace.field("event_offset")
+    ne = trace.field("n_events")
+    for k in range(60):
+        rows = [out[eo[3 * k + j]: eo[3 * k + j] + ne[3 * k + j]] for j in range(3)]
+        assert np.array_equal(rows[0], rows[1]) and np.array_equal(rows[0], rows[2])
+        assert np.array_equal(ptel[3 * k], ptel[3 * k + 1]) and np.array_equal(ptel[3 * k], ptel[3 * k + 2])
+
+
+def test_batch_composition_independent(oracle_mod):
+    """I10: a pool's outputs do not depend on the other pools of the batch or on their order."""
+    trace = randtrace.random_batch(21, 50, U_range=(2, 30), n_events=(1, 50))
+    out, ptel, ctel = _check_clean(oracle_mod, trace)
+    perm = np.random.default_rng(0).permutation(trace.n_pools)
+    sub = trace.subset(perm)
+    out2, ptel2, ctel2 = _check_clean(oracle_mod, sub)
+    eo, ne, so, ns = (trace.field(k) for k in ("event_offset", "n_events", "claim_slot_offset",
+                                                "n_claim_slots"))
+    eo2, so2 = sub.field("event_offset"), sub.field("claim_slot_offset")
+    for j, i in enumerate(perm):
+        assert np.array_equal(out[eo[i]: eo[i] + ne[i]], out2[eo2[j]: eo2[j] + ne[i]])
+        assert np.array_equal(ptel[i], ptel2[j])
+        assert np.array_equal(ctel[so[i]: so[i] + ns[i]], ctel2[so2[j]: so2[j] + ns[i]])
+
+
+def _brute_compare(oracle_mod, trace):
+    from oracle import brute
+    out, ptel, ctel = _check_clean(oracle_mod, trace)
+    eo, ne, so, ns = (trace.field(k) for k in ("event_offset", "n_events", "claim_slot_offset",
+                                                "n_claim_slots"))
+    for i in range(trace.n_pools):
+        bo, btel, bsl = brute.replay_pool(trace.desc[i], trace.events[eo[i]: eo[i] + ne[i]])
+        got = out[eo[i]: eo[i] + ne[i]]
+        if ne[i]:
+            assert np.array_equal(np.asarray(bo, np.int64), got.astype(np.int64)), (i, bo, got.tolist())
+        assert np.array_equal(np.asarray(btel), ptel[i]), (i, btel, ptel[i].tolist())
+        if ns[i]:
+            assert np.array_equal(np.asarray(bsl), ctel[so[i]: so[i] + ns[i]]), i
+
+
+@pytest.mark.parametrize("seed", [101, 102, 103, 104])
+def test_bruteforce_random(oracle_mod, seed):
+    """Oracle == brute-force model on random pools of <= 8 blocks, all policies, incl. malformed
+    events and table overflows."""
+    trace = randtrace.random_batch(seed, 400, U_range=(1, 9), n_events=(1, 16), n_chains=3)
+    _brute_compare(oracle_mod, trace)
+
+
+def test_bruteforce_exhaustive_pairs(oracle_mod, tg):
+    """Every ordered pair of events from a small alphabet, on a 4-block pool prepared with two
+    claims and a live request, under all four policies."""
+    prep = [tg.claim(2, 0, 2, hard=1, prio=1), tg.prefill(1, 1, 1), tg.claim(1, 1, 1, prio=2, dur=3)]
+    alphabet = [tg.prefill(1), tg.prefill(2, 0, 2), tg.prefill(3, 1, 1), tg.prefill(4),
+                tg.extend(1, 0), tg.extend(2, 1), tg.claim(2, 0, 1, hard=1), tg.claim(3, 1, 3, prio=3),
+                tg.claim(1, 2, 1, hard=1, dur=1), tg.finish(0), tg.finish(1), tg.release(0),
+                tg.release(1), tg.demote(0), tg.nop()]
+    pools = []
+    for x in alphabet:
+        for y in alphabet:
+            for mode in range(4):
+                pools.append(dict(usable_blocks=4, mode=mode, n_chains=3, events=prep + [x, y]))
+    trace = tg.from_pools(pools)
+    _brute_compare(oracle_mod, trace)
