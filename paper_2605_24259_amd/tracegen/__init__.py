@@ -73,27 +73,27 @@ CONFIGS = {
                   chain_pick=0, n_chains=0, chain_len_min=0, chain_len_max=0,
                   claim_len=1, claim_len_min=8, claim_len_max=64, claim_thresh=0,
                   hard_permille=500, prio_max=3, dur_min=16, dur_max=128, extend_k=1,
-                  claim_cap=0, max_live_claims=0, max_live_requests=0),
+                  claim_cap=0, max_live_claims=64, max_live_requests=64),
     "zipf": dict(cfg_id=3, n_pools=65536, usable_blocks=2048, n_events=1024,
                  mix=(400, 300, 150, 100, 50, 0), prefill_dist=1, prefill_min=4, prefill_max=1536,
                  chain_pick=1, n_chains=256, chain_len_min=32, chain_len_max=512,
                  claim_len=0, claim_len_min=0, claim_len_max=0, claim_thresh=0,
                  hard_permille=250, prio_max=3, dur_min=64, dur_max=512, extend_k=1,
-                 claim_cap=0, max_live_claims=0, max_live_requests=0),
+                 claim_cap=0, max_live_claims=64, max_live_requests=256),
     "nested": dict(cfg_id=4, n_pools=16384, usable_blocks=16384, n_events=2048,
                    mix=(300, 250, 200, 100, 50, 100), prefill_dist=1, prefill_min=16,
                    prefill_max=8192,
                    chain_pick=2, n_chains=64, chain_len_min=4096, chain_len_max=4096,
                    claim_len=2, claim_len_min=64, claim_len_max=4096, claim_thresh=1,
                    hard_permille=500, prio_max=3, dur_min=128, dur_max=1024, extend_k=1,
-                   claim_cap=0, max_live_claims=0, max_live_requests=0),
+                   claim_cap=0, max_live_claims=256, max_live_requests=256),
     "huge": dict(cfg_id=5, n_pools=64, usable_blocks=262144, n_events=65536,
                  mix=(400, 300, 150, 100, 50, 0), prefill_dist=1, prefill_min=4,
                  prefill_max=196608,
                  chain_pick=1, n_chains=256, chain_len_min=4096, chain_len_max=65536,
                  claim_len=0, claim_len_min=0, claim_len_max=0, claim_thresh=0,
                  hard_permille=250, prio_max=3, dur_min=4096, dur_max=32768, extend_k=1,
-                 claim_cap=4096, max_live_claims=4096, max_live_requests=0),
+                 claim_cap=4096, max_live_claims=4096, max_live_requests=16384),
 }
 
 

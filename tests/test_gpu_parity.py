@@ -1,0 +1,217 @@
+"""GPU parity: the HIP replay (through the C ABI) against the CPU oracle, bit-exact.
+
+Everything on the path is integer, so the bar is exact equality of every outcome word, every pool
+telemetry word and every claim telemetry word.  Small cases compare every pool; the full-size
+workloads run in the launch configuration the benchmark times and compare a sample of pools that
+the oracle replays in seconds (for the 262,144-block pools, the leading events of sampled pools:
+the replay is causal, so a prefix of a pool's outcomes is an exact sample).
+"""
+import numpy as np
+import pytest
+
+from tests import golden_fixtures as gf
+from tests import randtrace
+from tests.gpu_util import compare_pools, gpu_replay, say
+
+pytestmark = pytest.mark.gpu
+
+ORACLE_THREADS = 16
+
+
+def _both(oracle_mod, trace, pools=None):
+    say(f"case {trace.name}: {trace.n_pools} pools, {trace.n_events} events")
+    gpu = gpu_replay(trace)
+    ora = oracle_mod.replay(trace.desc, trace.events, trace.n_claim_slots, pools=pools,
+                            threads=ORACLE_THREADS)
+    assert not ora[3].any(), "oracle invariant check failed"
+    return gpu, ora
+
+
+def test_probe(oracle_mod, tg):
+    trace = tg.probe()
+    gpu, ora = _both(oracle_mod, trace)
+    compare_pools(trace, gpu, ora)
+    codes = gpu[0][:, 0] & 255
+    # LRU, soft, no-admit: the active prefill evicts 50 resident blocks; hard: attributed refusal
+    assert list(codes[1::2]) == [1, 1, 1, 2]
+    assert gpu[0][7].tolist()[1:] == [0, 60, 70]
+
+
+def test_golden_fixtures(oracle_mod, tg):
+    fx = gf.all_fixtures()
+    trace = gf.to_trace(tg, fx)
+    gpu, ora = _both(oracle_mod, trace)
+    errs = gf.check(fx, trace, *gpu)
+    assert not errs, "\n".join(errs)
+    compare_pools(trace, gpu, ora)
+
+
+def test_capacity_sweep(oracle_mod, tg):
+    pools = [dict(usable_blocks=U, mode=m, n_chains=2,
+                  events=[tg.claim(60, 0, 60, hard=1, prio=3), tg.prefill(70, 1, 0)])
+             for m in range(4) for U in range(1, 201)]
+    trace = tg.from_pools(pools, "capacity-sweep")
+    gpu, ora = _both(oracle_mod, trace)
+    compare_pools(trace, gpu, ora)
+
+
+@pytest.mark.parametrize("seed", [1, 2, 3, 4])
+def test_random_tiny(oracle_mod, seed):
+    """Pools of <= 12 blocks with malformed events and table overflows, all policies."""
+    trace = randtrace.random_batch(seed, 3000, U_range=(1, 13), n_events=(0, 40), n_chains=3)
+    gpu, ora = _both(oracle_mod, trace)
+    compare_pools(trace, gpu, ora)
+
+
+@pytest.mark.parametrize("seed", [11, 12, 13])
+def test_random_medium(oracle_mod, seed):
+    """Several tiles of events per pool (up to 400 > 64-event prefetch), ragged tails, up to 9 chains."""
+    trace = randtrace.random_batch(seed, 400, U_range=(8, 300), n_events=(1, 400), n_chains=9,
+                                   p_malformed=0.01, tight_every=7)
+    gpu, ora = _both(oracle_mod, trace)
+    compare_pools(trace, gpu, ora)
+
+
+def test_edge_cases(oracle_mod, tg):
+    """Empty pools, one-block pools, no chains, a maximal pool size, a pool whose events all fail."""
+    pools = [
+        dict(usable_blocks=1, mode=0, n_chains=0, events=[]),
+        dict(usable_blocks=1, mode=3, n_chains=0, events=[tg.prefill(1), tg.extend(1), tg.finish()]),
+        dict(usable_blocks=1, mode=1, n_chains=1, events=[tg.claim(1, 0, 1, hard=1), tg.prefill(1),
+                                                         tg.release(), tg.prefill(1)]),
+        dict(usable_blocks=(1 << 22), mode=3, n_chains=2,
+             events=[tg.claim(60, 0, 60, hard=1, prio=3), tg.prefill(70, 1, 0),
+                     tg.prefill(1 << 24, -1, 0), tg.extend(1 << 24), tg.finish(7)]),
+        dict(usable_blocks=50, mode=2, n_chains=1,
+             events=[tg.ev(9), tg.prefill(0), tg.claim(0, 0), tg.claim(5, 3), tg.claim(5, 0, 6),
+                     tg.prefill(5, 7, 5), tg.extend(0), tg.nop()]),
+        dict(usable_blocks=80, mode=3, n_chains=2, max_live_claims=0, max_live_requests=0,
+             n_claim_slots=0, events=[tg.claim(10, 0), tg.prefill(5), tg.claim(10, 1)]),
+    ]
+    trace = tg.from_pools(pools, "edges")
+    gpu, ora = _both(oracle_mod, trace)
+    compare_pools(trace, gpu, ora)
+
+
+def test_small_full(oracle_mod, tg):
+    """4,096 pools x 80 blocks x 256 events: every pool compared."""
+    trace = tg.generate("small")
+    gpu, ora = _both(oracle_mod, trace)
+    compare_pools(trace, gpu, ora)
+
+
+def _sample(n_pools, k):
+    idx = np.unique(np.linspace(0, n_pools - 1, k).astype(int))
+    return [int(i) for i in idx]
+
+
+def _properties(trace, gpu):
+    """Identities that hold for every pool at any size."""
+    out, pt, ct = gpu
+    U = trace.field("usable_blocks").astype(np.int64)
+    ne = trace.field("n_events")
+    assert (pt[:, 31] & ~7 == 0).all(), "internal fault or descriptor status"
+    assert (pt[:, :10].sum(1) == ne).all()
+    assert (pt[:, 25] + pt[:, 26] + pt[:, 27] == U).all()
+    assert (pt[:, 24] <= U).all() and (pt[:, 24] >= pt[:, 25]).all()
+    code = out[:, 0] & 255
+    ref = (code == 2) | (code == 3)
+    Ue = np.repeat(U, ne)
+    assert (out[ref, 2].astype(np.int64) + out[ref, 3] > Ue[ref]).all()
+
+
+def test_zipf_full_sampled(oracle_mod, tg):
+    """65,536 pools x 2,048 blocks x 1,024 events (the benchmark workload)."""
+    trace = tg.generate("zipf")
+    pools = _sample(trace.n_pools, 96)
+    gpu, ora = _both(oracle_mod, trace, pools=pools)
+    compare_pools(trace, gpu, ora, pools=pools)
+    _properties(trace, gpu)
+
+
+def test_nested_full_sampled(oracle_mod, tg):
+    """16,384 pools x 16,384 blocks x 2,048 events, nested claims, demotion-heavy."""
+    trace = tg.generate("nested")
+    pools = _sample(trace.n_pools, 6)
+    gpu, ora = _both(oracle_mod, trace, pools=pools)
+    compare_pools(trace, gpu, ora, pools=pools)
+    _properties(trace, gpu)
+
+
+def test_huge_full_prefix_sampled(oracle_mod, tg):
+    """64 pools x 262,144 blocks x 65,536 events; the oracle replays the first 1,500 events of
+    sampled pools and their outcomes must equal the GPU's first 1,500 outcomes."""
+    trace = tg.generate("huge")
+    say(f"case huge: {trace.n_pools} pools, {trace.n_events} events")
+    gpu = gpu_replay(trace)
+    _properties(trace, gpu)
+    pools = [0, 21, 42, 63]
+    sub = trace.subset(pools)
+    pre = 1500
+    d = sub.desc.copy()
+    evs = []
+    for j in range(len(pools)):
+        d[j, 2] = pre
+        d[j, 8:10] = np.array([j * pre], np.int64).view(np.int32)
+        evs.append(sub.events[j * 65536: j * 65536 + pre])
+    ora = oracle_mod.replay(d, np.concatenate(evs), sub.n_claim_slots, threads=4)
+    assert not ora[3].any()
+    eo = trace.field("event_offset")
+    for j, p in enumerate(pools):
+        a = gpu[0][eo[p]: eo[p] + pre]
+        b = ora[0][j * pre: (j + 1) * pre]
+        assert np.array_equal(a, b), (p, int(np.nonzero((a != b).any(1))[0][0]))
+
+
+def test_batch_order_independent(oracle_mod, tg):
+    """I10: reversing and subsetting the batch changes no pool's outputs."""
+    trace = randtrace.random_batch(31, 500, U_range=(4, 120), n_events=(1, 150), n_chains=5)
+    g1 = gpu_replay(trace)
+    perm = list(range(trace.n_pools))[::-1][::2]
+    sub = trace.subset(perm)
+    g2 = gpu_replay(sub)
+    eo, ne = trace.field("event_offset"), trace.field("n_events")
+    eo2 = sub.field("event_offset")
+    for j, i in enumerate(perm):
+        assert np.array_equal(g1[0][eo[i]: eo[i] + ne[i]], g2[0][eo2[j]: eo2[j] + ne[i]])
+        assert np.array_equal(g1[1][i], g2[1][j])
+
+
+def test_repeat_deterministic(tg):
+    trace = tg.generate("zipf", n_pools=2048)
+    a = gpu_replay(trace)
+    b = gpu_replay(trace)
+    for x, y in zip(a, b):
+        assert np.array_equal(x, y)
+
+
+def test_abi_queries(oracle_mod, tg):
+    import paper_2605_24259_amd as rkc
+    trace = tg.generate("small", n_pools=64)
+    db = rkc.DeviceBatch.from_trace(trace).replay()
+    out, pt, ct = db.results()
+    eo, so, ns = trace.field("event_offset"), trace.field("claim_slot_offset"), trace.field("n_claim_slots")
+    for p in (0, 17, 63):
+        st, o = db.query_outcomes(p, 3, 100)
+        assert st == 0 and np.array_equal(o, out[eo[p] + 3: eo[p] + 103])
+        st, ptel, ctel, n = db.query_telemetry(p, 1000)
+        assert st == 0 and n == ns[p]
+        assert np.array_equal(ptel, pt[p]) and np.array_equal(ctel, ct[so[p]: so[p] + ns[p]])
+    assert db.query_outcomes(64, 0, 1)[0] == -3
+    assert db.query_outcomes(0, 250, 10)[0] == -3
+    assert db.query_outcomes(-1, 0, 1)[0] == -3
+
+
+def test_descriptor_outside_batch_limits(tg):
+    """A pool whose descriptor exceeds the launch's declared limits is not replayed: its outcomes
+    are INVALID and its status carries the descriptor bit (an ABI fault, not a contract outcome)."""
+    import paper_2605_24259_amd as rkc
+    trace = tg.from_pools([dict(usable_blocks=80, mode=0, n_chains=2, events=[tg.prefill(5)] * 3),
+                           dict(usable_blocks=80, mode=3, n_chains=2, events=[tg.prefill(5)] * 3)])
+    lim = trace.limits()
+    trace.desc[1, 0] = 81  # U above the batch maximum of 80
+    db = rkc.DeviceBatch(trace.desc, trace.events, trace.n_claim_slots, lim).replay()
+    out, pt, ct = db.results()
+    assert (out[:3, 0] & 255 == 0).all()
+    assert (out[3:, 0] & 255 == 9).all() and pt[1, 31] == 256 and pt[1, 9] == 3
+    assert db.query_telemetry(1, 0)[0] == -7
