@@ -1,0 +1,198 @@
+"""Benchmark: replayed allocator events/s of the batched resident-claim replay on one MI355X.
+
+A step is one launch that replays every pool of the workload from empty pools through every event
+(expiry, validation, feasibility, victim selection, commit, lifecycle, predicate sweep, outcome and
+telemetry emission).  Inputs are resident in HBM before timing starts; outputs are fully
+overwritten by every launch, so repeated steps are identical.
+
+Default workload: 65,536 pools x 2,048 usable blocks x 1,024 events (prefixes shared through 256
+Zipf(1.1) chains per pool), i.e. 67,108,864 events per step.
+
+Prints one JSON line (rank 0).  Also:
+  --mode copy   runs only a plain device copy of known size (calibrates rocprofv3 byte counters and
+                gives the measured copy ceiling).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, AMD published peak
+BYTES_EVENT, BYTES_OUTCOME, BYTES_CLAIM_SLOT, BYTES_POOL_TEL, BYTES_DESC = 16, 16, 40, 128, 48
+COPY_BYTES = 1 << 30
+METRIC = "replayed allocator events/sec (1 GPU) + % of HBM peak; bit-exact vs oracle"
+
+
+def credited_bytes(trace) -> int:
+    """Algorithmic bytes of one replay launch: events in, outcomes out, claim slots out, pool
+    telemetry out, descriptors in.  Scratch, LDS traffic and re-reads are not credited."""
+    return (trace.n_events * (BYTES_EVENT + BYTES_OUTCOME) + trace.n_claim_slots * BYTES_CLAIM_SLOT
+            + trace.n_pools * (BYTES_POOL_TEL + BYTES_DESC))
+
+
+def copy_ceiling(torch, reps=20):
+    n = COPY_BYTES // 4
+    a = torch.empty(n, dtype=torch.int32, device="cuda").fill_(1)
+    b = torch.empty_like(a)
+    for _ in range(3):
+        b.copy_(a)
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    s.record()
+    for _ in range(reps):
+        b.copy_(a)
+    e.record()
+    torch.cuda.synchronize()
+    ms = s.elapsed_time(e) / reps
+    return 2.0 * COPY_BYTES / (ms * 1e-3) / 1e9
+
+
+def cpu_baseline(trace, seconds_budget=12.0):
+    """The oracle as it stands, on the host's cores, over a bounded sample of the same workload:
+    leading pools in chunks until the wall budget is spent."""
+    import oracle
+    threads = max(1, min(16, os.cpu_count() or 1))
+    eo = trace.field("event_offset")
+    done_pools, done_events = 0, 0
+    t0 = time.perf_counter()
+    chunk = threads * 8
+    while done_pools < trace.n_pools and time.perf_counter() - t0 < seconds_budget:
+        pools = list(range(done_pools, min(trace.n_pools, done_pools + chunk)))
+        sub = trace.subset(pools)
+        oracle.replay(sub.desc, sub.events, sub.n_claim_slots, threads=threads)
+        done_pools += len(pools)
+        done_events += sub.n_events
+    wall = time.perf_counter() - t0
+    return dict(value=done_events / wall, unit="events/s", cores=threads, kind="oracle",
+                sample=f"first {done_pools} pools of the workload ({done_events} events), "
+                       f"{threads} threads, {wall:.1f} s wall")
+
+
+def traffic_from_profiles(kernel_sha):
+    """HBM bytes per launch from committed rocprofv3 counter summaries, if they were taken on this
+    kernel source; else None."""
+    path = os.path.join(ROOT, "profiles", "rkc_replay_wave_zipf_traffic.json")
+    if not os.path.exists(path):
+        return None
+    d = json.load(open(path))
+    if d.get("kernel_source_sha256") != kernel_sha:
+        return None
+    return d.get("traffic_bytes_per_launch")
+
+
+def kernel_source_sha():
+    import hashlib
+    src = os.path.join(ROOT, "paper_2605_24259_amd", "csrc", "rkc_replay.hip")
+    return hashlib.sha256(open(src, "rb").read()).hexdigest()
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="zipf", choices=["small", "zipf", "nested", "huge"])
+    ap.add_argument("--mode", default="replay", choices=["replay", "copy"])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-parity", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py: this build replays on one GPU only (pools are independent; a multi-GPU "
+              "run would split the pool range across ranks, which is not implemented)", flush=True)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    if args.mode == "copy":
+        gbps = copy_ceiling(torch, reps=args.steps)
+        print(json.dumps(dict(mode="copy", bytes_per_copy=2 * COPY_BYTES, gbps=round(gbps, 1))), flush=True)
+        return
+
+    import paper_2605_24259_amd as rkc
+    from paper_2605_24259_amd import tracegen as tg
+
+    trace = tg.generate(args.workload)
+    db = rkc.DeviceBatch.from_trace(trace)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    for _ in range(args.warmup):
+        db.replay(stream)
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    start.record(stream)
+    for _ in range(args.steps):
+        db.replay(stream)
+    end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_per_step = start.elapsed_time(end) / args.steps
+    events = trace.n_events
+    value = events / (ms_per_step * 1e-3)
+    cbytes = credited_bytes(trace)
+    achieved = cbytes / (ms_per_step * 1e-3) / 1e9
+
+    parity = None
+    if not args.no_parity:
+        import oracle
+        out, ptel, ctel = db.results()
+        pools = [int(i) for i in np.linspace(0, trace.n_pools - 1, 16).astype(int)]
+        sub = trace.subset(pools)
+        o_out, o_pt, o_ct, chk = oracle.replay(sub.desc, sub.events, sub.n_claim_slots, threads=16)
+        eo, ne, so, ns = (trace.field(k) for k in ("event_offset", "n_events", "claim_slot_offset",
+                                                    "n_claim_slots"))
+        eo2, so2 = sub.field("event_offset"), sub.field("claim_slot_offset")
+        ok = not chk.any()
+        for j, p in enumerate(pools):
+            ok &= np.array_equal(out[eo[p]: eo[p] + ne[p]], o_out[eo2[j]: eo2[j] + ne[p]])
+            ok &= np.array_equal(ptel[p], o_pt[j])
+            ok &= np.array_equal(ctel[so[p]: so[p] + ns[p]], o_ct[so2[j]: so2[j] + ns[p]])
+        parity = f"{'bit-exact' if ok else 'MISMATCH'} vs oracle on {len(pools)} sampled pools"
+
+    ceiling = copy_ceiling(torch)
+    base = None if args.no_cpu_baseline else cpu_baseline(trace)
+    lim = trace.limits()
+    line = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "events/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int32",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{args.workload}: {trace.n_pools} pools x {lim['max_usable_blocks']} usable "
+                        f"blocks x {lim['max_events']} events",
+            "pools": trace.n_pools, "usable_blocks": lim["max_usable_blocks"],
+            "events_per_pool": lim["max_events"], "events_per_step": events,
+            "claim_slots": trace.n_claim_slots, "parallelism": "one wavefront per pool",
+        },
+        "roofline": {
+            "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBPS, 4),
+            "traffic": traffic_from_profiles(kernel_source_sha()),
+            "credited_bytes_per_launch": cbytes,
+            "copy_ceiling_gbps": round(ceiling, 1),
+            "frac_of_copy_ceiling": round(achieved / ceiling, 4),
+        },
+        "cpu_baseline": base,
+        "parity": parity,
+        "wall_s": round(wall, 3),
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

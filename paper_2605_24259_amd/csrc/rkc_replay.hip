@@ -39,6 +39,11 @@ typedef int32_t i32;
 typedef uint64_t u64;
 typedef int64_t i64;
 
+// Explicit address spaces for arrays reached through a run-time choice (LDS part or global part
+// of the node arena), so each access compiles to a ds_ or global_ instruction, never a flat one.
+typedef __attribute__((address_space(3))) uint4 lds_uint4;
+typedef __attribute__((address_space(1))) uint4 glb_uint4;
+
 constexpr u32 NIL = 0xFFFFFFFFu;
 constexpr u64 KEY_INF = ~0ull;
 constexpr u32 EXP_NEVER = 0xFFFFFFFFu;
@@ -68,38 +73,60 @@ __device__ __forceinline__ u64 make_key(u32 level, u32 lu, u32 pos) {
 // ---- wave primitives ------------------------------------------------------------------------
 __device__ __forceinline__ u32 lane_id() { return __lane_id(); }
 
-__device__ __forceinline__ u32 wave_max(u32 v) {
-  for (int o = 32; o > 0; o >>= 1) v = max(v, (u32)__shfl_xor((int)v, o));
-  return v;
-}
-__device__ __forceinline__ u32 wave_min(u32 v) {
-  for (int o = 32; o > 0; o >>= 1) v = min(v, (u32)__shfl_xor((int)v, o));
-  return v;
-}
-__device__ __forceinline__ u32 wave_sum(u32 v) {
-  for (int o = 32; o > 0; o >>= 1) v += (u32)__shfl_xor((int)v, o);
-  return v;
-}
-__device__ __forceinline__ u64 shfl_xor64(u64 v, int o) {
-  u32 lo = (u32)__shfl_xor((int)(u32)v, o);
-  u32 hi = (u32)__shfl_xor((int)(u32)(v >> 32), o);
-  return ((u64)hi << 32) | lo;
-}
-__device__ __forceinline__ u64 wave_min64(u64 v) {
-  for (int o = 32; o > 0; o >>= 1) {
-    u64 w = shfl_xor64(v, o);
-    v = w < v ? w : v;
-  }
-  return v;
-}
 __device__ __forceinline__ u64 ballot(bool p) { return __ballot(p); }
 __device__ __forceinline__ i32 rdlane(i32 v, u32 l) { return __builtin_amdgcn_readlane(v, (int)l); }
+
+// Cross-lane reductions with DPP row permutes (no LDS round trip): within each 16-lane row,
+// combine lanes i^1, i^2, the mirrored half-row and the mirrored row, so every lane of a row holds
+// the row's result; then combine the four rows through readlane.  All 64 lanes must be active.
+template <int CTRL>
+__device__ __forceinline__ u32 dpp(u32 v) {
+  return (u32)__builtin_amdgcn_update_dpp((int)v, (int)v, CTRL, 0xF, 0xF, false);
+}
+constexpr int kDppXor1 = 0xB1;       // quad_perm [1,0,3,2]
+constexpr int kDppXor2 = 0x4E;       // quad_perm [2,3,0,1]
+constexpr int kDppHalfMirror = 0x141;
+constexpr int kDppMirror = 0x140;
+
+struct OpMax { __device__ static u32 f(u32 a, u32 b) { return a > b ? a : b; } };
+struct OpMin { __device__ static u32 f(u32 a, u32 b) { return a < b ? a : b; } };
+struct OpAdd { __device__ static u32 f(u32 a, u32 b) { return a + b; } };
+
+template <class Op>
+__device__ __forceinline__ u32 wave_reduce(u32 v) {
+  v = Op::f(v, dpp<kDppXor1>(v));
+  v = Op::f(v, dpp<kDppXor2>(v));
+  v = Op::f(v, dpp<kDppHalfMirror>(v));
+  v = Op::f(v, dpp<kDppMirror>(v));
+  const u32 r0 = (u32)rdlane((i32)v, 0), r1 = (u32)rdlane((i32)v, 16);
+  const u32 r2 = (u32)rdlane((i32)v, 32), r3 = (u32)rdlane((i32)v, 48);
+  return Op::f(Op::f(r0, r1), Op::f(r2, r3));
+}
+__device__ __forceinline__ u32 wave_max(u32 v) { return wave_reduce<OpMax>(v); }
+__device__ __forceinline__ u32 wave_min(u32 v) { return wave_reduce<OpMin>(v); }
+__device__ __forceinline__ u32 wave_sum(u32 v) { return wave_reduce<OpAdd>(v); }
+
+template <int CTRL>
+__device__ __forceinline__ u64 dpp64(u64 v) {
+  return ((u64)dpp<CTRL>((u32)(v >> 32)) << 32) | dpp<CTRL>((u32)v);
+}
+__device__ __forceinline__ u64 min64(u64 a, u64 b) { return a < b ? a : b; }
+__device__ __forceinline__ u64 rdlane64(u64 v, u32 l) {
+  return ((u64)(u32)rdlane((i32)(u32)(v >> 32), l) << 32) | (u32)rdlane((i32)(u32)v, l);
+}
+__device__ __forceinline__ u64 wave_min64(u64 v) {
+  v = min64(v, dpp64<kDppXor1>(v));
+  v = min64(v, dpp64<kDppXor2>(v));
+  v = min64(v, dpp64<kDppHalfMirror>(v));
+  v = min64(v, dpp64<kDppMirror>(v));
+  return min64(min64(rdlane64(v, 0), rdlane64(v, 16)), min64(rdlane64(v, 32), rdlane64(v, 48)));
+}
 
 // ---- launch geometry (computed on the host) ---------------------------------------------------
 struct Layout {
   u32 chains, reqs, claims, nodes_lds;
   u32 off_n, off_hold, off_prot, off_covA, off_covS, off_tpend, off_lv, off_stop, off_sbot,
-      off_mark, off_key, off_tel, off_rq, off_cl, off_node;
+      off_mark, off_key, off_tel, off_rq, off_cl, off_node, off_bt, off_nx;
   u32 lds_bytes;
   u64 scr_pool_bytes, scr_off_node, scr_off_fifo, scr_off_slot, scr_off_rq, scr_off_cl;
   u32 fifo_cap, node_cap;
@@ -122,6 +149,8 @@ enum : u32 { MK_SWEEP = 1, MK_RECOMP = 2 };
 // internal-consistency fault bit in the pool status word: set only if a structural bound that
 // the algorithm guarantees is ever violated; loops stop instead of running on.
 constexpr u32 kFault = 0x80000000u;
+// chains whose top keys live in registers (four per lane)
+constexpr u32 kRegChains = 256;
 
 struct AllocRes {
   bool ok;
@@ -141,13 +170,15 @@ struct Pool {
   u32 lane;
   // LDS arrays
   u32 *n, *hold, *prot, *covA, *covS, *tpend, *lv, *stop, *sbot, *mark, *tel;
-  u64* topkey;
+  u32 *bt, *nx;   // cached bottom of each touch stack: its step, and the extent of the pair above
+  u64* topkey;    // chains >= kRegChains; lower chains keep their top key in registers (kr)
+  u64 kr0, kr1, kr2, kr3;  // top key of chain 64 * k + lane, k = 0..3
   u32 *rq_id, *rq_c, *rq_R, *rq_len;
   u32 *cl_id, *cl_c, *cl_L, *cl_T, *cl_meta, *cl_exp, *cl_slot, *cl_blk;
   u32 *cl_dem, *cl_exst, *cl_pf, *cl_harm;  // demote / expire / predicate-failure / harm steps
   u32 cl_cap, rq_cap;
-  uint4* node_lds;
-  uint4* node_glb;
+  lds_uint4* node_lds;
+  glb_uint4* node_glb;
   u32 nl;
   uint4* fifo;
   u32 fifo_cap;
@@ -155,6 +186,7 @@ struct Pool {
   rkc_claim_telemetry* rec;
   // scalar state (wave-uniform)
   i32 F, A, PR, peak;
+  i32 Eall;       // sum over chains of max(0, n - max(hold, prot)): evictable shared blocks
   u32 nreq, ncl, nslot;
   u32 next_exp;
   u32 free_head, bump;
@@ -163,13 +195,28 @@ struct Pool {
   u32 status;
   u32 node_cap;
 
-  // -- nodes (x = extent, y = step, z = up (newer), w = down (older)) --
-  __device__ __forceinline__ uint4* node(u32 i) { return i < nl ? node_lds + i : node_glb + (i - nl); }
+  // -- nodes (x = extent, y = step, z = up (newer), w = down (older)); the first nl live in LDS,
+  //    the rest in global scratch (both read and written by every lane with uniform addresses) --
+  __device__ __forceinline__ uint4 nget(u32 i) {
+    uint4 v;
+    if (i < nl) { const lds_uint4& r = node_lds[i]; v = make_uint4(r.x, r.y, r.z, r.w); }
+    else { const glb_uint4& r = node_glb[i - nl]; v = make_uint4(r.x, r.y, r.z, r.w); }
+    return v;
+  }
+  __device__ __forceinline__ u32 nget_x(u32 i) { u32 v; if (i < nl) v = node_lds[i].x; else v = node_glb[i - nl].x; return v; }
+  __device__ __forceinline__ u32 nget_z(u32 i) { u32 v; if (i < nl) v = node_lds[i].z; else v = node_glb[i - nl].z; return v; }
+  __device__ __forceinline__ u32 nget_w(u32 i) { u32 v; if (i < nl) v = node_lds[i].w; else v = node_glb[i - nl].w; return v; }
+  __device__ __forceinline__ void nset(u32 i, uint4 v) {
+    if (i < nl) { node_lds[i].x = v.x; node_lds[i].y = v.y; node_lds[i].z = v.z; node_lds[i].w = v.w; }
+    else { node_glb[i - nl].x = v.x; node_glb[i - nl].y = v.y; node_glb[i - nl].z = v.z; node_glb[i - nl].w = v.w; }
+  }
+  __device__ __forceinline__ void nset_z(u32 i, u32 v) { if (i < nl) node_lds[i].z = v; else node_glb[i - nl].z = v; }
+  __device__ __forceinline__ void nset_w(u32 i, u32 v) { if (i < nl) node_lds[i].w = v; else node_glb[i - nl].w = v; }
   __device__ __forceinline__ u32 node_alloc() {
     u32 i;
     if (free_head != NIL) {
       i = free_head;
-      free_head = node(i)->w;
+      free_head = nget_w(i);
     } else if (bump < node_cap) {
       i = bump++;
     } else {
@@ -180,8 +227,33 @@ struct Pool {
     return i;
   }
   __device__ __forceinline__ void node_free(u32 i) {
-    node(i)->w = free_head;
+    nset_w(i, free_head);
     free_head = i;
+  }
+
+  // -- top keys: registers for chains < kRegChains, LDS above --
+  __device__ __forceinline__ void set_key(u32 c, u64 k) {
+    if (c < kRegChains) {
+      const u32 l = c & 63u, s = c >> 6;
+      if (lane == l) {
+        if (s == 0) kr0 = k;
+        else if (s == 1) kr1 = k;
+        else if (s == 2) kr2 = k;
+        else kr3 = k;
+      }
+    } else {
+      topkey[c] = k;
+    }
+  }
+
+  // -- chain counters: every change of n, hold or prot keeps Eall and PR (protected cached
+  //    blocks, hard-protection pools) exact --
+  __device__ __forceinline__ i32 evictable(u32 nn, u32 hh, u32 pp) { return max(0, (i32)nn - (i32)max(hh, pp)); }
+  __device__ __forceinline__ void chain_update(u32 c, u32 nn, u32 hh, u32 pp) {
+    const u32 n0 = n[c], h0 = hold[c], p0 = prot[c];
+    Eall += evictable(nn, hh, pp) - evictable(n0, h0, p0);
+    PR += max(0, (i32)pp - (i32)hh) - max(0, (i32)p0 - (i32)h0);
+    n[c] = nn; hold[c] = hh; prot[c] = pp;
   }
 
   __device__ __forceinline__ void lists_fence() {
@@ -199,49 +271,54 @@ struct Pool {
     return lvl;
   }
 
-  // Key of chain c's top candidate; advances the touch stack's bottom to the pair covering n-1.
+  // Key of chain c's top candidate.  The stack bottom is the newest pair covering position n-1
+  // exactly when the pair above it (extent nx) does not reach n-1; otherwise advance the bottom.
   __device__ __forceinline__ u64 top_key(u32 c) {
-    u32 nn = n[c];
-    u32 lo = max(hold[c], prot[c]);
+    const u32 nn = n[c];
+    const u32 lo = max(hold[c], prot[c]);
     if (nn <= lo) return KEY_INF;
-    u32 b = sbot[c];
-    if (b == NIL) { status |= kFault; return KEY_INF; }
-    for (u32 guard = 0; guard < node_cap; guard++) {
-      u32 up = node(b)->z;
-      if (up != NIL && node(up)->x >= nn) {
-        node(up)->w = NIL;
+    u32 t_bot = bt[c];
+    if (nx[c] >= nn) {
+      u32 b = sbot[c];
+      if (b == NIL) { status |= kFault; return KEY_INF; }
+      u32 up = nget_z(b);
+      for (u32 guard = 0; guard < node_cap && up != NIL && nget_x(up) >= nn; guard++) {
+        nset_w(up, NIL);
         node_free(b);
         b = up;
-      } else {
-        break;
+        up = nget_z(b);
       }
+      sbot[c] = b;
+      t_bot = nget(b).y;
+      bt[c] = t_bot;
+      nx[c] = up != NIL ? nget_x(up) : 0u;
     }
-    sbot[c] = b;
-    return make_key(level_at(c, nn - 1), node(b)->y, nn - 1);
+    return make_key(level_at(c, nn - 1), t_bot, nn - 1);
   }
-  __device__ __forceinline__ void refresh(u32 c) { topkey[c] = top_key(c); }
+  __device__ __forceinline__ void refresh(u32 c) { set_key(c, top_key(c)); }
 
   // Record a touch of positions [0, x) of chain c at step t.
   __device__ __forceinline__ void touch(u32 c, u32 x, u32 t) {
     if (x == 0) return;
     u32 tp = stop[c];
-    for (u32 guard = 0; guard < node_cap && tp != NIL && node(tp)->x <= x; guard++) {
-      u32 d = node(tp)->w;
+    for (u32 guard = 0; guard < node_cap && tp != NIL && nget_x(tp) <= x; guard++) {
+      const u32 d = nget_w(tp);
       node_free(tp);
       tp = d;
     }
-    u32 nw = node_alloc();
-    *node(nw) = make_uint4(x, t, NIL, tp);
-    if (tp != NIL) node(tp)->z = nw; else sbot[c] = nw;
+    const u32 nw = node_alloc();
+    nset(nw, make_uint4(x, t, NIL, tp));
+    if (tp != NIL) {
+      nset_z(tp, nw);
+      if (tp == sbot[c]) nx[c] = x;   // the new pair sits right above the bottom
+    } else {
+      sbot[c] = nw;                   // the new pair is the whole stack
+      bt[c] = t;
+      nx[c] = 0;
+    }
     stop[c] = nw;
   }
 
-  __device__ __forceinline__ i32 prot_cached(u32 c) { return max(0, (i32)prot[c] - (i32)hold[c]); }
-  __device__ __forceinline__ void set_hold(u32 c, u32 v) {
-    PR -= prot_cached(c);
-    hold[c] = v;
-    PR += prot_cached(c);
-  }
 
   // Recompute chain c's claim maxima from the live-claim list.
   __device__ __forceinline__ void recompute(u32 c) {
@@ -262,9 +339,7 @@ struct Pool {
     }
     pr = wave_max(pr); l1 = wave_max(l1); l2 = wave_max(l2); l3 = wave_max(l3); l4 = wave_max(l4);
     ca = wave_max(ca); cs = wave_max(cs); tp = wave_max(tp);
-    PR -= prot_cached(c);
-    prot[c] = pr;
-    PR += prot_cached(c);
+    chain_update(c, n[c], hold[c], pr);
     lv[4 * c + 0] = l1; lv[4 * c + 1] = l2; lv[4 * c + 2] = l3; lv[4 * c + 3] = l4;
     covA[c] = ca; covS[c] = cs; tpend[c] = tp;
     refresh(c);
@@ -289,14 +364,12 @@ struct Pool {
   // Candidates: shared-chain tops above max(hold, prot) (and above the hits on chain hc), plus the
   // private FIFO runs.
   __device__ __forceinline__ i32 candidates(i32 hc, u32 h) {
-    u32 s = 0;
-    for (u32 c = lane; c < (u32)n_chains; c += 64) {
-      u32 lo = max(hold[c], prot[c]);
-      if ((i32)c == hc) lo = max(lo, h);
-      u32 nn = n[c];
-      s += nn > lo ? nn - lo : 0;
+    i32 e = Eall + fblocks;
+    if (hc >= 0) {
+      const u32 nn = n[hc], lo = max(hold[hc], prot[hc]);
+      e -= evictable(nn, lo, 0) - evictable(nn, max(lo, h), 0);
     }
-    return (i32)wave_sum(s) + fblocks;
+    return e;
   }
 
   __device__ __forceinline__ void fifo_pop_front() {
@@ -326,9 +399,19 @@ struct Pool {
       if (guard > (u32)U + 1) { status |= kFault; break; }
       u64 k1 = KEY_INF, k2 = KEY_INF;
       u32 i1 = NIL;
-      for (u32 c = lane; c < (u32)n_chains; c += 64) {
+      const bool hc_empty = hc >= 0 && n[hc] <= h;  // every candidate of the hit chain is a hit
+      const u64 krs[4] = {kr0, kr1, kr2, kr3};
+#pragma unroll
+      for (u32 q = 0; q < 4; q++) {
+        const u32 c = 64 * q + lane;
+        u64 k = krs[q];
+        if (hc_empty && (i32)c == hc) k = KEY_INF;
+        if (k < k1) { k2 = k1; k1 = k; i1 = c; }
+        else if (k < k2) k2 = k;
+      }
+      for (u32 c = kRegChains + lane; c < (u32)n_chains; c += 64) {
         u64 k = topkey[c];
-        if ((i32)c == hc && n[c] <= h) k = KEY_INF;
+        if (hc_empty && (i32)c == hc) k = KEY_INF;
         if (k < k1) { k2 = k1; k1 = k; i1 = c; }
         else if (k < k2) k2 = k;
       }
@@ -369,8 +452,7 @@ struct Pool {
         u32 lvb = 0;
         if (soft_levels())
           for (u32 v = lvl + 1; v <= 4; v++) lvb = max(lvb, lv[4 * c + v - 1]);
-        u32 up = node(sbot[c])->z;
-        u32 lub = up != NIL ? node(up)->x : 0;
+        const u32 lub = nx[c];  // positions below it were touched later
         u32 run_lo = max(lo, max(lvb, lub));
         u32 m_run = nn - run_lo;
         if (tie) m_run = nn - max(run_lo, p2 + 1);
@@ -383,7 +465,7 @@ struct Pool {
         r.resident += res;
         r.post += res - strict;
         r.unclaimed += (i32)m - res;
-        n[c] = nw;
+        chain_update(c, nw, hold[c], prot[c]);
         refresh(c);
         if (nw < tpend[c]) {
           mark[c] |= MK_SWEEP;
@@ -522,7 +604,7 @@ struct Pool {
   }
 
   // One event.  Returns the outcome words.
-  __device__ __forceinline__ void step(u32 t, i32 w0, i32 w1, i32 w2, i32 w3, i32 o[4]) {
+  __device__ __forceinline__ int4 step(u32 t, i32 w0, i32 w1, i32 w2, i32 w3) {
     const u32 uw0 = (u32)w0;
     const u32 type = uw0 & 15u, hardq = (uw0 >> 4) & 1u, prio = (uw0 >> 5) & 3u, dur = uw0 >> 16;
     u32 flags = 0, expired = 0, n16 = NIL;
@@ -574,8 +656,8 @@ struct Pool {
         if (hc >= 0) {
           const u32 c = (u32)hc;
           R = mode == RKC_MODE_NOADMIT ? h : (u32)P;
-          if (mode != RKC_MODE_NOADMIT && (u32)P > n[c]) n[c] = (u32)P;
-          set_hold(c, max(hold[c], R));
+          const u32 nn = (mode != RKC_MODE_NOADMIT && (u32)P > n[c]) ? (u32)P : n[c];
+          chain_update(c, nn, max(hold[c], R), prot[c]);
           touch(c, R, t);
           refresh(c);
         }
@@ -621,7 +703,7 @@ struct Pool {
         write_record(s, (i32)t, packed_of(m), -1, -1, -1, -1, -1, -1, 0);
         code = RKC_OC_MATFAIL; id = (i32)t; a = need; b = F + r.E;
       } else {
-        if ((u32)L > n[c]) n[c] = (u32)L;
+        if ((u32)L > n[c]) chain_update(c, (u32)L, hold[c], prot[c]);
         touch(c, (u32)L, t);
         u32 st;
         if (mode == RKC_MODE_LRU || mode == RKC_MODE_NOADMIT) {
@@ -637,8 +719,15 @@ struct Pool {
         cl_id[k] = t; cl_c[k] = c; cl_L[k] = (u32)L; cl_T[k] = (u32)T; cl_meta[k] = m;
         cl_exp[k] = ex; cl_slot[k] = s; cl_blk[k] = 0;
         cl_dem[k] = NIL; cl_exst[k] = NIL; cl_pf[k] = NIL; cl_harm[k] = NIL;
-        __builtin_amdgcn_wave_barrier();
-        recompute(c);
+        // a new live claim only raises the chain's maxima
+        covA[c] = max(covA[c], (u32)L);
+        covS[c] = max(covS[c], (u32)L);
+        tpend[c] = max(tpend[c], (u32)T);
+        if (mode == RKC_MODE_HARD && st == ST_MATERIALIZED && eff == RKC_PROT_HARD)
+          chain_update(c, n[c], hold[c], max(prot[c], (u32)L));
+        if (soft_levels() && st == ST_MATERIALIZED && eff == RKC_PROT_SOFT)
+          lv[4 * c + prio] = max(lv[4 * c + prio], (u32)L);
+        refresh(c);
         next_exp = min(next_exp, ex);
         code = r.resident > 0 ? RKC_OC_EVICT_RESIDENT : RKC_OC_ADMIT;
         id = (i32)t; a = r.resident; b = need;
@@ -662,22 +751,21 @@ struct Pool {
             if (rq_c[j] == c) hn = max(hn, rq_R[j]);
           hn = wave_max(hn);
           turned += max(0, (i32)R - (i32)hn);
-          set_hold(c, hn);
+          chain_update(c, n[c], hn, prot[c]);
           touch(c, R, t);
           refresh(c);
         }
+        // write no-admit drops the request's own blocks; otherwise they become a private run
         const i32 own = (i32)(len - R);
-        if (mode == RKC_MODE_NOADMIT) {
-          dropped = own;
-          F += own;
-        } else {
-          turned += own;
-          if (own > 0) {
-            if (fhead == ftail) { ft = t; flo = R; ftop = len; }
-            fifo[ftail % fifo_cap] = make_uint4(t, R, len, 0);
-            ftail++;
-            fblocks += own;
-          }
+        const bool drop = mode == RKC_MODE_NOADMIT;
+        dropped = drop ? own : 0;
+        turned += drop ? 0 : own;
+        F += dropped;
+        fblocks += drop ? 0 : own;
+        if (!drop && own > 0) {
+          if (fhead == ftail) { ft = t; flo = R; ftop = len; }
+          fifo[ftail % fifo_cap] = make_uint4(t, R, len, 0);
+          ftail++;
         }
         A -= turned + dropped;
         code = RKC_OC_FINISHED; id = (i32)rid; a = turned; b = dropped;
@@ -743,8 +831,7 @@ struct Pool {
     if (n16 == NIL) n16 = min(expired, 65535u);
     tel[code] += 1;
     peak = max(peak, A);
-    o[0] = (i32)((u32)code | (flags << 8) | (n16 << 16));
-    o[1] = id; o[2] = a; o[3] = b;
+    return make_int4((i32)((u32)code | (flags << 8) | (n16 << 16)), id, a, b);
   }
 };
 
@@ -788,6 +875,7 @@ __global__ __launch_bounds__(64) void rkc_replay_wave(Args g) {
   P.tpend = (u32*)(lds + L.off_tpend); P.lv = (u32*)(lds + L.off_lv);
   P.stop = (u32*)(lds + L.off_stop); P.sbot = (u32*)(lds + L.off_sbot);
   P.mark = (u32*)(lds + L.off_mark); P.topkey = (u64*)(lds + L.off_key);
+  P.bt = (u32*)(lds + L.off_bt); P.nx = (u32*)(lds + L.off_nx);
   P.tel = (u32*)(lds + L.off_tel);
   unsigned char* scr = g.scratch + (u64)pool * L.scr_pool_bytes;
   u32* rq = kGL ? (u32*)(scr + L.scr_off_rq) : (u32*)(lds + L.off_rq);
@@ -800,9 +888,9 @@ __global__ __launch_bounds__(64) void rkc_replay_wave(Args g) {
   P.cl_blk = cl + 7 * L.claims; P.cl_dem = cl + 8 * L.claims; P.cl_exst = cl + 9 * L.claims;
   P.cl_pf = cl + 10 * L.claims; P.cl_harm = cl + 11 * L.claims;
   P.node_cap = L.node_cap;
-  P.node_lds = (uint4*)(lds + L.off_node);
+  P.node_lds = (lds_uint4*)(lds + L.off_node);
   P.nl = L.nodes_lds;
-  P.node_glb = (uint4*)(scr + L.scr_off_node);
+  P.node_glb = (glb_uint4*)(scr + L.scr_off_node);
   P.fifo = (uint4*)(scr + L.scr_off_fifo);
   P.fifo_cap = L.fifo_cap;
   P.slot_cl = (uint2*)(scr + L.scr_off_slot);
@@ -811,10 +899,12 @@ __global__ __launch_bounds__(64) void rkc_replay_wave(Args g) {
   for (i32 c = (i32)P.lane; c < P.n_chains; c += 64) {
     P.n[c] = 0; P.hold[c] = 0; P.prot[c] = 0; P.covA[c] = 0; P.covS[c] = 0; P.tpend[c] = 0;
     P.lv[4 * c] = 0; P.lv[4 * c + 1] = 0; P.lv[4 * c + 2] = 0; P.lv[4 * c + 3] = 0;
-    P.stop[c] = NIL; P.sbot[c] = NIL; P.mark[c] = 0; P.topkey[c] = KEY_INF;
+    P.stop[c] = NIL; P.sbot[c] = NIL; P.mark[c] = 0; P.bt[c] = 0; P.nx[c] = 0;
+    if ((u32)c >= kRegChains) P.topkey[c] = KEY_INF;
   }
+  P.kr0 = P.kr1 = P.kr2 = P.kr3 = KEY_INF;
   if (P.lane < 32) P.tel[P.lane] = 0;
-  P.F = P.U; P.A = 0; P.PR = 0; P.peak = 0;
+  P.F = P.U; P.A = 0; P.PR = 0; P.peak = 0; P.Eall = 0;
   P.nreq = 0; P.ncl = 0; P.nslot = 0; P.next_exp = EXP_NEVER;
   P.free_head = NIL; P.bump = 0;
   P.fhead = 0; P.ftail = 0; P.ft = 0; P.flo = 0; P.ftop = 0; P.fblocks = 0;
@@ -832,10 +922,9 @@ __global__ __launch_bounds__(64) void rkc_replay_wave(Args g) {
     }
     int4 mine = make_int4(0, 0, 0, 0);
     for (i32 k = 0; k < cnt; k++) {
-      i32 o[4];
-      P.step((u32)(base + k), rdlane(e.x, (u32)k), rdlane(e.y, (u32)k), rdlane(e.z, (u32)k),
-             rdlane(e.w, (u32)k), o);
-      if ((i32)P.lane == k) mine = make_int4(o[0], o[1], o[2], o[3]);
+      const int4 o = P.step((u32)(base + k), rdlane(e.x, (u32)k), rdlane(e.y, (u32)k),
+                            rdlane(e.z, (u32)k), rdlane(e.w, (u32)k));
+      if ((i32)P.lane == k) mine = o;
     }
     if ((i32)P.lane < cnt) out[base + P.lane] = rkc_outcome{{mine.x, mine.y, mine.z, mine.w}};
   }
@@ -887,11 +976,12 @@ bool make_layout(const rkc_batch* b, Layout* L, bool global_lists) {
   u64 o = 0;
   auto take = [&](u64 bytes, u64 al) { o = align_up(o, al); u64 r = o; o += bytes; return (u32)r; };
   const u64 C = L->chains;
-  L->off_key = take(8 * C, 16);
+  L->off_key = take(8 * (C > kRegChains ? C - 0 : 1), 16);
   L->off_n = take(4 * C, 4); L->off_hold = take(4 * C, 4); L->off_prot = take(4 * C, 4);
   L->off_covA = take(4 * C, 4); L->off_covS = take(4 * C, 4); L->off_tpend = take(4 * C, 4);
   L->off_lv = take(16 * C, 16); L->off_stop = take(4 * C, 4); L->off_sbot = take(4 * C, 4);
   L->off_mark = take(4 * C, 4); L->off_tel = take(128, 16);
+  L->off_bt = take(4 * C, 4); L->off_nx = take(4 * C, 4);
   if (!global_lists) {
     L->off_rq = take(16ull * L->reqs, 16);
     L->off_cl = take(48ull * L->claims, 16);
