@@ -6,24 +6,29 @@
 // The pool is not kept one block at a time.  Because every touch, hit, hold, protection and claim
 // coverage is a leading range [0, x) of a chain, the registered positions of every shared chain are
 // always a leading run [0, n_c) and eviction always takes a chain from its top.  The kernel therefore
-// keeps, per shared chain:
+// keeps one 64-byte record per shared chain in LDS:
 //   n      registered length              hold   leading positions held ACTIVE by live requests
 //   prot   max L of materialized hard claims (hard-protection pools)
 //   lv[v]  max L of claims that rank victims at soft level v (priority + 1)
 //   covA   max L of live claims           covS   max L of live claims not demoted / expired
 //   tpend  max T of claims whose predicate has not failed yet
 //   a touch stack: (x, t) pairs, x strictly decreasing, t increasing; position p was last touched
-//          at the t of the newest pair with x > p
-//   topkey the eviction key (level, last use, -pos) of the chain's top candidate
-// Finished requests' private blocks form runs (finish step, [lo, top)); runs finish in step order,
-// so they sit in a FIFO and the front run is always the oldest.
+//          at the t of the newest pair with x > p; its bottom pair's step (bt) and the extent of
+//          the pair above it (nx) are cached in the record
+// and the eviction key (level, last use, -pos) of each chain's top candidate (in registers for the
+// first 256 chains).  Finished requests' private blocks form runs (finish step, [lo, top)); runs
+// finish in step order, so they sit in a FIFO and the front run is always the oldest.
 //
 // Victim selection takes the (need - F) smallest keys (level asc, last use asc, pos desc) over all
 // candidates (§3.1 soft priority; §5.3 ordinary eviction after free blocks; hard-protected blocks
 // excluded).  It merges chain tops: a wave min-reduction finds the chain with the smallest top key
 // and the runner-up key, then whole runs of equal (level, last use) are evicted at once.
 //
-// LDS holds the per-chain arrays, the live-request and live-claim lists and the first touch-stack
+// Everything the pool's logic reads with a uniform address is moved into scalar registers
+// (readfirstlane), so the per-event state machine runs on the scalar unit; lanes are used for scans
+// over claims and requests, for DPP reductions, and to hold the pool's counters (lane k = word k).
+//
+// LDS holds the chain records, the live-request and live-claim lists and the first touch-stack
 // nodes; global scratch holds the remaining nodes, the FIFO ring and the per-slot (chain, L) table.
 // Scratch is only read back by the lane(s) that wrote it, or after a workgroup fence.
 #include <hip/hip_runtime.h>
@@ -39,10 +44,34 @@ typedef int32_t i32;
 typedef uint64_t u64;
 typedef int64_t i64;
 
-// Explicit address spaces for arrays reached through a run-time choice (LDS part or global part
-// of the node arena), so each access compiles to a ds_ or global_ instruction, never a flat one.
+// Explicit address spaces, so every access compiles to a ds_ or global_ instruction, never a flat one.
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) u32 lds_u32;
+typedef __attribute__((address_space(3))) u32x4 lds_u32x4;
 typedef __attribute__((address_space(3))) uint4 lds_uint4;
+typedef __attribute__((address_space(3))) u64 lds_u64;
+typedef __attribute__((address_space(1))) u32 glb_u32;
 typedef __attribute__((address_space(1))) uint4 glb_uint4;
+
+// Storage width of LDS-resident pool state: 16-bit words when every stored position, step, index
+// and count is below 0xFFFF (usable blocks <= 32,767, events <= 65,533), else 32-bit words.  All
+// arithmetic is 32-bit; the all-ones word of either width stands for NIL.
+template <typename W> struct Store;
+template <> struct Store<uint16_t> {
+  typedef __attribute__((address_space(3))) uint16_t lds_w;
+  typedef unsigned short w4 __attribute__((ext_vector_type(4)));
+  typedef __attribute__((address_space(3))) w4 lds_w4;
+  static constexpr u32 wnil = 0xFFFFu;
+};
+template <> struct Store<u32> {
+  typedef lds_u32 lds_w;
+  typedef u32x4 w4;
+  typedef lds_u32x4 lds_w4;
+  static constexpr u32 wnil = 0xFFFFFFFFu;
+};
+// lists in LDS with the pool's word width, or in global scratch as 32-bit words
+template <typename W, bool kGL> struct ListMem { typedef typename Store<W>::lds_w word; };
+template <typename W> struct ListMem<W, true> { typedef glb_u32 word; };
 
 constexpr u32 NIL = 0xFFFFFFFFu;
 constexpr u64 KEY_INF = ~0ull;
@@ -52,6 +81,24 @@ constexpr u32 EXP_NEVER = 0xFFFFFFFFu;
 enum : u32 { ST_SUBMITTED = 0, ST_OBSERVED = 1, ST_MATERIALIZED = 2, ST_DEMOTED = 3, ST_EXPIRED = 4,
              ST_RELEASED = 5, ST_HARMED = 6, ST_REJECTED = 7 };
 enum : u32 { DEC_ACCEPTED = 1, DEC_APPROX = 2, DEC_SHADOW = 3, DEC_REJECTED = 4 };
+
+// chain record words (four 16-byte groups)
+enum : u32 { CF_N = 0, CF_HOLD = 1, CF_PROT = 2, CF_BT = 3,          // group 0
+             CF_NX = 4, CF_COVA = 5, CF_COVS = 6, CF_TPEND = 7,      // group 1
+             CF_LV = 8,                                              // group 2: lv[0..3]
+             CF_STOP = 12, CF_SBOT = 13,                             // group 3
+             CF_WORDS = 16 };
+
+// live-claim list arrays (struct of arrays, capacity cl_cap each)
+enum : u32 { CL_ID = 0, CL_C, CL_L, CL_T, CL_META, CL_EXP, CL_SLOT, CL_BLK, CL_DEM, CL_EXST, CL_PF,
+             CL_HARM, CL_ARRAYS };
+// live-request list arrays
+enum : u32 { RQ_ID = 0, RQ_C, RQ_R, RQ_LEN, RQ_ARRAYS };
+
+// pool telemetry words kept in lane k of one register
+enum : u32 { TW_VICTIMS = 10, TW_RESIDENT = 11, TW_POST = 12, TW_DROPPED = 13, TW_HITS = 14,
+             TW_ACCEPTED = 15, TW_HARM = 19, TW_PREDFAIL = 20, TW_EXPIRED = 21, TW_DEMOTED = 22,
+             TW_RELEASED = 23 };
 
 // live-claim meta word: state[0:3) eff[3:5) hard[5] prio[6:8) pending[8] decision[9:12)
 __device__ __forceinline__ u32 m_state(u32 m) { return m & 7u; }
@@ -72,9 +119,11 @@ __device__ __forceinline__ u64 make_key(u32 level, u32 lu, u32 pos) {
 
 // ---- wave primitives ------------------------------------------------------------------------
 __device__ __forceinline__ u32 lane_id() { return __lane_id(); }
-
 __device__ __forceinline__ u64 ballot(bool p) { return __ballot(p); }
 __device__ __forceinline__ i32 rdlane(i32 v, u32 l) { return __builtin_amdgcn_readlane(v, (int)l); }
+// a value every lane holds identically, moved to a scalar register
+__device__ __forceinline__ u32 ufl(u32 v) { return (u32)__builtin_amdgcn_readfirstlane((int)v); }
+__device__ __forceinline__ uint4 ufl4(uint4 v) { return make_uint4(ufl(v.x), ufl(v.y), ufl(v.z), ufl(v.w)); }
 
 // Cross-lane reductions with DPP row permutes (no LDS round trip): within each 16-lane row,
 // combine lanes i^1, i^2, the mirrored half-row and the mirrored row, so every lane of a row holds
@@ -125,12 +174,11 @@ __device__ __forceinline__ u64 wave_min64(u64 v) {
 // ---- launch geometry (computed on the host) ---------------------------------------------------
 struct Layout {
   u32 chains, reqs, claims, nodes_lds;
-  u32 off_n, off_hold, off_prot, off_covA, off_covS, off_tpend, off_lv, off_stop, off_sbot,
-      off_mark, off_key, off_tel, off_rq, off_cl, off_node, off_bt, off_nx;
+  u32 off_chain, off_mark, off_key, off_rq, off_cl, off_node;
   u32 lds_bytes;
   u64 scr_pool_bytes, scr_off_node, scr_off_fifo, scr_off_slot, scr_off_rq, scr_off_cl;
   u32 fifo_cap, node_cap;
-  u32 global_lists;
+  u32 global_lists, narrow;
 };
 
 struct Args {
@@ -162,28 +210,34 @@ struct AllocRes {
 // kGL: the live-request and live-claim lists live in global scratch instead of LDS (pools whose
 // lists do not fit on chip).  Lane-parallel writes to them are then followed by a workgroup fence
 // before any other lane reads them.
-template <bool kGL>
+template <typename W, bool kGL>
 struct Pool {
+  typedef typename ListMem<W, kGL>::word lword;
+  typedef typename Store<W>::lds_w lds_w;
+  typedef typename Store<W>::w4 w4;
+  typedef typename Store<W>::lds_w4 lds_w4;
+  static constexpr u32 kListNil = kGL ? 0xFFFFFFFFu : Store<W>::wnil;
+  static constexpr u32 kWordNil = Store<W>::wnil;
   // descriptor
   i32 U, mode, n_events, n_chains, max_claims, max_reqs, n_slots;
-  i64 ev_off, slot_off;
   u32 lane;
-  // LDS arrays
-  u32 *n, *hold, *prot, *covA, *covS, *tpend, *lv, *stop, *sbot, *mark, *tel;
-  u32 *bt, *nx;   // cached bottom of each touch stack: its step, and the extent of the pair above
-  u64* topkey;    // chains >= kRegChains; lower chains keep their top key in registers (kr)
-  u64 kr0, kr1, kr2, kr3;  // top key of chain 64 * k + lane, k = 0..3
-  u32 *rq_id, *rq_c, *rq_R, *rq_len;
-  u32 *cl_id, *cl_c, *cl_L, *cl_T, *cl_meta, *cl_exp, *cl_slot, *cl_blk;
-  u32 *cl_dem, *cl_exst, *cl_pf, *cl_harm;  // demote / expire / predicate-failure / harm steps
-  u32 cl_cap, rq_cap;
-  lds_uint4* node_lds;
-  glb_uint4* node_glb;
-  u32 nl;
+  // memory
+  lds_w* ch;          // chain records, CF_WORDS words each
+  lds_u32* mk;        // per-chain mark bits
+  lds_u64* tk;        // top keys of chains >= kRegChains
+  lword* rq;          // live requests, RQ_ARRAYS arrays of rq_cap
+  lword* cl;          // live claims, CL_ARRAYS arrays of cl_cap
+  u32 rq_cap, cl_cap;
+  lds_w4* node_lds;   // nodes [0, nl)
+  glb_uint4* node_glb;  // nodes [nl, node_cap), 32-bit words
+  u32 nl, node_cap;
   uint4* fifo;
   u32 fifo_cap;
   uint2* slot_cl;
   rkc_claim_telemetry* rec;
+  // registers
+  u64 kr0, kr1, kr2, kr3;  // top key of chain 64 * k + lane, k = 0..3
+  u32 tv;                  // pool telemetry word `lane` (lanes 0..31)
   // scalar state (wave-uniform)
   i32 F, A, PR, peak;
   i32 Eall;       // sum over chains of max(0, n - max(hold, prot)): evictable shared blocks
@@ -193,25 +247,60 @@ struct Pool {
   u32 fhead, ftail, ft, flo, ftop;
   i32 fblocks;
   u32 status;
-  u32 node_cap;
+
+  // -- telemetry words held lane-distributed --
+  __device__ __forceinline__ void tadd(u32 w, u32 v) { tv += lane == w ? v : 0u; }
+
+  // -- chain records --
+  __device__ __forceinline__ static u32 widen(u32 v, u32 wnil) { return v == wnil ? NIL : v; }
+  __device__ __forceinline__ u32 cf(u32 c, u32 f) { return ufl(ch[c * CF_WORDS + f]); }
+  __device__ __forceinline__ u32 cfn(u32 c, u32 f) { return widen(cf(c, f), kWordNil); }  // NIL-able field
+  __device__ __forceinline__ void cs(u32 c, u32 f, u32 v) { ch[c * CF_WORDS + f] = (W)v; }
+  __device__ __forceinline__ uint4 cg(u32 c, u32 g) {
+    const w4 v = ((lds_w4*)(ch + c * CF_WORDS))[g];
+    return ufl4(make_uint4(v.x, v.y, v.z, v.w));
+  }
+  __device__ __forceinline__ void cgs(u32 c, u32 g, uint4 v) {
+    w4 w;
+    w.x = (W)v.x; w.y = (W)v.y; w.z = (W)v.z; w.w = (W)v.w;
+    ((lds_w4*)(ch + c * CF_WORDS))[g] = w;
+  }
+
+  // -- lists --
+  __device__ __forceinline__ lword* cla(u32 k) { return cl + k * cl_cap; }
+  __device__ __forceinline__ lword* rqa(u32 k) { return rq + k * rq_cap; }
+  __device__ __forceinline__ static u32 lnil(u32 v) { return v == kListNil ? NIL : v; }
+  __device__ __forceinline__ void lists_fence() {
+    if (kGL) __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
+  }
 
   // -- nodes (x = extent, y = step, z = up (newer), w = down (older)); the first nl live in LDS,
-  //    the rest in global scratch (both read and written by every lane with uniform addresses) --
+  //    the rest in global scratch (read and written by every lane with uniform addresses) --
   __device__ __forceinline__ uint4 nget(u32 i) {
     uint4 v;
-    if (i < nl) { const lds_uint4& r = node_lds[i]; v = make_uint4(r.x, r.y, r.z, r.w); }
-    else { const glb_uint4& r = node_glb[i - nl]; v = make_uint4(r.x, r.y, r.z, r.w); }
-    return v;
+    if (i < nl) {
+      const w4 r = node_lds[i];
+      v = make_uint4(r.x, r.y, widen(r.z, kWordNil), widen(r.w, kWordNil));
+    } else {
+      const glb_uint4& r = node_glb[i - nl];
+      v = make_uint4(r.x, r.y, r.z, r.w);
+    }
+    return ufl4(v);
   }
-  __device__ __forceinline__ u32 nget_x(u32 i) { u32 v; if (i < nl) v = node_lds[i].x; else v = node_glb[i - nl].x; return v; }
-  __device__ __forceinline__ u32 nget_z(u32 i) { u32 v; if (i < nl) v = node_lds[i].z; else v = node_glb[i - nl].z; return v; }
-  __device__ __forceinline__ u32 nget_w(u32 i) { u32 v; if (i < nl) v = node_lds[i].w; else v = node_glb[i - nl].w; return v; }
+  __device__ __forceinline__ u32 nget_x(u32 i) { u32 v; if (i < nl) v = node_lds[i].x; else v = node_glb[i - nl].x; return ufl(v); }
+  __device__ __forceinline__ u32 nget_z(u32 i) { u32 v; if (i < nl) v = widen(node_lds[i].z, kWordNil); else v = node_glb[i - nl].z; return ufl(v); }
+  __device__ __forceinline__ u32 nget_w(u32 i) { u32 v; if (i < nl) v = widen(node_lds[i].w, kWordNil); else v = node_glb[i - nl].w; return ufl(v); }
   __device__ __forceinline__ void nset(u32 i, uint4 v) {
-    if (i < nl) { node_lds[i].x = v.x; node_lds[i].y = v.y; node_lds[i].z = v.z; node_lds[i].w = v.w; }
-    else { node_glb[i - nl].x = v.x; node_glb[i - nl].y = v.y; node_glb[i - nl].z = v.z; node_glb[i - nl].w = v.w; }
+    if (i < nl) {
+      w4 w;
+      w.x = (W)v.x; w.y = (W)v.y; w.z = (W)v.z; w.w = (W)v.w;
+      node_lds[i] = w;
+    } else {
+      node_glb[i - nl].x = v.x; node_glb[i - nl].y = v.y; node_glb[i - nl].z = v.z; node_glb[i - nl].w = v.w;
+    }
   }
-  __device__ __forceinline__ void nset_z(u32 i, u32 v) { if (i < nl) node_lds[i].z = v; else node_glb[i - nl].z = v; }
-  __device__ __forceinline__ void nset_w(u32 i, u32 v) { if (i < nl) node_lds[i].w = v; else node_glb[i - nl].w = v; }
+  __device__ __forceinline__ void nset_z(u32 i, u32 v) { if (i < nl) node_lds[i].z = (W)v; else node_glb[i - nl].z = v; }
+  __device__ __forceinline__ void nset_w(u32 i, u32 v) { if (i < nl) node_lds[i].w = (W)v; else node_glb[i - nl].w = v; }
   __device__ __forceinline__ u32 node_alloc() {
     u32 i;
     if (free_head != NIL) {
@@ -242,44 +331,47 @@ struct Pool {
         else kr3 = k;
       }
     } else {
-      topkey[c] = k;
+      tk[c] = k;
     }
   }
 
   // -- chain counters: every change of n, hold or prot keeps Eall and PR (protected cached
   //    blocks, hard-protection pools) exact --
-  __device__ __forceinline__ i32 evictable(u32 nn, u32 hh, u32 pp) { return max(0, (i32)nn - (i32)max(hh, pp)); }
-  __device__ __forceinline__ void chain_update(u32 c, u32 nn, u32 hh, u32 pp) {
-    const u32 n0 = n[c], h0 = hold[c], p0 = prot[c];
-    Eall += evictable(nn, hh, pp) - evictable(n0, h0, p0);
-    PR += max(0, (i32)pp - (i32)hh) - max(0, (i32)p0 - (i32)h0);
-    n[c] = nn; hold[c] = hh; prot[c] = pp;
-  }
-
-  __device__ __forceinline__ void lists_fence() {
-    if (kGL) __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
+  __device__ __forceinline__ static i32 evictable(u32 nn, u32 hh, u32 pp) { return max(0, (i32)nn - (i32)max(hh, pp)); }
+  __device__ __forceinline__ void chain_update(u32 c, uint4 g0, u32 nn, u32 hh, u32 pp) {
+    Eall += evictable(nn, hh, pp) - evictable(g0.x, g0.y, g0.z);
+    PR += max(0, (i32)pp - (i32)hh) - max(0, (i32)g0.z - (i32)g0.y);
+    cgs(c, 0, make_uint4(nn, hh, pp, g0.w));
   }
 
   __device__ __forceinline__ bool soft_levels() const { return mode == RKC_MODE_SOFT || mode == RKC_MODE_HARD; }
 
-  __device__ __forceinline__ u32 level_at(u32 c, u32 p) {
-    if (!soft_levels()) return 0;
+  // soft level of position p and the lowest position sharing it
+  __device__ __forceinline__ u32 level_at(uint4 lv, u32 p, u32& lvb) {
     u32 lvl = 0;
-#pragma unroll
-    for (u32 v = 1; v <= 4; v++)
-      if (lv[4 * c + v - 1] > p) lvl = v;
+    lvb = 0;
+    if (soft_levels()) {
+      if (lv.x > p) lvl = 1;
+      if (lv.y > p) lvl = 2;
+      if (lv.z > p) lvl = 3;
+      if (lv.w > p) lvl = 4;
+      if (lvl < 1) lvb = max(lvb, lv.x);
+      if (lvl < 2) lvb = max(lvb, lv.y);
+      if (lvl < 3) lvb = max(lvb, lv.z);
+      if (lvl < 4) lvb = max(lvb, lv.w);
+    }
     return lvl;
   }
 
   // Key of chain c's top candidate.  The stack bottom is the newest pair covering position n-1
   // exactly when the pair above it (extent nx) does not reach n-1; otherwise advance the bottom.
   __device__ __forceinline__ u64 top_key(u32 c) {
-    const u32 nn = n[c];
-    const u32 lo = max(hold[c], prot[c]);
-    if (nn <= lo) return KEY_INF;
-    u32 t_bot = bt[c];
-    if (nx[c] >= nn) {
-      u32 b = sbot[c];
+    const uint4 g0 = cg(c, 0);
+    const u32 nn = g0.x;
+    if (nn <= max(g0.y, g0.z)) return KEY_INF;
+    u32 t_bot = g0.w;
+    if (cf(c, CF_NX) >= nn) {
+      u32 b = cfn(c, CF_SBOT);
       if (b == NIL) { status |= kFault; return KEY_INF; }
       u32 up = nget_z(b);
       for (u32 guard = 0; guard < node_cap && up != NIL && nget_x(up) >= nn; guard++) {
@@ -288,19 +380,22 @@ struct Pool {
         b = up;
         up = nget_z(b);
       }
-      sbot[c] = b;
+      cs(c, CF_SBOT, b);
       t_bot = nget(b).y;
-      bt[c] = t_bot;
-      nx[c] = up != NIL ? nget_x(up) : 0u;
+      cs(c, CF_BT, t_bot);
+      cs(c, CF_NX, up != NIL ? nget_x(up) : 0u);
     }
-    return make_key(level_at(c, nn - 1), t_bot, nn - 1);
+    u32 lvb;
+    const u32 lvl = level_at(cg(c, 2), nn - 1, lvb);
+    return make_key(lvl, t_bot, nn - 1);
   }
   __device__ __forceinline__ void refresh(u32 c) { set_key(c, top_key(c)); }
 
   // Record a touch of positions [0, x) of chain c at step t.
   __device__ __forceinline__ void touch(u32 c, u32 x, u32 t) {
     if (x == 0) return;
-    u32 tp = stop[c];
+    u32 tp = cfn(c, CF_STOP);
+    const u32 sb = cfn(c, CF_SBOT);
     for (u32 guard = 0; guard < node_cap && tp != NIL && nget_x(tp) <= x; guard++) {
       const u32 d = nget_w(tp);
       node_free(tp);
@@ -310,53 +405,53 @@ struct Pool {
     nset(nw, make_uint4(x, t, NIL, tp));
     if (tp != NIL) {
       nset_z(tp, nw);
-      if (tp == sbot[c]) nx[c] = x;   // the new pair sits right above the bottom
+      if (tp == sb) cs(c, CF_NX, x);   // the new pair sits right above the bottom
     } else {
-      sbot[c] = nw;                   // the new pair is the whole stack
-      bt[c] = t;
-      nx[c] = 0;
+      cs(c, CF_SBOT, nw);              // the new pair is the whole stack
+      cs(c, CF_BT, t);
+      cs(c, CF_NX, 0);
     }
-    stop[c] = nw;
+    cs(c, CF_STOP, nw);
   }
-
 
   // Recompute chain c's claim maxima from the live-claim list.
   __device__ __forceinline__ void recompute(u32 c) {
-    u32 pr = 0, l1 = 0, l2 = 0, l3 = 0, l4 = 0, ca = 0, cs = 0, tp = 0;
+    u32 pr = 0, l1 = 0, l2 = 0, l3 = 0, l4 = 0, ca = 0, cso = 0, tp = 0;
     const bool hardm = mode == RKC_MODE_HARD, softl = soft_levels();
     for (u32 i = lane; i < ncl; i += 64) {
-      if (cl_c[i] != c) continue;
-      u32 m = cl_meta[i], L = cl_L[i], st = m_state(m);
+      if (cla(CL_C)[i] != c) continue;
+      const u32 m = cla(CL_META)[i], L = cla(CL_L)[i], st = m_state(m);
       ca = max(ca, L);
-      if (st == ST_OBSERVED || st == ST_MATERIALIZED || st == ST_HARMED) cs = max(cs, L);
+      if (st == ST_OBSERVED || st == ST_MATERIALIZED || st == ST_HARMED) cso = max(cso, L);
       if (hardm && st == ST_MATERIALIZED && m_eff(m) == RKC_PROT_HARD) pr = max(pr, L);
       if (softl && ((st == ST_MATERIALIZED && m_eff(m) == RKC_PROT_SOFT) || st == ST_DEMOTED)) {
-        u32 p = m_prio(m);
+        const u32 p = m_prio(m);
         if (p == 0) l1 = max(l1, L); else if (p == 1) l2 = max(l2, L);
         else if (p == 2) l3 = max(l3, L); else l4 = max(l4, L);
       }
-      if (m_pending(m) && st != ST_HARMED) tp = max(tp, cl_T[i]);
+      if (m_pending(m)) tp = max(tp, cla(CL_T)[i]);
     }
     pr = wave_max(pr); l1 = wave_max(l1); l2 = wave_max(l2); l3 = wave_max(l3); l4 = wave_max(l4);
-    ca = wave_max(ca); cs = wave_max(cs); tp = wave_max(tp);
-    chain_update(c, n[c], hold[c], pr);
-    lv[4 * c + 0] = l1; lv[4 * c + 1] = l2; lv[4 * c + 2] = l3; lv[4 * c + 3] = l4;
-    covA[c] = ca; covS[c] = cs; tpend[c] = tp;
+    ca = wave_max(ca); cso = wave_max(cso); tp = wave_max(tp);
+    const uint4 g0 = cg(c, 0);
+    chain_update(c, g0, g0.x, g0.y, pr);
+    cgs(c, 2, make_uint4(l1, l2, l3, l4));
+    cs(c, CF_COVA, ca); cs(c, CF_COVS, cso); cs(c, CF_TPEND, tp);
     refresh(c);
   }
 
   // Recompute every chain whose mark has bit `bit`, and clear the marks.
   __device__ __forceinline__ void recompute_marked(u32 bit) {
     for (u32 base = 0; base < (u32)n_chains; base += 64) {
-      u32 c = base + lane;
-      bool mk = c < (u32)n_chains && (mark[c] & bit);
-      u64 b = ballot(mk);
+      const u32 c = base + lane;
+      const bool m = c < (u32)n_chains && (mk[c] & bit);
+      u64 b = ballot(m);
       while (b) {
-        u32 l = (u32)__builtin_ctzll(b);
+        const u32 l = (u32)__builtin_ctzll(b);
         b &= b - 1;
-        u32 cc = base + l;
+        const u32 cc = base + l;
         recompute(cc);
-        mark[cc] &= ~bit;
+        mk[cc] &= ~bit;
       }
     }
   }
@@ -366,8 +461,9 @@ struct Pool {
   __device__ __forceinline__ i32 candidates(i32 hc, u32 h) {
     i32 e = Eall + fblocks;
     if (hc >= 0) {
-      const u32 nn = n[hc], lo = max(hold[hc], prot[hc]);
-      e -= evictable(nn, lo, 0) - evictable(nn, max(lo, h), 0);
+      const uint4 g0 = cg((u32)hc, 0);
+      const u32 lo = max(g0.y, g0.z);
+      e -= evictable(g0.x, lo, 0) - evictable(g0.x, max(lo, h), 0);
     }
     return e;
   }
@@ -375,7 +471,7 @@ struct Pool {
   __device__ __forceinline__ void fifo_pop_front() {
     fhead++;
     if (fhead != ftail) {
-      uint4 e = fifo[fhead % fifo_cap];
+      const uint4 e = ufl4(fifo[fhead % fifo_cap]);
       ft = e.x; flo = e.y; ftop = e.z;
     }
   }
@@ -387,7 +483,7 @@ struct Pool {
       F -= need;
       return r;
     }
-    i32 E = candidates(hc, h);
+    const i32 E = candidates(hc, h);
     r.E = E;
     if ((i64)need > (i64)F + E) {
       r.ok = false;
@@ -397,9 +493,10 @@ struct Pool {
     F = 0;
     for (u32 guard = 0; K > 0; guard++) {
       if (guard > (u32)U + 1) { status |= kFault; break; }
+      // every remaining candidate of the hit chain is a hit (evictions may have reached the hits)
+      const bool hc_empty = hc >= 0 && cf((u32)hc, CF_N) <= h;
       u64 k1 = KEY_INF, k2 = KEY_INF;
       u32 i1 = NIL;
-      const bool hc_empty = hc >= 0 && n[hc] <= h;  // every candidate of the hit chain is a hit
       const u64 krs[4] = {kr0, kr1, kr2, kr3};
 #pragma unroll
       for (u32 q = 0; q < 4; q++) {
@@ -410,25 +507,24 @@ struct Pool {
         else if (k < k2) k2 = k;
       }
       for (u32 c = kRegChains + lane; c < (u32)n_chains; c += 64) {
-        u64 k = topkey[c];
+        u64 k = tk[c];
         if (hc_empty && (i32)c == hc) k = KEY_INF;
         if (k < k1) { k2 = k1; k1 = k; i1 = c; }
         else if (k < k2) k2 = k;
       }
-      u64 m1 = wave_min64(k1);
-      u64 kf = (fhead != ftail) ? make_key(0, ft, ftop - 1) : KEY_INF;
+      const u64 m1 = wave_min64(k1);
+      const u64 kf = (fhead != ftail) ? make_key(0, ft, ftop - 1) : KEY_INF;
       u64 best, second;
       u32 src;
       if (kf < m1) {
         best = kf; second = m1; src = NIL;
       } else {
-        u64 bl = ballot(k1 == m1);
-        u32 l = (u32)__builtin_ctzll(bl);
+        const u64 bl = ballot(k1 == m1);
+        const u32 l = (u32)__builtin_ctzll(bl);
         src = (u32)rdlane((i32)i1, l);
-        u64 mine = (lane == l) ? k2 : k1;
-        u64 m2 = wave_min64(mine);
+        const u64 m2 = wave_min64(lane == l ? k2 : k1);
         best = m1;
-        second = m2 < kf ? m2 : kf;
+        second = min64(m2, kf);
       }
       if (best == KEY_INF) { status |= kFault; break; }
       const bool tie = second != KEY_INF && (second >> 32) == (best >> 32);
@@ -436,7 +532,7 @@ struct Pool {
       if (src == NIL) {
         u32 m_run = ftop - flo;
         if (tie) m_run = ftop - max(flo, p2 + 1);
-        u32 m = min((u32)K, m_run);
+        const u32 m = min((u32)K, m_run);
         if (m == 0 || m > ftop - flo) { status |= kFault; break; }
         ftop -= m;
         fblocks -= (i32)m;
@@ -445,30 +541,29 @@ struct Pool {
         K -= (i32)m;
         if (ftop == flo) fifo_pop_front();
       } else {
-        u32 c = src, nn = n[c], p = nn - 1;
-        u32 lo = max(hold[c], prot[c]);
+        const u32 c = src;
+        const uint4 g0 = cg(c, 0), g1 = cg(c, 1);
+        const u32 nn = g0.x;
+        u32 lo = max(g0.y, g0.z);
         if ((i32)c == hc) lo = max(lo, h);
-        u32 lvl = level_at(c, p);
-        u32 lvb = 0;
-        if (soft_levels())
-          for (u32 v = lvl + 1; v <= 4; v++) lvb = max(lvb, lv[4 * c + v - 1]);
-        const u32 lub = nx[c];  // positions below it were touched later
-        u32 run_lo = max(lo, max(lvb, lub));
+        u32 lvb;
+        level_at(cg(c, 2), nn - 1, lvb);
+        u32 run_lo = max(lo, max(lvb, g1.x));  // positions below nx were touched later
         u32 m_run = nn - run_lo;
         if (tie) m_run = nn - max(run_lo, p2 + 1);
-        u32 m = min((u32)K, m_run);
+        const u32 m = min((u32)K, m_run);
         if (m == 0 || m > nn) { status |= kFault; break; }
-        u32 nw = nn - m;
-        i32 res = max(0, (i32)min(nn, covA[c]) - (i32)nw);
-        i32 strict = max(0, (i32)min(nn, covS[c]) - (i32)nw);
+        const u32 nw = nn - m;
+        const i32 res = max(0, (i32)min(nn, g1.y) - (i32)nw);
+        const i32 strict = max(0, (i32)min(nn, g1.z) - (i32)nw);
         r.victims += (i32)m;
         r.resident += res;
         r.post += res - strict;
         r.unclaimed += (i32)m - res;
-        chain_update(c, nw, hold[c], prot[c]);
+        chain_update(c, g0, nw, g0.y, g0.z);
         refresh(c);
-        if (nw < tpend[c]) {
-          mark[c] |= MK_SWEEP;
+        if (nw < g1.w) {
+          mk[c] |= MK_SWEEP;
           any_sweep = true;
         }
         K -= (i32)m;
@@ -481,50 +576,53 @@ struct Pool {
   __device__ __forceinline__ u32 sweep(u32 t) {
     u32 pf = 0, hm = 0;
     for (u32 i = lane; i < ncl; i += 64) {
-      u32 c = cl_c[i];
-      if (!(mark[c] & MK_SWEEP)) continue;
-      u32 m = cl_meta[i], st = m_state(m);
-      if (!m_pending(m) || st == ST_HARMED) continue;
-      if (n[c] >= cl_T[i]) continue;
+      const u32 c = cla(CL_C)[i];
+      if (!(mk[c] & MK_SWEEP)) continue;
+      u32 m = cla(CL_META)[i];
+      const u32 st = m_state(m);
+      if (!m_pending(m)) continue;
+      if (ch[c * CF_WORDS + CF_N] >= cla(CL_T)[i]) continue;
       m &= ~(1u << 8);
       pf++;
-      cl_pf[i] = t;
+      cla(CL_PF)[i] = t;
       if (st == ST_MATERIALIZED) {
         m = m_with_state(m, ST_HARMED);
         hm++;
-        cl_harm[i] = t;
+        cla(CL_HARM)[i] = t;
       }
-      cl_meta[i] = m;
+      cla(CL_META)[i] = m;
     }
     lists_fence();
     pf = wave_sum(pf);
     hm = wave_sum(hm);
-    tel[20] += pf;
-    tel[19] += hm;
+    tadd(TW_PREDFAIL, pf);
+    tadd(TW_HARM, hm);
     recompute_marked(MK_SWEEP);
     return (pf ? (u32)RKC_FL_PRED_FAIL : 0u) | (hm ? (u32)RKC_FL_HARM : 0u);
   }
 
   // Refusal record of an active event that cannot be served (§3.4; §5.4 refusal record).
-  __device__ __forceinline__ void refusal(i32 need, i32 hc, u32 h, i32 Hc, i32& code, i32& id, i32& a, i32& b,
-                          u32& n16) {
+  __device__ __forceinline__ void refusal(i32 need, i32 hc, u32 h, i32 Hc, i32& code, i32& id,
+                                          i32& a, i32& b, u32& n16) {
     i32 Pr = PR;
-    if (mode == RKC_MODE_HARD && hc >= 0)
-      Pr -= max(0, (i32)min(prot[hc], h) - (i32)hold[hc]);
-    i64 req = (i64)A + Hc + need;
+    if (mode == RKC_MODE_HARD && hc >= 0) {
+      const uint4 g0 = cg((u32)hc, 0);
+      Pr -= max(0, (i32)min(g0.z, h) - (i32)g0.y);
+    }
+    const i64 req = (i64)A + Hc + need;
     if (Pr > 0 && req <= U) {
       code = RKC_OC_REFUSED_CLAIM;
       u32 mn = NIL, cnt = 0;
       for (u32 i = lane; i < ncl; i += 64) {
-        u32 m = cl_meta[i];
+        const u32 m = cla(CL_META)[i];
         if (m_state(m) != ST_MATERIALIZED || m_eff(m) != RKC_PROT_HARD) continue;
-        u32 c = cl_c[i];
-        u32 cov = hold[c];
+        const u32 c = cla(CL_C)[i];
+        u32 cov = ch[c * CF_WORDS + CF_HOLD];
         if ((i32)c == hc) cov = max(cov, h);
-        if (cl_L[i] <= cov) continue;
-        cl_blk[i] += 1;
+        if (cla(CL_L)[i] <= cov) continue;
+        cla(CL_BLK)[i] += 1;
         cnt++;
-        mn = min(mn, cl_id[i]);
+        mn = min(mn, (u32)cla(CL_ID)[i]);
       }
       lists_fence();
       id = (i32)wave_min(mn);
@@ -541,30 +639,32 @@ struct Pool {
   // Claim records: words 0..8 are written exactly once (lane k writes word k), when the claim is
   // final (rejected at birth, released, or live at the end); word 9 (lead_end) is written by the
   // final pass.
-  __device__ __forceinline__ void write_record(u32 slot, i32 id, u32 packed, i32 accept, i32 dem, i32 exst, i32 rel,
-                               i32 pf, i32 harm, i32 blk) {
+  __device__ __forceinline__ void write_record(u32 slot, i32 id, u32 packed, i32 accept, i32 dem,
+                                               i32 exst, i32 rel, i32 pf, i32 harm, i32 blk) {
     if (lane < 9) {
-      i32 v = lane == 0 ? id : lane == 1 ? (i32)packed : lane == 2 ? accept : lane == 3 ? dem
-            : lane == 4 ? exst : lane == 5 ? rel : lane == 6 ? pf : lane == 7 ? harm : blk;
+      const i32 v = lane == 0 ? id : lane == 1 ? (i32)packed : lane == 2 ? accept : lane == 3 ? dem
+                  : lane == 4 ? exst : lane == 5 ? rel : lane == 6 ? pf : lane == 7 ? harm : blk;
       rec[slot].w[lane] = v;
     }
   }
-  __device__ __forceinline__ i32 step_or_none(u32 v) { return v == NIL ? -1 : (i32)v; }
+  __device__ __forceinline__ static i32 step_or_none(u32 v) { return v == NIL ? -1 : (i32)v; }
   __device__ __forceinline__ void write_live_record(u32 i, u32 state, i32 rel) {
-    write_record(cl_slot[i], (i32)cl_id[i], packed_of(m_with_state(cl_meta[i], state)), (i32)cl_id[i],
-                 step_or_none(cl_dem[i]), step_or_none(cl_exst[i]), rel, step_or_none(cl_pf[i]),
-                 step_or_none(cl_harm[i]), (i32)cl_blk[i]);
+    const u32 id = ufl(cla(CL_ID)[i]);
+    write_record(ufl(cla(CL_SLOT)[i]), (i32)id, packed_of(m_with_state(ufl(cla(CL_META)[i]), state)),
+                 (i32)id, step_or_none(lnil(ufl(cla(CL_DEM)[i]))), step_or_none(lnil(ufl(cla(CL_EXST)[i]))),
+                 rel, step_or_none(lnil(ufl(cla(CL_PF)[i]))), step_or_none(lnil(ufl(cla(CL_HARM)[i]))),
+                 (i32)ufl(cla(CL_BLK)[i]));
   }
 
   // Remove entry i of a struct-of-arrays list (narr arrays of capacity cap) by shifting the tail
   // down one place; lanes read their source entries before any lane writes.
-  __device__ __forceinline__ void list_remove(u32* base0, u32 cap, u32 narr, u32 len, u32 i) {
+  __device__ __forceinline__ void list_remove(lword* base0, u32 cap, u32 narr, u32 len, u32 i) {
     for (u32 base = i; base + 1 < len; base += 64) {
       const u32 j = base + lane;
       const bool act = j + 1 < len;
       for (u32 k = 0; k < narr; k++) {
-        u32* a = base0 + k * cap;
-        u32 v = act ? a[j + 1] : 0;
+        lword* a = base0 + k * cap;
+        const u32 v = act ? (u32)a[j + 1] : 0u;
         __builtin_amdgcn_wave_barrier();
         if (act) a[j] = v;
         __builtin_amdgcn_wave_barrier();
@@ -572,20 +672,17 @@ struct Pool {
     }
     lists_fence();
   }
-  __device__ __forceinline__ void claim_remove(u32 i) {
-    list_remove(cl_id, cl_cap, 12, ncl, i);
-    ncl--;
-  }
 
   __device__ __forceinline__ void expire(u32 t, u32& flags, u32& expired) {
     u32 cnt = 0, nx = EXP_NEVER;
     for (u32 i = lane; i < ncl; i += 64) {
-      u32 m = cl_meta[i], st = m_state(m), ex = cl_exp[i];
-      if ((st != ST_MATERIALIZED && st != ST_DEMOTED) || ex == EXP_NEVER) continue;
+      const u32 m = cla(CL_META)[i], st = m_state(m), dur = cla(CL_EXP)[i];
+      if ((st != ST_MATERIALIZED && st != ST_DEMOTED) || dur == 0) continue;
+      const u32 ex = (u32)cla(CL_ID)[i] + dur;
       if (ex <= t) {
-        cl_meta[i] = m_with_state(m, ST_EXPIRED);
-        cl_exst[i] = t;
-        mark[cl_c[i]] |= MK_RECOMP;
+        cla(CL_META)[i] = m_with_state(m, ST_EXPIRED);
+        cla(CL_EXST)[i] = t;
+        mk[cla(CL_C)[i]] |= MK_RECOMP;
         cnt++;
       } else {
         nx = min(nx, ex);
@@ -598,14 +695,18 @@ struct Pool {
       __builtin_amdgcn_wave_barrier();
       recompute_marked(MK_RECOMP);
       flags |= RKC_FL_EXPIRED;
-      tel[21] += cnt;
+      tadd(TW_EXPIRED, cnt);
     }
     expired = cnt;
   }
 
+  __device__ __forceinline__ void count_victims(const AllocRes& r, u32 hits) {
+    tv += lane == TW_VICTIMS ? (u32)r.victims : lane == TW_RESIDENT ? (u32)r.resident
+        : lane == TW_POST ? (u32)r.post : lane == TW_HITS ? hits : 0u;
+  }
+
   // One event.  Returns the outcome words.
-  __device__ __forceinline__ int4 step(u32 t, i32 w0, i32 w1, i32 w2, i32 w3) {
-    const u32 uw0 = (u32)w0;
+  __device__ __forceinline__ int4 step(u32 t, u32 uw0, i32 w1, i32 w2, i32 w3) {
     const u32 type = uw0 & 15u, hardq = (uw0 >> 4) & 1u, prio = (uw0 >> 5) & 3u, dur = uw0 >> 16;
     u32 flags = 0, expired = 0, n16 = NIL;
     i32 code = RKC_OC_NOOP, id = -1, a = 0, b = 0;
@@ -627,8 +728,9 @@ struct Pool {
         invalid = true;
         status |= RKC_PS_SLOT_TABLE;
       } else {
-        u32 s = nslot++;
-        bool bad = w1 < 1 || w1 > RKC_MAX_FIELD_BLOCKS || w2 < 0 || w2 >= n_chains || w3 < 0 || w3 > w1;
+        const u32 s = nslot++;
+        const bool bad = w1 < 1 || w1 > RKC_MAX_FIELD_BLOCKS || w2 < 0 || w2 >= n_chains || w3 < 0 ||
+                         w3 > w1;
         if (bad) invalid = true;
         else if (ncl >= (u32)max_claims) { invalid = true; status |= RKC_PS_CLAIM_TABLE; }
         // (chain, L) of a valid claim for its final lead_end; invalid claims report 0
@@ -644,10 +746,11 @@ struct Pool {
     } else if (type == RKC_EV_PREFILL) {
       const i32 S = w1, P = w3;
       const i32 hc = P > 0 ? w2 : -1;
-      const u32 h = hc >= 0 ? min((u32)P, n[hc]) : 0u;
+      uint4 g0 = hc >= 0 ? cg((u32)hc, 0) : make_uint4(0, 0, 0, 0);
+      const u32 h = hc >= 0 ? min((u32)P, g0.x) : 0u;
       const i32 need = S - (i32)h;
-      const i32 Hc = hc >= 0 ? max(0, (i32)h - (i32)hold[hc]) : 0;
-      AllocRes r = alloc(need, hc, h, any_sweep);
+      const i32 Hc = hc >= 0 ? max(0, (i32)h - (i32)g0.y) : 0;
+      const AllocRes r = alloc(need, hc, h, any_sweep);
       if (!r.ok) {
         refusal(need, hc, h, Hc, code, id, a, b, n16);
       } else {
@@ -655,19 +758,21 @@ struct Pool {
         u32 R = 0;
         if (hc >= 0) {
           const u32 c = (u32)hc;
+          g0 = cg(c, 0);  // victims may have shortened this chain above the hits
           R = mode == RKC_MODE_NOADMIT ? h : (u32)P;
-          const u32 nn = (mode != RKC_MODE_NOADMIT && (u32)P > n[c]) ? (u32)P : n[c];
-          chain_update(c, nn, max(hold[c], R), prot[c]);
+          const u32 nn = (mode != RKC_MODE_NOADMIT && (u32)P > g0.x) ? (u32)P : g0.x;
+          chain_update(c, g0, nn, max(g0.y, R), g0.z);
           touch(c, R, t);
           refresh(c);
         }
         const u32 k = nreq++;
-        rq_id[k] = t; rq_c[k] = hc >= 0 ? (u32)hc : NIL; rq_R[k] = R; rq_len[k] = (u32)S;
+        rqa(RQ_ID)[k] = t; rqa(RQ_C)[k] = hc >= 0 ? (u32)hc : kListNil; rqa(RQ_R)[k] = R;
+        rqa(RQ_LEN)[k] = (u32)S;
         code = r.resident > 0 ? RKC_OC_EVICT_RESIDENT : RKC_OC_ADMIT;
         id = (i32)t; a = r.resident; b = (i32)h;
         if (r.post) flags |= RKC_FL_POST_RELEASE_LOSS;
         if (r.unclaimed) flags |= RKC_FL_EVICT_UNCLAIMED;
-        tel[10] += r.victims; tel[11] += r.resident; tel[12] += r.post; tel[14] += h;
+        count_victims(r, h);
       }
     } else if (type == RKC_EV_EXTEND) {
       if (nreq == 0) {
@@ -675,17 +780,17 @@ struct Pool {
       } else {
         const u32 i = (u32)w2 % nreq;
         const i32 need = w1;
-        AllocRes r = alloc(need, -1, 0, any_sweep);
+        const AllocRes r = alloc(need, -1, 0, any_sweep);
         if (!r.ok) {
           refusal(need, -1, 0, 0, code, id, a, b, n16);
         } else {
           A += need;
-          rq_len[i] += (u32)need;
+          rqa(RQ_LEN)[i] = ufl(rqa(RQ_LEN)[i]) + (u32)need;
           code = r.resident > 0 ? RKC_OC_EVICT_RESIDENT : RKC_OC_ADMIT;
-          id = (i32)rq_id[i]; a = r.resident; b = A;
+          id = (i32)ufl(rqa(RQ_ID)[i]); a = r.resident; b = A;
           if (r.post) flags |= RKC_FL_POST_RELEASE_LOSS;
           if (r.unclaimed) flags |= RKC_FL_EVICT_UNCLAIMED;
-          tel[10] += r.victims; tel[11] += r.resident; tel[12] += r.post;
+          count_victims(r, 0);
         }
       }
     } else if (type == RKC_EV_CLAIM) {
@@ -693,17 +798,20 @@ struct Pool {
       const u32 c = (u32)w2, s = nslot - 1;
       const u32 eff = mode == RKC_MODE_HARD ? (hardq ? RKC_PROT_HARD : RKC_PROT_SOFT)
                     : mode == RKC_MODE_SOFT ? RKC_PROT_SOFT : RKC_PROT_NONE;
-      const u32 h = min((u32)L, n[c]);
+      const u32 h = min((u32)L, cf(c, CF_N));
       const i32 need = L - (i32)h;
-      AllocRes r = alloc(need, (i32)c, h, any_sweep);
+      const AllocRes r = alloc(need, (i32)c, h, any_sweep);
       u32 dec;
       if (!r.ok) {
         dec = (mode == RKC_MODE_LRU || mode == RKC_MODE_NOADMIT) ? DEC_SHADOW : DEC_REJECTED;
-        u32 m = ST_REJECTED | (eff << 3) | (hardq << 5) | (prio << 6) | (dec << 9);
+        const u32 m = ST_REJECTED | (eff << 3) | (hardq << 5) | (prio << 6) | (dec << 9);
         write_record(s, (i32)t, packed_of(m), -1, -1, -1, -1, -1, -1, 0);
         code = RKC_OC_MATFAIL; id = (i32)t; a = need; b = F + r.E;
       } else {
-        if ((u32)L > n[c]) chain_update(c, (u32)L, hold[c], prot[c]);
+        const uint4 g0 = cg(c, 0);
+        // a materialized hard claim in a hard-protection pool protects [0, L)
+        const u32 pr = (mode == RKC_MODE_HARD && hardq) ? max(g0.z, (u32)L) : g0.z;
+        chain_update(c, g0, max(g0.x, (u32)L), g0.y, pr);
         touch(c, (u32)L, t);
         u32 st;
         if (mode == RKC_MODE_LRU || mode == RKC_MODE_NOADMIT) {
@@ -715,50 +823,52 @@ struct Pool {
         }
         const u32 m = st | (eff << 3) | (hardq << 5) | (prio << 6) | (1u << 8) | (dec << 9);
         const u32 k = ncl++;
-        const u32 ex = (dur > 0 && st == ST_MATERIALIZED) ? t + dur : EXP_NEVER;
-        cl_id[k] = t; cl_c[k] = c; cl_L[k] = (u32)L; cl_T[k] = (u32)T; cl_meta[k] = m;
-        cl_exp[k] = ex; cl_slot[k] = s; cl_blk[k] = 0;
-        cl_dem[k] = NIL; cl_exst[k] = NIL; cl_pf[k] = NIL; cl_harm[k] = NIL;
+        // only a materialized claim with a duration expires (shadow claims never do)
+        const u32 dur_eff = st == ST_MATERIALIZED ? dur : 0u;
+        const u32 ex = dur_eff > 0 ? t + dur_eff : EXP_NEVER;
+        cla(CL_ID)[k] = t; cla(CL_C)[k] = c; cla(CL_L)[k] = (u32)L; cla(CL_T)[k] = (u32)T;
+        cla(CL_META)[k] = m; cla(CL_EXP)[k] = dur_eff; cla(CL_SLOT)[k] = s; cla(CL_BLK)[k] = 0;
+        cla(CL_DEM)[k] = kListNil; cla(CL_EXST)[k] = kListNil; cla(CL_PF)[k] = kListNil;
+        cla(CL_HARM)[k] = kListNil;
         // a new live claim only raises the chain's maxima
-        covA[c] = max(covA[c], (u32)L);
-        covS[c] = max(covS[c], (u32)L);
-        tpend[c] = max(tpend[c], (u32)T);
-        if (mode == RKC_MODE_HARD && st == ST_MATERIALIZED && eff == RKC_PROT_HARD)
-          chain_update(c, n[c], hold[c], max(prot[c], (u32)L));
+        const uint4 g1 = cg(c, 1);
+        cgs(c, 1, make_uint4(g1.x, max(g1.y, (u32)L), max(g1.z, (u32)L), max(g1.w, (u32)T)));
         if (soft_levels() && st == ST_MATERIALIZED && eff == RKC_PROT_SOFT)
-          lv[4 * c + prio] = max(lv[4 * c + prio], (u32)L);
+          cs(c, CF_LV + prio, max(cf(c, CF_LV + prio), (u32)L));
         refresh(c);
         next_exp = min(next_exp, ex);
         code = r.resident > 0 ? RKC_OC_EVICT_RESIDENT : RKC_OC_ADMIT;
         id = (i32)t; a = r.resident; b = need;
         if (r.post) flags |= RKC_FL_POST_RELEASE_LOSS;
         if (r.unclaimed) flags |= RKC_FL_EVICT_UNCLAIMED;
-        tel[10] += r.victims; tel[11] += r.resident; tel[12] += r.post;
+        count_victims(r, 0);
       }
-      tel[dec == DEC_ACCEPTED ? 15 : dec == DEC_APPROX ? 16 : dec == DEC_SHADOW ? 17 : 18] += 1;
+      tadd(TW_ACCEPTED + dec - DEC_ACCEPTED, 1);
     } else if (type == RKC_EV_FINISH) {
       if (nreq == 0) {
         code = RKC_OC_NOOP;
       } else {
         const u32 i = (u32)w1 % nreq;
-        const u32 rid = rq_id[i], c = rq_c[i], R = rq_R[i], len = rq_len[i];
-        list_remove(rq_id, rq_cap, 4, nreq, i);
+        const u32 rid = ufl(rqa(RQ_ID)[i]), c = lnil(ufl(rqa(RQ_C)[i])), R = ufl(rqa(RQ_R)[i]);
+        const u32 len = ufl(rqa(RQ_LEN)[i]);
+        list_remove(rq, rq_cap, RQ_ARRAYS, nreq, i);
         nreq--;
-        i32 turned = 0, dropped = 0;
+        i32 turned = 0;
         if (c != NIL) {
           u32 hn = 0;
           for (u32 j = lane; j < nreq; j += 64)
-            if (rq_c[j] == c) hn = max(hn, rq_R[j]);
+            if ((u32)rqa(RQ_C)[j] == c) hn = max(hn, (u32)rqa(RQ_R)[j]);
           hn = wave_max(hn);
           turned += max(0, (i32)R - (i32)hn);
-          chain_update(c, n[c], hn, prot[c]);
+          const uint4 g0 = cg(c, 0);
+          chain_update(c, g0, g0.x, hn, g0.z);
           touch(c, R, t);
           refresh(c);
         }
         // write no-admit drops the request's own blocks; otherwise they become a private run
         const i32 own = (i32)(len - R);
         const bool drop = mode == RKC_MODE_NOADMIT;
-        dropped = drop ? own : 0;
+        const i32 dropped = drop ? own : 0;
         turned += drop ? 0 : own;
         F += dropped;
         fblocks += drop ? 0 : own;
@@ -770,28 +880,29 @@ struct Pool {
         A -= turned + dropped;
         code = RKC_OC_FINISHED; id = (i32)rid; a = turned; b = dropped;
         if (dropped) flags |= RKC_FL_NOADMIT_DROP;
-        tel[13] += dropped;
+        tadd(TW_DROPPED, (u32)dropped);
       }
     } else if (type == RKC_EV_RELEASE) {
       if (ncl == 0) {
         code = RKC_OC_NOOP;
       } else {
         const u32 i = (u32)w1 % ncl;
-        const u32 qid = cl_id[i], c = cl_c[i], L = cl_L[i], T = cl_T[i];
+        const u32 qid = ufl(cla(CL_ID)[i]), c = ufl(cla(CL_C)[i]), L = ufl(cla(CL_L)[i]);
+        const u32 T = ufl(cla(CL_T)[i]);
         write_live_record(i, ST_RELEASED, (i32)t);
         __builtin_amdgcn_wave_barrier();
-        claim_remove(i);
+        list_remove(cl, cl_cap, CL_ARRAYS, ncl, i);
+        ncl--;
         recompute(c);
-        code = RKC_OC_RELEASED; id = (i32)qid; a = (i32)min(n[c], L); b = (i32)T;
-        tel[23] += 1;
+        code = RKC_OC_RELEASED; id = (i32)qid; a = (i32)min(cf(c, CF_N), L); b = (i32)T;
+        tadd(TW_RELEASED, 1);
       }
     } else if (type == RKC_EV_DEMOTE) {
       u32 cnt = 0;
-      const bool ok_mode = soft_levels();
-      if (ok_mode)
+      if (soft_levels())
         for (u32 base = 0; base < ncl; base += 64) {
-          u32 j = base + lane;
-          bool cand = j < ncl && m_state(cl_meta[j]) == ST_MATERIALIZED && m_hard(cl_meta[j]);
+          const u32 j = base + lane;
+          const bool cand = j < ncl && m_state(cla(CL_META)[j]) == ST_MATERIALIZED && m_hard(cla(CL_META)[j]);
           cnt += (u32)__builtin_popcountll(ballot(cand));
         }
       if (cnt == 0) {
@@ -799,10 +910,10 @@ struct Pool {
       } else {
         u32 k = (u32)w1 % cnt, pick = NIL;
         for (u32 base = 0; base < ncl && pick == NIL; base += 64) {
-          u32 j = base + lane;
-          bool cand = j < ncl && m_state(cl_meta[j]) == ST_MATERIALIZED && m_hard(cl_meta[j]);
-          u64 bl = ballot(cand);
-          u32 pc = (u32)__builtin_popcountll(bl);
+          const u32 j = base + lane;
+          const bool cand = j < ncl && m_state(cla(CL_META)[j]) == ST_MATERIALIZED && m_hard(cla(CL_META)[j]);
+          const u64 bl = ballot(cand);
+          const u32 pc = (u32)__builtin_popcountll(bl);
           if (k < pc) {
             u64 x = bl;
             for (u32 q = 0; q < k; q++) x &= x - 1;
@@ -811,13 +922,14 @@ struct Pool {
             k -= pc;
           }
         }
-        const u32 i = pick, c = cl_c[i];
-        cl_meta[i] = m_with_state(cl_meta[i], ST_DEMOTED);
-        cl_dem[i] = t;
+        const u32 i = pick, c = ufl(cla(CL_C)[i]);
+        cla(CL_META)[i] = m_with_state(ufl(cla(CL_META)[i]), ST_DEMOTED);
+        cla(CL_DEM)[i] = t;
         __builtin_amdgcn_wave_barrier();
         recompute(c);
-        code = RKC_OC_DEMOTED; id = (i32)cl_id[i]; a = (i32)min(n[c], cl_L[i]); b = (i32)cl_T[i];
-        tel[22] += 1;
+        code = RKC_OC_DEMOTED; id = (i32)ufl(cla(CL_ID)[i]);
+        a = (i32)min(cf(c, CF_N), ufl(cla(CL_L)[i])); b = (i32)ufl(cla(CL_T)[i]);
+        tadd(TW_DEMOTED, 1);
       }
     } else {
       code = RKC_OC_NOOP;
@@ -829,29 +941,29 @@ struct Pool {
     }
     if (code == RKC_OC_NOOP || code == RKC_OC_INVALID) { id = -1; a = 0; b = 0; }
     if (n16 == NIL) n16 = min(expired, 65535u);
-    tel[code] += 1;
+    tadd((u32)code, 1);
     peak = max(peak, A);
     return make_int4((i32)((u32)code | (flags << 8) | (n16 << 16)), id, a, b);
   }
 };
 
-template <bool kGL>
+template <typename W, bool kGL>
 __global__ __launch_bounds__(64) void rkc_replay_wave(Args g) {
-  extern __shared__ __align__(16) unsigned char lds[];
+  extern __shared__ __align__(16) unsigned char lds_raw[];
   const u32 pool = blockIdx.x;
   if ((i32)pool >= g.n_pools) return;
   const Layout& L = g.L;
-  Pool<kGL> P;
+  Pool<W, kGL> P;
   P.lane = lane_id();
   const rkc_pool_desc d = g.pools[pool];
   P.U = d.usable_blocks; P.mode = d.mode; P.n_events = d.n_events; P.n_chains = d.n_chains;
   P.max_claims = d.max_live_claims; P.max_reqs = d.max_live_requests; P.n_slots = d.n_claim_slots;
-  P.ev_off = d.event_offset; P.slot_off = d.claim_slot_offset;
+  const i64 ev_off = d.event_offset, slot_off = d.claim_slot_offset;
   rkc_pool_telemetry* ptel = g.pool_tel + pool;
 
   // Descriptor checks against the batch limits the launch was sized for.
-  const bool ev_ok = P.n_events >= 0 && P.ev_off >= 0 && P.ev_off + P.n_events <= g.n_events_total;
-  const bool sl_ok = P.n_slots >= 0 && P.slot_off >= 0 && P.slot_off + P.n_slots <= g.n_slots_total;
+  const bool ev_ok = P.n_events >= 0 && ev_off >= 0 && ev_off + P.n_events <= g.n_events_total;
+  const bool sl_ok = P.n_slots >= 0 && slot_off >= 0 && slot_off + P.n_slots <= g.n_slots_total;
   const bool ok = ev_ok && sl_ok && P.U >= 1 && P.U <= g.max_usable && P.U <= RKC_MAX_USABLE_BLOCKS &&
                   P.mode >= 0 && P.mode <= 3 && P.n_events <= g.max_events && P.n_chains >= 0 &&
                   P.n_chains <= g.max_chains && P.max_claims >= 0 && P.max_claims <= g.max_claims &&
@@ -860,50 +972,52 @@ __global__ __launch_bounds__(64) void rkc_replay_wave(Args g) {
   if (!ok) {
     if (ev_ok)
       for (i32 i = (i32)P.lane; i < P.n_events; i += 64)
-        g.outcomes[P.ev_off + i] = rkc_outcome{{RKC_OC_INVALID, -1, 0, 0}};
+        g.outcomes[ev_off + i] = rkc_outcome{{RKC_OC_INVALID, -1, 0, 0}};
     if (sl_ok)
       for (i32 i = (i32)P.lane; i < P.n_slots; i += 64)
-        g.claim_tel[P.slot_off + i] = rkc_claim_telemetry{{-1, 0, -1, -1, -1, -1, -1, -1, 0, 0}};
+        g.claim_tel[slot_off + i] = rkc_claim_telemetry{{-1, 0, -1, -1, -1, -1, -1, -1, 0, 0}};
     if (P.lane < 32)
       ptel->w[P.lane] = P.lane == 31 ? RKC_PS_DESCRIPTOR : (P.lane == RKC_OC_INVALID && ev_ok) ? P.n_events : 0;
     return;
   }
 
-  // LDS carve-up
-  P.n = (u32*)(lds + L.off_n); P.hold = (u32*)(lds + L.off_hold); P.prot = (u32*)(lds + L.off_prot);
-  P.covA = (u32*)(lds + L.off_covA); P.covS = (u32*)(lds + L.off_covS);
-  P.tpend = (u32*)(lds + L.off_tpend); P.lv = (u32*)(lds + L.off_lv);
-  P.stop = (u32*)(lds + L.off_stop); P.sbot = (u32*)(lds + L.off_sbot);
-  P.mark = (u32*)(lds + L.off_mark); P.topkey = (u64*)(lds + L.off_key);
-  P.bt = (u32*)(lds + L.off_bt); P.nx = (u32*)(lds + L.off_nx);
-  P.tel = (u32*)(lds + L.off_tel);
+  // memory carve-up
+  typedef typename Pool<W, kGL>::lword lword;
+  typedef typename Pool<W, kGL>::lds_w lds_w;
+  typedef typename Pool<W, kGL>::lds_w4 lds_w4;
+  lds_u32* lds = (lds_u32*)lds_raw;
+  P.ch = (lds_w*)(lds + L.off_chain / 4);
+  P.mk = lds + L.off_mark / 4;
+  P.tk = (lds_u64*)(lds + L.off_key / 4);
   unsigned char* scr = g.scratch + (u64)pool * L.scr_pool_bytes;
-  u32* rq = kGL ? (u32*)(scr + L.scr_off_rq) : (u32*)(lds + L.off_rq);
+  if (kGL) {
+    P.rq = (lword*)(scr + L.scr_off_rq);
+    P.cl = (lword*)(scr + L.scr_off_cl);
+  } else {
+    P.rq = (lword*)(lds + L.off_rq / 4);
+    P.cl = (lword*)(lds + L.off_cl / 4);
+  }
   P.rq_cap = L.reqs;
-  P.rq_id = rq; P.rq_c = rq + L.reqs; P.rq_R = rq + 2 * L.reqs; P.rq_len = rq + 3 * L.reqs;
-  u32* cl = kGL ? (u32*)(scr + L.scr_off_cl) : (u32*)(lds + L.off_cl);
   P.cl_cap = L.claims;
-  P.cl_id = cl; P.cl_c = cl + L.claims; P.cl_L = cl + 2 * L.claims; P.cl_T = cl + 3 * L.claims;
-  P.cl_meta = cl + 4 * L.claims; P.cl_exp = cl + 5 * L.claims; P.cl_slot = cl + 6 * L.claims;
-  P.cl_blk = cl + 7 * L.claims; P.cl_dem = cl + 8 * L.claims; P.cl_exst = cl + 9 * L.claims;
-  P.cl_pf = cl + 10 * L.claims; P.cl_harm = cl + 11 * L.claims;
-  P.node_cap = L.node_cap;
-  P.node_lds = (lds_uint4*)(lds + L.off_node);
-  P.nl = L.nodes_lds;
+  P.node_lds = (lds_w4*)(lds + L.off_node / 4);
   P.node_glb = (glb_uint4*)(scr + L.scr_off_node);
+  P.nl = L.nodes_lds;
+  P.node_cap = L.node_cap;
   P.fifo = (uint4*)(scr + L.scr_off_fifo);
   P.fifo_cap = L.fifo_cap;
   P.slot_cl = (uint2*)(scr + L.scr_off_slot);
-  P.rec = g.claim_tel + P.slot_off;
+  P.rec = g.claim_tel + slot_off;
 
   for (i32 c = (i32)P.lane; c < P.n_chains; c += 64) {
-    P.n[c] = 0; P.hold[c] = 0; P.prot[c] = 0; P.covA[c] = 0; P.covS[c] = 0; P.tpend[c] = 0;
-    P.lv[4 * c] = 0; P.lv[4 * c + 1] = 0; P.lv[4 * c + 2] = 0; P.lv[4 * c + 3] = 0;
-    P.stop[c] = NIL; P.sbot[c] = NIL; P.mark[c] = 0; P.bt[c] = 0; P.nx[c] = 0;
-    if ((u32)c >= kRegChains) P.topkey[c] = KEY_INF;
+    P.cgs((u32)c, 0, make_uint4(0, 0, 0, 0));
+    P.cgs((u32)c, 1, make_uint4(0, 0, 0, 0));
+    P.cgs((u32)c, 2, make_uint4(0, 0, 0, 0));
+    P.cgs((u32)c, 3, make_uint4(NIL, NIL, 0, 0));
+    P.mk[c] = 0;
+    if ((u32)c >= kRegChains) P.tk[c] = KEY_INF;
   }
   P.kr0 = P.kr1 = P.kr2 = P.kr3 = KEY_INF;
-  if (P.lane < 32) P.tel[P.lane] = 0;
+  P.tv = 0;
   P.F = P.U; P.A = 0; P.PR = 0; P.peak = 0; P.Eall = 0;
   P.nreq = 0; P.ncl = 0; P.nslot = 0; P.next_exp = EXP_NEVER;
   P.free_head = NIL; P.bump = 0;
@@ -911,8 +1025,8 @@ __global__ __launch_bounds__(64) void rkc_replay_wave(Args g) {
   P.status = 0;
   __syncthreads();
 
-  const rkc_event* ev = g.events + P.ev_off;
-  rkc_outcome* out = g.outcomes + P.ev_off;
+  const rkc_event* ev = g.events + ev_off;
+  rkc_outcome* out = g.outcomes + ev_off;
   for (i32 base = 0; base < P.n_events; base += 64) {
     const i32 cnt = min(64, P.n_events - base);
     int4 e = make_int4(0, 0, 0, 0);
@@ -922,7 +1036,7 @@ __global__ __launch_bounds__(64) void rkc_replay_wave(Args g) {
     }
     int4 mine = make_int4(0, 0, 0, 0);
     for (i32 k = 0; k < cnt; k++) {
-      const int4 o = P.step((u32)(base + k), rdlane(e.x, (u32)k), rdlane(e.y, (u32)k),
+      const int4 o = P.step((u32)(base + k), (u32)rdlane(e.x, (u32)k), rdlane(e.y, (u32)k),
                             rdlane(e.z, (u32)k), rdlane(e.w, (u32)k));
       if ((i32)P.lane == k) mine = o;
     }
@@ -930,14 +1044,14 @@ __global__ __launch_bounds__(64) void rkc_replay_wave(Args g) {
   }
 
   // Final claim records of the claims still live ...
-  for (u32 i = 0; i < P.ncl; i++) P.write_live_record(i, m_state(P.cl_meta[i]), -1);
+  for (u32 i = 0; i < P.ncl; i++) P.write_live_record(i, m_state(ufl((u32)P.cla(CL_META)[i])), -1);
   // ... then lead_end = min(final leading registered length, L) for every used slot, and blank
   // records for unused slots.
   __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
   for (i32 s = (i32)P.lane; s < P.n_slots; s += 64) {
     if (s < (i32)P.nslot) {
       const uint2 cl2 = P.slot_cl[s];
-      P.rec[s].w[9] = cl2.x == NIL ? 0 : (i32)min(P.n[cl2.x], cl2.y);
+      P.rec[s].w[9] = cl2.x == NIL ? 0 : (i32)min((u32)P.ch[cl2.x * CF_WORDS + CF_N], cl2.y);
     } else {
       P.rec[s] = rkc_claim_telemetry{{-1, 0, -1, -1, -1, -1, -1, -1, 0, 0}};
     }
@@ -945,7 +1059,7 @@ __global__ __launch_bounds__(64) void rkc_replay_wave(Args g) {
   __builtin_amdgcn_wave_barrier();
   if (P.lane < 32) {
     const u32 w = P.lane;
-    i32 v = (i32)P.tel[w];
+    i32 v = (i32)P.tv;
     if (w == 24) v = P.peak;
     else if (w == 25) v = P.A;
     else if (w == 26) v = P.U - P.F - P.A;
@@ -961,36 +1075,42 @@ __global__ __launch_bounds__(64) void rkc_replay_wave(Args g) {
 // ---- host side -----------------------------------------------------------------------------
 u64 align_up(u64 v, u64 a) { return (v + a - 1) / a * a; }
 
-constexpr u32 kNodesLds = 64;
+constexpr u32 kNodesLdsNarrow = 128, kNodesLdsWide = 64;
 
 constexpr u64 kLdsBudget = 160 * 1024;
 
-bool make_layout(const rkc_batch* b, Layout* L, bool global_lists) {
+// 16-bit storage holds every stored value of the batch below 0xFFFF
+bool narrow_ok(const rkc_batch* b) {
+  return b->max_usable_blocks <= 32767 && b->max_events <= 65533 && b->max_chains <= 65534 &&
+         b->max_claim_slots <= 65534;
+}
+
+bool make_layout(const rkc_batch* b, Layout* L, bool narrow, bool global_lists) {
   memset(L, 0, sizeof *L);
+  L->narrow = narrow;
   L->global_lists = global_lists;
+  const u64 ws = narrow ? 2 : 4;
   L->chains = (u32)(b->max_chains > 0 ? b->max_chains : 1);
   L->reqs = (u32)(b->max_live_requests > 0 ? b->max_live_requests : 1);
   L->claims = (u32)(b->max_live_claims > 0 ? b->max_live_claims : 1);
   L->node_cap = (u32)b->max_events + 2;
-  L->nodes_lds = L->node_cap < kNodesLds ? L->node_cap : kNodesLds;
+  const u32 nlds = narrow ? kNodesLdsNarrow : kNodesLdsWide;
+  L->nodes_lds = L->node_cap < nlds ? L->node_cap : nlds;
   u64 o = 0;
   auto take = [&](u64 bytes, u64 al) { o = align_up(o, al); u64 r = o; o += bytes; return (u32)r; };
   const u64 C = L->chains;
-  L->off_key = take(8 * (C > kRegChains ? C - 0 : 1), 16);
-  L->off_n = take(4 * C, 4); L->off_hold = take(4 * C, 4); L->off_prot = take(4 * C, 4);
-  L->off_covA = take(4 * C, 4); L->off_covS = take(4 * C, 4); L->off_tpend = take(4 * C, 4);
-  L->off_lv = take(16 * C, 16); L->off_stop = take(4 * C, 4); L->off_sbot = take(4 * C, 4);
-  L->off_mark = take(4 * C, 4); L->off_tel = take(128, 16);
-  L->off_bt = take(4 * C, 4); L->off_nx = take(4 * C, 4);
+  L->off_chain = take(ws * CF_WORDS * C, 16);
+  L->off_key = take(8 * (C > kRegChains ? C : 1), 16);
+  L->off_mark = take(4 * C, 16);
   if (!global_lists) {
-    L->off_rq = take(16ull * L->reqs, 16);
-    L->off_cl = take(48ull * L->claims, 16);
+    L->off_rq = take(ws * RQ_ARRAYS * L->reqs, 16);
+    L->off_cl = take(ws * CL_ARRAYS * L->claims, 16);
   }
-  L->off_node = take(16ull * L->nodes_lds, 16);
+  L->off_node = take(4 * ws * L->nodes_lds, 16);
   o = align_up(o, 16);
   if (o > kLdsBudget) return false;
   L->lds_bytes = (u32)o;
-  // scratch per pool: spilled nodes, FIFO ring, slot table
+  // scratch per pool: spilled nodes, FIFO ring, slot table, and the lists when they are global
   L->fifo_cap = (u32)b->max_events + 1;
   u64 s = 0;
   L->scr_off_node = s; s += 16ull * (L->node_cap - L->nodes_lds); s = align_up(s, 256);
@@ -998,16 +1118,18 @@ bool make_layout(const rkc_batch* b, Layout* L, bool global_lists) {
   L->scr_off_slot = s; s += 8ull * (u64)(b->max_claim_slots > 0 ? b->max_claim_slots : 1);
   s = align_up(s, 256);
   if (global_lists) {
-    L->scr_off_rq = s; s += 16ull * L->reqs; s = align_up(s, 256);
-    L->scr_off_cl = s; s += 48ull * L->claims;
+    L->scr_off_rq = s; s += 4ull * RQ_ARRAYS * L->reqs; s = align_up(s, 256);
+    L->scr_off_cl = s; s += 4ull * CL_ARRAYS * L->claims;
   }
   L->scr_pool_bytes = align_up(s, 256);
   return true;
 }
 
-// Lists in LDS when the whole pool state fits, else in global scratch.
+// Narrowest storage that fits: 16-bit words in LDS, else 32-bit words in LDS, else 32-bit words
+// with the lists in global scratch.
 bool choose_layout(const rkc_batch* b, Layout* L) {
-  return make_layout(b, L, false) || make_layout(b, L, true);
+  return (narrow_ok(b) && make_layout(b, L, true, false)) || make_layout(b, L, false, false) ||
+         make_layout(b, L, false, true);
 }
 
 rkc_status check_batch(const rkc_batch* b) {
@@ -1026,6 +1148,16 @@ rkc_status check_batch(const rkc_batch* b) {
       ((uintptr_t)b->d_pool_tel & 15) || ((uintptr_t)b->d_claim_tel & 7) || ((uintptr_t)b->d_scratch & 255))
     return RKC_E_ALIGN;
   return RKC_OK;
+}
+
+template <typename W, bool kGL>
+rkc_status launch(const Args& g, unsigned n_pools, hipStream_t s) {
+  const void* fn = (const void*)rkc_replay_wave<W, kGL>;
+  if (g.L.lds_bytes > 64 * 1024 &&
+      hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)g.L.lds_bytes) != hipSuccess)
+    return RKC_E_HIP;
+  hipLaunchKernelGGL((rkc_replay_wave<W, kGL>), dim3(n_pools), dim3(64), g.L.lds_bytes, s, g);
+  return hipGetLastError() == hipSuccess ? RKC_OK : RKC_E_HIP;
 }
 
 }  // namespace
@@ -1056,19 +1188,9 @@ rkc_status rkc_replay_batch(const rkc_batch* b, void* s) {
   g.n_pools = b->n_pools; g.max_usable = b->max_usable_blocks; g.max_events = b->max_events;
   g.max_chains = b->max_chains; g.max_reqs = b->max_live_requests; g.max_claims = b->max_live_claims;
   g.max_slots = b->max_claim_slots;
-  const void* fn = g.L.global_lists ? (const void*)rkc_replay_wave<true> : (const void*)rkc_replay_wave<false>;
-  if (g.L.lds_bytes > 64 * 1024) {
-    if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)g.L.lds_bytes) != hipSuccess)
-      return RKC_E_HIP;
-  }
-  if (g.L.global_lists)
-    hipLaunchKernelGGL(rkc_replay_wave<true>, dim3((unsigned)b->n_pools), dim3(64), g.L.lds_bytes,
-                       (hipStream_t)s, g);
-  else
-    hipLaunchKernelGGL(rkc_replay_wave<false>, dim3((unsigned)b->n_pools), dim3(64), g.L.lds_bytes,
-                       (hipStream_t)s, g);
-  if (hipGetLastError() != hipSuccess) return RKC_E_HIP;
-  return RKC_OK;
+  if (g.L.narrow) return launch<uint16_t, false>(g, (unsigned)b->n_pools, (hipStream_t)s);
+  if (g.L.global_lists) return launch<u32, true>(g, (unsigned)b->n_pools, (hipStream_t)s);
+  return launch<u32, false>(g, (unsigned)b->n_pools, (hipStream_t)s);
 }
 
 static rkc_status read_desc(const rkc_batch* b, int32_t pool, rkc_pool_desc* d, void* s) {

@@ -215,3 +215,23 @@ def test_descriptor_outside_batch_limits(tg):
     assert (out[:3, 0] & 255 == 0).all()
     assert (out[3:, 0] & 255 == 9).all() and pt[1, 31] == 256 and pt[1, 9] == 3
     assert db.query_telemetry(1, 0)[0] == -7
+
+
+@pytest.mark.parametrize("variant", ["narrow", "wide", "wide_global_lists"])
+def test_storage_layouts_agree(oracle_mod, tg, variant):
+    """The same pools replayed with 16-bit LDS state, 32-bit LDS state and 32-bit state with the
+    lists in global scratch (chosen by the batch's declared limits) match the oracle exactly."""
+    import paper_2605_24259_amd as rkc
+    trace = randtrace.random_batch(41, 600, U_range=(2, 200), n_events=(1, 200), n_chains=7,
+                                   tight_every=9)
+    lim = dict(trace.limits())
+    if variant == "wide":
+        lim["max_usable_blocks"] = 40000          # above the 16-bit bound
+    elif variant == "wide_global_lists":
+        lim["max_usable_blocks"] = 40000
+        lim["max_live_requests"] = 20000          # lists no longer fit in LDS
+        lim["max_live_claims"] = 4096
+    say(f"case layouts/{variant}")
+    gpu = rkc.DeviceBatch(trace.desc, trace.events, trace.n_claim_slots, lim).replay().results()
+    ora = oracle_mod.replay(trace.desc, trace.events, trace.n_claim_slots, threads=ORACLE_THREADS)
+    compare_pools(trace, gpu, ora)
