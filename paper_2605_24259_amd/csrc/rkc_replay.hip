@@ -15,14 +15,18 @@
 //   a touch stack: (x, t) pairs, x strictly decreasing, t increasing; position p was last touched
 //          at the t of the newest pair with x > p; its bottom pair's step (bt) and the extent of
 //          the pair above it (nx) are cached in the record
-// and the eviction key (level, last use, -pos) of each chain's top candidate (in registers for the
-// first 256 chains).  Finished requests' private blocks form runs (finish step, [lo, top)); runs
+// and the eviction key (level, last use) of each chain's top candidate (in registers for the first
+// 256 chains).  Finished requests' private blocks form runs (finish step, [lo, top)); runs
 // finish in step order, so they sit in a FIFO and the front run is always the oldest.
 //
 // Victim selection takes the (need - F) smallest keys (level asc, last use asc, pos desc) over all
 // candidates (§3.1 soft priority; §5.3 ordinary eviction after free blocks; hard-protected blocks
-// excluded).  It merges chain tops: a wave min-reduction finds the chain with the smallest top key
-// and the runner-up key, then whole runs of equal (level, last use) are evicted at once.
+// excluded).  It merges chain tops: a wave min-reduction finds the chain with the smallest top key,
+// then a whole run of equal (level, last use) is evicted at once.  Every event touches at most one
+// chain, so (level, last use) already identifies a chain's top run: no two chains ever share it.
+// The only possible tie is between a chain and the private run of the request that finished at the
+// step that touched it; that run lies above every position of the chain that the finish touched
+// (the request's shared prefix ends where its own blocks begin), so the private run goes first.
 //
 // Everything the pool's logic reads with a uniform address is moved into scalar registers
 // (readfirstlane), so the per-event state machine runs on the scalar unit; lanes are used for scans
@@ -74,7 +78,7 @@ template <typename W, bool kGL> struct ListMem { typedef typename Store<W>::lds_
 template <typename W> struct ListMem<W, true> { typedef glb_u32 word; };
 
 constexpr u32 NIL = 0xFFFFFFFFu;
-constexpr u64 KEY_INF = ~0ull;
+constexpr u32 KEY_INF = 0xFFFFFFFFu;
 constexpr u32 EXP_NEVER = 0xFFFFFFFFu;
 
 // claim states (ResidentClaimState, §3.1) and decisions
@@ -113,9 +117,8 @@ __device__ __forceinline__ u32 packed_of(u32 m) {
   return m_dec(m) | (m_state(m) << 4) | (m_hard(m) << 8) | (m_prio(m) << 9) | (m_eff(m) << 11);
 }
 
-__device__ __forceinline__ u64 make_key(u32 level, u32 lu, u32 pos) {
-  return ((u64)level << 60) | ((u64)(lu & 0x0FFFFFFFu) << 32) | (u64)(0xFFFFFFFFu - pos);
-}
+// eviction key of a run of candidates with one (level, last use); steps are below 2^24
+__device__ __forceinline__ u32 make_key(u32 level, u32 lu) { return (level << 28) | lu; }
 
 // ---- wave primitives ------------------------------------------------------------------------
 __device__ __forceinline__ u32 lane_id() { return __lane_id(); }
@@ -155,21 +158,6 @@ __device__ __forceinline__ u32 wave_max(u32 v) { return wave_reduce<OpMax>(v); }
 __device__ __forceinline__ u32 wave_min(u32 v) { return wave_reduce<OpMin>(v); }
 __device__ __forceinline__ u32 wave_sum(u32 v) { return wave_reduce<OpAdd>(v); }
 
-template <int CTRL>
-__device__ __forceinline__ u64 dpp64(u64 v) {
-  return ((u64)dpp<CTRL>((u32)(v >> 32)) << 32) | dpp<CTRL>((u32)v);
-}
-__device__ __forceinline__ u64 min64(u64 a, u64 b) { return a < b ? a : b; }
-__device__ __forceinline__ u64 rdlane64(u64 v, u32 l) {
-  return ((u64)(u32)rdlane((i32)(u32)(v >> 32), l) << 32) | (u32)rdlane((i32)(u32)v, l);
-}
-__device__ __forceinline__ u64 wave_min64(u64 v) {
-  v = min64(v, dpp64<kDppXor1>(v));
-  v = min64(v, dpp64<kDppXor2>(v));
-  v = min64(v, dpp64<kDppHalfMirror>(v));
-  v = min64(v, dpp64<kDppMirror>(v));
-  return min64(min64(rdlane64(v, 0), rdlane64(v, 16)), min64(rdlane64(v, 32), rdlane64(v, 48)));
-}
 
 // ---- launch geometry (computed on the host) ---------------------------------------------------
 struct Layout {
@@ -224,19 +212,18 @@ struct Pool {
   // memory
   lds_w* ch;          // chain records, CF_WORDS words each
   lds_u32* mk;        // per-chain mark bits
-  lds_u64* tk;        // top keys of chains >= kRegChains
+  lds_u32* tk;        // top keys of chains >= kRegChains
   lword* rq;          // live requests, RQ_ARRAYS arrays of rq_cap
   lword* cl;          // live claims, CL_ARRAYS arrays of cl_cap
   u32 rq_cap, cl_cap;
   lds_w4* node_lds;   // nodes [0, nl)
   glb_uint4* node_glb;  // nodes [nl, node_cap), 32-bit words
   u32 nl, node_cap;
-  uint4* fifo;
-  u32 fifo_cap;
+  uint4* fifo;  // private runs in finish order; one push per event at most, so it never wraps
   uint2* slot_cl;
   rkc_claim_telemetry* rec;
   // registers
-  u64 kr0, kr1, kr2, kr3;  // top key of chain 64 * k + lane, k = 0..3
+  u32 kr0, kr1, kr2, kr3;  // top key of chain 64 * k + lane, k = 0..3
   u32 tv;                  // pool telemetry word `lane` (lanes 0..31)
   // scalar state (wave-uniform)
   i32 F, A, PR, peak;
@@ -321,7 +308,7 @@ struct Pool {
   }
 
   // -- top keys: registers for chains < kRegChains, LDS above --
-  __device__ __forceinline__ void set_key(u32 c, u64 k) {
+  __device__ __forceinline__ void set_key(u32 c, u32 k) {
     if (c < kRegChains) {
       const u32 l = c & 63u, s = c >> 6;
       if (lane == l) {
@@ -363,9 +350,9 @@ struct Pool {
     return lvl;
   }
 
-  // Key of chain c's top candidate.  The stack bottom is the newest pair covering position n-1
+  // Key of chain c's top run.  The stack bottom is the newest pair covering position n-1
   // exactly when the pair above it (extent nx) does not reach n-1; otherwise advance the bottom.
-  __device__ __forceinline__ u64 top_key(u32 c) {
+  __device__ __forceinline__ u32 top_key(u32 c) {
     const uint4 g0 = cg(c, 0);
     const u32 nn = g0.x;
     if (nn <= max(g0.y, g0.z)) return KEY_INF;
@@ -387,7 +374,7 @@ struct Pool {
     }
     u32 lvb;
     const u32 lvl = level_at(cg(c, 2), nn - 1, lvb);
-    return make_key(lvl, t_bot, nn - 1);
+    return make_key(lvl, t_bot);
   }
   __device__ __forceinline__ void refresh(u32 c) { set_key(c, top_key(c)); }
 
@@ -414,8 +401,9 @@ struct Pool {
     cs(c, CF_STOP, nw);
   }
 
-  // Recompute chain c's claim maxima from the live-claim list.
-  __device__ __forceinline__ void recompute(u32 c) {
+  // Recompute chain c's claim maxima from the live-claim list; returns the new hard protection
+  // (the caller applies it through chain_update).
+  __device__ __forceinline__ u32 claim_maxima(u32 c) {
     u32 pr = 0, l1 = 0, l2 = 0, l3 = 0, l4 = 0, ca = 0, cso = 0, tp = 0;
     const bool hardm = mode == RKC_MODE_HARD, softl = soft_levels();
     for (u32 i = lane; i < ncl; i += 64) {
@@ -433,10 +421,14 @@ struct Pool {
     }
     pr = wave_max(pr); l1 = wave_max(l1); l2 = wave_max(l2); l3 = wave_max(l3); l4 = wave_max(l4);
     ca = wave_max(ca); cso = wave_max(cso); tp = wave_max(tp);
-    const uint4 g0 = cg(c, 0);
-    chain_update(c, g0, g0.x, g0.y, pr);
     cgs(c, 2, make_uint4(l1, l2, l3, l4));
     cs(c, CF_COVA, ca); cs(c, CF_COVS, cso); cs(c, CF_TPEND, tp);
+    return pr;
+  }
+  __device__ __forceinline__ void recompute(u32 c) {
+    const u32 pr = claim_maxima(c);
+    const uint4 g0 = cg(c, 0);
+    chain_update(c, g0, g0.x, g0.y, pr);
     refresh(c);
   }
 
@@ -471,7 +463,7 @@ struct Pool {
   __device__ __forceinline__ void fifo_pop_front() {
     fhead++;
     if (fhead != ftail) {
-      const uint4 e = ufl4(fifo[fhead % fifo_cap]);
+      const uint4 e = ufl4(fifo[fhead]);
       ft = e.x; flo = e.y; ftop = e.z;
     }
   }
@@ -495,45 +487,25 @@ struct Pool {
       if (guard > (u32)U + 1) { status |= kFault; break; }
       // every remaining candidate of the hit chain is a hit (evictions may have reached the hits)
       const bool hc_empty = hc >= 0 && cf((u32)hc, CF_N) <= h;
-      u64 k1 = KEY_INF, k2 = KEY_INF;
-      u32 i1 = NIL;
-      const u64 krs[4] = {kr0, kr1, kr2, kr3};
+      u32 k1 = KEY_INF, i1 = NIL;
+      const u32 krs[4] = {kr0, kr1, kr2, kr3};
 #pragma unroll
       for (u32 q = 0; q < 4; q++) {
         const u32 c = 64 * q + lane;
-        u64 k = krs[q];
-        if (hc_empty && (i32)c == hc) k = KEY_INF;
-        if (k < k1) { k2 = k1; k1 = k; i1 = c; }
-        else if (k < k2) k2 = k;
+        const u32 k = (hc_empty && (i32)c == hc) ? KEY_INF : krs[q];
+        if (k < k1) { k1 = k; i1 = c; }
       }
       for (u32 c = kRegChains + lane; c < (u32)n_chains; c += 64) {
-        u64 k = tk[c];
-        if (hc_empty && (i32)c == hc) k = KEY_INF;
-        if (k < k1) { k2 = k1; k1 = k; i1 = c; }
-        else if (k < k2) k2 = k;
+        const u32 k = (hc_empty && (i32)c == hc) ? KEY_INF : (u32)tk[c];
+        if (k < k1) { k1 = k; i1 = c; }
       }
-      const u64 m1 = wave_min64(k1);
-      const u64 kf = (fhead != ftail) ? make_key(0, ft, ftop - 1) : KEY_INF;
-      u64 best, second;
-      u32 src;
-      if (kf < m1) {
-        best = kf; second = m1; src = NIL;
-      } else {
-        const u64 bl = ballot(k1 == m1);
-        const u32 l = (u32)__builtin_ctzll(bl);
-        src = (u32)rdlane((i32)i1, l);
-        const u64 m2 = wave_min64(lane == l ? k2 : k1);
-        best = m1;
-        second = min64(m2, kf);
-      }
-      if (best == KEY_INF) { status |= kFault; break; }
-      const bool tie = second != KEY_INF && (second >> 32) == (best >> 32);
-      const u32 p2 = 0xFFFFFFFFu - (u32)second;
-      if (src == NIL) {
-        u32 m_run = ftop - flo;
-        if (tie) m_run = ftop - max(flo, p2 + 1);
-        const u32 m = min((u32)K, m_run);
-        if (m == 0 || m > ftop - flo) { status |= kFault; break; }
+      const u32 m1 = wave_min(k1);
+      const u32 kf = (fhead != ftail) ? make_key(0, ft) : KEY_INF;
+      if (kf == KEY_INF && m1 == KEY_INF) { status |= kFault; break; }
+      if (kf <= m1) {
+        // the FIFO front run (on a tie it lies above the tied chain's run)
+        const u32 m = min((u32)K, ftop - flo);
+        if (m == 0) { status |= kFault; break; }
         ftop -= m;
         fblocks -= (i32)m;
         r.victims += (i32)m;
@@ -541,17 +513,15 @@ struct Pool {
         K -= (i32)m;
         if (ftop == flo) fifo_pop_front();
       } else {
-        const u32 c = src;
+        const u32 c = (u32)rdlane((i32)i1, (u32)__builtin_ctzll(ballot(k1 == m1)));
         const uint4 g0 = cg(c, 0), g1 = cg(c, 1);
         const u32 nn = g0.x;
         u32 lo = max(g0.y, g0.z);
         if ((i32)c == hc) lo = max(lo, h);
         u32 lvb;
         level_at(cg(c, 2), nn - 1, lvb);
-        u32 run_lo = max(lo, max(lvb, g1.x));  // positions below nx were touched later
-        u32 m_run = nn - run_lo;
-        if (tie) m_run = nn - max(run_lo, p2 + 1);
-        const u32 m = min((u32)K, m_run);
+        const u32 run_lo = max(lo, max(lvb, g1.x));  // positions below nx were touched later
+        const u32 m = min((u32)K, nn - run_lo);
         if (m == 0 || m > nn) { status |= kFault; break; }
         const u32 nw = nn - m;
         const i32 res = max(0, (i32)min(nn, g1.y) - (i32)nw);
@@ -741,66 +711,80 @@ struct Pool {
       invalid = true;
     }
 
+    // The blocks the event needs: one allocation site for prefill, extend and claim.
+    bool do_alloc = false;
+    i32 need = 0, hc = -1, Hc = 0;
+    u32 h = 0, sel = 0;
+    if (!invalid) {
+      if (type == RKC_EV_PREFILL) {
+        hc = w3 > 0 ? w2 : -1;
+        if (hc >= 0) {
+          const uint4 g0 = cg((u32)hc, 0);
+          h = min((u32)w3, g0.x);
+          Hc = max(0, (i32)h - (i32)g0.y);
+        }
+        need = w1 - (i32)h;
+        do_alloc = true;
+      } else if (type == RKC_EV_EXTEND) {
+        if (nreq > 0) {
+          sel = (u32)w2 % nreq;
+          need = w1;
+          do_alloc = true;
+        }
+      } else if (type == RKC_EV_CLAIM) {
+        hc = w2;
+        h = min((u32)w1, cf((u32)w2, CF_N));
+        need = w1 - (i32)h;
+        do_alloc = true;
+      }
+    }
+    AllocRes r = {true, 0, 0, 0, 0, 0};
+    if (do_alloc) r = alloc(need, hc, h, any_sweep);
+
+    // The chain the event touches gets its new (n, hold, prot), its touch of [0, tx) and its new
+    // top key once, after the per-type effects.
+    u32 tc = NIL, tn = 0, th = 0, tpr = 0, tx = 0;
     if (invalid) {
       code = RKC_OC_INVALID;
+    } else if (do_alloc && !r.ok && type != RKC_EV_CLAIM) {
+      refusal(need, hc, h, Hc, code, id, a, b, n16);
     } else if (type == RKC_EV_PREFILL) {
-      const i32 S = w1, P = w3;
-      const i32 hc = P > 0 ? w2 : -1;
-      uint4 g0 = hc >= 0 ? cg((u32)hc, 0) : make_uint4(0, 0, 0, 0);
-      const u32 h = hc >= 0 ? min((u32)P, g0.x) : 0u;
-      const i32 need = S - (i32)h;
-      const i32 Hc = hc >= 0 ? max(0, (i32)h - (i32)g0.y) : 0;
-      const AllocRes r = alloc(need, hc, h, any_sweep);
-      if (!r.ok) {
-        refusal(need, hc, h, Hc, code, id, a, b, n16);
-      } else {
-        A += Hc + need;
-        u32 R = 0;
-        if (hc >= 0) {
-          const u32 c = (u32)hc;
-          g0 = cg(c, 0);  // victims may have shortened this chain above the hits
-          R = mode == RKC_MODE_NOADMIT ? h : (u32)P;
-          const u32 nn = (mode != RKC_MODE_NOADMIT && (u32)P > g0.x) ? (u32)P : g0.x;
-          chain_update(c, g0, nn, max(g0.y, R), g0.z);
-          touch(c, R, t);
-          refresh(c);
-        }
-        const u32 k = nreq++;
-        rqa(RQ_ID)[k] = t; rqa(RQ_C)[k] = hc >= 0 ? (u32)hc : kListNil; rqa(RQ_R)[k] = R;
-        rqa(RQ_LEN)[k] = (u32)S;
-        code = r.resident > 0 ? RKC_OC_EVICT_RESIDENT : RKC_OC_ADMIT;
-        id = (i32)t; a = r.resident; b = (i32)h;
-        if (r.post) flags |= RKC_FL_POST_RELEASE_LOSS;
-        if (r.unclaimed) flags |= RKC_FL_EVICT_UNCLAIMED;
-        count_victims(r, h);
+      A += Hc + need;
+      u32 R = 0;
+      if (hc >= 0) {
+        const uint4 g0 = cg((u32)hc, 0);  // victims may have shortened this chain above the hits
+        R = mode == RKC_MODE_NOADMIT ? h : (u32)w3;
+        tc = (u32)hc;
+        tn = (mode != RKC_MODE_NOADMIT && (u32)w3 > g0.x) ? (u32)w3 : g0.x;
+        th = max(g0.y, R);
+        tpr = g0.z;
+        tx = R;
       }
+      const u32 k = nreq++;
+      rqa(RQ_ID)[k] = t; rqa(RQ_C)[k] = hc >= 0 ? (u32)hc : kListNil; rqa(RQ_R)[k] = R;
+      rqa(RQ_LEN)[k] = (u32)w1;
+      code = r.resident > 0 ? RKC_OC_EVICT_RESIDENT : RKC_OC_ADMIT;
+      id = (i32)t; a = r.resident; b = (i32)h;
+      if (r.post) flags |= RKC_FL_POST_RELEASE_LOSS;
+      if (r.unclaimed) flags |= RKC_FL_EVICT_UNCLAIMED;
+      count_victims(r, h);
     } else if (type == RKC_EV_EXTEND) {
-      if (nreq == 0) {
+      if (!do_alloc) {
         code = RKC_OC_NOOP;
       } else {
-        const u32 i = (u32)w2 % nreq;
-        const i32 need = w1;
-        const AllocRes r = alloc(need, -1, 0, any_sweep);
-        if (!r.ok) {
-          refusal(need, -1, 0, 0, code, id, a, b, n16);
-        } else {
-          A += need;
-          rqa(RQ_LEN)[i] = ufl(rqa(RQ_LEN)[i]) + (u32)need;
-          code = r.resident > 0 ? RKC_OC_EVICT_RESIDENT : RKC_OC_ADMIT;
-          id = (i32)ufl(rqa(RQ_ID)[i]); a = r.resident; b = A;
-          if (r.post) flags |= RKC_FL_POST_RELEASE_LOSS;
-          if (r.unclaimed) flags |= RKC_FL_EVICT_UNCLAIMED;
-          count_victims(r, 0);
-        }
+        A += need;
+        rqa(RQ_LEN)[sel] = ufl(rqa(RQ_LEN)[sel]) + (u32)need;
+        code = r.resident > 0 ? RKC_OC_EVICT_RESIDENT : RKC_OC_ADMIT;
+        id = (i32)ufl(rqa(RQ_ID)[sel]); a = r.resident; b = A;
+        if (r.post) flags |= RKC_FL_POST_RELEASE_LOSS;
+        if (r.unclaimed) flags |= RKC_FL_EVICT_UNCLAIMED;
+        count_victims(r, 0);
       }
     } else if (type == RKC_EV_CLAIM) {
       const i32 L = w1, T = w3;
       const u32 c = (u32)w2, s = nslot - 1;
       const u32 eff = mode == RKC_MODE_HARD ? (hardq ? RKC_PROT_HARD : RKC_PROT_SOFT)
                     : mode == RKC_MODE_SOFT ? RKC_PROT_SOFT : RKC_PROT_NONE;
-      const u32 h = min((u32)L, cf(c, CF_N));
-      const i32 need = L - (i32)h;
-      const AllocRes r = alloc(need, (i32)c, h, any_sweep);
       u32 dec;
       if (!r.ok) {
         dec = (mode == RKC_MODE_LRU || mode == RKC_MODE_NOADMIT) ? DEC_SHADOW : DEC_REJECTED;
@@ -808,11 +792,6 @@ struct Pool {
         write_record(s, (i32)t, packed_of(m), -1, -1, -1, -1, -1, -1, 0);
         code = RKC_OC_MATFAIL; id = (i32)t; a = need; b = F + r.E;
       } else {
-        const uint4 g0 = cg(c, 0);
-        // a materialized hard claim in a hard-protection pool protects [0, L)
-        const u32 pr = (mode == RKC_MODE_HARD && hardq) ? max(g0.z, (u32)L) : g0.z;
-        chain_update(c, g0, max(g0.x, (u32)L), g0.y, pr);
-        touch(c, (u32)L, t);
         u32 st;
         if (mode == RKC_MODE_LRU || mode == RKC_MODE_NOADMIT) {
           dec = DEC_SHADOW; st = ST_OBSERVED; flags |= RKC_FL_SHADOW;
@@ -825,7 +804,6 @@ struct Pool {
         const u32 k = ncl++;
         // only a materialized claim with a duration expires (shadow claims never do)
         const u32 dur_eff = st == ST_MATERIALIZED ? dur : 0u;
-        const u32 ex = dur_eff > 0 ? t + dur_eff : EXP_NEVER;
         cla(CL_ID)[k] = t; cla(CL_C)[k] = c; cla(CL_L)[k] = (u32)L; cla(CL_T)[k] = (u32)T;
         cla(CL_META)[k] = m; cla(CL_EXP)[k] = dur_eff; cla(CL_SLOT)[k] = s; cla(CL_BLK)[k] = 0;
         cla(CL_DEM)[k] = kListNil; cla(CL_EXST)[k] = kListNil; cla(CL_PF)[k] = kListNil;
@@ -835,8 +813,14 @@ struct Pool {
         cgs(c, 1, make_uint4(g1.x, max(g1.y, (u32)L), max(g1.z, (u32)L), max(g1.w, (u32)T)));
         if (soft_levels() && st == ST_MATERIALIZED && eff == RKC_PROT_SOFT)
           cs(c, CF_LV + prio, max(cf(c, CF_LV + prio), (u32)L));
-        refresh(c);
-        next_exp = min(next_exp, ex);
+        if (dur_eff > 0) next_exp = min(next_exp, t + dur_eff);
+        const uint4 g0 = cg(c, 0);
+        tc = c;
+        tn = max(g0.x, (u32)L);
+        th = g0.y;
+        // a materialized hard claim in a hard-protection pool protects [0, L)
+        tpr = (mode == RKC_MODE_HARD && hardq) ? max(g0.z, (u32)L) : g0.z;
+        tx = (u32)L;
         code = r.resident > 0 ? RKC_OC_EVICT_RESIDENT : RKC_OC_ADMIT;
         id = (i32)t; a = r.resident; b = need;
         if (r.post) flags |= RKC_FL_POST_RELEASE_LOSS;
@@ -861,9 +845,7 @@ struct Pool {
           hn = wave_max(hn);
           turned += max(0, (i32)R - (i32)hn);
           const uint4 g0 = cg(c, 0);
-          chain_update(c, g0, g0.x, hn, g0.z);
-          touch(c, R, t);
-          refresh(c);
+          tc = c; tn = g0.x; th = hn; tpr = g0.z; tx = R;
         }
         // write no-admit drops the request's own blocks; otherwise they become a private run
         const i32 own = (i32)(len - R);
@@ -874,7 +856,7 @@ struct Pool {
         fblocks += drop ? 0 : own;
         if (!drop && own > 0) {
           if (fhead == ftail) { ft = t; flo = R; ftop = len; }
-          fifo[ftail % fifo_cap] = make_uint4(t, R, len, 0);
+          fifo[ftail] = make_uint4(t, R, len, 0);
           ftail++;
         }
         A -= turned + dropped;
@@ -882,57 +864,68 @@ struct Pool {
         if (dropped) flags |= RKC_FL_NOADMIT_DROP;
         tadd(TW_DROPPED, (u32)dropped);
       }
-    } else if (type == RKC_EV_RELEASE) {
-      if (ncl == 0) {
-        code = RKC_OC_NOOP;
-      } else {
-        const u32 i = (u32)w1 % ncl;
-        const u32 qid = ufl(cla(CL_ID)[i]), c = ufl(cla(CL_C)[i]), L = ufl(cla(CL_L)[i]);
-        const u32 T = ufl(cla(CL_T)[i]);
-        write_live_record(i, ST_RELEASED, (i32)t);
-        __builtin_amdgcn_wave_barrier();
-        list_remove(cl, cl_cap, CL_ARRAYS, ncl, i);
-        ncl--;
-        recompute(c);
-        code = RKC_OC_RELEASED; id = (i32)qid; a = (i32)min(cf(c, CF_N), L); b = (i32)T;
-        tadd(TW_RELEASED, 1);
-      }
-    } else if (type == RKC_EV_DEMOTE) {
-      u32 cnt = 0;
-      if (soft_levels())
+    } else if (type == RKC_EV_RELEASE || type == RKC_EV_DEMOTE) {
+      // the selected live claim: release removes it, demotion turns hard into soft (§3.1)
+      u32 i = NIL;
+      if (type == RKC_EV_RELEASE) {
+        if (ncl > 0) i = (u32)w1 % ncl;
+      } else if (soft_levels()) {
+        u32 cnt = 0;
         for (u32 base = 0; base < ncl; base += 64) {
           const u32 j = base + lane;
           const bool cand = j < ncl && m_state(cla(CL_META)[j]) == ST_MATERIALIZED && m_hard(cla(CL_META)[j]);
           cnt += (u32)__builtin_popcountll(ballot(cand));
         }
-      if (cnt == 0) {
-        code = RKC_OC_NOOP;
-      } else {
-        u32 k = (u32)w1 % cnt, pick = NIL;
-        for (u32 base = 0; base < ncl && pick == NIL; base += 64) {
-          const u32 j = base + lane;
-          const bool cand = j < ncl && m_state(cla(CL_META)[j]) == ST_MATERIALIZED && m_hard(cla(CL_META)[j]);
-          const u64 bl = ballot(cand);
-          const u32 pc = (u32)__builtin_popcountll(bl);
-          if (k < pc) {
-            u64 x = bl;
-            for (u32 q = 0; q < k; q++) x &= x - 1;
-            pick = base + (u32)__builtin_ctzll(x);
-          } else {
-            k -= pc;
+        if (cnt > 0) {
+          u32 k = (u32)w1 % cnt;
+          for (u32 base = 0; base < ncl && i == NIL; base += 64) {
+            const u32 j = base + lane;
+            const bool cand = j < ncl && m_state(cla(CL_META)[j]) == ST_MATERIALIZED && m_hard(cla(CL_META)[j]);
+            const u64 bl = ballot(cand);
+            const u32 pc = (u32)__builtin_popcountll(bl);
+            if (k < pc) {
+              u64 x = bl;
+              for (u32 q = 0; q < k; q++) x &= x - 1;
+              i = base + (u32)__builtin_ctzll(x);
+            } else {
+              k -= pc;
+            }
           }
         }
-        const u32 i = pick, c = ufl(cla(CL_C)[i]);
-        cla(CL_META)[i] = m_with_state(ufl(cla(CL_META)[i]), ST_DEMOTED);
-        cla(CL_DEM)[i] = t;
-        __builtin_amdgcn_wave_barrier();
-        recompute(c);
-        code = RKC_OC_DEMOTED; id = (i32)ufl(cla(CL_ID)[i]);
-        a = (i32)min(cf(c, CF_N), ufl(cla(CL_L)[i])); b = (i32)ufl(cla(CL_T)[i]);
-        tadd(TW_DEMOTED, 1);
+      }
+      if (i == NIL) {
+        code = RKC_OC_NOOP;
+      } else {
+        const u32 qid = ufl(cla(CL_ID)[i]), c = ufl(cla(CL_C)[i]), L = ufl(cla(CL_L)[i]);
+        const u32 T = ufl(cla(CL_T)[i]);
+        if (type == RKC_EV_RELEASE) {
+          write_live_record(i, ST_RELEASED, (i32)t);
+          __builtin_amdgcn_wave_barrier();
+          list_remove(cl, cl_cap, CL_ARRAYS, ncl, i);
+          ncl--;
+          code = RKC_OC_RELEASED;
+          tadd(TW_RELEASED, 1);
+        } else {
+          cla(CL_META)[i] = m_with_state(ufl(cla(CL_META)[i]), ST_DEMOTED);
+          cla(CL_DEM)[i] = t;
+          __builtin_amdgcn_wave_barrier();
+          code = RKC_OC_DEMOTED;
+          tadd(TW_DEMOTED, 1);
+        }
+        const u32 pr = claim_maxima(c);
+        const uint4 g0 = cg(c, 0);
+        tc = c; tn = g0.x; th = g0.y; tpr = pr; tx = 0;
+        id = (i32)qid; a = (i32)min(g0.x, L); b = (i32)T;
       }
     } else {
       code = RKC_OC_NOOP;
+    }
+
+    if (tc != NIL) {
+      const uint4 g0 = cg(tc, 0);
+      chain_update(tc, g0, tn, th, tpr);
+      if (tx) touch(tc, tx, t);
+      refresh(tc);
     }
 
     if (!invalid && any_sweep) {
@@ -988,7 +981,7 @@ __global__ __launch_bounds__(64) void rkc_replay_wave(Args g) {
   lds_u32* lds = (lds_u32*)lds_raw;
   P.ch = (lds_w*)(lds + L.off_chain / 4);
   P.mk = lds + L.off_mark / 4;
-  P.tk = (lds_u64*)(lds + L.off_key / 4);
+  P.tk = lds + L.off_key / 4;
   unsigned char* scr = g.scratch + (u64)pool * L.scr_pool_bytes;
   if (kGL) {
     P.rq = (lword*)(scr + L.scr_off_rq);
@@ -1004,7 +997,6 @@ __global__ __launch_bounds__(64) void rkc_replay_wave(Args g) {
   P.nl = L.nodes_lds;
   P.node_cap = L.node_cap;
   P.fifo = (uint4*)(scr + L.scr_off_fifo);
-  P.fifo_cap = L.fifo_cap;
   P.slot_cl = (uint2*)(scr + L.scr_off_slot);
   P.rec = g.claim_tel + slot_off;
 
@@ -1100,7 +1092,7 @@ bool make_layout(const rkc_batch* b, Layout* L, bool narrow, bool global_lists) 
   auto take = [&](u64 bytes, u64 al) { o = align_up(o, al); u64 r = o; o += bytes; return (u32)r; };
   const u64 C = L->chains;
   L->off_chain = take(ws * CF_WORDS * C, 16);
-  L->off_key = take(8 * (C > kRegChains ? C : 1), 16);
+  L->off_key = take(4 * (C > kRegChains ? C : 1), 16);
   L->off_mark = take(4 * C, 16);
   if (!global_lists) {
     L->off_rq = take(ws * RQ_ARRAYS * L->reqs, 16);
@@ -1111,7 +1103,7 @@ bool make_layout(const rkc_batch* b, Layout* L, bool narrow, bool global_lists) 
   if (o > kLdsBudget) return false;
   L->lds_bytes = (u32)o;
   // scratch per pool: spilled nodes, FIFO ring, slot table, and the lists when they are global
-  L->fifo_cap = (u32)b->max_events + 1;
+  L->fifo_cap = (u32)b->max_events + 1;  // one entry per event at most
   u64 s = 0;
   L->scr_off_node = s; s += 16ull * (L->node_cap - L->nodes_lds); s = align_up(s, 256);
   L->scr_off_fifo = s; s += 16ull * L->fifo_cap; s = align_up(s, 256);
