@@ -189,7 +189,7 @@ constexpr u32 kFault = 0x80000000u;
 constexpr u32 kRegChains = 256;
 
 struct AllocRes {
-  bool ok;
+  u32 ok;
   i32 E;  // evictable candidates before the event (valid when need > F)
   i32 victims, resident, post, unclaimed;
 };
@@ -469,8 +469,8 @@ struct Pool {
   }
 
   // ALLOC: FREE blocks first, then the (need - F) smallest-key candidates.
-  __device__ __forceinline__ AllocRes alloc(i32 need, i32 hc, u32 h, bool& any_sweep) {
-    AllocRes r = {true, 0, 0, 0, 0, 0};
+  __device__ __forceinline__ AllocRes alloc(i32 need, i32 hc, u32 h, u32& sweep_due) {
+    AllocRes r = {1, 0, 0, 0, 0, 0};
     if (need <= F) {
       F -= need;
       return r;
@@ -478,7 +478,7 @@ struct Pool {
     const i32 E = candidates(hc, h);
     r.E = E;
     if ((i64)need > (i64)F + E) {
-      r.ok = false;
+      r.ok = 0;
       return r;
     }
     i32 K = need - F;
@@ -534,7 +534,7 @@ struct Pool {
         refresh(c);
         if (nw < g1.w) {
           mk[c] |= MK_SWEEP;
-          any_sweep = true;
+          sweep_due = 1;
         }
         K -= (i32)m;
       }
@@ -676,162 +676,169 @@ struct Pool {
   }
 
   // One event.  Returns the outcome words.
+  //
+  // Control flow is kept to two switches over a small integer: uniform conditions held in u32
+  // words (not bools) compile to scalar compares and branches instead of lane-mask selects.
+  enum : u32 { K_NOOP = 0, K_INVALID, K_PREFILL, K_EXTEND, K_CLAIM, K_FINISH, K_RELEASE, K_DEMOTE,
+              K_REFUSED };
   __device__ __forceinline__ int4 step(u32 t, u32 uw0, i32 w1, i32 w2, i32 w3) {
     const u32 type = uw0 & 15u, hardq = (uw0 >> 4) & 1u, prio = (uw0 >> 5) & 3u, dur = uw0 >> 16;
-    u32 flags = 0, expired = 0, n16 = NIL;
+    u32 flags = 0, expired = 0, n16 = NIL, sweep_due = 0;
     i32 code = RKC_OC_NOOP, id = -1, a = 0, b = 0;
-    bool any_sweep = false;
 
     if (t >= next_exp) expire(t, flags, expired);
 
-    // validation (malformed events and table limits)
-    bool invalid = false;
-    if (type == RKC_EV_PREFILL) {
-      if (w1 < 1 || w1 > RKC_MAX_FIELD_BLOCKS || w3 < 0 || w3 > w1 ||
-          (w3 > 0 && (w2 < 0 || w2 >= n_chains)))
-        invalid = true;
-      else if (nreq >= (u32)max_reqs) { invalid = true; status |= RKC_PS_REQUEST_TABLE; }
-    } else if (type == RKC_EV_EXTEND) {
-      invalid = w1 < 1 || w1 > RKC_MAX_FIELD_BLOCKS;
-    } else if (type == RKC_EV_CLAIM) {
-      if (nslot >= (u32)n_slots) {
-        invalid = true;
-        status |= RKC_PS_SLOT_TABLE;
-      } else {
-        const u32 s = nslot++;
-        const bool bad = w1 < 1 || w1 > RKC_MAX_FIELD_BLOCKS || w2 < 0 || w2 >= n_chains || w3 < 0 ||
-                         w3 > w1;
-        if (bad) invalid = true;
-        else if (ncl >= (u32)max_claims) { invalid = true; status |= RKC_PS_CLAIM_TABLE; }
-        // (chain, L) of a valid claim for its final lead_end; invalid claims report 0
-        slot_cl[s] = invalid ? make_uint2(NIL, 0) : make_uint2((u32)w2, (u32)w1);
-        if (invalid) write_record(s, (i32)t, 0, -1, -1, -1, -1, -1, -1, 0);
-      }
-    } else if (type > RKC_EV_NOP) {
-      invalid = true;
-    }
-
-    // The blocks the event needs: one allocation site for prefill, extend and claim.
-    bool do_alloc = false;
+    // Decode: validity (malformed events and table limits) and the allocation request.
+    u32 kind = K_NOOP, sel = 0, h = 0, s = 0;
     i32 need = 0, hc = -1, Hc = 0;
-    u32 h = 0, sel = 0;
-    if (!invalid) {
-      if (type == RKC_EV_PREFILL) {
-        hc = w3 > 0 ? w2 : -1;
-        if (hc >= 0) {
-          const uint4 g0 = cg((u32)hc, 0);
-          h = min((u32)w3, g0.x);
-          Hc = max(0, (i32)h - (i32)g0.y);
+    const u32 fieldbad = (u32)(w1 < 1) | (u32)(w1 > RKC_MAX_FIELD_BLOCKS);
+    const u32 chainbad = (u32)(w2 < 0) | (u32)(w2 >= n_chains);
+    const u32 thrbad = (u32)(w3 < 0) | (u32)(w3 > w1);
+    switch (type) {
+      case RKC_EV_PREFILL:
+        if (fieldbad | thrbad | ((u32)(w3 > 0) & chainbad)) {
+          kind = K_INVALID;
+        } else if (nreq >= (u32)max_reqs) {
+          kind = K_INVALID;
+          status |= RKC_PS_REQUEST_TABLE;
+        } else {
+          kind = K_PREFILL;
+          if (w3 > 0) {
+            hc = w2;
+            const uint4 g0 = cg((u32)hc, 0);
+            h = min((u32)w3, g0.x);
+            Hc = max(0, (i32)h - (i32)g0.y);
+          }
+          need = w1 - (i32)h;
         }
-        need = w1 - (i32)h;
-        do_alloc = true;
-      } else if (type == RKC_EV_EXTEND) {
-        if (nreq > 0) {
+        break;
+      case RKC_EV_EXTEND:
+        if (fieldbad) {
+          kind = K_INVALID;
+        } else if (nreq > 0) {
+          kind = K_EXTEND;
           sel = (u32)w2 % nreq;
           need = w1;
-          do_alloc = true;
         }
-      } else if (type == RKC_EV_CLAIM) {
-        hc = w2;
-        h = min((u32)w1, cf((u32)w2, CF_N));
-        need = w1 - (i32)h;
-        do_alloc = true;
-      }
+        break;
+      case RKC_EV_CLAIM:
+        if (nslot >= (u32)n_slots) {
+          kind = K_INVALID;
+          status |= RKC_PS_SLOT_TABLE;
+        } else {
+          s = nslot++;
+          u32 ok = 0;
+          if (fieldbad | chainbad | thrbad) {
+          } else if (ncl >= (u32)max_claims) {
+            status |= RKC_PS_CLAIM_TABLE;
+          } else {
+            ok = 1;
+          }
+          // (chain, L) of a valid claim for its final lead_end; invalid claims report 0
+          slot_cl[s] = ok ? make_uint2((u32)w2, (u32)w1) : make_uint2(NIL, 0);
+          if (ok) {
+            kind = K_CLAIM;
+            hc = w2;
+            h = min((u32)w1, cf((u32)w2, CF_N));
+            need = w1 - (i32)h;
+          } else {
+            kind = K_INVALID;
+            write_record(s, (i32)t, 0, -1, -1, -1, -1, -1, -1, 0);
+          }
+        }
+        break;
+      case RKC_EV_FINISH: kind = nreq > 0 ? K_FINISH : K_NOOP; break;
+      case RKC_EV_RELEASE: kind = ncl > 0 ? K_RELEASE : K_NOOP; break;
+      case RKC_EV_DEMOTE: kind = K_DEMOTE; break;
+      case RKC_EV_NOP: break;
+      default: kind = K_INVALID; break;
     }
-    AllocRes r = {true, 0, 0, 0, 0, 0};
-    if (do_alloc) r = alloc(need, hc, h, any_sweep);
 
-    // The chain the event touches gets its new (n, hold, prot), its touch of [0, tx) and its new
-    // top key once, after the per-type effects.
-    u32 tc = NIL, tn = 0, th = 0, tpr = 0, tx = 0;
-    if (invalid) {
-      code = RKC_OC_INVALID;
-    } else if (do_alloc && !r.ok && type != RKC_EV_CLAIM) {
+    // One allocation site for prefill, extend and claim.
+    AllocRes r = {1, 0, 0, 0, 0, 0};
+    if (kind == K_PREFILL || kind == K_EXTEND || kind == K_CLAIM) r = alloc(need, hc, h, sweep_due);
+    if (!r.ok && kind != K_CLAIM) {
       refusal(need, hc, h, Hc, code, id, a, b, n16);
-    } else if (type == RKC_EV_PREFILL) {
-      A += Hc + need;
-      u32 R = 0;
-      if (hc >= 0) {
-        const uint4 g0 = cg((u32)hc, 0);  // victims may have shortened this chain above the hits
-        R = mode == RKC_MODE_NOADMIT ? h : (u32)w3;
-        tc = (u32)hc;
-        tn = (mode != RKC_MODE_NOADMIT && (u32)w3 > g0.x) ? (u32)w3 : g0.x;
-        th = max(g0.y, R);
-        tpr = g0.z;
-        tx = R;
+      kind = K_REFUSED;  // no further effect
+    }
+
+    // Effects; the chain the event touches gets its new (n, hold, prot), its touch of [0, tx)
+    // and its new top key once, after the switch.
+    u32 tc = NIL, tn = 0, th = 0, tpr = 0, tx = 0;
+    switch (kind) {
+      case K_INVALID:
+        code = RKC_OC_INVALID;
+        break;
+      case K_PREFILL: {
+        A += Hc + need;
+        u32 R = 0;
+        if (hc >= 0) {
+          const uint4 g0 = cg((u32)hc, 0);  // victims may have shortened this chain above the hits
+          R = mode == RKC_MODE_NOADMIT ? h : (u32)w3;
+          tc = (u32)hc;
+          tn = (mode != RKC_MODE_NOADMIT && (u32)w3 > g0.x) ? (u32)w3 : g0.x;
+          th = max(g0.y, R);
+          tpr = g0.z;
+          tx = R;
+        }
+        const u32 k = nreq++;
+        rqa(RQ_ID)[k] = t; rqa(RQ_C)[k] = hc >= 0 ? (u32)hc : kListNil; rqa(RQ_R)[k] = R;
+        rqa(RQ_LEN)[k] = (u32)w1;
+        id = (i32)t; b = (i32)h;
+        count_victims(r, h);
+        break;
       }
-      const u32 k = nreq++;
-      rqa(RQ_ID)[k] = t; rqa(RQ_C)[k] = hc >= 0 ? (u32)hc : kListNil; rqa(RQ_R)[k] = R;
-      rqa(RQ_LEN)[k] = (u32)w1;
-      code = r.resident > 0 ? RKC_OC_EVICT_RESIDENT : RKC_OC_ADMIT;
-      id = (i32)t; a = r.resident; b = (i32)h;
-      if (r.post) flags |= RKC_FL_POST_RELEASE_LOSS;
-      if (r.unclaimed) flags |= RKC_FL_EVICT_UNCLAIMED;
-      count_victims(r, h);
-    } else if (type == RKC_EV_EXTEND) {
-      if (!do_alloc) {
-        code = RKC_OC_NOOP;
-      } else {
+      case K_EXTEND:
         A += need;
         rqa(RQ_LEN)[sel] = ufl(rqa(RQ_LEN)[sel]) + (u32)need;
-        code = r.resident > 0 ? RKC_OC_EVICT_RESIDENT : RKC_OC_ADMIT;
-        id = (i32)ufl(rqa(RQ_ID)[sel]); a = r.resident; b = A;
-        if (r.post) flags |= RKC_FL_POST_RELEASE_LOSS;
-        if (r.unclaimed) flags |= RKC_FL_EVICT_UNCLAIMED;
+        id = (i32)ufl(rqa(RQ_ID)[sel]); b = A;
         count_victims(r, 0);
-      }
-    } else if (type == RKC_EV_CLAIM) {
-      const i32 L = w1, T = w3;
-      const u32 c = (u32)w2, s = nslot - 1;
-      const u32 eff = mode == RKC_MODE_HARD ? (hardq ? RKC_PROT_HARD : RKC_PROT_SOFT)
-                    : mode == RKC_MODE_SOFT ? RKC_PROT_SOFT : RKC_PROT_NONE;
-      u32 dec;
-      if (!r.ok) {
-        dec = (mode == RKC_MODE_LRU || mode == RKC_MODE_NOADMIT) ? DEC_SHADOW : DEC_REJECTED;
-        const u32 m = ST_REJECTED | (eff << 3) | (hardq << 5) | (prio << 6) | (dec << 9);
-        write_record(s, (i32)t, packed_of(m), -1, -1, -1, -1, -1, -1, 0);
-        code = RKC_OC_MATFAIL; id = (i32)t; a = need; b = F + r.E;
-      } else {
-        u32 st;
-        if (mode == RKC_MODE_LRU || mode == RKC_MODE_NOADMIT) {
-          dec = DEC_SHADOW; st = ST_OBSERVED; flags |= RKC_FL_SHADOW;
-        } else if (mode == RKC_MODE_SOFT && hardq) {
-          dec = DEC_APPROX; st = ST_MATERIALIZED; flags |= RKC_FL_LOWERED;
+        break;
+      case K_CLAIM: {
+        const i32 L = w1, T = w3;
+        const u32 c = (u32)w2;
+        const u32 eff = mode == RKC_MODE_HARD ? (hardq ? RKC_PROT_HARD : RKC_PROT_SOFT)
+                      : mode == RKC_MODE_SOFT ? RKC_PROT_SOFT : RKC_PROT_NONE;
+        const u32 shadow = (u32)(mode == RKC_MODE_LRU) | (u32)(mode == RKC_MODE_NOADMIT);
+        u32 dec;
+        if (!r.ok) {
+          dec = shadow ? DEC_SHADOW : DEC_REJECTED;
+          const u32 m = ST_REJECTED | (eff << 3) | (hardq << 5) | (prio << 6) | (dec << 9);
+          write_record(s, (i32)t, packed_of(m), -1, -1, -1, -1, -1, -1, 0);
+          code = RKC_OC_MATFAIL; id = (i32)t; a = need; b = F + r.E;
         } else {
-          dec = DEC_ACCEPTED; st = ST_MATERIALIZED;
+          const u32 lowered = (u32)(mode == RKC_MODE_SOFT) & hardq;
+          dec = shadow ? DEC_SHADOW : lowered ? DEC_APPROX : DEC_ACCEPTED;
+          const u32 st = shadow ? ST_OBSERVED : ST_MATERIALIZED;
+          flags |= shadow ? (u32)RKC_FL_SHADOW : lowered ? (u32)RKC_FL_LOWERED : 0u;
+          const u32 m = st | (eff << 3) | (hardq << 5) | (prio << 6) | (1u << 8) | (dec << 9);
+          const u32 k = ncl++;
+          // only a materialized claim with a duration expires (shadow claims never do)
+          const u32 dur_eff = shadow ? 0u : dur;
+          cla(CL_ID)[k] = t; cla(CL_C)[k] = c; cla(CL_L)[k] = (u32)L; cla(CL_T)[k] = (u32)T;
+          cla(CL_META)[k] = m; cla(CL_EXP)[k] = dur_eff; cla(CL_SLOT)[k] = s; cla(CL_BLK)[k] = 0;
+          cla(CL_DEM)[k] = kListNil; cla(CL_EXST)[k] = kListNil; cla(CL_PF)[k] = kListNil;
+          cla(CL_HARM)[k] = kListNil;
+          // a new live claim only raises the chain's maxima
+          const uint4 g1 = cg(c, 1);
+          cgs(c, 1, make_uint4(g1.x, max(g1.y, (u32)L), max(g1.z, (u32)L), max(g1.w, (u32)T)));
+          if (soft_levels() && !shadow && eff == RKC_PROT_SOFT)
+            cs(c, CF_LV + prio, max(cf(c, CF_LV + prio), (u32)L));
+          if (dur_eff > 0) next_exp = min(next_exp, t + dur_eff);
+          const uint4 g0 = cg(c, 0);
+          tc = c;
+          tn = max(g0.x, (u32)L);
+          th = g0.y;
+          // a materialized hard claim in a hard-protection pool protects [0, L)
+          tpr = (mode == RKC_MODE_HARD && hardq) ? max(g0.z, (u32)L) : g0.z;
+          tx = (u32)L;
+          id = (i32)t; b = need;
+          count_victims(r, 0);
         }
-        const u32 m = st | (eff << 3) | (hardq << 5) | (prio << 6) | (1u << 8) | (dec << 9);
-        const u32 k = ncl++;
-        // only a materialized claim with a duration expires (shadow claims never do)
-        const u32 dur_eff = st == ST_MATERIALIZED ? dur : 0u;
-        cla(CL_ID)[k] = t; cla(CL_C)[k] = c; cla(CL_L)[k] = (u32)L; cla(CL_T)[k] = (u32)T;
-        cla(CL_META)[k] = m; cla(CL_EXP)[k] = dur_eff; cla(CL_SLOT)[k] = s; cla(CL_BLK)[k] = 0;
-        cla(CL_DEM)[k] = kListNil; cla(CL_EXST)[k] = kListNil; cla(CL_PF)[k] = kListNil;
-        cla(CL_HARM)[k] = kListNil;
-        // a new live claim only raises the chain's maxima
-        const uint4 g1 = cg(c, 1);
-        cgs(c, 1, make_uint4(g1.x, max(g1.y, (u32)L), max(g1.z, (u32)L), max(g1.w, (u32)T)));
-        if (soft_levels() && st == ST_MATERIALIZED && eff == RKC_PROT_SOFT)
-          cs(c, CF_LV + prio, max(cf(c, CF_LV + prio), (u32)L));
-        if (dur_eff > 0) next_exp = min(next_exp, t + dur_eff);
-        const uint4 g0 = cg(c, 0);
-        tc = c;
-        tn = max(g0.x, (u32)L);
-        th = g0.y;
-        // a materialized hard claim in a hard-protection pool protects [0, L)
-        tpr = (mode == RKC_MODE_HARD && hardq) ? max(g0.z, (u32)L) : g0.z;
-        tx = (u32)L;
-        code = r.resident > 0 ? RKC_OC_EVICT_RESIDENT : RKC_OC_ADMIT;
-        id = (i32)t; a = r.resident; b = need;
-        if (r.post) flags |= RKC_FL_POST_RELEASE_LOSS;
-        if (r.unclaimed) flags |= RKC_FL_EVICT_UNCLAIMED;
-        count_victims(r, 0);
+        tadd(TW_ACCEPTED + dec - DEC_ACCEPTED, 1);
+        break;
       }
-      tadd(TW_ACCEPTED + dec - DEC_ACCEPTED, 1);
-    } else if (type == RKC_EV_FINISH) {
-      if (nreq == 0) {
-        code = RKC_OC_NOOP;
-      } else {
+      case K_FINISH: {
         const u32 i = (u32)w1 % nreq;
         const u32 rid = ufl(rqa(RQ_ID)[i]), c = lnil(ufl(rqa(RQ_C)[i])), R = ufl(rqa(RQ_R)[i]);
         const u32 len = ufl(rqa(RQ_LEN)[i]);
@@ -849,12 +856,12 @@ struct Pool {
         }
         // write no-admit drops the request's own blocks; otherwise they become a private run
         const i32 own = (i32)(len - R);
-        const bool drop = mode == RKC_MODE_NOADMIT;
-        const i32 dropped = drop ? own : 0;
-        turned += drop ? 0 : own;
+        const i32 dropped = mode == RKC_MODE_NOADMIT ? own : 0;
+        const i32 kept = own - dropped;
+        turned += kept;
         F += dropped;
-        fblocks += drop ? 0 : own;
-        if (!drop && own > 0) {
+        fblocks += kept;
+        if (kept > 0) {
           if (fhead == ftail) { ft = t; flo = R; ftop = len; }
           fifo[ftail] = make_uint4(t, R, len, 0);
           ftail++;
@@ -863,62 +870,69 @@ struct Pool {
         code = RKC_OC_FINISHED; id = (i32)rid; a = turned; b = dropped;
         if (dropped) flags |= RKC_FL_NOADMIT_DROP;
         tadd(TW_DROPPED, (u32)dropped);
+        break;
       }
-    } else if (type == RKC_EV_RELEASE || type == RKC_EV_DEMOTE) {
-      // the selected live claim: release removes it, demotion turns hard into soft (§3.1)
-      u32 i = NIL;
-      if (type == RKC_EV_RELEASE) {
-        if (ncl > 0) i = (u32)w1 % ncl;
-      } else if (soft_levels()) {
-        u32 cnt = 0;
-        for (u32 base = 0; base < ncl; base += 64) {
-          const u32 j = base + lane;
-          const bool cand = j < ncl && m_state(cla(CL_META)[j]) == ST_MATERIALIZED && m_hard(cla(CL_META)[j]);
-          cnt += (u32)__builtin_popcountll(ballot(cand));
-        }
-        if (cnt > 0) {
-          u32 k = (u32)w1 % cnt;
-          for (u32 base = 0; base < ncl && i == NIL; base += 64) {
+      case K_RELEASE:
+      case K_DEMOTE: {
+        // the selected live claim: release removes it, demotion turns hard into soft (§3.1)
+        u32 i = NIL;
+        if (kind == K_RELEASE) {
+          i = (u32)w1 % ncl;
+        } else if (soft_levels()) {
+          u32 cnt = 0;
+          for (u32 base = 0; base < ncl; base += 64) {
             const u32 j = base + lane;
             const bool cand = j < ncl && m_state(cla(CL_META)[j]) == ST_MATERIALIZED && m_hard(cla(CL_META)[j]);
-            const u64 bl = ballot(cand);
-            const u32 pc = (u32)__builtin_popcountll(bl);
-            if (k < pc) {
-              u64 x = bl;
-              for (u32 q = 0; q < k; q++) x &= x - 1;
-              i = base + (u32)__builtin_ctzll(x);
-            } else {
-              k -= pc;
+            cnt += (u32)__builtin_popcountll(ballot(cand));
+          }
+          if (cnt > 0) {
+            u32 k = (u32)w1 % cnt;
+            for (u32 base = 0; base < ncl && i == NIL; base += 64) {
+              const u32 j = base + lane;
+              const bool cand = j < ncl && m_state(cla(CL_META)[j]) == ST_MATERIALIZED && m_hard(cla(CL_META)[j]);
+              const u64 bl = ballot(cand);
+              const u32 pc = (u32)__builtin_popcountll(bl);
+              if (k < pc) {
+                u64 x = bl;
+                for (u32 q = 0; q < k; q++) x &= x - 1;
+                i = base + (u32)__builtin_ctzll(x);
+              } else {
+                k -= pc;
+              }
             }
           }
         }
-      }
-      if (i == NIL) {
-        code = RKC_OC_NOOP;
-      } else {
-        const u32 qid = ufl(cla(CL_ID)[i]), c = ufl(cla(CL_C)[i]), L = ufl(cla(CL_L)[i]);
-        const u32 T = ufl(cla(CL_T)[i]);
-        if (type == RKC_EV_RELEASE) {
-          write_live_record(i, ST_RELEASED, (i32)t);
-          __builtin_amdgcn_wave_barrier();
-          list_remove(cl, cl_cap, CL_ARRAYS, ncl, i);
-          ncl--;
-          code = RKC_OC_RELEASED;
-          tadd(TW_RELEASED, 1);
-        } else {
-          cla(CL_META)[i] = m_with_state(ufl(cla(CL_META)[i]), ST_DEMOTED);
-          cla(CL_DEM)[i] = t;
-          __builtin_amdgcn_wave_barrier();
-          code = RKC_OC_DEMOTED;
-          tadd(TW_DEMOTED, 1);
+        if (i != NIL) {
+          const u32 qid = ufl(cla(CL_ID)[i]), c = ufl(cla(CL_C)[i]), L = ufl(cla(CL_L)[i]);
+          const u32 T = ufl(cla(CL_T)[i]);
+          if (kind == K_RELEASE) {
+            write_live_record(i, ST_RELEASED, (i32)t);
+            __builtin_amdgcn_wave_barrier();
+            list_remove(cl, cl_cap, CL_ARRAYS, ncl, i);
+            ncl--;
+            code = RKC_OC_RELEASED;
+            tadd(TW_RELEASED, 1);
+          } else {
+            cla(CL_META)[i] = m_with_state(ufl(cla(CL_META)[i]), ST_DEMOTED);
+            cla(CL_DEM)[i] = t;
+            __builtin_amdgcn_wave_barrier();
+            code = RKC_OC_DEMOTED;
+            tadd(TW_DEMOTED, 1);
+          }
+          const u32 pr = claim_maxima(c);
+          const uint4 g0 = cg(c, 0);
+          tc = c; tn = g0.x; th = g0.y; tpr = pr; tx = 0;
+          id = (i32)qid; a = (i32)min(g0.x, L); b = (i32)T;
         }
-        const u32 pr = claim_maxima(c);
-        const uint4 g0 = cg(c, 0);
-        tc = c; tn = g0.x; th = g0.y; tpr = pr; tx = 0;
-        id = (i32)qid; a = (i32)min(g0.x, L); b = (i32)T;
+        break;
       }
-    } else {
-      code = RKC_OC_NOOP;
+      default:
+        break;
+    }
+    if (kind == K_PREFILL || kind == K_EXTEND || (kind == K_CLAIM && r.ok)) {
+      code = r.resident > 0 ? RKC_OC_EVICT_RESIDENT : RKC_OC_ADMIT;
+      a = r.resident;
+      flags |= (r.post ? (u32)RKC_FL_POST_RELEASE_LOSS : 0u) | (r.unclaimed ? (u32)RKC_FL_EVICT_UNCLAIMED : 0u);
     }
 
     if (tc != NIL) {
@@ -928,12 +942,15 @@ struct Pool {
       refresh(tc);
     }
 
-    if (!invalid && any_sweep) {
+    if (sweep_due) {
       __builtin_amdgcn_wave_barrier();
       flags |= sweep(t);
     }
-    if (code == RKC_OC_NOOP || code == RKC_OC_INVALID) { id = -1; a = 0; b = 0; }
-    if (n16 == NIL) n16 = min(expired, 65535u);
+    const u32 quiet = (u32)(code == RKC_OC_NOOP) | (u32)(code == RKC_OC_INVALID);
+    id = quiet ? -1 : id;
+    a = quiet ? 0 : a;
+    b = quiet ? 0 : b;
+    n16 = n16 == NIL ? min(expired, 65535u) : n16;
     tadd((u32)code, 1);
     peak = max(peak, A);
     return make_int4((i32)((u32)code | (flags << 8) | (n16 << 16)), id, a, b);
