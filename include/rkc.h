@@ -215,7 +215,7 @@ typedef struct rkc_batch {
   int32_t max_live_requests; /* >= every pool's max_live_requests                                */
   int32_t max_live_claims;   /* >= every pool's max_live_claims                                  */
   int32_t max_claim_slots;   /* >= every pool's n_claim_slots                                    */
-  int32_t flags;             /* must be 0                                                        */
+  int32_t flags;             /* 0, or RKC_FLAG_GENERAL_KERNEL; other bits are an error           */
   int64_t n_events_total;    /* length of the event and outcome arrays                           */
   int64_t n_claim_slots_total; /* length of the claim telemetry array                            */
   const rkc_pool_desc* d_pools;     /* [n_pools], 16-byte aligned                               */
@@ -226,6 +226,12 @@ typedef struct rkc_batch {
   void* d_scratch;                  /* >= rkc_scratch_bytes(b) bytes, 256-byte aligned          */
   size_t scratch_bytes;
 } rkc_batch;
+
+/* rkc_batch.flags: replay with the general kernel even when the batch fits the compact one (the
+ * compact kernel is chosen for usable blocks <= 32,767, events <= 65,533, chains <= 256, live
+ * claims <= 64 and live requests <= 256).  Both give identical outputs; the flag exists so the
+ * general kernel can be checked on the same inputs. */
+#define RKC_FLAG_GENERAL_KERNEL 1
 
 typedef enum rkc_status {
   RKC_OK = 0,

@@ -14,6 +14,9 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "librkc.so")
 _lib = None
 
+# rkc_batch.flags: replay with the general kernel even where the compact one applies
+FLAG_GENERAL_KERNEL = 1
+
 # status codes (rkc_status)
 STATUS = {0: "ok", -1: "null pointer", -2: "misaligned pointer", -3: "argument out of range",
           -4: "unsupported size or mode", -5: "scratch buffer missing or too small",
@@ -86,7 +89,7 @@ def _stream_ptr(stream):
 class DeviceBatch:
     """Device-resident inputs, outputs and scratch of one replay launch (torch tensors)."""
 
-    def __init__(self, desc, events, n_claim_slots: int, limits: dict, device="cuda"):
+    def __init__(self, desc, events, n_claim_slots: int, limits: dict, device="cuda", flags: int = 0):
         import torch
         if not torch.cuda.is_available():
             raise RuntimeError("no GPU: the replay runs only in the HIP kernels")
@@ -106,7 +109,7 @@ class DeviceBatch:
         for k in ("max_usable_blocks", "max_events", "max_chains", "max_live_requests",
                   "max_live_claims", "max_claim_slots"):
             setattr(b, k, int(limits[k]))
-        b.flags = 0
+        b.flags = int(flags)
         b.n_events_total = n_ev
         b.n_claim_slots_total = self.n_claim_slots
         b.d_pools = self.desc.data_ptr()
@@ -123,8 +126,8 @@ class DeviceBatch:
         self.n_events = n_ev
 
     @classmethod
-    def from_trace(cls, trace, device="cuda"):
-        return cls(trace.desc, trace.events, trace.n_claim_slots, trace.limits(), device)
+    def from_trace(cls, trace, device="cuda", flags: int = 0):
+        return cls(trace.desc, trace.events, trace.n_claim_slots, trace.limits(), device, flags)
 
     def replay(self, stream=None):
         """Enqueue the replay on `stream` (default: torch's current stream)."""

@@ -6,7 +6,7 @@ import subprocess
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
-SRC = os.path.join(PKG, "csrc", "rkc_replay.hip")
+SRCS = [os.path.join(PKG, "csrc", f) for f in ("rkc_replay.hip", "rkc_lean.hip")]
 LIB = os.path.join(PKG, "librkc.so")
 ARCH = "gfx950"
 
@@ -26,7 +26,7 @@ def hipcc() -> str:
 
 def build(verbose: bool = False) -> str:
     tmp = LIB + ".tmp%d" % os.getpid()
-    cmd = [hipcc(), *HIPCC_FLAGS, SRC, "-o", tmp]
+    cmd = [hipcc(), *HIPCC_FLAGS, *SRCS, "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.check_call(cmd)

@@ -1,0 +1,33 @@
+// rkc_lean.h -- internal interface between the C ABI (rkc_replay.hip) and the compact replay
+// kernel (rkc_lean.hip).  Not part of the public ABI.
+#ifndef RKC_LEAN_H
+#define RKC_LEAN_H
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "rkc.h"
+
+struct rkc_lean_args {
+  const rkc_pool_desc* pools;
+  const rkc_event* events;
+  rkc_outcome* outcomes;
+  rkc_pool_telemetry* pool_tel;
+  rkc_claim_telemetry* claim_tel;
+  void* scratch;
+  int64_t n_events_total, n_slots_total;
+  int32_t n_pools, max_usable, max_events, max_chains, max_reqs, max_claims, max_slots;
+  // layout: LDS byte offsets, node split, per-pool scratch regions
+  uint32_t ns, node_cap, nodes_lds;
+  uint32_t off_keys, off_hist, off_chains, off_reqs, off_nodes, lds_bytes;
+  uint64_t scr_pool_bytes, scr_off_nodes, scr_off_fifo, scr_off_slots;
+};
+
+// Fill the layout part of g for batch b; false when b is outside the compact kernel's limits
+// (usable blocks <= 32,767, events <= 65,533, chains <= 256, live claims <= 64, live requests <= 256).
+bool rkc_lean_layout(const rkc_batch* b, rkc_lean_args* g);
+
+// Launch the compact kernel (one 64-lane workgroup per pool) on stream s.
+rkc_status rkc_lean_launch(const rkc_lean_args* g, hipStream_t s);
+
+#endif

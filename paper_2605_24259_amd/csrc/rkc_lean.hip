@@ -1,0 +1,909 @@
+// rkc_lean.hip -- the compact replay kernel for pools whose whole state fits in 16-bit words.
+//
+// Same contract, same outputs, as the general kernel in rkc_replay.hip; this variant serves the
+// batches whose limits allow a tighter encoding:
+//   usable blocks <= 32,767, events per pool <= 65,533, shared chains <= 256,
+//   live claims <= 64, live requests <= 256, claim slots <= 65,534.
+// One 64-lane wavefront replays one pool.  The per-event state machine runs on the scalar unit:
+// every branch is on a wave-uniform value, so no exec-mask juggling happens on the event path.
+//
+// Representation (why it is exact is explained in rkc_replay.hip): the registered positions of
+// every shared chain are a leading run [0, n), eviction takes chains from the top, and every
+// touch, hold, protection and coverage is a leading range.  Per chain, one 16-byte LDS record
+//   n | hold, prot | bt, nx | covA, stop | sbot       (16-bit halves)
+// n registered length, hold leading positions held by live requests, prot protection extent of
+// materialized hard claims (hard-protection pools), covA the largest footprint of a live claim on
+// the chain, and a touch stack of (extent, step) nodes (top stop, bottom sbot; bt = bottom step,
+// nx = extent of the node above the bottom).  Everything else a claim implies for its chain --
+// soft levels, which victims are resident or post-release, which predicates can fail -- lies
+// inside [0, covA) and is computed from the claim lanes only when a position below covA is
+// involved.  Each chain's eviction key lives in LDS as one 32-bit word
+//   key = level << 25 | last use << 9 | (chain + 1)
+// so one wave min-reduction over the keys both orders candidates (level, last use) and names the
+// chain; a finished request's private run has key level 0 | finish step << 9 | 0, which puts it
+// ahead of a chain touched at the same step (it lies above that chain's touched prefix).  A run
+// boundary taken above the true one only splits a run of equal keys into several iterations.
+//
+// Live claims sit one per lane in six VGPRs (16-bit halves), so expiry, attribution, predicate
+// sweeps and claim maxima are single vector passes with DPP reductions.  Live requests are a
+// compact id-ordered list in LDS (8 bytes each).  Touch-stack nodes use LDS first, then global
+// scratch; finished requests' private runs form a FIFO in global scratch.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "rkc.h"
+#include "rkc_lean.h"
+
+namespace {
+
+typedef uint32_t u32;
+typedef int32_t i32;
+typedef uint64_t u64;
+typedef int64_t i64;
+
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) u32 lds_u32;
+typedef __attribute__((address_space(3))) u32x2 lds_u32x2;
+typedef __attribute__((address_space(3))) u32x4 lds_u32x4;
+typedef __attribute__((address_space(1))) u32x2 glb_u32x2;
+
+constexpr u32 NIL = 0xFFFFu;       // 16-bit nil (positions, steps, indices are all below it)
+constexpr u32 KINF = 0xFFFFFFFFu;  // key of a chain with no candidate
+constexpr u32 NEVER = 0xFFFFFFFFu;
+
+enum : u32 { ST_SUBMITTED = 0, ST_OBSERVED = 1, ST_MATERIALIZED = 2, ST_DEMOTED = 3, ST_EXPIRED = 4,
+             ST_RELEASED = 5, ST_HARMED = 6, ST_REJECTED = 7 };
+enum : u32 { DEC_ACCEPTED = 1, DEC_APPROX = 2, DEC_SHADOW = 3, DEC_REJECTED = 4 };
+// pool telemetry words accumulated lane-distributed
+enum : u32 { TW_VICTIMS = 10, TW_RESIDENT = 11, TW_POST = 12, TW_DROPPED = 13, TW_HITS = 14,
+             TW_ACCEPTED = 15, TW_HARM = 19, TW_PREDFAIL = 20, TW_EXPIRED = 21, TW_DEMOTED = 22,
+             TW_RELEASED = 23 };
+
+// live-claim meta (low half of qc): state[0:3) eff[3:5) hard[5] prio[6:8) pending[8] decision[9:12)
+__device__ __forceinline__ u32 m_state(u32 m) { return m & 7u; }
+__device__ __forceinline__ u32 m_eff(u32 m) { return (m >> 3) & 3u; }
+__device__ __forceinline__ u32 m_hard(u32 m) { return (m >> 5) & 1u; }
+__device__ __forceinline__ u32 m_prio(u32 m) { return (m >> 6) & 3u; }
+__device__ __forceinline__ u32 m_pend(u32 m) { return (m >> 8) & 1u; }
+__device__ __forceinline__ u32 m_dec(u32 m) { return (m >> 9) & 7u; }
+__device__ __forceinline__ u32 packed_of(u32 m) {
+  return m_dec(m) | (m_state(m) << 4) | (m_hard(m) << 8) | (m_prio(m) << 9) | (m_eff(m) << 11);
+}
+
+__device__ __forceinline__ u32 lo16(u32 v) { return v & 0xFFFFu; }
+__device__ __forceinline__ u32 hi16(u32 v) { return v >> 16; }
+__device__ __forceinline__ u32 pk(u32 lo, u32 hi) { return (lo & 0xFFFFu) | (hi << 16); }
+__device__ __forceinline__ i32 st16(u32 v) { return v == NIL ? -1 : (i32)v; }  // step field
+
+// ---- wave primitives (all 64 lanes active) ----------------------------------------------------
+__device__ __forceinline__ u32 ufl(u32 v) { return (u32)__builtin_amdgcn_readfirstlane((int)v); }
+__device__ __forceinline__ u32 rdl(u32 v, u32 l) { return (u32)__builtin_amdgcn_readlane((int)v, (int)l); }
+// lane l of `old` replaced by the uniform value v
+__device__ __forceinline__ u32 wrl(u32 old, u32 v, u32 l) { return __lane_id() == l ? v : old; }
+__device__ __forceinline__ u64 ballot(bool p) { return __ballot(p); }
+
+// every source lane exists for the permutes used here, so the moved value never needs an old
+// value and the move folds into the consuming min / max / add
+template <int CTRL>
+__device__ __forceinline__ u32 dpp(u32 v) {
+  return (u32)__builtin_amdgcn_mov_dpp((int)v, CTRL, 0xF, 0xF, true);
+}
+struct OpMax { __device__ static u32 f(u32 a, u32 b) { return a > b ? a : b; } };
+struct OpMin { __device__ static u32 f(u32 a, u32 b) { return a < b ? a : b; } };
+struct OpAdd { __device__ static u32 f(u32 a, u32 b) { return a + b; } };
+// Row-level butterflies (quad perms, half-row and row mirrors), then the four row results.
+template <class Op>
+__device__ __forceinline__ u32 wreduce(u32 v) {
+  v = Op::f(v, dpp<0xB1>(v));   // quad_perm [1,0,3,2]
+  v = Op::f(v, dpp<0x4E>(v));   // quad_perm [2,3,0,1]
+  v = Op::f(v, dpp<0x141>(v));  // row_half_mirror
+  v = Op::f(v, dpp<0x140>(v));  // row_mirror
+  return Op::f(Op::f(rdl(v, 0), rdl(v, 16)), Op::f(rdl(v, 32), rdl(v, 48)));
+}
+__device__ __forceinline__ u32 wmax(u32 v) { return wreduce<OpMax>(v); }
+__device__ __forceinline__ u32 wmin(u32 v) { return wreduce<OpMin>(v); }
+__device__ __forceinline__ u32 wsum(u32 v) { return wreduce<OpAdd>(v); }
+// lane l receives lane l + 1's value (lane 63 keeps its own)
+__device__ __forceinline__ u32 shift_down(u32 v) {
+  return (u32)__builtin_amdgcn_update_dpp((int)v, (int)v, 0x130 /* wave_shl:1 */, 0xF, 0xF, false);
+}
+
+// chain record: n | hold, prot | bt, nx | covA, stop | sbot (16-bit halves, 16 bytes)
+struct G0 { u32 n, hold, prot, bt, nx, covA, stop, sbot; };
+
+struct AllocRes {
+  u32 ok, E, victims, resident, post, unclaimed;
+};
+
+// ---- one pool ---------------------------------------------------------------------------------
+template <int NS>
+struct Lean {
+  static constexpr u32 KC = 64u * NS;  // key slots (chains padded to whole lanes)
+  // descriptor: the policy in a scalar, the rarely used limits one per lane of `cst`
+  u32 mode;
+  u32 cst;  // lane 0 U, 1 chains, 2 live-claim cap, 3 live-request cap, 4 claim slots, 5 node cap
+  u32 lane;
+  __device__ __forceinline__ u32 U() const { return rdl(cst, 0); }
+  __device__ __forceinline__ u32 nch() const { return rdl(cst, 1); }
+  __device__ __forceinline__ u32 maxq() const { return rdl(cst, 2); }
+  __device__ __forceinline__ u32 maxr() const { return rdl(cst, 3); }
+  __device__ __forceinline__ u32 nslots() const { return rdl(cst, 4); }
+  __device__ __forceinline__ u32 ncap() const { return rdl(cst, 5); }
+  // soft levels and acceptance (soft, hard pools: mode bit 0), hard protection, write no-admit
+  __device__ __forceinline__ bool softl() const { return mode & 1u; }
+  __device__ __forceinline__ bool shadm() const { return !(mode & 1u); }
+  __device__ __forceinline__ bool hardm() const { return mode == RKC_MODE_HARD; }
+  __device__ __forceinline__ bool noadm() const { return mode == RKC_MODE_NOADMIT; }
+  // memory
+  lds_u32* kk;
+  lds_u32* hist;  // outcomes per code (16 counters; entry 15 collects the lanes past the end)
+  lds_u32x4* ch;
+  lds_u32x2* rq;
+  lds_u32x2* ndl;
+  glb_u32x2* ndg;
+  static constexpr u32 NL = 64;  // nodes [0, NL) in LDS, the rest in global scratch
+  uint4* fifo;
+  uint2* slotcl;
+  rkc_claim_telemetry* rec;
+  // live claims, one per lane
+  u32 qa;  // id | chain
+  u32 qb;  // L | T
+  u32 qc;  // meta | slot
+  u32 qd;  // duration | blocked count
+  u32 qe;  // demote step | expire step
+  u32 qf;  // predicate-failure step | harm step
+  u32 tv;  // pool telemetry word `lane` (lanes 0..31)
+  // scalars
+  u32 F, A, PR, peak, Eall, fbl;
+  u32 nreq, ncl, nslot, nexp;
+  u32 fnode, bump;              // node free list, bump allocator
+  u32 qh, qt, ft, flo, ftop;    // FIFO of private runs: head, tail, front run
+  u32 vic, post;
+  u32 status;
+
+  // -- telemetry: word w lives in lane w of tv.  The word index is made opaque here so that the
+  //    lane comparison is done where it is used, instead of being hoisted out of the event loop as
+  //    one 64-bit lane mask per word (which exhausts the scalar registers). --
+  __device__ __forceinline__ void tadd(u32 w, u32 v) {
+    asm volatile("" : "+s"(w));
+    tv += lane == w ? v : 0u;
+  }
+
+  // -- chain records --
+  __device__ __forceinline__ G0 rd0(u32 c) {
+    const u32x4 v = ch[c];
+    const u32 a = ufl(v.x), b = ufl(v.y), d = ufl(v.z), e = ufl(v.w);
+    return G0{lo16(a), hi16(a), lo16(b), hi16(b), lo16(d), hi16(d), lo16(e), hi16(e)};
+  }
+  __device__ __forceinline__ void wr0(u32 c, const G0& g) {
+    u32x4 v;
+    v.x = pk(g.n, g.hold); v.y = pk(g.prot, g.bt); v.z = pk(g.nx, g.covA); v.w = pk(g.stop, g.sbot);
+    ch[c] = v;
+  }
+  __device__ __forceinline__ u32 chain_n(u32 c) { return lo16(((lds_u32*)(ch + c))[0]); }
+  __device__ __forceinline__ u32 chain_hold(u32 c) { return hi16(((lds_u32*)(ch + c))[0]); }
+
+  // -- touch-stack nodes: x | t, up | down --
+  __device__ __forceinline__ u32x2 nget(u32 i) {
+    u32x2 v;
+    if (i < NL) v = ndl[i]; else v = ndg[i - NL];
+    v.x = ufl(v.x); v.y = ufl(v.y);
+    return v;
+  }
+  __device__ __forceinline__ void nset(u32 i, u32x2 v) {
+    if (i < NL) ndl[i] = v; else ndg[i - NL] = v;
+  }
+  __device__ __forceinline__ void nset_y(u32 i, u32 y) {
+    if (i < NL) ((lds_u32*)(ndl + i))[1] = y; else ((__attribute__((address_space(1))) u32*)(ndg + (i - NL)))[1] = y;
+  }
+  __device__ __forceinline__ u32 nalloc() {
+    u32 i;
+    if (fnode != NIL) {
+      i = fnode;
+      fnode = hi16(nget(i).y);
+    } else if (bump < ncap()) {
+      i = bump++;
+    } else {
+      status |= 0x80000000u;  // cannot happen: one node per touch, at most node cap - 2 touches
+      i = 0;
+    }
+    return i;
+  }
+
+  // -- chain counters: Eall (evictable shared blocks) and PR (protected cached blocks) --
+  __device__ __forceinline__ static u32 evictable(u32 n, u32 hold, u32 prot) {
+    const u32 lo = max(hold, prot);
+    return n > lo ? n - lo : 0u;
+  }
+  __device__ __forceinline__ static u32 protd(u32 hold, u32 prot) { return prot > hold ? prot - hold : 0u; }
+
+  // -- what the claims on a chain imply, computed from the claim lanes when it matters --
+  // this lane's claim is live on chain c
+  __device__ __forceinline__ bool on_chain(u32 c) const { return lane < ncl && hi16(qa) == c; }
+  // ... and ranks victims at soft level prio + 1 (accepted soft or lowered claims still
+  // materialized, and demoted claims; §3.1 soft priority, demotion to soft)
+  __device__ __forceinline__ bool leveled(u32 c) const {
+    const u32 m = lo16(qc), st = m_state(m);
+    return on_chain(c) && ((st == ST_MATERIALIZED && m_eff(m) == RKC_PROT_SOFT) || st == ST_DEMOTED);
+  }
+  // soft level of position p of chain c
+  __device__ __forceinline__ u32 level_of(u32 c, u32 p) const {
+    return wmax(leveled(c) && lo16(qb) > p ? m_prio(lo16(qc)) + 1u : 0u);
+  }
+  // positions at or above the result have a level <= lvl: the largest footprint of the claims
+  // ranking above lvl (they all end at or below the position where level lvl starts)
+  __device__ __forceinline__ u32 level_floor(u32 c, u32 lvl) const {
+    return wmax(leveled(c) && m_prio(lo16(qc)) + 1u > lvl ? lo16(qb) : 0u);
+  }
+
+  // Key of chain c's top run; advances a stale stack bottom (the node above it reaches n).
+  __device__ __forceinline__ u32 top_key(u32 c, G0& g) {
+    if (g.n <= max(g.hold, g.prot)) return KINF;
+    if (g.nx >= g.n) {
+      u32 b = g.sbot;
+      u32x2 nb = nget(b);
+      u32 up = lo16(nb.y), nxv = 0;
+      for (u32 guard = 0; guard < 0x10000u && up != NIL; guard++) {
+        const u32x2 nu = nget(up);
+        nxv = lo16(nu.x);
+        if (nxv < g.n) break;
+        // node b leaves the stack: free it; up becomes the bottom (its down link is cut)
+        nset_y(b, pk(NIL, fnode));
+        fnode = b;
+        b = up;
+        nb = nu;
+        up = lo16(nb.y);
+        nxv = 0;
+      }
+      nset_y(b, pk(up, NIL));
+      g.sbot = b;
+      g.bt = hi16(nb.x);
+      g.nx = nxv;
+    }
+    // no claim reaches the top position unless covA >= n
+    const u32 lvl = (softl() && g.covA >= g.n) ? level_of(c, g.n - 1) : 0u;
+    return (lvl << 25) | (g.bt << 9) | (c + 1);
+  }
+
+  // Record a touch of positions [0, x) of chain c at step t (x > 0).
+  __device__ __forceinline__ void touch(G0& g, u32 x, u32 t) {
+    u32 tp = g.stop, tpd = NIL;
+    for (u32 guard = 0; guard < 0x10000u && tp != NIL; guard++) {
+      const u32x2 nt = nget(tp);
+      tpd = hi16(nt.y);
+      if (lo16(nt.x) > x) break;
+      nset_y(tp, pk(NIL, fnode));
+      fnode = tp;
+      tp = tpd;
+    }
+    const u32 nw = nalloc();
+    nset(nw, u32x2{pk(x, t), pk(NIL, tp)});
+    if (tp != NIL) {
+      nset_y(tp, pk(nw, tpd));
+      if (tp == g.sbot) g.nx = x;  // the new node sits right above the bottom
+    } else {
+      g.sbot = nw;                 // the new node is the whole stack
+      g.bt = t;
+      g.nx = 0;
+    }
+    g.stop = nw;
+  }
+
+  // Apply new (n, hold, prot) to chain c (keeping Eall and PR exact), optionally touch [0, x)
+  // at t, refresh the key and store the record.
+  __device__ __forceinline__ void commit(u32 c, G0 g, u32 nn, u32 hh, u32 pp, u32 x, u32 t) {
+    Eall += evictable(nn, hh, pp) - evictable(g.n, g.hold, g.prot);
+    PR += protd(hh, pp) - protd(g.hold, g.prot);
+    g.n = nn; g.hold = hh; g.prot = pp;
+    if (x) touch(g, x, t);
+    kk[c] = top_key(c, g);
+    wr0(c, g);
+  }
+
+  // After a lifecycle change of claims on chain c: the extent of its live claims, its hard
+  // protection extent (hard-protection pools), and its key (soft levels may have changed).
+  __device__ __forceinline__ void recompute(u32 c) {
+    const u32 L = lo16(qb), m = lo16(qc);
+    const bool on = on_chain(c);
+    const u32 pp = wmax((on && hardm() && m_state(m) == ST_MATERIALIZED && m_eff(m) == RKC_PROT_HARD) ? L : 0u);
+    G0 g = rd0(c);
+    g.covA = wmax(on ? L : 0u);
+    commit(c, g, g.n, g.hold, pp, 0, 0);
+  }
+  // recompute every chain named by a claim lane in `mask`
+  __device__ __forceinline__ void recompute_lanes(u64 mask) {
+    const u32 cl = hi16(qa);
+    for (u32 guard = 0; mask && guard < 64; guard++) {
+      const u32 l = (u32)__builtin_ctzll(mask);
+      const u32 c = rdl(cl, l);
+      recompute(c);
+      mask &= ~ballot(cl == c);
+    }
+  }
+
+  // Claim record words 0..8 of slot s (word 9, lead_end, is written at the end).
+  __device__ __forceinline__ void write_record(u32 s, i32 id, u32 packed, i32 acc, i32 dem, i32 exs,
+                                               i32 rel, i32 pf, i32 harm, i32 blk) {
+    if (lane < 9) {
+      const i32 v = lane == 0 ? id : lane == 1 ? (i32)packed : lane == 2 ? acc : lane == 3 ? dem
+                  : lane == 4 ? exs : lane == 5 ? rel : lane == 6 ? pf : lane == 7 ? harm : blk;
+      rec[s].w[lane] = v;
+    }
+  }
+  // Record of the live claim in this lane (the caller selects the lanes).
+  __device__ __forceinline__ void write_own_record(u32 state, i32 rel) {
+    const u32 id = lo16(qa), m = lo16(qc);
+    const u32 mm = (m & ~7u) | state;
+    rkc_claim_telemetry* r = rec + hi16(qc);
+    r->w[0] = (i32)id; r->w[1] = (i32)packed_of(mm); r->w[2] = (i32)id;
+    r->w[3] = st16(lo16(qe)); r->w[4] = st16(hi16(qe)); r->w[5] = rel;
+    r->w[6] = st16(lo16(qf)); r->w[7] = st16(hi16(qf)); r->w[8] = (i32)hi16(qd);
+  }
+
+  // Expiry at the start of step t (claims materialized or demoted with a duration).
+  __device__ __forceinline__ void expire(u32 t, u32& flags, u32& expired) {
+    const u32 m = lo16(qc), st = m_state(m), dur = lo16(qd);
+    const bool cand = lane < ncl && (st == ST_MATERIALIZED || st == ST_DEMOTED) && dur != 0;
+    const u32 ex = lo16(qa) + dur;
+    const bool hit = cand && ex <= t;
+    qc = hit ? pk((m & ~7u) | ST_EXPIRED, hi16(qc)) : qc;
+    qe = hit ? pk(lo16(qe), t) : qe;
+    const u64 hm = ballot(hit);
+    nexp = wmin(cand && !hit ? ex : NEVER);
+    expired = (u32)__builtin_popcountll(hm);
+    if (hm) {
+      recompute_lanes(hm);
+      flags |= RKC_FL_EXPIRED;
+      tadd(TW_EXPIRED, expired);
+    }
+  }
+
+  // Predicate sweep after evictions: a claim whose chain now holds fewer than T leading blocks
+  // fails for the first time; a materialized (accepted) claim is harmed (§3.2).
+  __device__ __forceinline__ u32 sweep(u32 t) {
+    const u32 m = lo16(qc), T = hi16(qb), c = hi16(qa);
+    const u32 nc = chain_n(c);
+    const bool fail = lane < ncl && m_pend(m) && nc < T;
+    const bool harm = fail && m_state(m) == ST_MATERIALIZED;
+    const u32 m2 = (m & ~(1u << 8) & ~(harm ? 7u : 0u)) | (harm ? ST_HARMED : 0u);
+    qc = fail ? pk(m2, hi16(qc)) : qc;
+    qf = fail ? pk(t, harm ? t : hi16(qf)) : qf;
+    const u64 fm = ballot(fail), hmk = ballot(harm);
+    if (!fm) return 0;
+    const u32 pf = (u32)__builtin_popcountll(fm), hc = (u32)__builtin_popcountll(hmk);
+    tadd(TW_PREDFAIL, pf);
+    tadd(TW_HARM, hc);
+    recompute_lanes(fm);
+    return RKC_FL_PRED_FAIL | (hc ? (u32)RKC_FL_HARM : 0u);
+  }
+
+  __device__ __forceinline__ void fifo_pop() {
+    qh++;
+    if (qh != qt) {
+      const uint4 e = fifo[qh];
+      ft = ufl(e.x); flo = ufl(e.y); ftop = ufl(e.z);
+    }
+  }
+
+  // ALLOC: FREE blocks first, then the (need - F) smallest-key candidates (§3.1 soft priority;
+  // §5.3 ordinary eviction; hard-protected blocks are never candidates).  hc >= 0 names the chain
+  // whose leading h blocks are the event's own hits (not candidates).
+  __device__ __forceinline__ AllocRes alloc(u32 need, i32 hc, u32 h, const G0& ghc, u32& sweep_due) {
+    AllocRes r = {1, 0, 0, 0, 0, 0};
+    if (need <= F) {
+      F -= need;
+      return r;
+    }
+    u32 E = Eall + fbl;
+    u32 hlo = 0;  // candidates of chain hc start at hlo
+    if (hc >= 0) {
+      const u32 lo = max(ghc.hold, ghc.prot);
+      hlo = max(lo, h);
+      E -= evictable(ghc.n, lo, 0) - evictable(ghc.n, hlo, 0);
+    }
+    r.E = E;
+    if ((u64)need > (u64)F + E) {
+      r.ok = 0;
+      return r;
+    }
+    u32 K = need - F;
+    F = 0;
+    // the hit chain stops being a candidate once only hits remain
+    if (hc >= 0 && ghc.n <= hlo) kk[hc] = KINF;
+    for (u32 guard = 0; K > 0; guard++) {
+      if (guard > 0x10000u) { status |= 0x80000000u; break; }
+      u32 kmin;
+      if (NS == 4) {
+        const u32x4 k4 = ((lds_u32x4*)kk)[lane];
+        kmin = min(min(k4.x, k4.y), min(k4.z, k4.w));
+      } else if (NS == 2) {
+        const u32x2 k2 = ((lds_u32x2*)kk)[lane];
+        kmin = min(k2.x, k2.y);
+      } else {
+        kmin = kk[lane];
+      }
+      const u32 m1 = wmin(kmin);
+      const u32 kf = qh != qt ? (ft << 9) : KINF;
+      if (kf < m1) {
+        // the oldest finished request's private run (level 0)
+        const u32 m = min(K, ftop - flo);
+        ftop -= m;
+        fbl -= m;
+        r.victims += m;
+        r.unclaimed += m;
+        K -= m;
+        if (ftop == flo) fifo_pop();
+      } else {
+        if (m1 == KINF) { status |= 0x80000000u; break; }
+        const u32 c = (m1 & 511u) - 1u;
+        G0 g = rd0(c);
+        const u32 nn = g.n;
+        u32 lo = max(g.hold, g.prot);
+        if ((i32)c == hc) lo = max(lo, h);
+        // the top run shares (level, last use): positions below nx were touched later, positions
+        // below a higher-level claim's footprint rank higher (only claims within covA matter)
+        u32 run_lo = max(lo, g.nx);
+        if (softl() && g.covA > run_lo) run_lo = max(run_lo, level_floor(c, m1 >> 25));
+        const u32 m = min(K, nn - run_lo);
+        const u32 nw = nn - m;
+        u32 rs = 0, sc = 0;
+        if (g.covA > nw) {
+          // victims inside live claims: resident; inside only demoted / expired ones: post-release
+          const u32 st = m_state(lo16(qc));
+          const bool on = on_chain(c);
+          const u32 covS = wmax((on && (st == ST_OBSERVED || st == ST_MATERIALIZED || st == ST_HARMED)) ? lo16(qb) : 0u);
+          rs = min(nn, g.covA) - nw;
+          sc = min(nn, covS) > nw ? min(nn, covS) - nw : 0u;
+          // a claim whose predicate still holds needs more than nw leading blocks
+          if (ballot(on && m_pend(lo16(qc)) && hi16(qb) > nw)) sweep_due = 1;
+        }
+        r.victims += m;
+        r.resident += rs;
+        r.post += rs - sc;
+        r.unclaimed += m - rs;
+        Eall -= m;
+        g.n = nw;
+        K -= m;
+        u32 key = top_key(c, g);
+        if ((i32)c == hc && nw <= lo) key = KINF;
+        kk[c] = key;
+        wr0(c, g);
+      }
+    }
+    return r;
+  }
+
+  // Refusal record of an active event that cannot be served (§3.4; §5.4 refusal record).
+  __device__ __forceinline__ void refusal(u32 need, i32 hc, u32 h, u32 Hc, const G0& ghc, u32& code,
+                                          i32& id, i32& a, i32& b, u32& n16) {
+    u32 Pr = PR;
+    if (hardm() && hc >= 0) {
+      const u32 p = min(ghc.prot, h);
+      Pr -= p > ghc.hold ? p - ghc.hold : 0u;
+    }
+    const u64 req = (u64)A + Hc + need;
+    if (Pr > 0 && req <= U()) {
+      code = RKC_OC_REFUSED_CLAIM;
+      const u32 m = lo16(qc), c = hi16(qa);
+      u32 cov = chain_hold(c);
+      if ((i32)c == hc) cov = max(cov, h);
+      const bool blk = lane < ncl && m_state(m) == ST_MATERIALIZED && m_eff(m) == RKC_PROT_HARD &&
+                       lo16(qb) > cov;
+      qd += blk ? (1u << 16) : 0u;
+      const u64 bm = ballot(blk);
+      id = (i32)wmin(blk ? lo16(qa) : NEVER);
+      n16 = min((u32)__builtin_popcountll(bm), 65535u);
+    } else {
+      code = RKC_OC_REFUSED_CAPACITY;
+      id = -1;
+      n16 = 0;
+    }
+    a = (i32)Pr;
+    b = (i32)req;
+  }
+
+  __device__ __forceinline__ void served(const AllocRes& r, u32& code, u32& flags, i32& a) {
+    code = r.resident ? RKC_OC_EVICT_RESIDENT : RKC_OC_ADMIT;
+    a = (i32)r.resident;
+    flags |= (r.post ? (u32)RKC_FL_POST_RELEASE_LOSS : 0u) | (r.unclaimed ? (u32)RKC_FL_EVICT_UNCLAIMED : 0u);
+    vic += r.victims;
+    post += r.post;
+  }
+
+  // Remove request entry i from the compact list of n entries (n <= 256).
+  __device__ __forceinline__ void rq_remove(u32 i, u32 n) {
+    for (u32 base = i; base + 1 < n; base += 64) {
+      const u32 j = base + lane;
+      const u32 src = min(j + 1, n - 1);
+      const u32x2 v = rq[src];
+      __builtin_amdgcn_wave_barrier();
+      if (j + 1 < n) rq[j] = v;
+      __builtin_amdgcn_wave_barrier();
+    }
+  }
+  // largest R of the live requests on chain c
+  __device__ __forceinline__ u32 rq_hold(u32 c, u32 n) {
+    u32 hv = 0;
+    for (u32 base = 0; base < n; base += 64) {
+      const u32 j = base + lane;
+      const u32x2 v = rq[min(j, n - 1)];
+      hv = max(hv, (j < n && hi16(v.x) == c) ? lo16(v.y) : 0u);
+    }
+    return wmax(hv);
+  }
+
+  // One event; returns the outcome words through o.
+  __device__ __forceinline__ void step(u32 t, u32 w0, u32 w1, u32 w2, u32 w3, u32& o0, i32& o1, i32& o2, i32& o3) {
+    const u32 type = w0 & 15u;
+    u32 flags = 0, expired = 0, n16 = NEVER, sweep_due = 0;
+    u32 code = RKC_OC_NOOP;
+    i32 id = -1, a = 0, b = 0;
+    if (t >= nexp) expire(t, flags, expired);
+    const i32 s1 = (i32)w1, s2 = (i32)w2, s3 = (i32)w3;
+    switch (type) {
+      case RKC_EV_PREFILL: {
+        if (s1 < 1 || s1 > RKC_MAX_FIELD_BLOCKS || s3 < 0 || s3 > s1 || (s3 > 0 && (s2 < 0 || w2 >= nch()))) {
+          code = RKC_OC_INVALID;
+          break;
+        }
+        if (nreq >= maxr()) { code = RKC_OC_INVALID; status |= RKC_PS_REQUEST_TABLE; break; }
+        const u32 S = w1, P = w3;
+        i32 hc = -1;
+        u32 h = 0, Hc = 0;
+        G0 g = {0, 0, 0, 0, 0, 0, 0, 0};
+        if (P > 0) {
+          hc = (i32)w2;
+          g = rd0(w2);
+          h = min(P, g.n);
+          Hc = h > g.hold ? h - g.hold : 0u;
+        }
+        const u32 need = S - h;
+        const AllocRes r = alloc(need, hc, h, g, sweep_due);
+        if (!r.ok) { refusal(need, hc, h, Hc, g, code, id, a, b, n16); break; }
+        A += Hc + need;
+        u32 R = 0;
+        if (hc >= 0) {
+          const G0 g2 = r.victims ? rd0(w2) : g;  // victims may have shortened this chain above the hits
+          R = noadm() ? h : P;
+          const u32 nn = (!noadm() && P > g2.n) ? P : g2.n;
+          commit(w2, g2, nn, max(g2.hold, R), g2.prot, R, t);
+        }
+        rq[nreq] = u32x2{pk(t, hc >= 0 ? w2 : NIL), pk(R, S)};
+        nreq++;
+        id = (i32)t;
+        b = (i32)h;
+        served(r, code, flags, a);
+        break;
+      }
+      case RKC_EV_EXTEND: {
+        if (s1 < 1 || s1 > RKC_MAX_FIELD_BLOCKS) { code = RKC_OC_INVALID; break; }
+        if (nreq == 0) break;
+        const u32 i = w2 % nreq, need = w1;
+        const G0 g = {0, 0, 0, 0, 0, 0, 0, 0};
+        const AllocRes r = alloc(need, -1, 0, g, sweep_due);
+        if (!r.ok) { refusal(need, -1, 0, 0, g, code, id, a, b, n16); break; }
+        A += need;
+        u32x2 e = rq[i];
+        e.x = ufl(e.x); e.y = ufl(e.y);
+        rq[i] = u32x2{e.x, pk(lo16(e.y), hi16(e.y) + need)};
+        id = (i32)lo16(e.x);
+        b = (i32)A;
+        served(r, code, flags, a);
+        break;
+      }
+      case RKC_EV_CLAIM: {
+        if (nslot >= nslots()) { code = RKC_OC_INVALID; status |= RKC_PS_SLOT_TABLE; break; }
+        const u32 s = nslot++;
+        bool ok = !(s1 < 1 || s1 > RKC_MAX_FIELD_BLOCKS || s2 < 0 || w2 >= nch() || s3 < 0 || s3 > s1);
+        if (ok && ncl >= maxq()) { status |= RKC_PS_CLAIM_TABLE; ok = false; }
+        slotcl[s] = ok ? make_uint2(w2, w1) : make_uint2(NEVER, 0);  // every lane, one value
+        if (!ok) {
+          write_record(s, (i32)t, 0, -1, -1, -1, -1, -1, -1, 0);
+          code = RKC_OC_INVALID;
+          break;
+        }
+        const u32 L = w1, c = w2, T = w3;
+        const u32 hardq = (w0 >> 4) & 1u, prio = (w0 >> 5) & 3u, dur = w0 >> 16;
+        const G0 g = rd0(c);
+        const u32 h = min(L, g.n), need = L - h;
+        const AllocRes r = alloc(need, (i32)c, h, g, sweep_due);
+        const u32 eff = hardm() ? (hardq ? RKC_PROT_HARD : RKC_PROT_SOFT) : (mode == RKC_MODE_SOFT ? RKC_PROT_SOFT : RKC_PROT_NONE);
+        if (!r.ok) {
+          const u32 dec = shadm() ? DEC_SHADOW : DEC_REJECTED;
+          const u32 m = ST_REJECTED | (eff << 3) | (hardq << 5) | (prio << 6) | (dec << 9);
+          write_record(s, (i32)t, packed_of(m), -1, -1, -1, -1, -1, -1, 0);
+          code = RKC_OC_MATFAIL;
+          id = (i32)t;
+          a = (i32)need;
+          b = (i32)(F + r.E);
+          tadd(TW_ACCEPTED + dec - DEC_ACCEPTED, 1);
+          break;
+        }
+        const u32 lowered = (mode == RKC_MODE_SOFT) && hardq;
+        const u32 dec = shadm() ? DEC_SHADOW : lowered ? DEC_APPROX : DEC_ACCEPTED;
+        const u32 st = shadm() ? ST_OBSERVED : ST_MATERIALIZED;
+        flags |= shadm() ? (u32)RKC_FL_SHADOW : lowered ? (u32)RKC_FL_LOWERED : 0u;
+        const u32 m = st | (eff << 3) | (hardq << 5) | (prio << 6) | (1u << 8) | (dec << 9);
+        const u32 dur_eff = shadm() ? 0u : dur;  // shadow claims never expire
+        const u32 k = ncl++;
+        qa = wrl(qa, pk(t, c), k);
+        qb = wrl(qb, pk(L, T), k);
+        qc = wrl(qc, pk(m, s), k);
+        qd = wrl(qd, dur_eff, k);
+        qe = wrl(qe, 0xFFFFFFFFu, k);
+        qf = wrl(qf, 0xFFFFFFFFu, k);
+        if (dur_eff > 0) nexp = min(nexp, t + dur_eff);
+        G0 g2 = r.victims ? rd0(c) : g;
+        g2.covA = max(g2.covA, L);
+        // a materialized hard claim in a hard-protection pool protects [0, L)
+        const u32 pp = (hardm() && hardq) ? max(g2.prot, L) : g2.prot;
+        commit(c, g2, max(g2.n, L), g2.hold, pp, L, t);
+        id = (i32)t;
+        b = (i32)need;
+        served(r, code, flags, a);
+        tadd(TW_ACCEPTED + dec - DEC_ACCEPTED, 1);
+        break;
+      }
+      case RKC_EV_FINISH: {
+        if (nreq == 0) break;
+        const u32 i = w1 % nreq;
+        u32x2 e = rq[i];
+        e.x = ufl(e.x); e.y = ufl(e.y);
+        const u32 rid = lo16(e.x), c = hi16(e.x), R = lo16(e.y), len = hi16(e.y);
+        rq_remove(i, nreq);
+        nreq--;
+        u32 turned = 0;
+        if (c != NIL) {
+          const u32 hn = rq_hold(c, nreq);
+          turned += R > hn ? R - hn : 0u;
+          const G0 g = rd0(c);
+          commit(c, g, g.n, hn, g.prot, R, t);
+        }
+        // write no-admit drops the request's own blocks; otherwise they become a private run
+        const u32 own = len - R;
+        const u32 dropped = noadm() ? own : 0u;
+        const u32 kept = own - dropped;
+        turned += kept;
+        F += dropped;
+        fbl += kept;
+        if (kept > 0) {
+          if (qh == qt) { ft = t; flo = R; ftop = len; }
+          fifo[qt] = make_uint4(t, R, len, 0);  // every lane, one value
+          qt++;
+        }
+        A -= turned + dropped;
+        code = RKC_OC_FINISHED;
+        id = (i32)rid;
+        a = (i32)turned;
+        b = (i32)dropped;
+        if (dropped) flags |= RKC_FL_NOADMIT_DROP;
+        tadd(TW_DROPPED, dropped);
+        break;
+      }
+      case RKC_EV_RELEASE:
+      case RKC_EV_DEMOTE: {
+        u32 i = NEVER;
+        if (type == RKC_EV_RELEASE) {
+          if (ncl > 0) i = w1 % ncl;
+        } else if (softl()) {
+          const u32 m = lo16(qc);
+          const u64 cm = ballot(lane < ncl && m_state(m) == ST_MATERIALIZED && m_hard(m));
+          const u32 cnt = (u32)__builtin_popcountll(cm);
+          if (cnt > 0) {
+            const u32 k = w1 % cnt;
+            const u32 rank = __builtin_amdgcn_mbcnt_hi((u32)(cm >> 32), __builtin_amdgcn_mbcnt_lo((u32)cm, 0u));
+            i = (u32)__builtin_ctzll(ballot(((cm >> lane) & 1ull) && rank == k));
+          }
+        }
+        if (i == NEVER) break;
+        const u32 qid = lo16(rdl(qa, i)), c = hi16(rdl(qa, i));
+        const u32 qbv = rdl(qb, i);
+        if (type == RKC_EV_RELEASE) {
+          if (lane == i) write_own_record(ST_RELEASED, (i32)t);
+          // close the gap: lanes >= i take their upper neighbour's claim
+          const bool up = lane >= i;
+          qa = up ? shift_down(qa) : qa; qb = up ? shift_down(qb) : qb; qc = up ? shift_down(qc) : qc;
+          qd = up ? shift_down(qd) : qd; qe = up ? shift_down(qe) : qe; qf = up ? shift_down(qf) : qf;
+          ncl--;
+          code = RKC_OC_RELEASED;
+          tadd(TW_RELEASED, 1);
+        } else {
+          const bool me = lane == i;
+          qc = me ? pk((lo16(qc) & ~7u) | ST_DEMOTED, hi16(qc)) : qc;
+          qe = me ? pk(t, hi16(qe)) : qe;
+          code = RKC_OC_DEMOTED;
+          tadd(TW_DEMOTED, 1);
+        }
+        recompute(c);
+        const u32 nc = ufl(chain_n(c));
+        id = (i32)qid;
+        a = (i32)min(nc, lo16(qbv));
+        b = (i32)hi16(qbv);
+        break;
+      }
+      case RKC_EV_NOP:
+        break;
+      default:
+        code = RKC_OC_INVALID;
+        break;
+    }
+    if (sweep_due) flags |= sweep(t);
+    const bool quiet = code == RKC_OC_NOOP || code == RKC_OC_INVALID;
+    o0 = code | (flags << 8) | ((n16 == NEVER ? min(expired, 65535u) : n16) << 16);
+    o1 = quiet ? -1 : id;
+    o2 = quiet ? 0 : a;
+    o3 = quiet ? 0 : b;
+    peak = max(peak, A);
+  }
+};
+
+template <int NS>
+__global__ __launch_bounds__(64) void rkc_lean(rkc_lean_args g) {
+  extern __shared__ __align__(16) unsigned char lds_raw[];
+  const u32 pool = blockIdx.x;
+  if ((i32)pool >= g.n_pools) return;
+  Lean<NS> P;
+  P.lane = __lane_id();
+  const rkc_pool_desc d = g.pools[pool];
+  const i64 ev_off = d.event_offset, slot_off = d.claim_slot_offset;
+  rkc_pool_telemetry* ptel = g.pool_tel + pool;
+  const bool ev_ok = d.n_events >= 0 && ev_off >= 0 && ev_off + d.n_events <= g.n_events_total;
+  const bool sl_ok = d.n_claim_slots >= 0 && slot_off >= 0 && slot_off + d.n_claim_slots <= g.n_slots_total;
+  const bool ok = ev_ok && sl_ok && d.usable_blocks >= 1 && d.usable_blocks <= g.max_usable &&
+                  d.mode >= 0 && d.mode <= 3 && d.n_events <= g.max_events && d.n_chains >= 0 &&
+                  d.n_chains <= g.max_chains && d.max_live_claims >= 0 && d.max_live_claims <= g.max_claims &&
+                  d.max_live_requests >= 0 && d.max_live_requests <= g.max_reqs &&
+                  d.n_claim_slots <= g.max_slots && d.reserved == 0;
+  if (!ok) {
+    const u32 lane = P.lane;
+    if (ev_ok)
+      for (i32 i = (i32)lane; i < d.n_events; i += 64) g.outcomes[ev_off + i] = rkc_outcome{{RKC_OC_INVALID, -1, 0, 0}};
+    if (sl_ok)
+      for (i32 i = (i32)lane; i < d.n_claim_slots; i += 64)
+        g.claim_tel[slot_off + i] = rkc_claim_telemetry{{-1, 0, -1, -1, -1, -1, -1, -1, 0, 0}};
+    if (lane < 32)
+      ptel->w[lane] = lane == 31 ? RKC_PS_DESCRIPTOR : (lane == RKC_OC_INVALID && ev_ok) ? d.n_events : 0;
+    return;
+  }
+  P.mode = (u32)d.mode;
+  {
+    const u32 l = P.lane;
+    P.cst = l == 0 ? (u32)d.usable_blocks : l == 1 ? (u32)d.n_chains : l == 2 ? (u32)d.max_live_claims
+          : l == 3 ? (u32)d.max_live_requests : l == 4 ? (u32)d.n_claim_slots : g.node_cap;
+  }
+  const u32 U = (u32)d.usable_blocks, nch = (u32)d.n_chains, nslots = (u32)d.n_claim_slots;
+
+  lds_u32* lds = (lds_u32*)lds_raw;
+  P.kk = lds + g.off_keys / 4;
+  P.ch = (lds_u32x4*)(lds + g.off_chains / 4);
+  P.rq = (lds_u32x2*)(lds + g.off_reqs / 4);
+  P.ndl = (lds_u32x2*)(lds + g.off_nodes / 4);
+  unsigned char* scr = (unsigned char*)g.scratch + (u64)pool * g.scr_pool_bytes;
+  P.ndg = (glb_u32x2*)(scr + g.scr_off_nodes);
+  P.fifo = (uint4*)(scr + g.scr_off_fifo);
+  P.slotcl = (uint2*)(scr + g.scr_off_slots);
+  P.rec = g.claim_tel + slot_off;
+
+  for (u32 c = P.lane; c < Lean<NS>::KC; c += 64) P.kk[c] = KINF;
+  P.hist = lds + g.off_hist / 4;
+  if (P.lane < 16) P.hist[P.lane] = 0;
+  const u32 nrec = nch > 0 ? nch : 1u;
+  for (u32 c = P.lane; c < nrec; c += 64) {
+    P.ch[c] = u32x4{0, 0, 0, pk(NIL, NIL)};
+  }
+  P.qa = P.qb = P.qc = P.qd = P.qe = P.qf = 0;
+  P.tv = 0;
+  P.F = U; P.A = 0; P.PR = 0; P.peak = 0; P.Eall = 0; P.fbl = 0;
+  P.nreq = 0; P.ncl = 0; P.nslot = 0; P.nexp = NEVER;
+  P.fnode = NIL; P.bump = 0;
+  P.qh = 0; P.qt = 0; P.ft = 0; P.flo = 0; P.ftop = 0;
+  P.vic = 0; P.post = 0;
+  P.status = 0;
+  __syncthreads();
+
+  const rkc_event* ev = g.events + ev_off;
+  rkc_outcome* out = g.outcomes + ev_off;
+  const u32 ne = (u32)d.n_events;
+  for (u32 base = 0; base < ne; base += 64) {
+    const u32 cnt = min(64u, ne - base);
+    u32 e0 = 0, e1 = 0, e2 = 0, e3 = 0;
+    if (P.lane < cnt) {
+      const int4 x = *(const int4*)(ev + base + P.lane);
+      e0 = (u32)x.x; e1 = (u32)x.y; e2 = (u32)x.z; e3 = (u32)x.w;
+    }
+    u32 o0 = 0, o1 = 0, o2 = 0, o3 = 0;
+    for (u32 k = 0; k < cnt; k++) {
+      u32 r0;
+      i32 r1, r2, r3;
+      P.step(base + k, rdl(e0, k), rdl(e1, k), rdl(e2, k), rdl(e3, k), r0, r1, r2, r3);
+      o0 = wrl(o0, r0, k); o1 = wrl(o1, (u32)r1, k); o2 = wrl(o2, (u32)r2, k); o3 = wrl(o3, (u32)r3, k);
+    }
+    if (P.lane < cnt) *(int4*)(out + base + P.lane) = make_int4((i32)o0, (i32)o1, (i32)o2, (i32)o3);
+    // outcomes per code; resident victims (a) and leading hits (b of a served prefill)
+    const u32 oc = o0 & 255u;
+    __hip_atomic_fetch_add(P.hist + (P.lane < cnt ? oc : 15u), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    const bool srv = P.lane < cnt && oc <= RKC_OC_EVICT_RESIDENT;
+    P.tadd(TW_RESIDENT, wsum(srv ? o2 : 0u));
+    P.tadd(TW_HITS, wsum(srv && (e0 & 15u) == RKC_EV_PREFILL ? o3 : 0u));
+  }
+
+  // Final records of the claims still live (each lane writes its own) ...
+  if (P.lane < P.ncl) P.write_own_record(m_state(lo16(P.qc)), -1);
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
+  // ... then lead_end = min(final leading registered length, L) of every used slot, and blank
+  // records for unused slots.
+  for (u32 s = P.lane; s < nslots; s += 64) {
+    if (s < P.nslot) {
+      const uint2 cl = P.slotcl[s];
+      u32 le = 0;
+      if (cl.x != NEVER) le = min(P.chain_n(cl.x), cl.y);
+      P.rec[s].w[9] = (i32)le;
+    } else {
+      P.rec[s] = rkc_claim_telemetry{{-1, 0, -1, -1, -1, -1, -1, -1, 0, 0}};
+    }
+  }
+  __syncthreads();
+  if (P.lane < 32) {
+    const u32 w = P.lane;
+    i32 v = (i32)P.tv;
+    if (w < 10) v += (i32)P.hist[w];
+    if (w == TW_VICTIMS) v = (i32)P.vic;
+    else if (w == TW_POST) v = (i32)P.post;
+    else if (w == 24) v = (i32)P.peak;
+    else if (w == 25) v = (i32)P.A;
+    else if (w == 26) v = (i32)(U - P.F - P.A);
+    else if (w == 27) v = (i32)P.F;
+    else if (w == 28) v = (i32)P.PR;
+    else if (w == 29) v = (i32)P.nreq;
+    else if (w == 30) v = (i32)P.ncl;
+    else if (w == 31) v = (i32)P.status;
+    ptel->w[w] = v;
+  }
+}
+
+u64 align_up(u64 v, u64 a) { return (v + a - 1) / a * a; }
+
+}  // namespace
+
+// Layout of the compact kernel for batch b, or false when the batch is outside its limits.
+bool rkc_lean_layout(const rkc_batch* b, rkc_lean_args* g) {
+  if (b->max_usable_blocks > 32767 || b->max_events > 65533 || b->max_chains > 256 ||
+      b->max_live_claims > 64 || b->max_live_requests > 256 || b->max_claim_slots > 65534)
+    return false;
+  const u32 chains = b->max_chains > 0 ? (u32)b->max_chains : 1u;
+  const u32 ns = chains <= 64 ? 1u : chains <= 128 ? 2u : 4u;
+  const u32 reqs = b->max_live_requests > 0 ? (u32)b->max_live_requests : 1u;
+  g->ns = ns;
+  g->node_cap = (u32)b->max_events + 2;
+  g->nodes_lds = 64;  // nodes kept in LDS by the compact kernel
+  u64 o = 0;
+  auto take = [&](u64 bytes) { o = align_up(o, 16); u64 r = o; o += bytes; return (u32)r; };
+  g->off_keys = take(4ull * 64 * ns);
+  g->off_hist = take(4ull * 16);
+  g->off_chains = take(16ull * chains);
+  g->off_reqs = take(8ull * reqs);
+  g->off_nodes = take(8ull * g->nodes_lds);
+  g->lds_bytes = (u32)align_up(o, 16);
+  u64 s = 0;
+  g->scr_off_nodes = s;
+  s += 8ull * (g->node_cap > g->nodes_lds ? g->node_cap - g->nodes_lds : 0u);
+  s = align_up(s, 256);
+  g->scr_off_fifo = s; s += 16ull * ((u64)b->max_events + 1); s = align_up(s, 256);
+  g->scr_off_slots = s; s += 8ull * (u64)(b->max_claim_slots > 0 ? b->max_claim_slots : 1);
+  g->scr_pool_bytes = align_up(s, 256);
+  return true;
+}
+
+rkc_status rkc_lean_launch(const rkc_lean_args* g, hipStream_t s) {
+  const void* fn = g->ns == 1 ? (const void*)rkc_lean<1> : g->ns == 2 ? (const void*)rkc_lean<2>
+                                                                      : (const void*)rkc_lean<4>;
+  if (g->lds_bytes > 64 * 1024 &&
+      hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)g->lds_bytes) != hipSuccess)
+    return RKC_E_HIP;
+  const dim3 grid((unsigned)g->n_pools), block(64);
+  if (g->ns == 1) hipLaunchKernelGGL(rkc_lean<1>, grid, block, g->lds_bytes, s, *g);
+  else if (g->ns == 2) hipLaunchKernelGGL(rkc_lean<2>, grid, block, g->lds_bytes, s, *g);
+  else hipLaunchKernelGGL(rkc_lean<4>, grid, block, g->lds_bytes, s, *g);
+  return hipGetLastError() == hipSuccess ? RKC_OK : RKC_E_HIP;
+}

@@ -40,6 +40,7 @@
 #include <string.h>
 
 #include "rkc.h"
+#include "rkc_lean.h"
 
 namespace {
 
@@ -1145,7 +1146,7 @@ rkc_status check_batch(const rkc_batch* b) {
   if (!b) return RKC_E_NULL;
   if (b->n_pools < 0 || b->max_usable_blocks < 0 || b->max_events < 0 || b->max_chains < 0 ||
       b->max_live_requests < 0 || b->max_live_claims < 0 || b->max_claim_slots < 0 ||
-      b->n_events_total < 0 || b->n_claim_slots_total < 0 || b->flags != 0)
+      b->n_events_total < 0 || b->n_claim_slots_total < 0 || (b->flags & ~RKC_FLAG_GENERAL_KERNEL) != 0)
     return RKC_E_RANGE;
   if (b->max_usable_blocks > RKC_MAX_USABLE_BLOCKS || b->max_events > RKC_MAX_EVENTS_PER_POOL)
     return RKC_E_UNSUPPORTED;
@@ -1169,6 +1170,13 @@ rkc_status launch(const Args& g, unsigned n_pools, hipStream_t s) {
   return hipGetLastError() == hipSuccess ? RKC_OK : RKC_E_HIP;
 }
 
+// The compact kernel serves every batch within its limits unless the caller asks for the
+// general one.
+bool use_lean(const rkc_batch* b, rkc_lean_args* g) {
+  memset(g, 0, sizeof *g);
+  return !(b->flags & RKC_FLAG_GENERAL_KERNEL) && rkc_lean_layout(b, g);
+}
+
 }  // namespace
 
 extern "C" {
@@ -1177,6 +1185,8 @@ int32_t rkc_abi_version(void) { return RKC_ABI_VERSION; }
 
 size_t rkc_scratch_bytes(const rkc_batch* b) {
   if (!b || b->n_pools <= 0) return 0;
+  rkc_lean_args lg;
+  if (use_lean(b, &lg)) return (size_t)(lg.scr_pool_bytes * (u64)b->n_pools);
   Layout L;
   if (!choose_layout(b, &L)) return 0;
   return (size_t)(L.scr_pool_bytes * (u64)b->n_pools);
@@ -1186,6 +1196,18 @@ rkc_status rkc_replay_batch(const rkc_batch* b, void* s) {
   rkc_status st = check_batch(b);
   if (st != RKC_OK) return st;
   if (b->n_pools == 0) return RKC_OK;
+  rkc_lean_args lg;
+  if (use_lean(b, &lg)) {
+    const u64 need = lg.scr_pool_bytes * (u64)b->n_pools;
+    if (!b->d_scratch || b->scratch_bytes < need) return RKC_E_SCRATCH;
+    lg.pools = b->d_pools; lg.events = b->d_events; lg.outcomes = b->d_outcomes;
+    lg.pool_tel = b->d_pool_tel; lg.claim_tel = b->d_claim_tel; lg.scratch = b->d_scratch;
+    lg.n_events_total = b->n_events_total; lg.n_slots_total = b->n_claim_slots_total;
+    lg.n_pools = b->n_pools; lg.max_usable = b->max_usable_blocks; lg.max_events = b->max_events;
+    lg.max_chains = b->max_chains; lg.max_reqs = b->max_live_requests; lg.max_claims = b->max_live_claims;
+    lg.max_slots = b->max_claim_slots;
+    return rkc_lean_launch(&lg, (hipStream_t)s);
+  }
   Args g;
   memset(&g, 0, sizeof g);
   if (!choose_layout(b, &g.L)) return RKC_E_UNSUPPORTED;

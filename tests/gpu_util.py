@@ -9,9 +9,9 @@ import numpy as np
 OUT_FIELDS = ("code|flags|n16", "id", "a", "b")
 
 
-def gpu_replay(trace):
+def gpu_replay(trace, flags=0):
     import paper_2605_24259_amd as rkc
-    db = rkc.DeviceBatch.from_trace(trace)
+    db = rkc.DeviceBatch.from_trace(trace, flags=flags)
     db.replay()
     return db.results()
 

@@ -63,13 +63,19 @@ def random_pool(rng: np.random.Generator, U: int, mode: int, n_events: int, n_ch
 
 
 def random_batch(seed: int, n_pools: int, U_range=(2, 9), n_events=(1, 14), n_chains=3,
-                 tight_every: int = 5, p_malformed: float = 0.03):
+                 tight_every: int = 5, p_malformed: float = 0.03, caps=None):
+    """caps = (live requests, live claims): table capacities of the pools that are not tight
+    (default: one entry per PREFILL / CLAIM event, which never overflows)."""
     from paper_2605_24259_amd import tracegen as tg
     rng = np.random.default_rng(seed)
     pools = []
     for i in range(n_pools):
         U = int(rng.integers(U_range[0], U_range[1]))
         ne = int(rng.integers(n_events[0], n_events[1] + 1))
-        pools.append(random_pool(rng, U, i % 4, ne, n_chains=n_chains, p_malformed=p_malformed,
-                                 tight_tables=(tight_every > 0 and i % tight_every == tight_every - 1)))
+        tight = tight_every > 0 and i % tight_every == tight_every - 1
+        pool = random_pool(rng, U, i % 4, ne, n_chains=n_chains, p_malformed=p_malformed,
+                           tight_tables=tight)
+        if caps is not None and not tight:
+            pool["max_live_requests"], pool["max_live_claims"] = caps
+        pools.append(pool)
     return tg.from_pools(pools, f"random{seed}")

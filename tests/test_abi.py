@@ -104,7 +104,7 @@ def test_host_argument_checks(lib):
     assert lib.rkc_replay_batch(ctypes.byref(_batch(d_outcomes=0x30008)), None) == -2
     assert lib.rkc_replay_batch(ctypes.byref(_batch(d_scratch=0x60010)), None) == -2
     assert lib.rkc_replay_batch(ctypes.byref(_batch(n_pools=-1)), None) == -3
-    assert lib.rkc_replay_batch(ctypes.byref(_batch(flags=1)), None) == -3
+    assert lib.rkc_replay_batch(ctypes.byref(_batch(flags=2)), None) == -3
     assert lib.rkc_replay_batch(ctypes.byref(_batch(max_usable_blocks=(1 << 22) + 1)), None) == -4
     # scratch too small (the batch needs > 0 bytes)
     b = _batch()
@@ -125,3 +125,16 @@ def test_scratch_grows_with_limits(lib):
     big = lib.rkc_scratch_bytes(ctypes.byref(_batch(max_events=4096)))
     many = lib.rkc_scratch_bytes(ctypes.byref(_batch(n_pools=20)))
     assert big > small and many == 10 * small
+
+
+@pytest.mark.parametrize("max_events", [0, 1, 13, 63, 64, 65, 1024])
+def test_scratch_is_proportional_to_the_limits(lib, max_events):
+    """Scratch per pool stays within a few bytes per event and claim slot for both kernels (the
+    compact one is chosen for these limits, the general one when the batch flag forces it)."""
+    for flags in (0, 1):
+        b = _batch(n_pools=1, max_events=max_events, flags=flags)
+        n = lib.rkc_scratch_bytes(ctypes.byref(b))
+        bound = 64 * (max_events + 2) + 16 * (b.max_claim_slots + 1) + 4096
+        if flags:
+            bound += 64 * (b.max_live_requests + b.max_live_claims)
+        assert 0 < n <= bound, (flags, max_events, n, bound)

@@ -65,9 +65,10 @@ def test_random_tiny(oracle_mod, seed):
 
 @pytest.mark.parametrize("seed", [11, 12, 13])
 def test_random_medium(oracle_mod, seed):
-    """Several tiles of events per pool (up to 400 > 64-event prefetch), ragged tails, up to 9 chains."""
+    """Several tiles of events per pool (up to 400 > 64-event prefetch), ragged tails, up to 9
+    chains; tables of 256 requests and 64 claims (the compact kernel's limits) or tighter."""
     trace = randtrace.random_batch(seed, 400, U_range=(8, 300), n_events=(1, 400), n_chains=9,
-                                   p_malformed=0.01, tight_every=7)
+                                   p_malformed=0.01, tight_every=7, caps=(256, 64))
     gpu, ora = _both(oracle_mod, trace)
     compare_pools(trace, gpu, ora)
 
@@ -235,3 +236,22 @@ def test_storage_layouts_agree(oracle_mod, tg, variant):
     gpu = rkc.DeviceBatch(trace.desc, trace.events, trace.n_claim_slots, lim).replay().results()
     ora = oracle_mod.replay(trace.desc, trace.events, trace.n_claim_slots, threads=ORACLE_THREADS)
     compare_pools(trace, gpu, ora)
+
+
+@pytest.mark.parametrize("case", ["small", "random"])
+def test_general_kernel_on_compact_batches(oracle_mod, tg, case):
+    """Batches that the compact kernel serves, replayed with the general kernel forced by the batch
+    flag: both kernels match the oracle on the same inputs."""
+    import paper_2605_24259_amd as rkc
+    if case == "small":
+        trace = tg.generate("small", n_pools=512)
+    else:
+        trace = randtrace.random_batch(21, 600, U_range=(1, 120), n_events=(0, 300), n_chains=9,
+                                       p_malformed=0.01, tight_every=5, caps=(256, 64))
+    say(f"case general-kernel/{case}")
+    ora = oracle_mod.replay(trace.desc, trace.events, trace.n_claim_slots, threads=ORACLE_THREADS)
+    assert not ora[3].any()
+    gen = gpu_replay(trace, flags=rkc.FLAG_GENERAL_KERNEL)
+    compare_pools(trace, gen, ora)
+    lean = gpu_replay(trace)
+    compare_pools(trace, lean, ora)
