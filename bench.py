@@ -74,10 +74,10 @@ def cpu_baseline(trace, seconds_budget=12.0):
                        f"{threads} threads, {wall:.1f} s wall")
 
 
-def traffic_from_profiles(kernel_sha):
-    """HBM bytes per launch from committed rocprofv3 counter summaries, if they were taken on this
-    kernel source; else None."""
-    path = os.path.join(ROOT, "profiles", "rkc_replay_wave_zipf_traffic.json")
+def traffic_from_profiles(kernel, workload, kernel_sha):
+    """HBM bytes per launch from the committed rocprofv3 counter summary of this kernel and
+    workload, if it was taken on the current kernel sources; else None."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_traffic.json")
     if not os.path.exists(path):
         return None
     d = json.load(open(path))
@@ -86,10 +86,22 @@ def traffic_from_profiles(kernel_sha):
     return d.get("traffic_bytes_per_launch")
 
 
+def kernel_name(lim):
+    """Which replay kernel the library picks for these batch limits (the compact one when every
+    limit fits its 16-bit encoding)."""
+    fits = (lim["max_usable_blocks"] <= 32767 and lim["max_events"] <= 65533 and lim["max_chains"] <= 256
+            and lim["max_live_claims"] <= 64 and lim["max_live_requests"] <= 256
+            and lim["max_claim_slots"] <= 65534)
+    return "rkc_lean" if fits else "rkc_replay_wave"
+
+
 def kernel_source_sha():
+    """SHA-256 over the HIP sources of both replay kernels (the counters describe one build)."""
     import hashlib
-    src = os.path.join(ROOT, "paper_2605_24259_amd", "csrc", "rkc_replay.hip")
-    return hashlib.sha256(open(src, "rb").read()).hexdigest()
+    h = hashlib.sha256()
+    for f in ("rkc_replay.hip", "rkc_lean.hip"):
+        h.update(open(os.path.join(ROOT, "paper_2605_24259_amd", "csrc", f), "rb").read())
+    return h.hexdigest()
 
 
 def main():
@@ -178,11 +190,12 @@ def main():
             "pools": trace.n_pools, "usable_blocks": lim["max_usable_blocks"],
             "events_per_pool": lim["max_events"], "events_per_step": events,
             "claim_slots": trace.n_claim_slots, "parallelism": "one wavefront per pool",
+            "kernel": kernel_name(lim),
         },
         "roofline": {
             "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBPS, 4),
-            "traffic": traffic_from_profiles(kernel_source_sha()),
+            "traffic": traffic_from_profiles(kernel_name(lim), args.workload, kernel_source_sha()),
             "credited_bytes_per_launch": cbytes,
             "copy_ceiling_gbps": round(ceiling, 1),
             "frac_of_copy_ceiling": round(achieved / ceiling, 4),
