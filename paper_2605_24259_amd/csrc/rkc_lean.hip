@@ -238,44 +238,59 @@ struct Lean {
   }
 
   // Key of chain c's top run; advances a stale stack bottom (the node above it reaches n).
+  // (Control flow on the event path is written without early exits: the compiler's structurizer
+  // turns every break / early return into flow blocks with register copies paid by every event.)
   __device__ __forceinline__ u32 top_key(u32 c, G0& g) {
-    if (g.n <= max(g.hold, g.prot)) return KINF;
-    if (g.nx >= g.n) {
-      u32 b = g.sbot;
-      u32x2 nb = nget(b);
-      u32 up = lo16(nb.y), nxv = 0;
-      for (u32 guard = 0; guard < 0x10000u && up != NIL; guard++) {
-        const u32x2 nu = nget(up);
-        nxv = lo16(nu.x);
-        if (nxv < g.n) break;
-        // node b leaves the stack: free it; up becomes the bottom (its down link is cut)
-        nset_y(b, pk(NIL, fnode));
-        fnode = b;
-        b = up;
-        nb = nu;
-        up = lo16(nb.y);
-        nxv = 0;
+    u32 key = KINF;
+    if (g.n > max(g.hold, g.prot)) {
+      if (g.nx >= g.n) {
+        u32 b = g.sbot;
+        u32x2 nb = nget(b);
+        u32 up = lo16(nb.y), nxv = 0;
+        bool go = up != NIL;
+        for (u32 guard = 0; go && guard < 0x10000u; guard++) {
+          const u32x2 nu = nget(up);
+          nxv = lo16(nu.x);
+          if (nxv >= g.n) {
+            // node b leaves the stack: free it; up becomes the bottom (its down link is cut)
+            nset_y(b, pk(NIL, fnode));
+            fnode = b;
+            b = up;
+            nb = nu;
+            up = lo16(nb.y);
+            nxv = 0;
+            go = up != NIL;
+          } else {
+            go = false;
+          }
+        }
+        nset_y(b, pk(up, NIL));
+        g.sbot = b;
+        g.bt = hi16(nb.x);
+        g.nx = nxv;
       }
-      nset_y(b, pk(up, NIL));
-      g.sbot = b;
-      g.bt = hi16(nb.x);
-      g.nx = nxv;
+      // no claim reaches the top position unless covA >= n
+      const u32 lvl = (softl() && g.covA >= g.n) ? level_of(c, g.n - 1) : 0u;
+      key = (lvl << 25) | (g.bt << 9) | (c + 1);
     }
-    // no claim reaches the top position unless covA >= n
-    const u32 lvl = (softl() && g.covA >= g.n) ? level_of(c, g.n - 1) : 0u;
-    return (lvl << 25) | (g.bt << 9) | (c + 1);
+    return key;
   }
 
   // Record a touch of positions [0, x) of chain c at step t (x > 0).
   __device__ __forceinline__ void touch(G0& g, u32 x, u32 t) {
     u32 tp = g.stop, tpd = NIL;
-    for (u32 guard = 0; guard < 0x10000u && tp != NIL; guard++) {
+    bool go = tp != NIL;
+    for (u32 guard = 0; go && guard < 0x10000u; guard++) {
       const u32x2 nt = nget(tp);
       tpd = hi16(nt.y);
-      if (lo16(nt.x) > x) break;
-      nset_y(tp, pk(NIL, fnode));
-      fnode = tp;
-      tp = tpd;
+      if (lo16(nt.x) <= x) {
+        nset_y(tp, pk(NIL, fnode));
+        fnode = tp;
+        tp = tpd;
+        go = tp != NIL;
+      } else {
+        go = false;
+      }
     }
     const u32 nw = nalloc();
     nset(nw, u32x2{pk(x, t), pk(NIL, tp)});
@@ -370,12 +385,15 @@ struct Lean {
     qc = fail ? pk(m2, hi16(qc)) : qc;
     qf = fail ? pk(t, harm ? t : hi16(qf)) : qf;
     const u64 fm = ballot(fail), hmk = ballot(harm);
-    if (!fm) return 0;
-    const u32 pf = (u32)__builtin_popcountll(fm), hc = (u32)__builtin_popcountll(hmk);
-    tadd(TW_PREDFAIL, pf);
-    tadd(TW_HARM, hc);
-    recompute_lanes(fm);
-    return RKC_FL_PRED_FAIL | (hc ? (u32)RKC_FL_HARM : 0u);
+    u32 fl = 0;
+    if (fm) {
+      const u32 pf = (u32)__builtin_popcountll(fm), hc = (u32)__builtin_popcountll(hmk);
+      tadd(TW_PREDFAIL, pf);
+      tadd(TW_HARM, hc);
+      recompute_lanes(fm);
+      fl = RKC_FL_PRED_FAIL | (hc ? (u32)RKC_FL_HARM : 0u);
+    }
+    return fl;
   }
 
   __device__ __forceinline__ void fifo_pop() {
@@ -393,90 +411,93 @@ struct Lean {
     AllocRes r = {1, 0, 0, 0, 0, 0};
     if (need <= F) {
       F -= need;
-      return r;
-    }
-    u32 E = Eall + fbl;
-    u32 hlo = 0;  // candidates of chain hc start at hlo
-    if (hc >= 0) {
-      const u32 lo = max(ghc.hold, ghc.prot);
-      hlo = max(lo, h);
-      E -= evictable(ghc.n, lo, 0) - evictable(ghc.n, hlo, 0);
-    }
-    r.E = E;
-    if ((u64)need > (u64)F + E) {
-      r.ok = 0;
-      return r;
-    }
-    u32 K = need - F;
-    F = 0;
-    // the hit chain stops being a candidate once only hits remain
-    if (hc >= 0 && ghc.n <= hlo) kk[hc] = KINF;
-    for (u32 guard = 0; K > 0; guard++) {
-      if (guard > 0x10000u) { status |= 0x80000000u; break; }
-      u32 kmin;
-      if (NS == 4) {
-        const u32x4 k4 = ((lds_u32x4*)kk)[lane];
-        kmin = min(min(k4.x, k4.y), min(k4.z, k4.w));
-      } else if (NS == 2) {
-        const u32x2 k2 = ((lds_u32x2*)kk)[lane];
-        kmin = min(k2.x, k2.y);
-      } else {
-        kmin = kk[lane];
+    } else {
+      u32 E = Eall + fbl;
+      u32 hlo = 0;  // candidates of chain hc start at hlo
+      if (hc >= 0) {
+        const u32 lo = max(ghc.hold, ghc.prot);
+        hlo = max(lo, h);
+        E -= evictable(ghc.n, lo, 0) - evictable(ghc.n, hlo, 0);
       }
-      const u32 m1 = wmin(kmin);
-      const u32 kf = qh != qt ? (ft << 9) : KINF;
-      if (kf < m1) {
-        // the oldest finished request's private run (level 0)
-        const u32 m = min(K, ftop - flo);
-        ftop -= m;
-        fbl -= m;
-        r.victims += m;
-        r.unclaimed += m;
-        K -= m;
-        if (ftop == flo) fifo_pop();
+      r.E = E;
+      if ((u64)need > (u64)F + E) {
+        r.ok = 0;
       } else {
-        if (m1 == KINF) { status |= 0x80000000u; break; }
-        const u32 c = (m1 & 511u) - 1u;
-        G0 g = rd0(c);
-        const u32 nn = g.n;
-        u32 lo = max(g.hold, g.prot);
-        if ((i32)c == hc) lo = max(lo, h);
-        // the top run shares (level, last use): positions below nx were touched later, positions
-        // below a higher-level claim's footprint rank higher (only claims within covA matter)
-        u32 run_lo = max(lo, g.nx);
-        if (softl() && g.covA > run_lo) run_lo = max(run_lo, level_floor(c, m1 >> 25));
-        const u32 m = min(K, nn - run_lo);
-        const u32 nw = nn - m;
-        u32 rs = 0, sc = 0;
-        if (g.covA > nw) {
-          // victims inside live claims: resident; inside only demoted / expired ones: post-release
-          const u32 st = m_state(lo16(qc));
-          const bool on = on_chain(c);
-          const u32 covS = wmax((on && (st == ST_OBSERVED || st == ST_MATERIALIZED || st == ST_HARMED)) ? lo16(qb) : 0u);
-          rs = min(nn, g.covA) - nw;
-          sc = min(nn, covS) > nw ? min(nn, covS) - nw : 0u;
-          // a claim whose predicate still holds needs more than nw leading blocks
-          if (ballot(on && m_pend(lo16(qc)) && hi16(qb) > nw)) sweep_due = 1;
+        u32 K = need - F;
+        F = 0;
+        // the hit chain stops being a candidate once only hits remain
+        if (hc >= 0 && ghc.n <= hlo) kk[hc] = KINF;
+        for (u32 guard = 0; K > 0; guard++) {
+          u32 kmin;
+          if (NS == 4) {
+            const u32x4 k4 = ((lds_u32x4*)kk)[lane];
+            kmin = min(min(k4.x, k4.y), min(k4.z, k4.w));
+          } else if (NS == 2) {
+            const u32x2 k2 = ((lds_u32x2*)kk)[lane];
+            kmin = min(k2.x, k2.y);
+          } else {
+            kmin = kk[lane];
+          }
+          const u32 m1 = wmin(kmin);
+          const u32 kf = qh != qt ? (ft << 9) : KINF;
+          if (kf < m1) {
+            // the oldest finished request's private run (level 0)
+            const u32 m = min(K, ftop - flo);
+            ftop -= m;
+            fbl -= m;
+            r.victims += m;
+            r.unclaimed += m;
+            K -= m;
+            if (ftop == flo) fifo_pop();
+          } else if (m1 != KINF) {
+            const u32 c = (m1 & 511u) - 1u;
+            G0 g = rd0(c);
+            const u32 nn = g.n;
+            u32 lo = max(g.hold, g.prot);
+            if ((i32)c == hc) lo = max(lo, h);
+            // the top run shares (level, last use): positions below nx were touched later,
+            // positions below a higher-level claim's footprint rank higher (only claims within
+            // covA matter)
+            u32 run_lo = max(lo, g.nx);
+            if (softl() && g.covA > run_lo) run_lo = max(run_lo, level_floor(c, m1 >> 25));
+            const u32 m = min(K, nn - run_lo);
+            const u32 nw = nn - m;
+            u32 rs = 0, sc = 0;
+            if (g.covA > nw) {
+              // victims inside live claims: resident; inside only demoted / expired ones: post-release
+              const u32 st = m_state(lo16(qc));
+              const bool on = on_chain(c);
+              const u32 covS = wmax((on && (st == ST_OBSERVED || st == ST_MATERIALIZED || st == ST_HARMED)) ? lo16(qb) : 0u);
+              rs = min(nn, g.covA) - nw;
+              sc = min(nn, covS) > nw ? min(nn, covS) - nw : 0u;
+              // a claim whose predicate still holds needs more than nw leading blocks
+              if (ballot(on && m_pend(lo16(qc)) && hi16(qb) > nw)) sweep_due = 1;
+            }
+            r.victims += m;
+            r.resident += rs;
+            r.post += rs - sc;
+            r.unclaimed += m - rs;
+            Eall -= m;
+            g.n = nw;
+            K -= m;
+            u32 key = top_key(c, g);
+            if ((i32)c == hc && nw <= lo) key = KINF;
+            kk[c] = key;
+            wr0(c, g);
+          } else {
+            status |= 0x80000000u;  // cannot happen: feasibility was checked
+            K = 0;
+          }
+          if (guard > 0x10000u) { status |= 0x80000000u; K = 0; }
         }
-        r.victims += m;
-        r.resident += rs;
-        r.post += rs - sc;
-        r.unclaimed += m - rs;
-        Eall -= m;
-        g.n = nw;
-        K -= m;
-        u32 key = top_key(c, g);
-        if ((i32)c == hc && nw <= lo) key = KINF;
-        kk[c] = key;
-        wr0(c, g);
       }
     }
     return r;
   }
 
   // Refusal record of an active event that cannot be served (§3.4; §5.4 refusal record).
-  __device__ __forceinline__ void refusal(u32 need, i32 hc, u32 h, u32 Hc, const G0& ghc, u32& code,
-                                          i32& id, i32& a, i32& b, u32& n16) {
+  struct Out;
+  __device__ __forceinline__ void refusal(u32 need, i32 hc, u32 h, u32 Hc, const G0& ghc, Out& o) {
     u32 Pr = PR;
     if (hardm() && hc >= 0) {
       const u32 p = min(ghc.prot, h);
@@ -484,7 +505,7 @@ struct Lean {
     }
     const u64 req = (u64)A + Hc + need;
     if (Pr > 0 && req <= U()) {
-      code = RKC_OC_REFUSED_CLAIM;
+      o.code = RKC_OC_REFUSED_CLAIM;
       const u32 m = lo16(qc), c = hi16(qa);
       u32 cov = chain_hold(c);
       if ((i32)c == hc) cov = max(cov, h);
@@ -492,21 +513,21 @@ struct Lean {
                        lo16(qb) > cov;
       qd += blk ? (1u << 16) : 0u;
       const u64 bm = ballot(blk);
-      id = (i32)wmin(blk ? lo16(qa) : NEVER);
-      n16 = min((u32)__builtin_popcountll(bm), 65535u);
+      o.id = (i32)wmin(blk ? lo16(qa) : NEVER);
+      o.n16 = min((u32)__builtin_popcountll(bm), 65535u);
     } else {
-      code = RKC_OC_REFUSED_CAPACITY;
-      id = -1;
-      n16 = 0;
+      o.code = RKC_OC_REFUSED_CAPACITY;
+      o.id = -1;
+      o.n16 = 0;
     }
-    a = (i32)Pr;
-    b = (i32)req;
+    o.a = (i32)Pr;
+    o.b = (i32)req;
   }
 
-  __device__ __forceinline__ void served(const AllocRes& r, u32& code, u32& flags, i32& a) {
-    code = r.resident ? RKC_OC_EVICT_RESIDENT : RKC_OC_ADMIT;
-    a = (i32)r.resident;
-    flags |= (r.post ? (u32)RKC_FL_POST_RELEASE_LOSS : 0u) | (r.unclaimed ? (u32)RKC_FL_EVICT_UNCLAIMED : 0u);
+  __device__ __forceinline__ void served(const AllocRes& r, Out& o) {
+    o.code = r.resident ? RKC_OC_EVICT_RESIDENT : RKC_OC_ADMIT;
+    o.a = (i32)r.resident;
+    o.flags |= (r.post ? (u32)RKC_FL_POST_RELEASE_LOSS : 0u) | (r.unclaimed ? (u32)RKC_FL_EVICT_UNCLAIMED : 0u);
     vic += r.victims;
     post += r.post;
   }
@@ -533,34 +554,35 @@ struct Lean {
     return wmax(hv);
   }
 
-  // One event; returns the outcome words through o.
-  __device__ __forceinline__ void step(u32 t, u32 w0, u32 w1, u32 w2, u32 w3, u32& o0, i32& o1, i32& o2, i32& o3) {
-    const u32 type = w0 & 15u;
-    u32 flags = 0, expired = 0, n16 = NEVER, sweep_due = 0;
-    u32 code = RKC_OC_NOOP;
-    i32 id = -1, a = 0, b = 0;
-    if (t >= nexp) expire(t, flags, expired);
+  // ---- event handlers: each fills the outcome fields; no early exits (see top_key) ----
+  struct Out {
+    u32 code, flags, n16, sweep_due;
+    i32 id, a, b;
+  };
+
+  __device__ __forceinline__ void ev_prefill(u32 t, u32 w1, u32 w2, u32 w3, Out& o) {
     const i32 s1 = (i32)w1, s2 = (i32)w2, s3 = (i32)w3;
-    switch (type) {
-      case RKC_EV_PREFILL: {
-        if (s1 < 1 || s1 > RKC_MAX_FIELD_BLOCKS || s3 < 0 || s3 > s1 || (s3 > 0 && (s2 < 0 || w2 >= nch()))) {
-          code = RKC_OC_INVALID;
-          break;
-        }
-        if (nreq >= maxr()) { code = RKC_OC_INVALID; status |= RKC_PS_REQUEST_TABLE; break; }
-        const u32 S = w1, P = w3;
-        i32 hc = -1;
-        u32 h = 0, Hc = 0;
-        G0 g = {0, 0, 0, 0, 0, 0, 0, 0};
-        if (P > 0) {
-          hc = (i32)w2;
-          g = rd0(w2);
-          h = min(P, g.n);
-          Hc = h > g.hold ? h - g.hold : 0u;
-        }
-        const u32 need = S - h;
-        const AllocRes r = alloc(need, hc, h, g, sweep_due);
-        if (!r.ok) { refusal(need, hc, h, Hc, g, code, id, a, b, n16); break; }
+    if (s1 < 1 || s1 > RKC_MAX_FIELD_BLOCKS || s3 < 0 || s3 > s1 || (s3 > 0 && (s2 < 0 || w2 >= nch()))) {
+      o.code = RKC_OC_INVALID;
+    } else if (nreq >= maxr()) {
+      o.code = RKC_OC_INVALID;
+      status |= RKC_PS_REQUEST_TABLE;
+    } else {
+      const u32 S = w1, P = w3;
+      i32 hc = -1;
+      u32 h = 0, Hc = 0;
+      G0 g = {0, 0, 0, 0, 0, 0, 0, 0};
+      if (P > 0) {
+        hc = (i32)w2;
+        g = rd0(w2);
+        h = min(P, g.n);
+        Hc = h > g.hold ? h - g.hold : 0u;
+      }
+      const u32 need = S - h;
+      const AllocRes r = alloc(need, hc, h, g, o.sweep_due);
+      if (!r.ok) {
+        refusal(need, hc, h, Hc, g, o);
+      } else {
         A += Hc + need;
         u32 R = 0;
         if (hc >= 0) {
@@ -571,169 +593,192 @@ struct Lean {
         }
         rq[nreq] = u32x2{pk(t, hc >= 0 ? w2 : NIL), pk(R, S)};
         nreq++;
-        id = (i32)t;
-        b = (i32)h;
-        served(r, code, flags, a);
-        break;
+        o.id = (i32)t;
+        o.b = (i32)h;
+        served(r, o);
       }
-      case RKC_EV_EXTEND: {
-        if (s1 < 1 || s1 > RKC_MAX_FIELD_BLOCKS) { code = RKC_OC_INVALID; break; }
-        if (nreq == 0) break;
-        const u32 i = w2 % nreq, need = w1;
-        const G0 g = {0, 0, 0, 0, 0, 0, 0, 0};
-        const AllocRes r = alloc(need, -1, 0, g, sweep_due);
-        if (!r.ok) { refusal(need, -1, 0, 0, g, code, id, a, b, n16); break; }
+    }
+  }
+
+  __device__ __forceinline__ void ev_extend(u32 w1, u32 w2, Out& o) {
+    const i32 s1 = (i32)w1;
+    if (s1 < 1 || s1 > RKC_MAX_FIELD_BLOCKS) {
+      o.code = RKC_OC_INVALID;
+    } else if (nreq > 0) {
+      const u32 i = w2 % nreq, need = w1;
+      const G0 g = {0, 0, 0, 0, 0, 0, 0, 0};
+      const AllocRes r = alloc(need, -1, 0, g, o.sweep_due);
+      if (!r.ok) {
+        refusal(need, -1, 0, 0, g, o);
+      } else {
         A += need;
         u32x2 e = rq[i];
         e.x = ufl(e.x); e.y = ufl(e.y);
         rq[i] = u32x2{e.x, pk(lo16(e.y), hi16(e.y) + need)};
-        id = (i32)lo16(e.x);
-        b = (i32)A;
-        served(r, code, flags, a);
-        break;
+        o.id = (i32)lo16(e.x);
+        o.b = (i32)A;
+        served(r, o);
       }
-      case RKC_EV_CLAIM: {
-        if (nslot >= nslots()) { code = RKC_OC_INVALID; status |= RKC_PS_SLOT_TABLE; break; }
-        const u32 s = nslot++;
-        bool ok = !(s1 < 1 || s1 > RKC_MAX_FIELD_BLOCKS || s2 < 0 || w2 >= nch() || s3 < 0 || s3 > s1);
-        if (ok && ncl >= maxq()) { status |= RKC_PS_CLAIM_TABLE; ok = false; }
-        slotcl[s] = ok ? make_uint2(w2, w1) : make_uint2(NEVER, 0);  // every lane, one value
-        if (!ok) {
-          write_record(s, (i32)t, 0, -1, -1, -1, -1, -1, -1, 0);
-          code = RKC_OC_INVALID;
-          break;
-        }
+    }
+  }
+
+  __device__ __forceinline__ void ev_claim(u32 t, u32 w0, u32 w1, u32 w2, u32 w3, Out& o) {
+    const i32 s1 = (i32)w1, s2 = (i32)w2, s3 = (i32)w3;
+    if (nslot >= nslots()) {
+      o.code = RKC_OC_INVALID;
+      status |= RKC_PS_SLOT_TABLE;
+    } else {
+      const u32 s = nslot++;
+      bool ok = !(s1 < 1 || s1 > RKC_MAX_FIELD_BLOCKS || s2 < 0 || w2 >= nch() || s3 < 0 || s3 > s1);
+      if (ok && ncl >= maxq()) { status |= RKC_PS_CLAIM_TABLE; ok = false; }
+      slotcl[s] = ok ? make_uint2(w2, w1) : make_uint2(NEVER, 0);  // every lane, one value
+      if (!ok) {
+        write_record(s, (i32)t, 0, -1, -1, -1, -1, -1, -1, 0);
+        o.code = RKC_OC_INVALID;
+      } else {
         const u32 L = w1, c = w2, T = w3;
         const u32 hardq = (w0 >> 4) & 1u, prio = (w0 >> 5) & 3u, dur = w0 >> 16;
         const G0 g = rd0(c);
         const u32 h = min(L, g.n), need = L - h;
-        const AllocRes r = alloc(need, (i32)c, h, g, sweep_due);
+        const AllocRes r = alloc(need, (i32)c, h, g, o.sweep_due);
         const u32 eff = hardm() ? (hardq ? RKC_PROT_HARD : RKC_PROT_SOFT) : (mode == RKC_MODE_SOFT ? RKC_PROT_SOFT : RKC_PROT_NONE);
         if (!r.ok) {
           const u32 dec = shadm() ? DEC_SHADOW : DEC_REJECTED;
           const u32 m = ST_REJECTED | (eff << 3) | (hardq << 5) | (prio << 6) | (dec << 9);
           write_record(s, (i32)t, packed_of(m), -1, -1, -1, -1, -1, -1, 0);
-          code = RKC_OC_MATFAIL;
-          id = (i32)t;
-          a = (i32)need;
-          b = (i32)(F + r.E);
+          o.code = RKC_OC_MATFAIL;
+          o.id = (i32)t;
+          o.a = (i32)need;
+          o.b = (i32)(F + r.E);
           tadd(TW_ACCEPTED + dec - DEC_ACCEPTED, 1);
-          break;
-        }
-        const u32 lowered = (mode == RKC_MODE_SOFT) && hardq;
-        const u32 dec = shadm() ? DEC_SHADOW : lowered ? DEC_APPROX : DEC_ACCEPTED;
-        const u32 st = shadm() ? ST_OBSERVED : ST_MATERIALIZED;
-        flags |= shadm() ? (u32)RKC_FL_SHADOW : lowered ? (u32)RKC_FL_LOWERED : 0u;
-        const u32 m = st | (eff << 3) | (hardq << 5) | (prio << 6) | (1u << 8) | (dec << 9);
-        const u32 dur_eff = shadm() ? 0u : dur;  // shadow claims never expire
-        const u32 k = ncl++;
-        qa = wrl(qa, pk(t, c), k);
-        qb = wrl(qb, pk(L, T), k);
-        qc = wrl(qc, pk(m, s), k);
-        qd = wrl(qd, dur_eff, k);
-        qe = wrl(qe, 0xFFFFFFFFu, k);
-        qf = wrl(qf, 0xFFFFFFFFu, k);
-        if (dur_eff > 0) nexp = min(nexp, t + dur_eff);
-        G0 g2 = r.victims ? rd0(c) : g;
-        g2.covA = max(g2.covA, L);
-        // a materialized hard claim in a hard-protection pool protects [0, L)
-        const u32 pp = (hardm() && hardq) ? max(g2.prot, L) : g2.prot;
-        commit(c, g2, max(g2.n, L), g2.hold, pp, L, t);
-        id = (i32)t;
-        b = (i32)need;
-        served(r, code, flags, a);
-        tadd(TW_ACCEPTED + dec - DEC_ACCEPTED, 1);
-        break;
-      }
-      case RKC_EV_FINISH: {
-        if (nreq == 0) break;
-        const u32 i = w1 % nreq;
-        u32x2 e = rq[i];
-        e.x = ufl(e.x); e.y = ufl(e.y);
-        const u32 rid = lo16(e.x), c = hi16(e.x), R = lo16(e.y), len = hi16(e.y);
-        rq_remove(i, nreq);
-        nreq--;
-        u32 turned = 0;
-        if (c != NIL) {
-          const u32 hn = rq_hold(c, nreq);
-          turned += R > hn ? R - hn : 0u;
-          const G0 g = rd0(c);
-          commit(c, g, g.n, hn, g.prot, R, t);
-        }
-        // write no-admit drops the request's own blocks; otherwise they become a private run
-        const u32 own = len - R;
-        const u32 dropped = noadm() ? own : 0u;
-        const u32 kept = own - dropped;
-        turned += kept;
-        F += dropped;
-        fbl += kept;
-        if (kept > 0) {
-          if (qh == qt) { ft = t; flo = R; ftop = len; }
-          fifo[qt] = make_uint4(t, R, len, 0);  // every lane, one value
-          qt++;
-        }
-        A -= turned + dropped;
-        code = RKC_OC_FINISHED;
-        id = (i32)rid;
-        a = (i32)turned;
-        b = (i32)dropped;
-        if (dropped) flags |= RKC_FL_NOADMIT_DROP;
-        tadd(TW_DROPPED, dropped);
-        break;
-      }
-      case RKC_EV_RELEASE:
-      case RKC_EV_DEMOTE: {
-        u32 i = NEVER;
-        if (type == RKC_EV_RELEASE) {
-          if (ncl > 0) i = w1 % ncl;
-        } else if (softl()) {
-          const u32 m = lo16(qc);
-          const u64 cm = ballot(lane < ncl && m_state(m) == ST_MATERIALIZED && m_hard(m));
-          const u32 cnt = (u32)__builtin_popcountll(cm);
-          if (cnt > 0) {
-            const u32 k = w1 % cnt;
-            const u32 rank = __builtin_amdgcn_mbcnt_hi((u32)(cm >> 32), __builtin_amdgcn_mbcnt_lo((u32)cm, 0u));
-            i = (u32)__builtin_ctzll(ballot(((cm >> lane) & 1ull) && rank == k));
-          }
-        }
-        if (i == NEVER) break;
-        const u32 qid = lo16(rdl(qa, i)), c = hi16(rdl(qa, i));
-        const u32 qbv = rdl(qb, i);
-        if (type == RKC_EV_RELEASE) {
-          if (lane == i) write_own_record(ST_RELEASED, (i32)t);
-          // close the gap: lanes >= i take their upper neighbour's claim
-          const bool up = lane >= i;
-          qa = up ? shift_down(qa) : qa; qb = up ? shift_down(qb) : qb; qc = up ? shift_down(qc) : qc;
-          qd = up ? shift_down(qd) : qd; qe = up ? shift_down(qe) : qe; qf = up ? shift_down(qf) : qf;
-          ncl--;
-          code = RKC_OC_RELEASED;
-          tadd(TW_RELEASED, 1);
         } else {
-          const bool me = lane == i;
-          qc = me ? pk((lo16(qc) & ~7u) | ST_DEMOTED, hi16(qc)) : qc;
-          qe = me ? pk(t, hi16(qe)) : qe;
-          code = RKC_OC_DEMOTED;
-          tadd(TW_DEMOTED, 1);
+          const u32 lowered = (mode == RKC_MODE_SOFT) && hardq;
+          const u32 dec = shadm() ? DEC_SHADOW : lowered ? DEC_APPROX : DEC_ACCEPTED;
+          const u32 st = shadm() ? ST_OBSERVED : ST_MATERIALIZED;
+          o.flags |= shadm() ? (u32)RKC_FL_SHADOW : lowered ? (u32)RKC_FL_LOWERED : 0u;
+          const u32 m = st | (eff << 3) | (hardq << 5) | (prio << 6) | (1u << 8) | (dec << 9);
+          const u32 dur_eff = shadm() ? 0u : dur;  // shadow claims never expire
+          const u32 k = ncl++;
+          qa = wrl(qa, pk(t, c), k);
+          qb = wrl(qb, pk(L, T), k);
+          qc = wrl(qc, pk(m, s), k);
+          qd = wrl(qd, dur_eff, k);
+          qe = wrl(qe, 0xFFFFFFFFu, k);
+          qf = wrl(qf, 0xFFFFFFFFu, k);
+          if (dur_eff > 0) nexp = min(nexp, t + dur_eff);
+          G0 g2 = r.victims ? rd0(c) : g;
+          g2.covA = max(g2.covA, L);
+          // a materialized hard claim in a hard-protection pool protects [0, L)
+          const u32 pp = (hardm() && hardq) ? max(g2.prot, L) : g2.prot;
+          commit(c, g2, max(g2.n, L), g2.hold, pp, L, t);
+          o.id = (i32)t;
+          o.b = (i32)need;
+          served(r, o);
+          tadd(TW_ACCEPTED + dec - DEC_ACCEPTED, 1);
         }
-        recompute(c);
-        const u32 nc = ufl(chain_n(c));
-        id = (i32)qid;
-        a = (i32)min(nc, lo16(qbv));
-        b = (i32)hi16(qbv);
-        break;
       }
-      case RKC_EV_NOP:
-        break;
-      default:
-        code = RKC_OC_INVALID;
-        break;
     }
-    if (sweep_due) flags |= sweep(t);
-    const bool quiet = code == RKC_OC_NOOP || code == RKC_OC_INVALID;
-    o0 = code | (flags << 8) | ((n16 == NEVER ? min(expired, 65535u) : n16) << 16);
-    o1 = quiet ? -1 : id;
-    o2 = quiet ? 0 : a;
-    o3 = quiet ? 0 : b;
+  }
+
+  __device__ __forceinline__ void ev_finish(u32 t, u32 w1, Out& o) {
+    if (nreq > 0) {
+      const u32 i = w1 % nreq;
+      u32x2 e = rq[i];
+      e.x = ufl(e.x); e.y = ufl(e.y);
+      const u32 rid = lo16(e.x), c = hi16(e.x), R = lo16(e.y), len = hi16(e.y);
+      rq_remove(i, nreq);
+      nreq--;
+      u32 turned = 0;
+      if (c != NIL) {
+        const u32 hn = rq_hold(c, nreq);
+        turned += R > hn ? R - hn : 0u;
+        const G0 g = rd0(c);
+        commit(c, g, g.n, hn, g.prot, R, t);
+      }
+      // write no-admit drops the request's own blocks; otherwise they become a private run
+      const u32 own = len - R;
+      const u32 dropped = noadm() ? own : 0u;
+      const u32 kept = own - dropped;
+      turned += kept;
+      F += dropped;
+      fbl += kept;
+      if (kept > 0) {
+        if (qh == qt) { ft = t; flo = R; ftop = len; }
+        fifo[qt] = make_uint4(t, R, len, 0);  // every lane, one value
+        qt++;
+      }
+      A -= turned + dropped;
+      o.code = RKC_OC_FINISHED;
+      o.id = (i32)rid;
+      o.a = (i32)turned;
+      o.b = (i32)dropped;
+      if (dropped) o.flags |= RKC_FL_NOADMIT_DROP;
+      tadd(TW_DROPPED, dropped);
+    }
+  }
+
+  // RELEASE (the selected live claim) or DEMOTE (the selected materialized hard-requested claim,
+  // hard -> soft; soft and hard pools only)
+  __device__ __forceinline__ void ev_lifecycle(u32 t, u32 type, u32 w1, Out& o) {
+    u32 i = NEVER;
+    if (type == RKC_EV_RELEASE) {
+      if (ncl > 0) i = w1 % ncl;
+    } else if (softl()) {
+      const u32 m = lo16(qc);
+      const u64 cm = ballot(lane < ncl && m_state(m) == ST_MATERIALIZED && m_hard(m));
+      const u32 cnt = (u32)__builtin_popcountll(cm);
+      if (cnt > 0) {
+        const u32 k = w1 % cnt;
+        const u32 rank = __builtin_amdgcn_mbcnt_hi((u32)(cm >> 32), __builtin_amdgcn_mbcnt_lo((u32)cm, 0u));
+        i = (u32)__builtin_ctzll(ballot(((cm >> lane) & 1ull) && rank == k));
+      }
+    }
+    if (i != NEVER) {
+      const u32 qid = lo16(rdl(qa, i)), c = hi16(rdl(qa, i));
+      const u32 qbv = rdl(qb, i);
+      if (type == RKC_EV_RELEASE) {
+        if (lane == i) write_own_record(ST_RELEASED, (i32)t);
+        // close the gap: lanes >= i take their upper neighbour's claim
+        const bool up = lane >= i;
+        qa = up ? shift_down(qa) : qa; qb = up ? shift_down(qb) : qb; qc = up ? shift_down(qc) : qc;
+        qd = up ? shift_down(qd) : qd; qe = up ? shift_down(qe) : qe; qf = up ? shift_down(qf) : qf;
+        ncl--;
+        o.code = RKC_OC_RELEASED;
+        tadd(TW_RELEASED, 1);
+      } else {
+        const bool me = lane == i;
+        qc = me ? pk((lo16(qc) & ~7u) | ST_DEMOTED, hi16(qc)) : qc;
+        qe = me ? pk(t, hi16(qe)) : qe;
+        o.code = RKC_OC_DEMOTED;
+        tadd(TW_DEMOTED, 1);
+      }
+      recompute(c);
+      const u32 nc = ufl(chain_n(c));
+      o.id = (i32)qid;
+      o.a = (i32)min(nc, lo16(qbv));
+      o.b = (i32)hi16(qbv);
+    }
+  }
+
+  // One event; returns the outcome words.  Dispatch is an if / else chain in order of how often
+  // the event types occur in the benchmark mixes.
+  __device__ __forceinline__ void step(u32 t, u32 w0, u32 w1, u32 w2, u32 w3, u32& o0, i32& o1, i32& o2, i32& o3) {
+    const u32 type = w0 & 15u;
+    u32 expired = 0;
+    Out o = {RKC_OC_NOOP, 0, NEVER, 0, -1, 0, 0};
+    if (t >= nexp) expire(t, o.flags, expired);
+    if (type == RKC_EV_PREFILL) ev_prefill(t, w1, w2, w3, o);
+    else if (type == RKC_EV_EXTEND) ev_extend(w1, w2, o);
+    else if (type == RKC_EV_CLAIM) ev_claim(t, w0, w1, w2, w3, o);
+    else if (type == RKC_EV_FINISH) ev_finish(t, w1, o);
+    else if (type == RKC_EV_RELEASE || type == RKC_EV_DEMOTE) ev_lifecycle(t, type, w1, o);
+    else if (type != RKC_EV_NOP) o.code = RKC_OC_INVALID;
+    if (o.sweep_due) o.flags |= sweep(t);
+    const bool quiet = o.code == RKC_OC_NOOP || o.code == RKC_OC_INVALID;
+    o0 = o.code | (o.flags << 8) | ((o.n16 == NEVER ? min(expired, 65535u) : o.n16) << 16);
+    o1 = quiet ? -1 : o.id;
+    o2 = quiet ? 0 : o.a;
+    o3 = quiet ? 0 : o.b;
     peak = max(peak, A);
   }
 };
