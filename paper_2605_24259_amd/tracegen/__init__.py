@@ -184,6 +184,31 @@ class Trace:
         t.meta["source_slot_offsets"] = [int(co[p]) for p in pools]
         return t
 
+    def prefix(self, pools, n_events: int) -> "Trace":
+        """A new batch of the given pools, each cut to its first n_events events (claim slots cut to
+        the CLAIM events kept).  Replay is causal, so the outcomes of a prefix equal the leading
+        outcomes of the full pool."""
+        sub = self.subset(pools)
+        ne = sub.field("n_events")
+        eo = sub.field("event_offset")
+        evs, rows, e_acc, s_acc = [], [], 0, 0
+        for j in range(sub.n_pools):
+            k = int(min(ne[j], n_events))
+            ev = sub.events[eo[j]: eo[j] + k]
+            row = sub.desc[j].copy()
+            n_sl = int(np.sum((ev[:, 0] & 15) == EV_CLAIM))
+            row[2] = k
+            row[6] = n_sl
+            row[8:10] = np.array([e_acc], np.int64).view(np.int32)
+            row[10:12] = np.array([s_acc], np.int64).view(np.int32)
+            rows.append(row)
+            evs.append(ev)
+            e_acc += k
+            s_acc += n_sl
+        desc = np.stack(rows) if rows else np.zeros((0, 12), np.int32)
+        events = np.concatenate(evs) if evs else np.zeros((0, 4), np.int32)
+        return Trace(desc, np.ascontiguousarray(events), s_acc, self.name + "[prefix]", dict(sub.meta))
+
     def sha256(self) -> str:
         h = hashlib.sha256()
         h.update(np.ascontiguousarray(self.desc).tobytes())

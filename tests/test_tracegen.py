@@ -66,3 +66,20 @@ def test_probe_layout(tg):
     assert t.n_pools == 4 and t.n_events == 8 and t.n_claim_slots == 4
     assert list(t.field("mode")) == [0, 1, 2, 3]
     assert list(t.field("usable_blocks")) == [80] * 4
+
+
+def test_prefix_replay_is_the_leading_part_of_the_full_replay(oracle_mod, tg):
+    """Trace.prefix keeps each pool's first events (and the CLAIM slots among them); replay is
+    causal, so the oracle's outcomes on the prefix equal the leading outcomes of the full pool."""
+    import numpy as np
+    t = tg.generate("small", n_pools=6)
+    full = oracle_mod.replay(t.desc, t.events, t.n_claim_slots)
+    eo = t.field("event_offset")
+    for k in (0, 1, 17, 100, 256):
+        p = t.prefix([0, 2, 5], k)
+        assert p.n_events == 3 * k
+        assert p.n_claim_slots == int(sum(((t.events[eo[i]: eo[i] + k, 0] & 15) == 2).sum() for i in (0, 2, 5)))
+        out = oracle_mod.replay(p.desc, p.events, p.n_claim_slots)
+        assert not out[3].any()
+        for j, i in enumerate((0, 2, 5)):
+            assert np.array_equal(out[0][j * k:(j + 1) * k], full[0][eo[i]: eo[i] + k])
