@@ -85,7 +85,7 @@ CONFIGS = {
                    prefill_max=8192,
                    chain_pick=2, n_chains=64, chain_len_min=4096, chain_len_max=4096,
                    claim_len=2, claim_len_min=64, claim_len_max=4096, claim_thresh=1,
-                   hard_permille=500, prio_max=3, dur_min=128, dur_max=1024, extend_k=1,
+                   hard_permille=500, prio_max=3, dur_min=128, dur_max=1024, extend_k=152,
                    claim_cap=0, max_live_claims=256, max_live_requests=256),
     "huge": dict(cfg_id=5, n_pools=64, usable_blocks=262144, n_events=65536,
                  mix=(400, 300, 150, 100, 50, 0), prefill_dist=1, prefill_min=4,

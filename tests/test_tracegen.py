@@ -83,3 +83,16 @@ def test_prefix_replay_is_the_leading_part_of_the_full_replay(oracle_mod, tg):
         assert not out[3].any()
         for j, i in enumerate((0, 2, 5)):
             assert np.array_equal(out[0][j * k:(j + 1) * k], full[0][eo[i]: eo[i] + k])
+
+
+def test_nested_active_load_is_calibrated(oracle_mod, tg):
+    """The nested workload's frozen extend size (tests/calibrate_nested.py) makes about 30 % of all
+    steps active refusals; on the first 64 pools the share is within sampling noise of that."""
+    import numpy as np
+    t = tg.generate("nested", n_pools=64)
+    assert t.meta["params"]["extend_k"] == 152
+    out = oracle_mod.replay(t.desc, t.events, t.n_claim_slots, threads=8)
+    assert not out[3].any()
+    code = out[0][:, 0] & 255
+    share = float(np.mean((code == 2) | (code == 3)))
+    assert 0.28 <= share <= 0.32, share
