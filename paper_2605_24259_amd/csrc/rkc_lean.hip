@@ -156,11 +156,26 @@ struct Lean {
   u32 tv;  // pool telemetry word `lane` (lanes 0..31)
   // scalars
   u32 F, A, PR, peak, Eall, fbl;
-  u32 nreq, ncl, nslot, nexp;
-  u32 fnode, bump;              // node free list, bump allocator
-  u32 qh, qt, ft, flo, ftop;    // FIFO of private runs: head, tail, front run
-  u32 vic, post;
-  u32 status;
+  u32 nreq, ncl, nexp;
+  // Scalars that only a few paths touch live in LDS (`cold`), so that the registers carried around
+  // the event loop are the hot counters only: node free list and bump allocator, the FIFO of
+  // private runs (head, tail, front run), claim slots used, victim counters and the status word.
+  lds_u32* cold;
+  // (QH..FLO is one 16-byte group and VIC, POST one 8-byte group: keep their word offsets aligned)
+  enum : u32 { C_QH = 0, C_QT, C_FT, C_FLO, C_FTOP, C_FNODE, C_BUMP, C_NSLOT, C_VIC, C_POST, C_STATUS, C_WORDS };
+  u32 fnode, bump;              // valid between cold_nodes_in() and cold_nodes_out()
+  u32 qh, qt, ft, flo, ftop;    // valid between cold_fifo_in() and cold_fifo_out()
+  __device__ __forceinline__ void cold_nodes_in() { fnode = ufl(cold[C_FNODE]); bump = ufl(cold[C_BUMP]); }
+  __device__ __forceinline__ void cold_nodes_out() { cold[C_FNODE] = fnode; cold[C_BUMP] = bump; }
+  __device__ __forceinline__ void cold_fifo_in() {
+    const u32x4 v = *(lds_u32x4*)(cold + C_QH);  // QH, QT, FT, FLO
+    qh = ufl(v.x); qt = ufl(v.y); ft = ufl(v.z); flo = ufl(v.w); ftop = ufl(cold[C_FTOP]);
+  }
+  __device__ __forceinline__ void cold_fifo_out() {
+    *(lds_u32x4*)(cold + C_QH) = u32x4{qh, qt, ft, flo};
+    cold[C_FTOP] = ftop;
+  }
+  __device__ __forceinline__ void set_status(u32 bits) { cold[C_STATUS] = ufl(cold[C_STATUS]) | bits; }
 
   // -- telemetry: word w lives in lane w of tv.  The word index is made opaque here so that the
   //    lane comparison is done where it is used, instead of being hoisted out of the event loop as
@@ -205,7 +220,7 @@ struct Lean {
     } else if (bump < ncap()) {
       i = bump++;
     } else {
-      status |= 0x80000000u;  // cannot happen: one node per touch, at most node cap - 2 touches
+      set_status(0x80000000u);  // cannot happen: one node per touch, at most node cap - 2 touches
       i = 0;
     }
     return i;
@@ -311,8 +326,10 @@ struct Lean {
     Eall += evictable(nn, hh, pp) - evictable(g.n, g.hold, g.prot);
     PR += protd(hh, pp) - protd(g.hold, g.prot);
     g.n = nn; g.hold = hh; g.prot = pp;
+    cold_nodes_in();
     if (x) touch(g, x, t);
     kk[c] = top_key(c, g);
+    cold_nodes_out();
     wr0(c, g);
   }
 
@@ -425,6 +442,8 @@ struct Lean {
       } else {
         u32 K = need - F;
         F = 0;
+        cold_fifo_in();
+        cold_nodes_in();
         // the hit chain stops being a candidate once only hits remain
         if (hc >= 0 && ghc.n <= hlo) kk[hc] = KINF;
         for (u32 guard = 0; K > 0; guard++) {
@@ -485,11 +504,13 @@ struct Lean {
             kk[c] = key;
             wr0(c, g);
           } else {
-            status |= 0x80000000u;  // cannot happen: feasibility was checked
+            set_status(0x80000000u);  // cannot happen: feasibility was checked
             K = 0;
           }
-          if (guard > 0x10000u) { status |= 0x80000000u; K = 0; }
+          if (guard > 0x10000u) { set_status(0x80000000u); K = 0; }
         }
+        cold_fifo_out();
+        cold_nodes_out();
       }
     }
     return r;
@@ -528,8 +549,10 @@ struct Lean {
     o.code = r.resident ? RKC_OC_EVICT_RESIDENT : RKC_OC_ADMIT;
     o.a = (i32)r.resident;
     o.flags |= (r.post ? (u32)RKC_FL_POST_RELEASE_LOSS : 0u) | (r.unclaimed ? (u32)RKC_FL_EVICT_UNCLAIMED : 0u);
-    vic += r.victims;
-    post += r.post;
+    if (r.victims) {
+      const u32x2 vp = *(lds_u32x2*)(cold + C_VIC);
+      *(lds_u32x2*)(cold + C_VIC) = u32x2{ufl(vp.x) + r.victims, ufl(vp.y) + r.post};
+    }
   }
 
   // Remove request entry i from the compact list of n entries (n <= 256).
@@ -566,7 +589,7 @@ struct Lean {
       o.code = RKC_OC_INVALID;
     } else if (nreq >= maxr()) {
       o.code = RKC_OC_INVALID;
-      status |= RKC_PS_REQUEST_TABLE;
+      set_status(RKC_PS_REQUEST_TABLE);
     } else {
       const u32 S = w1, P = w3;
       i32 hc = -1;
@@ -624,13 +647,15 @@ struct Lean {
 
   __device__ __forceinline__ void ev_claim(u32 t, u32 w0, u32 w1, u32 w2, u32 w3, Out& o) {
     const i32 s1 = (i32)w1, s2 = (i32)w2, s3 = (i32)w3;
+    const u32 nslot = ufl(cold[C_NSLOT]);
     if (nslot >= nslots()) {
       o.code = RKC_OC_INVALID;
-      status |= RKC_PS_SLOT_TABLE;
+      set_status(RKC_PS_SLOT_TABLE);
     } else {
-      const u32 s = nslot++;
+      const u32 s = nslot;
+      cold[C_NSLOT] = nslot + 1;
       bool ok = !(s1 < 1 || s1 > RKC_MAX_FIELD_BLOCKS || s2 < 0 || w2 >= nch() || s3 < 0 || s3 > s1);
-      if (ok && ncl >= maxq()) { status |= RKC_PS_CLAIM_TABLE; ok = false; }
+      if (ok && ncl >= maxq()) { set_status(RKC_PS_CLAIM_TABLE); ok = false; }
       slotcl[s] = ok ? make_uint2(w2, w1) : make_uint2(NEVER, 0);  // every lane, one value
       if (!ok) {
         write_record(s, (i32)t, 0, -1, -1, -1, -1, -1, -1, 0);
@@ -703,9 +728,11 @@ struct Lean {
       F += dropped;
       fbl += kept;
       if (kept > 0) {
+        cold_fifo_in();
         if (qh == qt) { ft = t; flo = R; ftop = len; }
         fifo[qt] = make_uint4(t, R, len, 0);  // every lane, one value
         qt++;
+        cold_fifo_out();
       }
       A -= turned + dropped;
       o.code = RKC_OC_FINISHED;
@@ -840,11 +867,9 @@ __global__ __launch_bounds__(64) void rkc_lean(rkc_lean_args g) {
   P.qa = P.qb = P.qc = P.qd = P.qe = P.qf = 0;
   P.tv = 0;
   P.F = U; P.A = 0; P.PR = 0; P.peak = 0; P.Eall = 0; P.fbl = 0;
-  P.nreq = 0; P.ncl = 0; P.nslot = 0; P.nexp = NEVER;
-  P.fnode = NIL; P.bump = 0;
-  P.qh = 0; P.qt = 0; P.ft = 0; P.flo = 0; P.ftop = 0;
-  P.vic = 0; P.post = 0;
-  P.status = 0;
+  P.nreq = 0; P.ncl = 0; P.nexp = NEVER;
+  P.cold = lds + g.off_cold / 4;
+  if (P.lane < Lean<NS>::C_WORDS) P.cold[P.lane] = P.lane == Lean<NS>::C_FNODE ? NIL : 0u;
   __syncthreads();
 
   const rkc_event* ev = g.events + ev_off;
@@ -873,13 +898,16 @@ __global__ __launch_bounds__(64) void rkc_lean(rkc_lean_args g) {
     P.tadd(TW_HITS, wsum(srv && (e0 & 15u) == RKC_EV_PREFILL ? o3 : 0u));
   }
 
+  const u32 nslot_used = ufl(P.cold[Lean<NS>::C_NSLOT]);
+  const u32 vic = ufl(P.cold[Lean<NS>::C_VIC]), post = ufl(P.cold[Lean<NS>::C_POST]);
+  const u32 status = ufl(P.cold[Lean<NS>::C_STATUS]);
   // Final records of the claims still live (each lane writes its own) ...
   if (P.lane < P.ncl) P.write_own_record(m_state(lo16(P.qc)), -1);
   __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
   // ... then lead_end = min(final leading registered length, L) of every used slot, and blank
   // records for unused slots.
   for (u32 s = P.lane; s < nslots; s += 64) {
-    if (s < P.nslot) {
+    if (s < nslot_used) {
       const uint2 cl = P.slotcl[s];
       u32 le = 0;
       if (cl.x != NEVER) le = min(P.chain_n(cl.x), cl.y);
@@ -893,8 +921,8 @@ __global__ __launch_bounds__(64) void rkc_lean(rkc_lean_args g) {
     const u32 w = P.lane;
     i32 v = (i32)P.tv;
     if (w < 10) v += (i32)P.hist[w];
-    if (w == TW_VICTIMS) v = (i32)P.vic;
-    else if (w == TW_POST) v = (i32)P.post;
+    if (w == TW_VICTIMS) v = (i32)vic;
+    else if (w == TW_POST) v = (i32)post;
     else if (w == 24) v = (i32)P.peak;
     else if (w == 25) v = (i32)P.A;
     else if (w == 26) v = (i32)(U - P.F - P.A);
@@ -902,7 +930,7 @@ __global__ __launch_bounds__(64) void rkc_lean(rkc_lean_args g) {
     else if (w == 28) v = (i32)P.PR;
     else if (w == 29) v = (i32)P.nreq;
     else if (w == 30) v = (i32)P.ncl;
-    else if (w == 31) v = (i32)P.status;
+    else if (w == 31) v = (i32)status;
     ptel->w[w] = v;
   }
 }
@@ -925,6 +953,7 @@ bool rkc_lean_layout(const rkc_batch* b, rkc_lean_args* g) {
   u64 o = 0;
   auto take = [&](u64 bytes) { o = align_up(o, 16); u64 r = o; o += bytes; return (u32)r; };
   g->off_keys = take(4ull * 64 * ns);
+  g->off_cold = take(4ull * 16);
   g->off_hist = take(4ull * 16);
   g->off_chains = take(16ull * chains);
   g->off_reqs = take(8ull * reqs);
