@@ -142,7 +142,9 @@ struct Lean {
   lds_u32x2* rq;
   lds_u32x2* ndl;
   glb_u32x2* ndg;
-  static constexpr u32 NL = 64;  // nodes [0, NL) in LDS, the rest in global scratch
+  // nodes [0, NL) in LDS, the rest in global scratch (a zipf pool of 256 chains peaks at ~80-115
+  // live nodes, the 80-block pools at ~35)
+  static constexpr u32 NL = NS == 4 ? 128u : 64u;
   uint4* fifo;
   uint2* slotcl;
   rkc_claim_telemetry* rec;
@@ -949,7 +951,7 @@ bool rkc_lean_layout(const rkc_batch* b, rkc_lean_args* g) {
   const u32 reqs = b->max_live_requests > 0 ? (u32)b->max_live_requests : 1u;
   g->ns = ns;
   g->node_cap = (u32)b->max_events + 2;
-  g->nodes_lds = 64;  // nodes kept in LDS by the compact kernel
+  g->nodes_lds = ns == 4 ? 128u : 64u;  // Lean<NS>::NL
   u64 o = 0;
   auto take = [&](u64 bytes) { o = align_up(o, 16); u64 r = o; o += bytes; return (u32)r; };
   g->off_keys = take(4ull * 64 * ns);
