@@ -146,7 +146,10 @@ struct Lean {
   // live nodes, the 80-block pools at ~35)
   static constexpr u32 NL = NS == 4 ? 128u : 64u;
   uint4* fifo;
-  uint2* slotcl;
+  // per claim slot: chain (NEVER when malformed), L, id | packed decision/state << 16, and 1 when
+  // the final pass writes the whole record (rejected or malformed claims), 0 when a live or
+  // released claim's record is written by its own lane
+  uint4* slotcl;
   rkc_claim_telemetry* rec;
   // live claims, one per lane
   u32 qa;  // id | chain
@@ -356,15 +359,6 @@ struct Lean {
     }
   }
 
-  // Claim record words 0..8 of slot s (word 9, lead_end, is written at the end).
-  __device__ __forceinline__ void write_record(u32 s, i32 id, u32 packed, i32 acc, i32 dem, i32 exs,
-                                               i32 rel, i32 pf, i32 harm, i32 blk) {
-    if (lane < 9) {
-      const i32 v = lane == 0 ? id : lane == 1 ? (i32)packed : lane == 2 ? acc : lane == 3 ? dem
-                  : lane == 4 ? exs : lane == 5 ? rel : lane == 6 ? pf : lane == 7 ? harm : blk;
-      rec[s].w[lane] = v;
-    }
-  }
   // Record of the live claim in this lane (the caller selects the lanes).
   __device__ __forceinline__ void write_own_record(u32 state, i32 rel) {
     const u32 id = lo16(qa), m = lo16(qc);
@@ -658,9 +652,8 @@ struct Lean {
       cold[C_NSLOT] = nslot + 1;
       bool ok = !(s1 < 1 || s1 > RKC_MAX_FIELD_BLOCKS || s2 < 0 || w2 >= nch() || s3 < 0 || s3 > s1);
       if (ok && ncl >= maxq()) { set_status(RKC_PS_CLAIM_TABLE); ok = false; }
-      slotcl[s] = ok ? make_uint2(w2, w1) : make_uint2(NEVER, 0);  // every lane, one value
       if (!ok) {
-        write_record(s, (i32)t, 0, -1, -1, -1, -1, -1, -1, 0);
+        slotcl[s] = make_uint4(NEVER, 0, t, 1);  // every lane, one value
         o.code = RKC_OC_INVALID;
       } else {
         const u32 L = w1, c = w2, T = w3;
@@ -672,13 +665,14 @@ struct Lean {
         if (!r.ok) {
           const u32 dec = shadm() ? DEC_SHADOW : DEC_REJECTED;
           const u32 m = ST_REJECTED | (eff << 3) | (hardq << 5) | (prio << 6) | (dec << 9);
-          write_record(s, (i32)t, packed_of(m), -1, -1, -1, -1, -1, -1, 0);
+          slotcl[s] = make_uint4(c, L, pk(t, packed_of(m)), 1);
           o.code = RKC_OC_MATFAIL;
           o.id = (i32)t;
           o.a = (i32)need;
           o.b = (i32)(F + r.E);
           tadd(TW_ACCEPTED + dec - DEC_ACCEPTED, 1);
         } else {
+          slotcl[s] = make_uint4(c, L, 0, 0);
           const u32 lowered = (mode == RKC_MODE_SOFT) && hardq;
           const u32 dec = shadm() ? DEC_SHADOW : lowered ? DEC_APPROX : DEC_ACCEPTED;
           const u32 st = shadm() ? ST_OBSERVED : ST_MATERIALIZED;
@@ -856,7 +850,7 @@ __global__ __launch_bounds__(64) void rkc_lean(rkc_lean_args g) {
   unsigned char* scr = (unsigned char*)g.scratch + (u64)pool * g.scr_pool_bytes;
   P.ndg = (glb_u32x2*)(scr + g.scr_off_nodes);
   P.fifo = (uint4*)(scr + g.scr_off_fifo);
-  P.slotcl = (uint2*)(scr + g.scr_off_slots);
+  P.slotcl = (uint4*)(scr + g.scr_off_slots);
   P.rec = g.claim_tel + slot_off;
 
   for (u32 c = P.lane; c < Lean<NS>::KC; c += 64) P.kk[c] = KINF;
@@ -910,10 +904,16 @@ __global__ __launch_bounds__(64) void rkc_lean(rkc_lean_args g) {
   // records for unused slots.
   for (u32 s = P.lane; s < nslots; s += 64) {
     if (s < nslot_used) {
-      const uint2 cl = P.slotcl[s];
+      const uint4 cl = P.slotcl[s];
       u32 le = 0;
       if (cl.x != NEVER) le = min(P.chain_n(cl.x), cl.y);
-      P.rec[s].w[9] = (i32)le;
+      if (cl.w) {
+        // rejected or malformed claim: no step ever happened to it
+        const i32 id = (i32)lo16(cl.z), packed = (i32)hi16(cl.z);
+        P.rec[s] = rkc_claim_telemetry{{id, packed, -1, -1, -1, -1, -1, -1, 0, (i32)le}};
+      } else {
+        P.rec[s].w[9] = (i32)le;
+      }
     } else {
       P.rec[s] = rkc_claim_telemetry{{-1, 0, -1, -1, -1, -1, -1, -1, 0, 0}};
     }
@@ -966,7 +966,7 @@ bool rkc_lean_layout(const rkc_batch* b, rkc_lean_args* g) {
   s += 8ull * (g->node_cap > g->nodes_lds ? g->node_cap - g->nodes_lds : 0u);
   s = align_up(s, 256);
   g->scr_off_fifo = s; s += 16ull * ((u64)b->max_events + 1); s = align_up(s, 256);
-  g->scr_off_slots = s; s += 8ull * (u64)(b->max_claim_slots > 0 ? b->max_claim_slots : 1);
+  g->scr_off_slots = s; s += 16ull * (u64)(b->max_claim_slots > 0 ? b->max_claim_slots : 1);
   g->scr_pool_bytes = align_up(s, 256);
   return true;
 }
