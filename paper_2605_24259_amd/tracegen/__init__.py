@@ -292,11 +292,53 @@ def probe(usable_blocks: int = 80, modes=(0, 1, 2, 3)) -> Trace:
     return from_pools(pools, "probe")
 
 
+# Capacity sweep (§5.3 capacity-sweep figure, generalized): every combination of resident claim
+# footprint R, active prefill size A, usable blocks U and pool policy is one pool replaying
+#   t0: CLAIM(L = R, chain 0, T = R, hard, priority 3, no expiry), t1: PREFILL(A private blocks).
+SWEEP_GRID = dict(residents=tuple(range(8, 257, 8)), actives=tuple(range(8, 257, 8)),
+                  usables=tuple(range(16, 513, 16)), modes=(MODE_LRU, MODE_SOFT, MODE_NOADMIT, MODE_HARD))
+
+
+def sweep(residents=SWEEP_GRID["residents"], actives=SWEEP_GRID["actives"], usables=SWEEP_GRID["usables"],
+          modes=SWEEP_GRID["modes"]) -> Trace:
+    """The capacity-sweep batch; pool index = ((mode_i * |R| + r_i) * |A| + a_i) * |U| + u_i."""
+    m, r, a, u = np.meshgrid(np.asarray(modes), np.asarray(residents), np.asarray(actives),
+                             np.asarray(usables), indexing="ij")
+    m, r, a, u = (x.reshape(-1).astype(np.int64) for x in (m, r, a, u))
+    n = m.size
+    desc = np.zeros((n, 12), np.int32)
+    desc[:, 0] = u
+    desc[:, 1] = m
+    desc[:, 2] = 2
+    desc[:, 3] = 2
+    desc[:, 4] = 1
+    desc[:, 5] = 1
+    desc[:, 6] = 1
+    idx = np.arange(n, dtype=np.int64)
+    desc[:, 8:10] = (2 * idx).view(np.int32).reshape(n, 2)
+    desc[:, 10:12] = idx.view(np.int32).reshape(n, 2)
+    ev = np.zeros((n, 2, 4), np.int64)
+    ev[:, 0, 0] = EV_CLAIM | (1 << 4) | (3 << 5)
+    ev[:, 0, 1] = r
+    ev[:, 0, 2] = 0
+    ev[:, 0, 3] = r
+    ev[:, 1, 0] = EV_PREFILL
+    ev[:, 1, 1] = a
+    ev[:, 1, 2] = 1
+    ev[:, 1, 3] = 0
+    t = Trace(desc, np.ascontiguousarray(ev.reshape(-1, 4).astype(np.int32)), n, "sweep")
+    t.meta["grid"] = dict(modes=tuple(modes), residents=tuple(residents), actives=tuple(actives),
+                          usables=tuple(usables))
+    return t
+
+
 def generate(name: str, n_pools: int | None = None, first_pool: int = 0, **overrides) -> Trace:
     """Draw a synthetic workload (see CONFIGS).  n_pools/first_pool select a slice of its pools;
     pool i always gets the same events whatever slice it is drawn in."""
     if name == "probe":
         return probe()
+    if name == "sweep":
+        return sweep()
     cfg = dict(CONFIGS[name])
     cfg.update(overrides)
     total = cfg.pop("n_pools")
