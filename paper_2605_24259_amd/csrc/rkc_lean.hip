@@ -117,11 +117,13 @@ struct AllocRes {
 };
 
 // ---- one pool ---------------------------------------------------------------------------------
-template <int NS>
+// NS: 64-key groups (chains <= 64 NS); MODE: the pool policy, fixed at compile time so that each
+// policy's event loop carries only the logic that policy can reach.
+template <int NS, int MODE>
 struct Lean {
   static constexpr u32 KC = 64u * NS;  // key slots (chains padded to whole lanes)
-  // descriptor: the policy in a scalar, the rarely used limits one per lane of `cst`
-  u32 mode;
+  // descriptor: the rarely used limits one per lane of `cst`
+  static constexpr u32 mode = MODE;
   u32 cst;  // lane 0 U, 1 chains, 2 live-claim cap, 3 live-request cap, 4 claim slots, 5 node cap
   u32 lane;
   __device__ __forceinline__ u32 U() const { return rdl(cst, 0); }
@@ -131,10 +133,10 @@ struct Lean {
   __device__ __forceinline__ u32 nslots() const { return rdl(cst, 4); }
   __device__ __forceinline__ u32 ncap() const { return rdl(cst, 5); }
   // soft levels and acceptance (soft, hard pools: mode bit 0), hard protection, write no-admit
-  __device__ __forceinline__ bool softl() const { return mode & 1u; }
-  __device__ __forceinline__ bool shadm() const { return !(mode & 1u); }
-  __device__ __forceinline__ bool hardm() const { return mode == RKC_MODE_HARD; }
-  __device__ __forceinline__ bool noadm() const { return mode == RKC_MODE_NOADMIT; }
+  __device__ __forceinline__ static constexpr bool softl() { return MODE & 1; }
+  __device__ __forceinline__ static constexpr bool shadm() { return !(MODE & 1); }
+  __device__ __forceinline__ static constexpr bool hardm() { return MODE == RKC_MODE_HARD; }
+  __device__ __forceinline__ static constexpr bool noadm() { return MODE == RKC_MODE_NOADMIT; }
   // memory
   lds_u32* kk;
   lds_u32* hist;  // outcomes per code (16 counters; entry 15 collects the lanes past the end)
@@ -806,35 +808,15 @@ struct Lean {
   }
 };
 
-template <int NS>
-__global__ __launch_bounds__(64) void rkc_lean(rkc_lean_args g) {
-  extern __shared__ __align__(16) unsigned char lds_raw[];
-  const u32 pool = blockIdx.x;
-  if ((i32)pool >= g.n_pools) return;
-  Lean<NS> P;
+// Replay of one pool with policy MODE (the descriptor has been checked by the caller).
+template <int NS, int MODE>
+__device__ __forceinline__ void replay_pool(const rkc_lean_args& g, const rkc_pool_desc& d, u32 pool,
+                                            unsigned char* lds_raw) {
+  typedef Lean<NS, MODE> LP;
+  LP P;
   P.lane = __lane_id();
-  const rkc_pool_desc d = g.pools[pool];
   const i64 ev_off = d.event_offset, slot_off = d.claim_slot_offset;
   rkc_pool_telemetry* ptel = g.pool_tel + pool;
-  const bool ev_ok = d.n_events >= 0 && ev_off >= 0 && ev_off + d.n_events <= g.n_events_total;
-  const bool sl_ok = d.n_claim_slots >= 0 && slot_off >= 0 && slot_off + d.n_claim_slots <= g.n_slots_total;
-  const bool ok = ev_ok && sl_ok && d.usable_blocks >= 1 && d.usable_blocks <= g.max_usable &&
-                  d.mode >= 0 && d.mode <= 3 && d.n_events <= g.max_events && d.n_chains >= 0 &&
-                  d.n_chains <= g.max_chains && d.max_live_claims >= 0 && d.max_live_claims <= g.max_claims &&
-                  d.max_live_requests >= 0 && d.max_live_requests <= g.max_reqs &&
-                  d.n_claim_slots <= g.max_slots && d.reserved == 0;
-  if (!ok) {
-    const u32 lane = P.lane;
-    if (ev_ok)
-      for (i32 i = (i32)lane; i < d.n_events; i += 64) g.outcomes[ev_off + i] = rkc_outcome{{RKC_OC_INVALID, -1, 0, 0}};
-    if (sl_ok)
-      for (i32 i = (i32)lane; i < d.n_claim_slots; i += 64)
-        g.claim_tel[slot_off + i] = rkc_claim_telemetry{{-1, 0, -1, -1, -1, -1, -1, -1, 0, 0}};
-    if (lane < 32)
-      ptel->w[lane] = lane == 31 ? RKC_PS_DESCRIPTOR : (lane == RKC_OC_INVALID && ev_ok) ? d.n_events : 0;
-    return;
-  }
-  P.mode = (u32)d.mode;
   {
     const u32 l = P.lane;
     P.cst = l == 0 ? (u32)d.usable_blocks : l == 1 ? (u32)d.n_chains : l == 2 ? (u32)d.max_live_claims
@@ -853,7 +835,7 @@ __global__ __launch_bounds__(64) void rkc_lean(rkc_lean_args g) {
   P.slotcl = (uint4*)(scr + g.scr_off_slots);
   P.rec = g.claim_tel + slot_off;
 
-  for (u32 c = P.lane; c < Lean<NS>::KC; c += 64) P.kk[c] = KINF;
+  for (u32 c = P.lane; c < LP::KC; c += 64) P.kk[c] = KINF;
   P.hist = lds + g.off_hist / 4;
   if (P.lane < 16) P.hist[P.lane] = 0;
   const u32 nrec = nch > 0 ? nch : 1u;
@@ -865,7 +847,7 @@ __global__ __launch_bounds__(64) void rkc_lean(rkc_lean_args g) {
   P.F = U; P.A = 0; P.PR = 0; P.peak = 0; P.Eall = 0; P.fbl = 0;
   P.nreq = 0; P.ncl = 0; P.nexp = NEVER;
   P.cold = lds + g.off_cold / 4;
-  if (P.lane < Lean<NS>::C_WORDS) P.cold[P.lane] = P.lane == Lean<NS>::C_FNODE ? NIL : 0u;
+  if (P.lane < LP::C_WORDS) P.cold[P.lane] = P.lane == LP::C_FNODE ? NIL : 0u;
   __syncthreads();
 
   const rkc_event* ev = g.events + ev_off;
@@ -894,9 +876,9 @@ __global__ __launch_bounds__(64) void rkc_lean(rkc_lean_args g) {
     P.tadd(TW_HITS, wsum(srv && (e0 & 15u) == RKC_EV_PREFILL ? o3 : 0u));
   }
 
-  const u32 nslot_used = ufl(P.cold[Lean<NS>::C_NSLOT]);
-  const u32 vic = ufl(P.cold[Lean<NS>::C_VIC]), post = ufl(P.cold[Lean<NS>::C_POST]);
-  const u32 status = ufl(P.cold[Lean<NS>::C_STATUS]);
+  const u32 nslot_used = ufl(P.cold[LP::C_NSLOT]);
+  const u32 vic = ufl(P.cold[LP::C_VIC]), post = ufl(P.cold[LP::C_POST]);
+  const u32 status = ufl(P.cold[LP::C_STATUS]);
   // Final records of the claims still live (each lane writes its own) ...
   if (P.lane < P.ncl) P.write_own_record(m_state(lo16(P.qc)), -1);
   __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
@@ -937,6 +919,40 @@ __global__ __launch_bounds__(64) void rkc_lean(rkc_lean_args g) {
   }
 }
 
+// One wavefront per pool; the pool's policy selects its specialized event loop once.
+template <int NS>
+__global__ __launch_bounds__(64) void rkc_lean(rkc_lean_args g) {
+  extern __shared__ __align__(16) unsigned char lds_raw[];
+  const u32 pool = blockIdx.x;
+  if ((i32)pool >= g.n_pools) return;
+  const u32 lane = __lane_id();
+  const rkc_pool_desc d = g.pools[pool];
+  const i64 ev_off = d.event_offset, slot_off = d.claim_slot_offset;
+  rkc_pool_telemetry* ptel = g.pool_tel + pool;
+  const bool ev_ok = d.n_events >= 0 && ev_off >= 0 && ev_off + d.n_events <= g.n_events_total;
+  const bool sl_ok = d.n_claim_slots >= 0 && slot_off >= 0 && slot_off + d.n_claim_slots <= g.n_slots_total;
+  const bool ok = ev_ok && sl_ok && d.usable_blocks >= 1 && d.usable_blocks <= g.max_usable &&
+                  d.mode >= 0 && d.mode <= 3 && d.n_events <= g.max_events && d.n_chains >= 0 &&
+                  d.n_chains <= g.max_chains && d.max_live_claims >= 0 && d.max_live_claims <= g.max_claims &&
+                  d.max_live_requests >= 0 && d.max_live_requests <= g.max_reqs &&
+                  d.n_claim_slots <= g.max_slots && d.reserved == 0;
+  if (!ok) {
+    if (ev_ok)
+      for (i32 i = (i32)lane; i < d.n_events; i += 64) g.outcomes[ev_off + i] = rkc_outcome{{RKC_OC_INVALID, -1, 0, 0}};
+    if (sl_ok)
+      for (i32 i = (i32)lane; i < d.n_claim_slots; i += 64)
+        g.claim_tel[slot_off + i] = rkc_claim_telemetry{{-1, 0, -1, -1, -1, -1, -1, -1, 0, 0}};
+    if (lane < 32)
+      ptel->w[lane] = lane == 31 ? RKC_PS_DESCRIPTOR : (lane == RKC_OC_INVALID && ev_ok) ? d.n_events : 0;
+    return;
+  }
+  const u32 mode = (u32)__builtin_amdgcn_readfirstlane(d.mode);
+  if (mode == RKC_MODE_LRU) replay_pool<NS, RKC_MODE_LRU>(g, d, pool, lds_raw);
+  else if (mode == RKC_MODE_SOFT) replay_pool<NS, RKC_MODE_SOFT>(g, d, pool, lds_raw);
+  else if (mode == RKC_MODE_NOADMIT) replay_pool<NS, RKC_MODE_NOADMIT>(g, d, pool, lds_raw);
+  else replay_pool<NS, RKC_MODE_HARD>(g, d, pool, lds_raw);
+}
+
 u64 align_up(u64 v, u64 a) { return (v + a - 1) / a * a; }
 
 }  // namespace
@@ -951,7 +967,7 @@ bool rkc_lean_layout(const rkc_batch* b, rkc_lean_args* g) {
   const u32 reqs = b->max_live_requests > 0 ? (u32)b->max_live_requests : 1u;
   g->ns = ns;
   g->node_cap = (u32)b->max_events + 2;
-  g->nodes_lds = ns == 4 ? 128u : 64u;  // Lean<NS>::NL
+  g->nodes_lds = ns == 4 ? 128u : 64u;  // LP::NL
   u64 o = 0;
   auto take = [&](u64 bytes) { o = align_up(o, 16); u64 r = o; o += bytes; return (u32)r; };
   g->off_keys = take(4ull * 64 * ns);
@@ -971,15 +987,18 @@ bool rkc_lean_layout(const rkc_batch* b, rkc_lean_args* g) {
   return true;
 }
 
-rkc_status rkc_lean_launch(const rkc_lean_args* g, hipStream_t s) {
-  const void* fn = g->ns == 1 ? (const void*)rkc_lean<1> : g->ns == 2 ? (const void*)rkc_lean<2>
-                                                                      : (const void*)rkc_lean<4>;
+template <int NS>
+rkc_status launch_ns(const rkc_lean_args* g, hipStream_t s) {
   if (g->lds_bytes > 64 * 1024 &&
-      hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)g->lds_bytes) != hipSuccess)
+      hipFuncSetAttribute((const void*)rkc_lean<NS>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                          (int)g->lds_bytes) != hipSuccess)
     return RKC_E_HIP;
-  const dim3 grid((unsigned)g->n_pools), block(64);
-  if (g->ns == 1) hipLaunchKernelGGL(rkc_lean<1>, grid, block, g->lds_bytes, s, *g);
-  else if (g->ns == 2) hipLaunchKernelGGL(rkc_lean<2>, grid, block, g->lds_bytes, s, *g);
-  else hipLaunchKernelGGL(rkc_lean<4>, grid, block, g->lds_bytes, s, *g);
+  hipLaunchKernelGGL((rkc_lean<NS>), dim3((unsigned)g->n_pools), dim3(64), g->lds_bytes, s, *g);
   return hipGetLastError() == hipSuccess ? RKC_OK : RKC_E_HIP;
+}
+
+rkc_status rkc_lean_launch(const rkc_lean_args* g, hipStream_t s) {
+  if (g->ns == 1) return launch_ns<1>(g, s);
+  if (g->ns == 2) return launch_ns<2>(g, s);
+  return launch_ns<4>(g, s);
 }
