@@ -24,7 +24,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, AMD published peak
-BYTES_EVENT, BYTES_OUTCOME, BYTES_CLAIM_SLOT, BYTES_POOL_TEL, BYTES_DESC = 16, 16, 40, 128, 48
+BYTES_EVENT, BYTES_OUTCOME, BYTES_CLAIM_SLOT, BYTES_POOL_TEL, BYTES_DESC = 16, 16, 40, 256, 48
 COPY_BYTES = 1 << 30
 METRIC = "replayed allocator events/sec (1 GPU) + % of HBM peak; bit-exact vs oracle"
 
@@ -125,7 +125,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--workload", default="zipf", choices=["small", "zipf", "nested", "huge", "sweep"])
+    ap.add_argument("--workload", default="zipf", choices=["small", "zipf", "nested", "huge", "sweep", "zipf_defer"])
     ap.add_argument("--mode", default="replay", choices=["replay", "copy"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-parity", action="store_true")

@@ -33,7 +33,7 @@
 extern "C" {
 #endif
 
-#define RKC_ABI_VERSION 1
+#define RKC_ABI_VERSION 2
 
 /* Hard limits of this implementation (checked on the host and per pool on the device). */
 #define RKC_MAX_USABLE_BLOCKS   (1 << 22) /* U per pool                                        */
@@ -60,6 +60,10 @@ extern "C" {
  *   RELEASE (4)  w1 = selector over live claims (ascending id): the claim is released.
  *   DEMOTE  (5)  w1 = selector over materialized hard-requested claims: hard -> soft (§3.1, §3.2).
  *   NOP     (6)  no operation.
+ *   RETRY   (7)  the scheduler retries the oldest deferred request (active deferral, §3.5
+ *                mechanism table "active deferral"; §5.4 live scheduler run: the active request is
+ *                deferred by the scheduler gate, then refused).  w1..w3 unused.  Only pools with
+ *                defer_limit > 0 ever hold deferred requests; with none queued RETRY is a NOOP.
  * Any other type, or out-of-range fields, makes the event malformed: outcome INVALID.
  * -------------------------------------------------------------------------------------------- */
 typedef struct rkc_event {
@@ -73,7 +77,8 @@ enum rkc_event_type {
   RKC_EV_FINISH = 3,
   RKC_EV_RELEASE = 4,
   RKC_EV_DEMOTE = 5,
-  RKC_EV_NOP = 6
+  RKC_EV_NOP = 6,
+  RKC_EV_RETRY = 7
 };
 
 /* Pool policy: how the runtime lowers claims (§3.5 mechanism table rows "native eviction",
@@ -96,7 +101,11 @@ typedef struct rkc_pool_desc {
   int32_t max_live_claims;   /* live-claim table capacity; a CLAIM beyond it is INVALID          */
   int32_t max_live_requests; /* live-request table capacity; a PREFILL beyond it is INVALID      */
   int32_t n_claim_slots;     /* telemetry slots; the k-th CLAIM event uses slot k                */
-  int32_t reserved;          /* must be 0                                                        */
+  int32_t defer_limit;       /* active deferral (0 = off): a PREFILL that would be refused and
+                                attributed to resident claims is DEFERRED instead and queued (FIFO,
+                                at most max_live_requests deep); a queued request receives at most
+                                defer_limit DEFERRED outcomes before a RETRY that still finds it
+                                blocked refuses it                                               */
   int64_t event_offset;      /* index of the pool's first event in the event (and outcome) array */
   int64_t claim_slot_offset; /* index of the pool's first slot in the claim telemetry array      */
 } rkc_pool_desc;
@@ -117,6 +126,11 @@ typedef struct rkc_pool_desc {
  *   DEMOTED / RELEASED      id = claim, a = min(leading registered length, L), b = T
  *   FINISHED                id = request, a = blocks turned cached, b = blocks dropped (no-admit)
  *   NOOP / INVALID          id = -1, a = 0, b = 0
+ *   DEFERRED                the refusal record of REFUSED_CLAIM (id = smallest blocking claim id,
+ *                           a = Pr, b = required, n16 = blocking claims): the request is queued
+ * RETRY reports the retried request: served -> ADMIT / EVICT_RESIDENT with id = the request (its
+ * PREFILL step), a = resident victims, b = leading hits; still blocked -> DEFERRED; refused for good
+ * -> REFUSED_CLAIM / REFUSED_CAPACITY; full live-request table -> INVALID (the request stays queued).
  * -------------------------------------------------------------------------------------------- */
 typedef struct rkc_outcome {
   int32_t w[4];
@@ -132,7 +146,8 @@ enum rkc_outcome_code {
   RKC_OC_RELEASED = 6,
   RKC_OC_FINISHED = 7,
   RKC_OC_NOOP = 8,
-  RKC_OC_INVALID = 9
+  RKC_OC_INVALID = 9,
+  RKC_OC_DEFERRED = 10
 };
 
 enum rkc_outcome_flag {
@@ -182,7 +197,7 @@ enum rkc_claim_state { /* §3.1 ResidentClaimState */
 enum rkc_protection { RKC_PROT_NONE = 0, RKC_PROT_SOFT = 1, RKC_PROT_HARD = 2 };
 
 /* ----------------------------------------------------------------------------------------------
- * Pool telemetry: 128 bytes = 32 x int32.
+ * Pool telemetry: 256 bytes = 64 x int32.
  *   [0..9]  outcomes per code          [10] victims  [11] resident victims  [12] post-release victims
  *   [13] blocks dropped by no-admit    [14] sum of leading hits of served prefills
  *   [15] accepted [16] accepted-approx [17] shadow [18] rejected                  (claim decisions)
@@ -191,9 +206,11 @@ enum rkc_protection { RKC_PROT_NONE = 0, RKC_PROT_SOFT = 1, RKC_PROT_HARD = 2 };
  *   [26] final cached blocks [27] final free blocks [28] final protected blocks
  *   [29] final live requests [30] final live claims
  *   [31] status: 0, or RKC_PS_* bits
+ *   [32] DEFERRED outcomes [33] deferred requests served by RETRY [34] deferred requests refused by
+ *   RETRY [35] deferred requests still queued at the end          [36..63] 0 (reserved)
  * -------------------------------------------------------------------------------------------- */
 typedef struct rkc_pool_telemetry {
-  int32_t w[32];
+  int32_t w[64];
 } rkc_pool_telemetry;
 
 enum rkc_pool_status {
@@ -247,8 +264,11 @@ typedef enum rkc_status {
 /* ABI version (RKC_ABI_VERSION). */
 int32_t rkc_abi_version(void);
 
-/* Device scratch bytes rkc_replay_batch needs for this batch (0 when pool state fits on chip).
- * Reads only the host-side limits of b; never fails (returns 0 for a NULL b). */
+/* Device scratch bytes rkc_replay_batch needs for this batch: per pool, the pool state that does not
+ * stay on chip (touch-stack nodes beyond the LDS part, the FIFO of finished requests' private runs,
+ * one entry per claim slot, a deferral ring of max_live_requests entries, and the live lists when
+ * they do not fit in LDS).  Reads only the host-side limits of b; never fails (returns 0 for a NULL
+ * b or an empty batch). */
 size_t rkc_scratch_bytes(const rkc_batch* b);
 
 /* Replay every pool of the batch from empty pools (all U blocks FREE, no claims, no requests).

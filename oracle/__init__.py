@@ -79,14 +79,14 @@ def replay(desc: np.ndarray, events: np.ndarray, n_claim_slots_total: int, pools
 
     desc: int32 [P, 12] (48-byte pool descriptors), events: int32 [E, 4].
     pools: iterable of pool indices to replay (default: all); other pools' outputs stay zero.
-    Returns (outcomes int32 [E,4], pool_tel int32 [P,32], claim_tel int32 [C,10], check int32 [P]).
+    Returns (outcomes int32 [E,4], pool_tel int32 [P,64], claim_tel int32 [C,10], check int32 [P]).
     """
     lib = _load()
     desc = np.ascontiguousarray(desc, dtype=np.int32).reshape(-1, 12)
     events = np.ascontiguousarray(events, dtype=np.int32).reshape(-1, 4)
     n_pools = desc.shape[0]
     out = np.zeros((events.shape[0], 4), np.int32)
-    ptel = np.zeros((n_pools, 32), np.int32)
+    ptel = np.zeros((n_pools, 64), np.int32)
     ctel = np.zeros((max(int(n_claim_slots_total), 1), 10), np.int32)
     check = np.zeros(n_pools, np.int32)
     todo = list(range(n_pools)) if pools is None else [int(i) for i in pools]

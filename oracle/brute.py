@@ -10,7 +10,8 @@ eight blocks.  Where the C oracle sorts candidates and walks the reuse index, th
     §5.3 BlockPool probe);
   * evaluates a claim's predicate as set containment: positions 0..T-1 of its chain are all present
     in the reuse index (§3.1 useful resident value; §5.4 L6);
-  * counts every quantity from explicit sets rather than counters.
+  * counts every quantity from explicit sets rather than counters;
+  * keeps deferred requests (active deferral, §3.5) as a plain list whose first element is retried.
 Only meant for tiny inputs: its cost is exponential in the pool size.
 """
 from __future__ import annotations
@@ -23,7 +24,10 @@ STATE_CODE = {"submitted": 0, "observed": 1, "materialized": 2, "demoted": 3, "e
               "released": 5, "harmed": 6, "rejected": 7}
 DEC_CODE = {None: 0, "accepted": 1, "approx": 2, "shadow": 3, "rejected": 4}
 CODES = {"admit": 0, "evict_resident": 1, "refused_claim": 2, "refused_capacity": 3,
-         "matfail": 4, "demoted": 5, "released": 6, "finished": 7, "noop": 8, "invalid": 9}
+         "matfail": 4, "demoted": 5, "released": 6, "finished": 7, "noop": 8, "invalid": 9,
+         "deferred": 10}
+TEL_WORD = {name: code for name, code in CODES.items()}
+TEL_WORD["deferred"] = 32
 LRU, SOFT, NOADMIT, HARD = range(4)
 MAXF = 1 << 24
 
@@ -34,14 +38,16 @@ def _s32(x: int) -> int:
 
 
 class Pool:
-    def __init__(self, U, mode, n_chains, max_claims, max_reqs, n_slots):
+    def __init__(self, U, mode, n_chains, max_claims, max_reqs, n_slots, defer_limit=0):
         self.U, self.mode, self.n_chains = U, mode, n_chains
         self.max_claims, self.max_reqs, self.n_slots = max_claims, max_reqs, n_slots
+        self.defer_limit = defer_limit
+        self.waiting = []        # deferred requests, oldest first
         self.blocks = [dict(state=FREE) for _ in range(U)]
         self.index = {}          # (chain, pos) -> block id
         self.reqs = {}           # id -> request dict
         self.claims = []         # slot order
-        self.tel = [0] * 32
+        self.tel = [0] * 64
         self.peak = 0
 
     # -- sets -------------------------------------------------------------------------------
@@ -191,48 +197,41 @@ class Pool:
                 elif len(self.live_claims()) >= self.max_claims:
                     invalid = True
                     self.tel[31] |= 2
-        elif typ > 6:
+        elif typ == 7:
+            if self.waiting and len(live_req) >= self.max_reqs:
+                invalid = True
+                self.tel[31] |= 1
+        elif typ > 7:
             invalid = True
 
         unreg = 0
         if invalid:
             code = "invalid"
         elif typ == 0:
-            S, c, P = e[1], e[2], e[3]
-            h = self.prefix_len(c, P) if P > 0 else 0
-            hits = {self.index[(c, p)] for p in range(h)}
-            need = S - h
-            ok, victims, _, _ = self.choose(need, hits)
-            if not ok:
-                code, oid, a, b, n16 = self.refusal(need, hits)
+            served, rec, fl, unreg = self._prefill(t, t, e[1], e[2], e[3])
+            code, oid, a, b, n16 = rec
+            flags |= fl
+            if not served and code == "refused_claim" and self.defer_limit > 0 \
+                    and len(self.waiting) < self.max_reqs:
+                self.waiting.append(dict(id=t, S=e[1], c=e[2], P=e[3], times=1))
+                code = "deferred"
+        elif typ == 7:
+            if not self.waiting:
+                code = "noop"
             else:
-                out, st = self.take(need, victims)
-                blks = []
-                for i in sorted(hits):
-                    bl = self.blocks[i]
-                    bl["ref"] += 1
-                    bl["state"], bl["lu"] = ACTIVE, t
-                    blks.append(i)
-                for j, i in enumerate(out):
-                    pos = h + j
-                    if pos < P:
-                        reg = self.mode != NOADMIT
-                        self.blocks[i] = dict(state=ACTIVE, ref=1, lu=t, prod=t, chain=c, pos=pos,
-                                              reg=reg)
-                        if reg:
-                            assert (c, pos) not in self.index
-                            self.index[(c, pos)] = i
-                    else:
-                        self.blocks[i] = dict(state=ACTIVE, ref=1, lu=t, prod=t, chain=None,
-                                              pos=pos, reg=False)
-                    blks.append(i)
-                self.reqs[t] = dict(live=True, blocks=blks, len=S)
-                code = "evict_resident" if st["resident"] else "admit"
-                oid, a, b = t, st["resident"], h
-                flags |= (8 if st["post"] else 0) | (16 if st["unclaimed"] else 0)
-                self._tel_victims(st)
-                self.tel[14] += h
-                unreg = st["unreg"]
+                w = self.waiting[0]
+                served, rec, fl, unreg = self._prefill(t, w["id"], w["S"], w["c"], w["P"])
+                code, oid, a, b, n16 = rec
+                flags |= fl
+                if served:
+                    self.waiting.pop(0)
+                    self.tel[33] += 1
+                elif code == "refused_claim" and w["times"] < self.defer_limit:
+                    w["times"] += 1
+                    code = "deferred"
+                else:
+                    self.waiting.pop(0)
+                    self.tel[34] += 1
         elif typ == 1:
             if not live_req:
                 code = "noop"
@@ -352,9 +351,44 @@ class Pool:
         if n16 is None:
             n16 = expired
         n16 = min(n16, 65535)
-        self.tel[CODES[code]] += 1
+        self.tel[TEL_WORD[code]] += 1
         self.peak = max(self.peak, len(self.ids(ACTIVE)))
         return [_s32(CODES[code] | (flags << 8) | (n16 << 16)), oid, a, b]
+
+    def _prefill(self, t, rid, S, c, P):
+        """Serve request rid (S blocks, chain c, shared prefix P) at step t.  Returns (served,
+        (code, id, a, b, n16), flags, blocks that left the reuse index)."""
+        h = self.prefix_len(c, P) if P > 0 else 0
+        hits = {self.index[(c, p)] for p in range(h)}
+        need = S - h
+        ok, victims, _, _ = self.choose(need, hits)
+        if not ok:
+            return False, self.refusal(need, hits), 0, 0
+        out, st = self.take(need, victims)
+        blks = []
+        for i in sorted(hits):
+            bl = self.blocks[i]
+            bl["ref"] += 1
+            bl["state"], bl["lu"] = ACTIVE, t
+            blks.append(i)
+        for j, i in enumerate(out):
+            pos = h + j
+            if pos < P:
+                reg = self.mode != NOADMIT
+                self.blocks[i] = dict(state=ACTIVE, ref=1, lu=t, prod=rid, chain=c, pos=pos, reg=reg)
+                if reg:
+                    assert (c, pos) not in self.index
+                    self.index[(c, pos)] = i
+            else:
+                self.blocks[i] = dict(state=ACTIVE, ref=1, lu=t, prod=rid, chain=None, pos=pos,
+                                      reg=False)
+            blks.append(i)
+        self.reqs[rid] = dict(live=True, blocks=blks, len=S)
+        self._tel_victims(st)
+        self.tel[14] += h
+        flags = (8 if st["post"] else 0) | (16 if st["unclaimed"] else 0)
+        code = "evict_resident" if st["resident"] else "admit"
+        return True, (code, rid, st["resident"], h, None), flags, st["unreg"]
 
     def _tel_victims(self, st):
         self.tel[10] += st["victims"]
@@ -370,6 +404,7 @@ class Pool:
         tel[28] = sum(self.protected(i) for i in range(self.U))
         tel[29] = len(self.live_request_ids())
         tel[30] = len(self.live_claims())
+        tel[35] = len(self.waiting)
         slots = []
         for s in range(self.n_slots):
             if s >= len(self.claims):
@@ -389,10 +424,11 @@ class Pool:
 
 def replay_pool(desc_row, events):
     """Replay one pool: desc_row = 12 int32 descriptor words, events = list of 4-int lists."""
-    U, mode, n_ev, n_chains, max_claims, max_reqs, n_slots = [int(x) for x in desc_row[:7]]
+    U, mode, n_ev, n_chains, max_claims, max_reqs, n_slots, defer_limit = \
+        [int(x) for x in desc_row[:8]]
     if U > 12:
         raise ValueError("the brute-force model enumerates subsets; use it on pools of <= 12 blocks")
-    p = Pool(U, mode, n_chains, max_claims, max_reqs, n_slots)
+    p = Pool(U, mode, n_chains, max_claims, max_reqs, n_slots, defer_limit)
     outs = [p.step(t, [int(x) for x in events[t]]) for t in range(n_ev)]
     tel, slots = p.finish_telemetry()
     return outs, tel, slots

@@ -12,7 +12,9 @@
  *     (chain, pos) in the index, §4.1 ledger rule "block ids map one-to-one to prefix positions");
  *   - claims carry the §3.1 schema fields (id, chain, footprint L, predicate threshold T,
  *     protection mode, priority, optional duration) plus decision, state and step telemetry;
- *   - every step runs: expiry, validation, dispatch, predicate sweep, emission.
+ *   - every step runs: expiry, validation, dispatch, predicate sweep, emission;
+ *   - a pool that defers (active deferral, §3.5) queues a prefill refused on behalf of resident
+ *     claims; RETRY events later serve it, defer it again or refuse it for good.
  *
  * Nothing here relies on the prefix shape of what survives: hits are the leading registered run,
  * the predicate walks the reuse index from position 0, victims are chosen by sorting every
@@ -28,11 +30,11 @@
 
 /* ---- this file's copy of the record layouts -------------------------------------------------- */
 enum { EV_PREFILL = 0, EV_EXTEND = 1, EV_CLAIM = 2, EV_FINISH = 3, EV_RELEASE = 4, EV_DEMOTE = 5,
-       EV_NOP = 6 };
+       EV_NOP = 6, EV_RETRY = 7 };
 enum { MODE_LRU = 0, MODE_SOFT = 1, MODE_NOADMIT = 2, MODE_HARD = 3 };
 enum { OC_ADMIT = 0, OC_EVICT_RESIDENT = 1, OC_REFUSED_CLAIM = 2, OC_REFUSED_CAPACITY = 3,
        OC_MATFAIL = 4, OC_DEMOTED = 5, OC_RELEASED = 6, OC_FINISHED = 7, OC_NOOP = 8,
-       OC_INVALID = 9 };
+       OC_INVALID = 9, OC_DEFERRED = 10 };
 enum { FL_EXPIRED = 1, FL_PRED_FAIL = 2, FL_HARM = 4, FL_POST_RELEASE = 8, FL_UNCLAIMED = 16,
        FL_NOADMIT_DROP = 32, FL_LOWERED = 64, FL_SHADOW = 128 };
 enum { DEC_NONE = 0, DEC_ACCEPTED = 1, DEC_APPROX = 2, DEC_SHADOW = 3, DEC_REJECTED = 4 };
@@ -47,7 +49,8 @@ enum { T_VICTIMS = 10, T_RESIDENT = 11, T_POSTREL = 12, T_DROPPED = 13, T_HITS =
        T_ACCEPTED = 15, T_APPROX = 16, T_SHADOW = 17, T_REJECTED = 18, T_HARM = 19,
        T_PREDFAIL = 20, T_EXPIRED = 21, T_DEMOTED = 22, T_RELEASED = 23, T_PEAK_ACTIVE = 24,
        T_ACTIVE = 25, T_CACHED = 26, T_FREE = 27, T_PROTECTED = 28, T_LIVE_REQ = 29,
-       T_LIVE_CLAIMS = 30, T_STATUS = 31 };
+       T_LIVE_CLAIMS = 30, T_STATUS = 31, T_DEFERRED = 32, T_RETRY_SERVED = 33,
+       T_RETRY_REFUSED = 34, T_QUEUED = 35, N_TEL = 64 };
 
 /* invariant check bits (oracle-only diagnostics) */
 enum {
@@ -94,8 +97,15 @@ typedef struct {
   int32_t blocked;
 } claim_t;
 
+/* A deferred active request waiting in the scheduler queue (active deferral, §3.5 mechanism table;
+ * §5.4 live scheduler run).  It holds no blocks while it waits. */
 typedef struct {
-  int32_t U, mode, n_events, n_chains, max_claims, max_reqs, n_slots;
+  int32_t id, S, chain, P; /* its PREFILL step and request fields */
+  int32_t deferrals;       /* DEFERRED outcomes it has received   */
+} deferred_t;
+
+typedef struct {
+  int32_t U, mode, n_events, n_chains, max_claims, max_reqs, n_slots, defer_limit;
   block_t* b;
   request_t* req;  /* indexed by request id (= step)           */
   claim_t* cl;     /* indexed by slot                          */
@@ -109,8 +119,10 @@ typedef struct {
   int32_t* bucket_next; /* per slot                              */
   int32_t* keyidx;
   int64_t* keys;
+  deferred_t* dq;  /* FIFO of deferred requests: dq[dq_head .. dq_tail) */
+  int32_t dq_head, dq_tail;
   int32_t check;
-  int32_t tel[32];
+  int32_t tel[N_TEL];
 } pool_t;
 
 /* ---- small helpers ---------------------------------------------------------------------------- */
@@ -405,19 +417,69 @@ static int32_t count_active(pool_t* p) {
   return a;
 }
 
+/* Serve an active prefill of request rid (S blocks, shared chain c, shared prefix P) at step t: the
+ * chain's leading registered run below P is hit and the rest allocated (§3.4 feasibility).  Served:
+ * returns 1 with o = {code, id, a, b, n16 = -1}; the blocks turn ACTIVE, last used at t, produced by
+ * rid, and shared positions below P enter the reuse index unless the pool is write no-admit (§1,
+ * §5.2).  Not servable: returns 0 with the refusal record in o. */
+static int serve_prefill(pool_t* p, int32_t t, int32_t rid, int32_t S, int32_t c, int32_t Pp,
+                         int32_t* o, int32_t* flags, int* unregistered) {
+  int32_t h = Pp > 0 ? leading_hits(p, c, Pp) : 0;
+  int64_t need = (int64_t)S - h;
+  if (h) mark_hits(p, c, h, 1);
+  alloc_t r = alloc_blocks(p, need);
+  if (!r.feasible) {
+    refusal(p, need, t, o);
+    if (h) mark_hits(p, c, h, 0);
+    return 0;
+  }
+  if (h) mark_hits(p, c, h, 0);
+  request_t* rq = &p->req[rid];
+  rq->live = 1; rq->chain = Pp > 0 ? c : -1; rq->P = Pp; rq->h = h; rq->S = S; rq->len = S;
+  for (int32_t pos = 0; pos < h; pos++) {
+    int32_t bid = *idx_at(p, c, pos);
+    block_t* b = &p->b[bid];
+    b->refcount++; b->state = BLK_ACTIVE; b->last_use = t;
+    req_push(rq, bid);
+  }
+  for (int64_t j = 0; j < need; j++) {
+    int32_t bid = p->taken[j];
+    block_t* b = &p->b[bid];
+    int32_t pos = h + (int32_t)j;
+    b->state = BLK_ACTIVE; b->refcount = 1; b->last_use = t; b->producer = rid; b->pos = pos;
+    if (pos < Pp) {
+      b->chain = c;
+      if (p->mode != MODE_NOADMIT) do_register(p, bid, c, pos);
+    } else {
+      b->chain = -1; b->owner = rid;
+    }
+    req_push(rq, bid);
+  }
+  o[0] = r.resident > 0 ? OC_EVICT_RESIDENT : OC_ADMIT;
+  o[1] = rid; o[2] = r.resident; o[3] = h; o[4] = -1;
+  if (r.post_release) *flags |= FL_POST_RELEASE;
+  if (r.unclaimed) *flags |= FL_UNCLAIMED;
+  p->tel[T_VICTIMS] += r.victims; p->tel[T_RESIDENT] += r.resident;
+  p->tel[T_POSTREL] += r.post_release; p->tel[T_HITS] += h;
+  *unregistered += r.unregistered;
+  return 1;
+}
+
 /* ---- one pool ---------------------------------------------------------------------------------- */
 
 static void pool_free(pool_t* p) {
   if (p->req) for (int32_t r = 0; r < p->n_events; r++) free(p->req[r].blk);
   free(p->b); free(p->req); free(p->cl); free(p->idx); free(p->idx_off); free(p->idx_len);
   free(p->tmp); free(p->taken); free(p->bucket_head); free(p->bucket_next); free(p->keys);
+  free(p->dq);
 }
 
 static int pool_init(pool_t* p, const int32_t* d, const int32_t* ev) {
   memset(p, 0, sizeof *p);
   p->U = d[0]; p->mode = d[1]; p->n_events = d[2]; p->n_chains = d[3];
-  p->max_claims = d[4]; p->max_reqs = d[5]; p->n_slots = d[6];
-  if (p->U < 1 || p->n_events < 0 || p->n_chains < 0 || p->n_slots < 0) return -1;
+  p->max_claims = d[4]; p->max_reqs = d[5]; p->n_slots = d[6]; p->defer_limit = d[7];
+  if (p->U < 1 || p->n_events < 0 || p->n_chains < 0 || p->n_slots < 0 || p->defer_limit < 0)
+    return -1;
   size_t U = (size_t)p->U, E = (size_t)(p->n_events > 0 ? p->n_events : 1);
   size_t NC = (size_t)(p->n_chains > 0 ? p->n_chains : 1);
   p->b = (block_t*)malloc(U * sizeof(block_t));
@@ -430,8 +492,9 @@ static int pool_init(pool_t* p, const int32_t* d, const int32_t* ev) {
   p->bucket_head = (int32_t*)malloc(NC * sizeof(int32_t));
   p->bucket_next = (int32_t*)malloc((size_t)(p->n_slots > 0 ? p->n_slots : 1) * sizeof(int32_t));
   p->keys = (int64_t*)malloc(U * 4 * sizeof(int64_t));
+  p->dq = (deferred_t*)malloc(E * sizeof(deferred_t)); /* each PREFILL is queued at most once */
   if (!p->b || !p->req || !p->cl || !p->idx_off || !p->idx_len || !p->tmp || !p->taken ||
-      !p->bucket_head || !p->bucket_next || !p->keys) return -1;
+      !p->bucket_head || !p->bucket_next || !p->keys || !p->dq) return -1;
   for (size_t i = 0; i < U; i++) clear_block(&p->b[i]);
   /* reuse-index extent per chain: the largest position any event could register */
   for (int32_t t = 0; t < p->n_events; t++) {
@@ -448,7 +511,7 @@ static int pool_init(pool_t* p, const int32_t* d, const int32_t* ev) {
   p->idx = (int32_t*)malloc((size_t)(total > 0 ? total : 1) * sizeof(int32_t));
   if (!p->idx) return -1;
   for (int64_t i = 0; i < total; i++) p->idx[i] = -1;
-  for (int i = 0; i < 32; i++) p->tel[i] = 0;
+  for (int i = 0; i < N_TEL; i++) p->tel[i] = 0;
   return 0;
 }
 
@@ -539,54 +602,49 @@ static int replay_pool(const int32_t* d, const int32_t* ev, int32_t* out, int32_
         if (L < 1 || L > MAX_FIELD_BLOCKS || c < 0 || c >= p->n_chains || T < 0 || T > L) invalid = 1;
         else if (n_live_cl >= p->max_claims) { invalid = 1; p->tel[T_STATUS] |= PS_CLAIM_TABLE; }
       }
-    } else if (type > EV_NOP) {
+    } else if (type == EV_RETRY) {
+      /* the retried request needs a live-request entry; without one it stays queued */
+      if (p->dq_head < p->dq_tail && n_live_req >= p->max_reqs) {
+        invalid = 1; p->tel[T_STATUS] |= PS_REQ_TABLE;
+      }
+    } else if (type > EV_RETRY) {
       invalid = 1;
     }
 
     if (invalid) {
       code = OC_INVALID;
     } else if (type == EV_PREFILL) {
-      /* 3a. active prefill: leading hits on the shared chain, then allocation */
-      int32_t S = e[1], c = e[2], Pp = e[3];
-      int32_t h = Pp > 0 ? leading_hits(p, c, Pp) : 0;
-      int64_t need = (int64_t)S - h;
-      if (h) mark_hits(p, c, h, 1);
-      alloc_t r = alloc_blocks(p, need);
-      if (!r.feasible) {
-        int32_t o[5];
-        refusal(p, need, t, o);
-        code = o[0]; id = o[1]; a = o[2]; bb = o[3]; n16 = o[4];
-        if (h) mark_hits(p, c, h, 0);
+      /* 3a. active prefill.  When the pool defers, a refusal attributed to resident claims queues
+       *     the request instead (§3.5 mechanism table "active deferral"; §3.2 table: an accepted hard
+       *     claim that blocks active admission yields an active refusal or deferral). */
+      int32_t o[5];
+      if (!serve_prefill(p, t, t, e[1], e[2], e[3], o, &flags, &unregistered) &&
+          o[0] == OC_REFUSED_CLAIM && p->defer_limit > 0 && p->dq_tail - p->dq_head < p->max_reqs) {
+        deferred_t* q = &p->dq[p->dq_tail++];
+        q->id = t; q->S = e[1]; q->chain = e[2]; q->P = e[3]; q->deferrals = 1;
+        o[0] = OC_DEFERRED;
+      }
+      code = o[0]; id = o[1]; a = o[2]; bb = o[3]; n16 = o[4];
+    } else if (type == EV_RETRY) {
+      /* 3e. the scheduler retries the oldest deferred request: it is served, deferred again while
+       *     it has deferrals left, or refused for good (§5.4 live scheduler run: deferred once, then
+       *     a terminal refusal). */
+      if (p->dq_head == p->dq_tail) {
+        code = OC_NOOP;
       } else {
-        if (h) mark_hits(p, c, h, 0);
-        request_t* rq = &p->req[t];
-        rq->live = 1; rq->chain = Pp > 0 ? c : -1; rq->P = Pp; rq->h = h; rq->S = S; rq->len = S;
-        for (int32_t pos = 0; pos < h; pos++) {
-          int32_t bid = *idx_at(p, c, pos);
-          block_t* b = &p->b[bid];
-          b->refcount++; b->state = BLK_ACTIVE; b->last_use = t;
-          req_push(rq, bid);
+        deferred_t* q = &p->dq[p->dq_head];
+        int32_t o[5];
+        if (serve_prefill(p, t, q->id, q->S, q->chain, q->P, o, &flags, &unregistered)) {
+          p->dq_head++;
+          p->tel[T_RETRY_SERVED]++;
+        } else if (o[0] == OC_REFUSED_CLAIM && q->deferrals < p->defer_limit) {
+          q->deferrals++;
+          o[0] = OC_DEFERRED;
+        } else {
+          p->dq_head++;
+          p->tel[T_RETRY_REFUSED]++;
         }
-        for (int64_t j = 0; j < need; j++) {
-          int32_t bid = p->taken[j];
-          block_t* b = &p->b[bid];
-          int32_t pos = h + (int32_t)j;
-          b->state = BLK_ACTIVE; b->refcount = 1; b->last_use = t; b->producer = t; b->pos = pos;
-          if (pos < Pp) {
-            b->chain = c;
-            if (p->mode != MODE_NOADMIT) do_register(p, bid, c, pos); /* write no-admit (§1, §5.2) */
-          } else {
-            b->chain = -1; b->owner = t;
-          }
-          req_push(rq, bid);
-        }
-        code = r.resident > 0 ? OC_EVICT_RESIDENT : OC_ADMIT;
-        id = t; a = r.resident; bb = h;
-        if (r.post_release) flags |= FL_POST_RELEASE;
-        if (r.unclaimed) flags |= FL_UNCLAIMED;
-        p->tel[T_VICTIMS] += r.victims; p->tel[T_RESIDENT] += r.resident;
-        p->tel[T_POSTREL] += r.post_release; p->tel[T_HITS] += h;
-        unregistered += r.unregistered;
+        code = o[0]; id = o[1]; a = o[2]; bb = o[3]; n16 = o[4];
       }
     } else if (type == EV_EXTEND) {
       /* 3b. decode / next chunk of a live request: new private blocks (§3.1 active live KV) */
@@ -757,7 +815,7 @@ static int replay_pool(const int32_t* d, const int32_t* ev, int32_t* out, int32_
     out[4 * (size_t)t + 1] = id;
     out[4 * (size_t)t + 2] = a;
     out[4 * (size_t)t + 3] = bb;
-    p->tel[code]++;
+    p->tel[code == OC_DEFERRED ? T_DEFERRED : code]++;
     int32_t act = count_active(p);
     if (act > peak) peak = act;
     check_step(p, t);
@@ -773,8 +831,8 @@ static int replay_pool(const int32_t* d, const int32_t* ev, int32_t* out, int32_
   for (int32_t s = 0; s < p->n_cl; s++) nlc += claim_live(&p->cl[s]);
   p->tel[T_PEAK_ACTIVE] = peak; p->tel[T_ACTIVE] = (int32_t)a; p->tel[T_CACHED] = (int32_t)c;
   p->tel[T_FREE] = (int32_t)f; p->tel[T_PROTECTED] = prot; p->tel[T_LIVE_REQ] = nlr;
-  p->tel[T_LIVE_CLAIMS] = nlc;
-  for (int i = 0; i < 32; i++) ptel[i] = p->tel[i];
+  p->tel[T_LIVE_CLAIMS] = nlc; p->tel[T_QUEUED] = p->dq_tail - p->dq_head;
+  for (int i = 0; i < N_TEL; i++) ptel[i] = p->tel[i];
 
   /* claim telemetry, one slot per CLAIM event in step order; unused slots are blank */
   for (int32_t s = 0; s < p->n_slots; s++) {
@@ -799,7 +857,7 @@ static int replay_pool(const int32_t* d, const int32_t* ev, int32_t* out, int32_
 }
 
 /* Batch entry: pools [first, first + count) of a batch laid out like the device ABI.
- * desc: 12 int32 per pool (48-byte records); events/outcomes: 4 int32 per event; pool_tel: 32 int32
+ * desc: 12 int32 per pool (48-byte records); events/outcomes: 4 int32 per event; pool_tel: 64 int32
  * per pool; claim_tel: 10 int32 per slot; check: one int32 per pool (invariant violation bits,
  * -1 when the pool could not be set up).  Returns the number of pools with a non-zero check. */
 int rkc_oracle_replay(const int32_t* desc, int32_t first, int32_t count, const int32_t* events,
@@ -809,7 +867,7 @@ int rkc_oracle_replay(const int32_t* desc, int32_t first, int32_t count, const i
     const int32_t* d = desc + 12 * (size_t)i;
     int64_t ev_off = (int64_t)(uint32_t)d[8] | ((int64_t)d[9] << 32);
     int64_t cl_off = (int64_t)(uint32_t)d[10] | ((int64_t)d[11] << 32);
-    int rc = replay_pool(d, events + 4 * ev_off, outcomes + 4 * ev_off, pool_tel + 32 * (size_t)i,
+    int rc = replay_pool(d, events + 4 * ev_off, outcomes + 4 * ev_off, pool_tel + N_TEL * (size_t)i,
                          claim_tel + 10 * cl_off, &check[i]);
     if (rc != 0) check[i] = -1;
     if (check[i] != 0) bad++;

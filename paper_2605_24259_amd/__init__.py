@@ -14,6 +14,10 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "librkc.so")
 _lib = None
 
+# layouts and codes of this binding (rkc.h RKC_ABI_VERSION)
+ABI_VERSION = 2
+POOL_TEL_WORDS = 64
+
 # rkc_batch.flags: replay with the general kernel even where the compact one applies
 FLAG_GENERAL_KERNEL = 1
 
@@ -72,6 +76,9 @@ def load():
         lib.rkc_query_telemetry.restype = ctypes.c_int
         lib.rkc_status_string.argtypes = [ctypes.c_int]
         lib.rkc_status_string.restype = ctypes.c_char_p
+        if lib.rkc_abi_version() != ABI_VERSION:
+            raise RuntimeError(f"{LIB_PATH} implements ABI {lib.rkc_abi_version()}, this binding "
+                               f"ABI {ABI_VERSION}; rebuild the library")
         _lib = lib
     return _lib
 
@@ -101,7 +108,7 @@ class DeviceBatch:
         n_ev = int(self.events.shape[0])
         self.n_claim_slots = int(n_claim_slots)
         self.outcomes = torch.empty((max(n_ev, 1), 4), dtype=torch.int32, device=self.device)
-        self.pool_tel = torch.empty((max(n_pools, 1), 32), dtype=torch.int32, device=self.device)
+        self.pool_tel = torch.empty((max(n_pools, 1), POOL_TEL_WORDS), dtype=torch.int32, device=self.device)
         self.claim_tel = torch.empty((max(self.n_claim_slots, 1), 10), dtype=torch.int32,
                                      device=self.device)
         b = Batch()
@@ -137,7 +144,7 @@ class DeviceBatch:
         return self
 
     def results(self):
-        """(outcomes [E,4], pool telemetry [P,32], claim telemetry [C,10]) as host numpy arrays."""
+        """(outcomes [E,4], pool telemetry [P,64], claim telemetry [C,10]) as host numpy arrays."""
         import torch
         torch.cuda.synchronize(self.device)
         return (self.outcomes[: self.n_events].cpu().numpy(), self.pool_tel[: self.n_pools].cpu().numpy(),
@@ -152,7 +159,7 @@ class DeviceBatch:
 
     def query_telemetry(self, pool: int, max_claims: int, stream=None):
         import numpy as np
-        ptel = np.zeros(32, np.int32)
+        ptel = np.zeros(POOL_TEL_WORDS, np.int32)
         ctel = np.zeros((max(max_claims, 1), 10), np.int32)
         n = ctypes.c_int32(0)
         st = load().rkc_query_telemetry(ctypes.byref(self.batch), pool, ctypes.c_void_p(ptel.ctypes.data),

@@ -20,7 +20,7 @@ struct rkc_lean_args {
   // layout: LDS byte offsets, node split, per-pool scratch regions
   uint32_t ns, node_cap, nodes_lds;
   uint32_t off_keys, off_hist, off_cold, off_chains, off_reqs, off_nodes, lds_bytes;
-  uint64_t scr_pool_bytes, scr_off_nodes, scr_off_fifo, scr_off_slots;
+  uint64_t scr_pool_bytes, scr_off_nodes, scr_off_fifo, scr_off_slots, scr_off_defer;
 };
 
 // Fill the layout part of g for batch b; false when b is outside the compact kernel's limits

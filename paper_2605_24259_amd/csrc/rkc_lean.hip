@@ -27,7 +27,8 @@
 // Live claims sit one per lane in six VGPRs (16-bit halves), so expiry, attribution, predicate
 // sweeps and claim maxima are single vector passes with DPP reductions.  Live requests are a
 // compact id-ordered list in LDS (8 bytes each).  Touch-stack nodes use LDS first, then global
-// scratch; finished requests' private runs form a FIFO in global scratch.
+// scratch; finished requests' private runs form a FIFO in global scratch, and so do the deferred
+// requests of hard-protection pools that defer (a ring of live-request-capacity entries).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -58,7 +59,7 @@ enum : u32 { DEC_ACCEPTED = 1, DEC_APPROX = 2, DEC_SHADOW = 3, DEC_REJECTED = 4 
 // pool telemetry words accumulated lane-distributed
 enum : u32 { TW_VICTIMS = 10, TW_RESIDENT = 11, TW_POST = 12, TW_DROPPED = 13, TW_HITS = 14,
              TW_ACCEPTED = 15, TW_HARM = 19, TW_PREDFAIL = 20, TW_EXPIRED = 21, TW_DEMOTED = 22,
-             TW_RELEASED = 23 };
+             TW_RELEASED = 23, TW_RETRY_SERVED = 33, TW_RETRY_REFUSED = 34 };
 
 // live-claim meta (low half of qc): state[0:3) eff[3:5) hard[5] prio[6:8) pending[8] decision[9:12)
 __device__ __forceinline__ u32 m_state(u32 m) { return m & 7u; }
@@ -118,13 +119,15 @@ struct AllocRes {
 
 // ---- one pool ---------------------------------------------------------------------------------
 // NS: 64-key groups (chains <= 64 NS); MODE: the pool policy, fixed at compile time so that each
-// policy's event loop carries only the logic that policy can reach.
-template <int NS, int MODE>
+// policy's event loop carries only the logic that policy can reach; DEFER: the pool defers (a
+// hard-protection pool with a defer limit), so its loop carries the deferral ring.
+template <int NS, int MODE, bool DEFER>
 struct Lean {
   static constexpr u32 KC = 64u * NS;  // key slots (chains padded to whole lanes)
   // descriptor: the rarely used limits one per lane of `cst`
   static constexpr u32 mode = MODE;
-  u32 cst;  // lane 0 U, 1 chains, 2 live-claim cap, 3 live-request cap, 4 claim slots, 5 node cap
+  u32 cst;  // lane 0 U, 1 chains, 2 live-claim cap, 3 live-request cap, 4 claim slots, 5 node cap,
+            // 6 defer limit
   u32 lane;
   __device__ __forceinline__ u32 U() const { return rdl(cst, 0); }
   __device__ __forceinline__ u32 nch() const { return rdl(cst, 1); }
@@ -132,11 +135,14 @@ struct Lean {
   __device__ __forceinline__ u32 maxr() const { return rdl(cst, 3); }
   __device__ __forceinline__ u32 nslots() const { return rdl(cst, 4); }
   __device__ __forceinline__ u32 ncap() const { return rdl(cst, 5); }
+  __device__ __forceinline__ u32 dlim() const { return rdl(cst, 6); }
   // soft levels and acceptance (soft, hard pools: mode bit 0), hard protection, write no-admit
   __device__ __forceinline__ static constexpr bool softl() { return MODE & 1; }
   __device__ __forceinline__ static constexpr bool shadm() { return !(MODE & 1); }
   __device__ __forceinline__ static constexpr bool hardm() { return MODE == RKC_MODE_HARD; }
   __device__ __forceinline__ static constexpr bool noadm() { return MODE == RKC_MODE_NOADMIT; }
+  // only hard protection attributes refusals to claims, so only hard-protection pools can defer
+  __device__ __forceinline__ static constexpr bool defers() { return MODE == RKC_MODE_HARD && DEFER; }
   // memory
   lds_u32* kk;
   lds_u32* hist;  // outcomes per code (16 counters; entry 15 collects the lanes past the end)
@@ -148,6 +154,7 @@ struct Lean {
   // live nodes, the 80-block pools at ~35)
   static constexpr u32 NL = NS == 4 ? 128u : 64u;
   uint4* fifo;
+  uint4* dq;  // deferred requests: PREFILL step, S, chain, P
   // per claim slot: chain (NEVER when malformed), L, id | packed decision/state << 16, and 1 when
   // the final pass writes the whole record (rejected or malformed claims), 0 when a live or
   // released claim's record is written by its own lane
@@ -160,16 +167,21 @@ struct Lean {
   u32 qd;  // duration | blocked count
   u32 qe;  // demote step | expire step
   u32 qf;  // predicate-failure step | harm step
-  u32 tv;  // pool telemetry word `lane` (lanes 0..31)
+  u32 tv;  // pool telemetry word `lane`
   // scalars
   u32 F, A, PR, peak, Eall, fbl;
   u32 nreq, ncl, nexp;
   // Scalars that only a few paths touch live in LDS (`cold`), so that the registers carried around
   // the event loop are the hot counters only: node free list and bump allocator, the FIFO of
-  // private runs (head, tail, front run), claim slots used, victim counters and the status word.
+  // private runs (head, tail, front run), claim slots used, victim counters, the status word, and
+  // the deferral ring (head, length, DEFERRED outcomes of the head entry; every entry behind the
+  // head has had exactly one).
   lds_u32* cold;
-  // (QH..FLO is one 16-byte group and VIC, POST one 8-byte group: keep their word offsets aligned)
-  enum : u32 { C_QH = 0, C_QT, C_FT, C_FLO, C_FTOP, C_FNODE, C_BUMP, C_NSLOT, C_VIC, C_POST, C_STATUS, C_WORDS };
+  // (QH..FLO is one 16-byte group, VIC, POST and DQH, DQL 8-byte groups: keep their word offsets
+  // aligned)
+  enum : u32 { C_QH = 0, C_QT, C_FT, C_FLO, C_FTOP, C_FNODE, C_BUMP, C_NSLOT, C_VIC, C_POST, C_STATUS,
+               C_DQC, C_DQH, C_DQL, C_WORDS };
+  static_assert(C_QH % 4 == 0 && C_VIC % 2 == 0 && C_DQH % 2 == 0 && C_WORDS <= 16, "cold block layout");
   u32 fnode, bump;              // valid between cold_nodes_in() and cold_nodes_out()
   u32 qh, qt, ft, flo, ftop;    // valid between cold_fifo_in() and cold_fifo_out()
   __device__ __forceinline__ void cold_nodes_in() { fnode = ufl(cold[C_FNODE]); bump = ufl(cold[C_BUMP]); }
@@ -564,6 +576,27 @@ struct Lean {
       __builtin_amdgcn_wave_barrier();
     }
   }
+  // Insert entry e at its id-ordered place in the compact list of n entries (n below the
+  // capacity): entries with larger ids move up one place, highest chunk first.
+  __device__ __forceinline__ void rq_insert(u32x2 e, u32 n) {
+    const u32 id = lo16(e.x);
+    u32 below = 0;
+    for (u32 base = 0; base < n; base += 64) {
+      const u32 j = base + lane;
+      below += (u32)(j < n && lo16(rq[min(j, n - 1)].x) < id);
+    }
+    const u32 k = wsum(below);
+    for (u32 top = n; top > k;) {
+      const u32 base = top - k > 64 ? top - 64 : k;
+      const u32 j = base + lane;
+      const u32x2 v = rq[min(j, top - 1)];
+      __builtin_amdgcn_wave_barrier();
+      if (j < top) rq[j + 1] = v;
+      __builtin_amdgcn_wave_barrier();
+      top = base;
+    }
+    rq[k] = e;
+  }
   // largest R of the live requests on chain c
   __device__ __forceinline__ u32 rq_hold(u32 c, u32 n) {
     u32 hv = 0;
@@ -581,6 +614,78 @@ struct Lean {
     i32 id, a, b;
   };
 
+  __device__ __forceinline__ void dq_pop(u32 dh, u32 dl) {
+    *(lds_u32x2*)(cold + C_DQH) = u32x2{dh + 1 == maxr() ? 0u : dh + 1, dl - 1};
+    cold[C_DQC] = 1;
+  }
+
+  // Serve request rid (S blocks, shared chain cc when P > 0, shared prefix P) at step t; late: a
+  // retried request, inserted into the live list by id and taken off the deferral ring (dh, dl).
+  // A refusal on behalf of resident claims defers the request in deferring pools (§3.5 active
+  // deferral): a new one enters the ring, a retried one is deferred again while its deferrals
+  // last, else refused for good (§5.4 live scheduler run).
+  __device__ __forceinline__ void admit(u32 t, u32 rid, u32 S, u32 cc, u32 P, bool late, u32 dh, u32 dl,
+                                        Out& o) {
+    i32 hc = -1;
+    u32 h = 0, Hc = 0;
+    G0 g = {0, 0, 0, 0, 0, 0, 0, 0};
+    if (P > 0) {
+      hc = (i32)cc;
+      g = rd0(cc);
+      h = min(P, g.n);
+      Hc = h > g.hold ? h - g.hold : 0u;
+    }
+    const u32 need = S - h;
+    const AllocRes r = alloc(need, hc, h, g, o.sweep_due);
+    if (!r.ok) {
+      refusal(need, hc, h, Hc, g, o);
+      if (defers()) {
+        const bool by_claim = o.code == RKC_OC_REFUSED_CLAIM;
+        if (late) {
+          const u32 cnt = ufl(cold[C_DQC]);
+          if (by_claim && cnt < dlim()) {
+            cold[C_DQC] = cnt + 1;
+            o.code = RKC_OC_DEFERRED;
+          } else {
+            dq_pop(dh, dl);
+            tadd(TW_RETRY_REFUSED, 1);
+          }
+        } else if (by_claim) {
+          const u32x2 hl = *(lds_u32x2*)(cold + C_DQH);
+          const u32 h0 = ufl(hl.x), l0 = ufl(hl.y);
+          if (l0 < maxr()) {
+            const u32 slot = h0 + l0 >= maxr() ? h0 + l0 - maxr() : h0 + l0;
+            dq[slot] = make_uint4(t, S, cc, P);  // every lane, one value
+            cold[C_DQL] = l0 + 1;
+            o.code = RKC_OC_DEFERRED;
+          }
+        }
+      }
+    } else {
+      A += Hc + need;
+      u32 R = 0;
+      if (hc >= 0) {
+        const G0 g2 = r.victims ? rd0(cc) : g;  // victims may have shortened this chain above the hits
+        R = noadm() ? h : P;
+        const u32 nn = (!noadm() && P > g2.n) ? P : g2.n;
+        commit(cc, g2, nn, max(g2.hold, R), g2.prot, R, t);
+      }
+      const u32x2 e = u32x2{pk(rid, hc >= 0 ? cc : NIL), pk(R, S)};
+      if (late) {
+        // the live list stays in id order: the retried request goes before later ids
+        rq_insert(e, nreq);
+        dq_pop(dh, dl);
+        tadd(TW_RETRY_SERVED, 1);
+      } else {
+        rq[nreq] = e;
+      }
+      nreq++;
+      o.id = (i32)rid;
+      o.b = (i32)h;
+      served(r, o);
+    }
+  }
+
   __device__ __forceinline__ void ev_prefill(u32 t, u32 w1, u32 w2, u32 w3, Out& o) {
     const i32 s1 = (i32)w1, s2 = (i32)w2, s3 = (i32)w3;
     if (s1 < 1 || s1 > RKC_MAX_FIELD_BLOCKS || s3 < 0 || s3 > s1 || (s3 > 0 && (s2 < 0 || w2 >= nch()))) {
@@ -589,34 +694,21 @@ struct Lean {
       o.code = RKC_OC_INVALID;
       set_status(RKC_PS_REQUEST_TABLE);
     } else {
-      const u32 S = w1, P = w3;
-      i32 hc = -1;
-      u32 h = 0, Hc = 0;
-      G0 g = {0, 0, 0, 0, 0, 0, 0, 0};
-      if (P > 0) {
-        hc = (i32)w2;
-        g = rd0(w2);
-        h = min(P, g.n);
-        Hc = h > g.hold ? h - g.hold : 0u;
-      }
-      const u32 need = S - h;
-      const AllocRes r = alloc(need, hc, h, g, o.sweep_due);
-      if (!r.ok) {
-        refusal(need, hc, h, Hc, g, o);
+      admit(t, t, w1, w2, w3, false, 0, 0, o);
+    }
+  }
+
+  // RETRY (deferring pools): the oldest deferred request is served, deferred again or refused.
+  __device__ __forceinline__ void ev_retry(u32 t, Out& o) {
+    const u32x2 hl = *(lds_u32x2*)(cold + C_DQH);
+    const u32 dh = ufl(hl.x), dl = ufl(hl.y);
+    if (dl > 0) {
+      if (nreq >= maxr()) {
+        o.code = RKC_OC_INVALID;  // the request stays queued
+        set_status(RKC_PS_REQUEST_TABLE);
       } else {
-        A += Hc + need;
-        u32 R = 0;
-        if (hc >= 0) {
-          const G0 g2 = r.victims ? rd0(w2) : g;  // victims may have shortened this chain above the hits
-          R = noadm() ? h : P;
-          const u32 nn = (!noadm() && P > g2.n) ? P : g2.n;
-          commit(w2, g2, nn, max(g2.hold, R), g2.prot, R, t);
-        }
-        rq[nreq] = u32x2{pk(t, hc >= 0 ? w2 : NIL), pk(R, S)};
-        nreq++;
-        o.id = (i32)t;
-        o.b = (i32)h;
-        served(r, o);
+        const uint4 q = dq[dh];
+        admit(t, ufl(q.x), ufl(q.y), ufl(q.z), ufl(q.w), true, dh, dl, o);
       }
     }
   }
@@ -797,7 +889,9 @@ struct Lean {
     else if (type == RKC_EV_CLAIM) ev_claim(t, w0, w1, w2, w3, o);
     else if (type == RKC_EV_FINISH) ev_finish(t, w1, o);
     else if (type == RKC_EV_RELEASE || type == RKC_EV_DEMOTE) ev_lifecycle(t, type, w1, o);
-    else if (type != RKC_EV_NOP) o.code = RKC_OC_INVALID;
+    else if (defers() && type == RKC_EV_RETRY) ev_retry(t, o);
+    else if ((type & ~1u) != RKC_EV_NOP) o.code = RKC_OC_INVALID;  // NOP, or RETRY with no ring
+    static_assert(RKC_EV_NOP == 6 && RKC_EV_RETRY == 7, "NOP and RETRY differ in bit 0 only");
     if (o.sweep_due) o.flags |= sweep(t);
     const bool quiet = o.code == RKC_OC_NOOP || o.code == RKC_OC_INVALID;
     o0 = o.code | (o.flags << 8) | ((o.n16 == NEVER ? min(expired, 65535u) : o.n16) << 16);
@@ -809,10 +903,10 @@ struct Lean {
 };
 
 // Replay of one pool with policy MODE (the descriptor has been checked by the caller).
-template <int NS, int MODE>
+template <int NS, int MODE, bool DEFER>
 __device__ __forceinline__ void replay_pool(const rkc_lean_args& g, const rkc_pool_desc& d, u32 pool,
                                             unsigned char* lds_raw) {
-  typedef Lean<NS, MODE> LP;
+  typedef Lean<NS, MODE, DEFER> LP;
   LP P;
   P.lane = __lane_id();
   const i64 ev_off = d.event_offset, slot_off = d.claim_slot_offset;
@@ -820,7 +914,8 @@ __device__ __forceinline__ void replay_pool(const rkc_lean_args& g, const rkc_po
   {
     const u32 l = P.lane;
     P.cst = l == 0 ? (u32)d.usable_blocks : l == 1 ? (u32)d.n_chains : l == 2 ? (u32)d.max_live_claims
-          : l == 3 ? (u32)d.max_live_requests : l == 4 ? (u32)d.n_claim_slots : g.node_cap;
+          : l == 3 ? (u32)d.max_live_requests : l == 4 ? (u32)d.n_claim_slots : l == 5 ? g.node_cap
+          : (u32)d.defer_limit;
   }
   const u32 U = (u32)d.usable_blocks, nch = (u32)d.n_chains, nslots = (u32)d.n_claim_slots;
 
@@ -833,6 +928,7 @@ __device__ __forceinline__ void replay_pool(const rkc_lean_args& g, const rkc_po
   P.ndg = (glb_u32x2*)(scr + g.scr_off_nodes);
   P.fifo = (uint4*)(scr + g.scr_off_fifo);
   P.slotcl = (uint4*)(scr + g.scr_off_slots);
+  P.dq = (uint4*)(scr + g.scr_off_defer);
   P.rec = g.claim_tel + slot_off;
 
   for (u32 c = P.lane; c < LP::KC; c += 64) P.kk[c] = KINF;
@@ -847,7 +943,7 @@ __device__ __forceinline__ void replay_pool(const rkc_lean_args& g, const rkc_po
   P.F = U; P.A = 0; P.PR = 0; P.peak = 0; P.Eall = 0; P.fbl = 0;
   P.nreq = 0; P.ncl = 0; P.nexp = NEVER;
   P.cold = lds + g.off_cold / 4;
-  if (P.lane < LP::C_WORDS) P.cold[P.lane] = P.lane == LP::C_FNODE ? NIL : 0u;
+  if (P.lane < LP::C_WORDS) P.cold[P.lane] = P.lane == LP::C_FNODE ? NIL : P.lane == LP::C_DQC ? 1u : 0u;
   __syncthreads();
 
   const rkc_event* ev = g.events + ev_off;
@@ -873,12 +969,13 @@ __device__ __forceinline__ void replay_pool(const rkc_lean_args& g, const rkc_po
     __hip_atomic_fetch_add(P.hist + (P.lane < cnt ? oc : 15u), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
     const bool srv = P.lane < cnt && oc <= RKC_OC_EVICT_RESIDENT;
     P.tadd(TW_RESIDENT, wsum(srv ? o2 : 0u));
-    P.tadd(TW_HITS, wsum(srv && (e0 & 15u) == RKC_EV_PREFILL ? o3 : 0u));
+    const u32 ty = e0 & 15u;
+    P.tadd(TW_HITS, wsum(srv && (ty == RKC_EV_PREFILL || (LP::defers() && ty == RKC_EV_RETRY)) ? o3 : 0u));
   }
 
   const u32 nslot_used = ufl(P.cold[LP::C_NSLOT]);
   const u32 vic = ufl(P.cold[LP::C_VIC]), post = ufl(P.cold[LP::C_POST]);
-  const u32 status = ufl(P.cold[LP::C_STATUS]);
+  const u32 status = ufl(P.cold[LP::C_STATUS]), queued = ufl(P.cold[LP::C_DQL]);
   // Final records of the claims still live (each lane writes its own) ...
   if (P.lane < P.ncl) P.write_own_record(m_state(lo16(P.qc)), -1);
   __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
@@ -901,10 +998,11 @@ __device__ __forceinline__ void replay_pool(const rkc_lean_args& g, const rkc_po
     }
   }
   __syncthreads();
-  if (P.lane < 32) {
+  {
     const u32 w = P.lane;
     i32 v = (i32)P.tv;
     if (w < 10) v += (i32)P.hist[w];
+    if (w == 32) v += (i32)P.hist[RKC_OC_DEFERRED];
     if (w == TW_VICTIMS) v = (i32)vic;
     else if (w == TW_POST) v = (i32)post;
     else if (w == 24) v = (i32)P.peak;
@@ -915,6 +1013,7 @@ __device__ __forceinline__ void replay_pool(const rkc_lean_args& g, const rkc_po
     else if (w == 29) v = (i32)P.nreq;
     else if (w == 30) v = (i32)P.ncl;
     else if (w == 31) v = (i32)status;
+    else if (w == 35) v = (i32)queued;
     ptel->w[w] = v;
   }
 }
@@ -935,22 +1034,23 @@ __global__ __launch_bounds__(64) void rkc_lean(rkc_lean_args g) {
                   d.mode >= 0 && d.mode <= 3 && d.n_events <= g.max_events && d.n_chains >= 0 &&
                   d.n_chains <= g.max_chains && d.max_live_claims >= 0 && d.max_live_claims <= g.max_claims &&
                   d.max_live_requests >= 0 && d.max_live_requests <= g.max_reqs &&
-                  d.n_claim_slots <= g.max_slots && d.reserved == 0;
+                  d.n_claim_slots <= g.max_slots && d.defer_limit >= 0;
   if (!ok) {
     if (ev_ok)
       for (i32 i = (i32)lane; i < d.n_events; i += 64) g.outcomes[ev_off + i] = rkc_outcome{{RKC_OC_INVALID, -1, 0, 0}};
     if (sl_ok)
       for (i32 i = (i32)lane; i < d.n_claim_slots; i += 64)
         g.claim_tel[slot_off + i] = rkc_claim_telemetry{{-1, 0, -1, -1, -1, -1, -1, -1, 0, 0}};
-    if (lane < 32)
-      ptel->w[lane] = lane == 31 ? RKC_PS_DESCRIPTOR : (lane == RKC_OC_INVALID && ev_ok) ? d.n_events : 0;
+    ptel->w[lane] = lane == 31 ? RKC_PS_DESCRIPTOR : (lane == RKC_OC_INVALID && ev_ok) ? d.n_events : 0;
     return;
   }
   const u32 mode = (u32)__builtin_amdgcn_readfirstlane(d.mode);
-  if (mode == RKC_MODE_LRU) replay_pool<NS, RKC_MODE_LRU>(g, d, pool, lds_raw);
-  else if (mode == RKC_MODE_SOFT) replay_pool<NS, RKC_MODE_SOFT>(g, d, pool, lds_raw);
-  else if (mode == RKC_MODE_NOADMIT) replay_pool<NS, RKC_MODE_NOADMIT>(g, d, pool, lds_raw);
-  else replay_pool<NS, RKC_MODE_HARD>(g, d, pool, lds_raw);
+  const u32 defer = (u32)__builtin_amdgcn_readfirstlane(d.defer_limit) > 0;
+  if (mode == RKC_MODE_LRU) replay_pool<NS, RKC_MODE_LRU, false>(g, d, pool, lds_raw);
+  else if (mode == RKC_MODE_SOFT) replay_pool<NS, RKC_MODE_SOFT, false>(g, d, pool, lds_raw);
+  else if (mode == RKC_MODE_NOADMIT) replay_pool<NS, RKC_MODE_NOADMIT, false>(g, d, pool, lds_raw);
+  else if (!defer) replay_pool<NS, RKC_MODE_HARD, false>(g, d, pool, lds_raw);
+  else replay_pool<NS, RKC_MODE_HARD, true>(g, d, pool, lds_raw);
 }
 
 u64 align_up(u64 v, u64 a) { return (v + a - 1) / a * a; }
@@ -983,6 +1083,8 @@ bool rkc_lean_layout(const rkc_batch* b, rkc_lean_args* g) {
   s = align_up(s, 256);
   g->scr_off_fifo = s; s += 16ull * ((u64)b->max_events + 1); s = align_up(s, 256);
   g->scr_off_slots = s; s += 16ull * (u64)(b->max_claim_slots > 0 ? b->max_claim_slots : 1);
+  s = align_up(s, 256);
+  g->scr_off_defer = s; s += 16ull * reqs;
   g->scr_pool_bytes = align_up(s, 256);
   return true;
 }

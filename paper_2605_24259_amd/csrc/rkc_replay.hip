@@ -103,7 +103,8 @@ enum : u32 { RQ_ID = 0, RQ_C, RQ_R, RQ_LEN, RQ_ARRAYS };
 // pool telemetry words kept in lane k of one register
 enum : u32 { TW_VICTIMS = 10, TW_RESIDENT = 11, TW_POST = 12, TW_DROPPED = 13, TW_HITS = 14,
              TW_ACCEPTED = 15, TW_HARM = 19, TW_PREDFAIL = 20, TW_EXPIRED = 21, TW_DEMOTED = 22,
-             TW_RELEASED = 23 };
+             TW_RELEASED = 23, TW_DEFERRED = 32, TW_RETRY_SERVED = 33, TW_RETRY_REFUSED = 34,
+             TW_QUEUED = 35 };
 
 // live-claim meta word: state[0:3) eff[3:5) hard[5] prio[6:8) pending[8] decision[9:12)
 __device__ __forceinline__ u32 m_state(u32 m) { return m & 7u; }
@@ -165,7 +166,7 @@ struct Layout {
   u32 chains, reqs, claims, nodes_lds;
   u32 off_chain, off_mark, off_key, off_rq, off_cl, off_node;
   u32 lds_bytes;
-  u64 scr_pool_bytes, scr_off_node, scr_off_fifo, scr_off_slot, scr_off_rq, scr_off_cl;
+  u64 scr_pool_bytes, scr_off_node, scr_off_fifo, scr_off_slot, scr_off_dq, scr_off_rq, scr_off_cl;
   u32 fifo_cap, node_cap;
   u32 global_lists, narrow;
 };
@@ -208,7 +209,7 @@ struct Pool {
   static constexpr u32 kListNil = kGL ? 0xFFFFFFFFu : Store<W>::wnil;
   static constexpr u32 kWordNil = Store<W>::wnil;
   // descriptor
-  i32 U, mode, n_events, n_chains, max_claims, max_reqs, n_slots;
+  i32 U, mode, n_events, n_chains, max_claims, max_reqs, n_slots, defer_limit;
   u32 lane;
   // memory
   lds_w* ch;          // chain records, CF_WORDS words each
@@ -222,10 +223,14 @@ struct Pool {
   u32 nl, node_cap;
   uint4* fifo;  // private runs in finish order; one push per event at most, so it never wraps
   uint2* slot_cl;
+  // deferred requests (active deferral): a ring of max_reqs entries (PREFILL step, S, chain, P);
+  // dq_cnt counts the DEFERRED outcomes of the head entry (every entry behind it has had one)
+  uint4* dq;
+  u32 dq_head, dq_len, dq_cnt;
   rkc_claim_telemetry* rec;
   // registers
   u32 kr0, kr1, kr2, kr3;  // top key of chain 64 * k + lane, k = 0..3
-  u32 tv;                  // pool telemetry word `lane` (lanes 0..31)
+  u32 tv;                  // pool telemetry word `lane`
   // scalar state (wave-uniform)
   i32 F, A, PR, peak;
   i32 Eall;       // sum over chains of max(0, n - max(hold, prot)): evictable shared blocks
@@ -644,6 +649,25 @@ struct Pool {
     lists_fence();
   }
 
+  // Open a gap at entry i of a struct-of-arrays list of len entries (len < cap) by shifting
+  // [i, len) up one place, highest chunk first; lanes read their entries before any lane writes.
+  __device__ __forceinline__ void list_open(lword* base0, u32 cap, u32 narr, u32 len, u32 i) {
+    for (u32 top = len; top > i;) {
+      const u32 base = top - i > 64 ? top - 64 : i;
+      const u32 j = base + lane;
+      const bool act = j < top;
+      for (u32 k = 0; k < narr; k++) {
+        lword* a = base0 + k * cap;
+        const u32 v = act ? (u32)a[j] : 0u;
+        __builtin_amdgcn_wave_barrier();
+        if (act) a[j + 1] = v;
+        __builtin_amdgcn_wave_barrier();
+      }
+      top = base;
+    }
+    lists_fence();
+  }
+
   __device__ __forceinline__ void expire(u32 t, u32& flags, u32& expired) {
     u32 cnt = 0, nx = EXP_NEVER;
     for (u32 i = lane; i < ncl; i += 64) {
@@ -689,8 +713,9 @@ struct Pool {
 
     if (t >= next_exp) expire(t, flags, expired);
 
-    // Decode: validity (malformed events and table limits) and the allocation request.
-    u32 kind = K_NOOP, sel = 0, h = 0, s = 0;
+    // Decode: validity (malformed events and table limits) and the allocation request.  A RETRY
+    // turns into the prefill of the oldest deferred request (id rid, its own S, chain and P).
+    u32 kind = K_NOOP, sel = 0, h = 0, s = 0, rid = t, retry = 0;
     i32 need = 0, hc = -1, Hc = 0;
     const u32 fieldbad = (u32)(w1 < 1) | (u32)(w1 > RKC_MAX_FIELD_BLOCKS);
     const u32 chainbad = (u32)(w2 < 0) | (u32)(w2 >= n_chains);
@@ -704,13 +729,19 @@ struct Pool {
           status |= RKC_PS_REQUEST_TABLE;
         } else {
           kind = K_PREFILL;
-          if (w3 > 0) {
-            hc = w2;
-            const uint4 g0 = cg((u32)hc, 0);
-            h = min((u32)w3, g0.x);
-            Hc = max(0, (i32)h - (i32)g0.y);
-          }
-          need = w1 - (i32)h;
+        }
+        break;
+      case RKC_EV_RETRY:
+        if (dq_len == 0) {
+          kind = K_NOOP;
+        } else if (nreq >= (u32)max_reqs) {
+          kind = K_INVALID;  // the request stays queued
+          status |= RKC_PS_REQUEST_TABLE;
+        } else {
+          const uint4 q = dq[dq_head];
+          rid = ufl(q.x); w1 = (i32)ufl(q.y); w2 = (i32)ufl(q.z); w3 = (i32)ufl(q.w);
+          retry = 1;
+          kind = K_PREFILL;
         }
         break;
       case RKC_EV_EXTEND:
@@ -754,12 +785,41 @@ struct Pool {
       case RKC_EV_NOP: break;
       default: kind = K_INVALID; break;
     }
+    if (kind == K_PREFILL) {
+      if (w3 > 0) {
+        hc = w2;
+        const uint4 g0 = cg((u32)hc, 0);
+        h = min((u32)w3, g0.x);
+        Hc = max(0, (i32)h - (i32)g0.y);
+      }
+      need = w1 - (i32)h;
+    }
 
     // One allocation site for prefill, extend and claim.
     AllocRes r = {1, 0, 0, 0, 0, 0};
     if (kind == K_PREFILL || kind == K_EXTEND || kind == K_CLAIM) r = alloc(need, hc, h, sweep_due);
     if (!r.ok && kind != K_CLAIM) {
       refusal(need, hc, h, Hc, code, id, a, b, n16);
+      // active deferral: a prefill refused on behalf of claims waits in the queue; a retried one
+      // is deferred again while its deferrals last, else refused for good
+      const u32 by_claim = (u32)(code == RKC_OC_REFUSED_CLAIM);
+      if (kind == K_PREFILL && retry) {
+        if (by_claim && dq_cnt < (u32)defer_limit) {
+          dq_cnt++;
+          code = RKC_OC_DEFERRED;
+        } else {
+          dq_head = dq_head + 1 == (u32)max_reqs ? 0u : dq_head + 1;
+          dq_len--;
+          dq_cnt = 1;
+          tadd(TW_RETRY_REFUSED, 1);
+        }
+      } else if (kind == K_PREFILL && by_claim && defer_limit > 0 && dq_len < (u32)max_reqs) {
+        u32 slot = dq_head + dq_len;
+        slot = slot >= (u32)max_reqs ? slot - (u32)max_reqs : slot;
+        dq[slot] = make_uint4(t, (u32)w1, (u32)w2, (u32)w3);  // every lane, one value
+        dq_len++;
+        code = RKC_OC_DEFERRED;
+      }
       kind = K_REFUSED;  // no further effect
     }
 
@@ -782,10 +842,23 @@ struct Pool {
           tpr = g0.z;
           tx = R;
         }
-        const u32 k = nreq++;
-        rqa(RQ_ID)[k] = t; rqa(RQ_C)[k] = hc >= 0 ? (u32)hc : kListNil; rqa(RQ_R)[k] = R;
+        // the live list stays in id order: a retried request goes before the later ids
+        u32 k = nreq;
+        if (retry) {
+          u32 below = 0;
+          for (u32 j = lane; j < nreq; j += 64) below += (u32)((u32)rqa(RQ_ID)[j] < rid);
+          k = wave_sum(below);
+          list_open(rq, rq_cap, RQ_ARRAYS, nreq, k);
+          dq_head = dq_head + 1 == (u32)max_reqs ? 0u : dq_head + 1;
+          dq_len--;
+          dq_cnt = 1;
+          tadd(TW_RETRY_SERVED, 1);
+        }
+        nreq++;
+        rqa(RQ_ID)[k] = rid; rqa(RQ_C)[k] = hc >= 0 ? (u32)hc : kListNil; rqa(RQ_R)[k] = R;
         rqa(RQ_LEN)[k] = (u32)w1;
-        id = (i32)t; b = (i32)h;
+        lists_fence();
+        id = (i32)rid; b = (i32)h;
         count_victims(r, h);
         break;
       }
@@ -952,7 +1025,7 @@ struct Pool {
     a = quiet ? 0 : a;
     b = quiet ? 0 : b;
     n16 = n16 == NIL ? min(expired, 65535u) : n16;
-    tadd((u32)code, 1);
+    tadd(code == RKC_OC_DEFERRED ? (u32)TW_DEFERRED : (u32)code, 1);
     peak = max(peak, A);
     return make_int4((i32)((u32)code | (flags << 8) | (n16 << 16)), id, a, b);
   }
@@ -979,7 +1052,7 @@ __global__ __launch_bounds__(64) void rkc_replay_wave(Args g) {
                   P.mode >= 0 && P.mode <= 3 && P.n_events <= g.max_events && P.n_chains >= 0 &&
                   P.n_chains <= g.max_chains && P.max_claims >= 0 && P.max_claims <= g.max_claims &&
                   P.max_reqs >= 0 && P.max_reqs <= g.max_reqs && P.n_slots <= g.max_slots &&
-                  d.reserved == 0;
+                  d.defer_limit >= 0;
   if (!ok) {
     if (ev_ok)
       for (i32 i = (i32)P.lane; i < P.n_events; i += 64)
@@ -987,8 +1060,7 @@ __global__ __launch_bounds__(64) void rkc_replay_wave(Args g) {
     if (sl_ok)
       for (i32 i = (i32)P.lane; i < P.n_slots; i += 64)
         g.claim_tel[slot_off + i] = rkc_claim_telemetry{{-1, 0, -1, -1, -1, -1, -1, -1, 0, 0}};
-    if (P.lane < 32)
-      ptel->w[P.lane] = P.lane == 31 ? RKC_PS_DESCRIPTOR : (P.lane == RKC_OC_INVALID && ev_ok) ? P.n_events : 0;
+    ptel->w[P.lane] = P.lane == 31 ? RKC_PS_DESCRIPTOR : (P.lane == RKC_OC_INVALID && ev_ok) ? P.n_events : 0;
     return;
   }
 
@@ -1016,6 +1088,8 @@ __global__ __launch_bounds__(64) void rkc_replay_wave(Args g) {
   P.node_cap = L.node_cap;
   P.fifo = (uint4*)(scr + L.scr_off_fifo);
   P.slot_cl = (uint2*)(scr + L.scr_off_slot);
+  P.dq = (uint4*)(scr + L.scr_off_dq);
+  P.defer_limit = d.defer_limit;
   P.rec = g.claim_tel + slot_off;
 
   for (i32 c = (i32)P.lane; c < P.n_chains; c += 64) {
@@ -1033,6 +1107,7 @@ __global__ __launch_bounds__(64) void rkc_replay_wave(Args g) {
   P.free_head = NIL; P.bump = 0;
   P.fhead = 0; P.ftail = 0; P.ft = 0; P.flo = 0; P.ftop = 0; P.fblocks = 0;
   P.status = 0;
+  P.dq_head = 0; P.dq_len = 0; P.dq_cnt = 1;
   __syncthreads();
 
   const rkc_event* ev = g.events + ev_off;
@@ -1067,7 +1142,7 @@ __global__ __launch_bounds__(64) void rkc_replay_wave(Args g) {
     }
   }
   __builtin_amdgcn_wave_barrier();
-  if (P.lane < 32) {
+  {
     const u32 w = P.lane;
     i32 v = (i32)P.tv;
     if (w == 24) v = P.peak;
@@ -1078,6 +1153,7 @@ __global__ __launch_bounds__(64) void rkc_replay_wave(Args g) {
     else if (w == 29) v = (i32)P.nreq;
     else if (w == 30) v = (i32)P.ncl;
     else if (w == 31) v = (i32)P.status;
+    else if (w == TW_QUEUED) v = (i32)P.dq_len;
     ptel->w[w] = v;
   }
 }
@@ -1127,6 +1203,7 @@ bool make_layout(const rkc_batch* b, Layout* L, bool narrow, bool global_lists) 
   L->scr_off_fifo = s; s += 16ull * L->fifo_cap; s = align_up(s, 256);
   L->scr_off_slot = s; s += 8ull * (u64)(b->max_claim_slots > 0 ? b->max_claim_slots : 1);
   s = align_up(s, 256);
+  L->scr_off_dq = s; s += 16ull * L->reqs; s = align_up(s, 256);  // deferred requests (ring)
   if (global_lists) {
     L->scr_off_rq = s; s += 4ull * RQ_ARRAYS * L->reqs; s = align_up(s, 256);
     L->scr_off_cl = s; s += 4ull * CL_ARRAYS * L->claims;

@@ -30,7 +30,7 @@ _lib = None
 
 SEED0 = 260524259
 
-EV_PREFILL, EV_EXTEND, EV_CLAIM, EV_FINISH, EV_RELEASE, EV_DEMOTE, EV_NOP = range(7)
+EV_PREFILL, EV_EXTEND, EV_CLAIM, EV_FINISH, EV_RELEASE, EV_DEMOTE, EV_NOP, EV_RETRY = range(8)
 MODE_LRU, MODE_SOFT, MODE_NOADMIT, MODE_HARD = range(4)
 MODE_NAMES = ("lru", "soft", "noadmit", "hard")
 
@@ -60,6 +60,9 @@ class GenParams(ctypes.Structure):
         ("claim_cap", ctypes.c_int32),
         ("max_live_claims", ctypes.c_int32),
         ("max_live_requests", ctypes.c_int32),
+        ("retry_permille", ctypes.c_int32),
+        ("defer_limit", ctypes.c_int32),
+        ("mode", ctypes.c_int32),
         ("zipf_s", ctypes.c_double),
         ("seed0", ctypes.c_uint64),
     ]
@@ -94,6 +97,16 @@ CONFIGS = {
                  claim_len=0, claim_len_min=0, claim_len_max=0, claim_thresh=0,
                  hard_permille=250, prio_max=3, dur_min=4096, dur_max=32768, extend_k=1,
                  claim_cap=4096, max_live_claims=4096, max_live_requests=16384),
+    # The zipf pools under hard protection with active deferral: a prefill refused on behalf of
+    # resident claims waits in the scheduler queue; 10% of the events are scheduler retries of the
+    # oldest waiting request, which is deferred at most 4 times before a terminal refusal.
+    "zipf_defer": dict(cfg_id=6, n_pools=65536, usable_blocks=2048, n_events=1024,
+                       mix=(400, 300, 150, 100, 50, 0), prefill_dist=1, prefill_min=4,
+                       prefill_max=1536, chain_pick=1, n_chains=256, chain_len_min=32,
+                       chain_len_max=512, claim_len=0, claim_len_min=0, claim_len_max=0,
+                       claim_thresh=0, hard_permille=500, prio_max=3, dur_min=64, dur_max=512,
+                       extend_k=1, claim_cap=0, max_live_claims=64, max_live_requests=256,
+                       mode=3, defer_limit=4, retry_permille=100),
 }
 
 
@@ -140,7 +153,7 @@ class Trace:
 
     def field(self, name: str) -> np.ndarray:
         cols = {"usable_blocks": 0, "mode": 1, "n_events": 2, "n_chains": 3, "max_live_claims": 4,
-                "max_live_requests": 5, "n_claim_slots": 6, "reserved": 7}
+                "max_live_requests": 5, "n_claim_slots": 6, "defer_limit": 7}
         if name in cols:
             return self.desc[:, cols[name]]
         if name == "event_offset":
@@ -227,6 +240,7 @@ def make_desc(pools: list[dict], n_events: list[int], n_slots: list[int]) -> np.
         desc[i, 4] = p.get("max_live_claims", max(n_slots[i], 1))
         desc[i, 5] = p.get("max_live_requests", max(n_events[i], 1))
         desc[i, 6] = p.get("n_claim_slots", n_slots[i])
+        desc[i, 7] = p.get("defer_limit", 0)
         desc[i, 8:10] = np.array([e_acc], np.int64).view(np.int32)
         desc[i, 10:12] = np.array([s_acc], np.int64).view(np.int32)
         e_acc += n_events[i]
@@ -272,9 +286,13 @@ def nop():
     return ev(EV_NOP)
 
 
+def retry():
+    return ev(EV_RETRY)
+
+
 def from_pools(pools: list[dict], name: str = "handmade") -> Trace:
     """Batch from explicit pools: each dict has usable_blocks, mode, events (list of 4-int lists),
-    optional n_chains / max_live_claims / max_live_requests / n_claim_slots."""
+    optional n_chains / max_live_claims / max_live_requests / n_claim_slots / defer_limit."""
     evs = [np.asarray(p["events"], np.int64).reshape(-1, 4) for p in pools]
     n_ev = [int(e.shape[0]) for e in evs]
     n_sl = [int(np.sum((e[:, 0] & 15) == EV_CLAIM)) if e.size else 0 for e in evs]
@@ -345,6 +363,7 @@ def generate(name: str, n_pools: int | None = None, first_pool: int = 0, **overr
     if n_pools is None:
         n_pools = total - first_pool
     g = GenParams()
+    g.mode = -1
     for k, v in cfg.items():
         if k == "mix":
             for i, x in enumerate(v):

@@ -80,11 +80,15 @@ typedef struct {
   int32_t claim_cap;       /* >0: at most this many outstanding claims (a CLAIM drawn at the cap
                               becomes a RELEASE)                                                 */
   int32_t max_live_claims, max_live_requests; /* <= 0: the pool's own CLAIM / PREFILL count      */
+  int32_t retry_permille;  /* > 0: share of RETRY events, drawn before the mix                   */
+  int32_t defer_limit;     /* the pools' defer limit (0 = no deferral)                           */
+  int32_t mode;            /* < 0: policy = pool index mod 4; else this policy for every pool    */
   double zipf_s;
   uint64_t seed0;
 } gen_params;
 
-enum { EV_PREFILL = 0, EV_EXTEND = 1, EV_CLAIM = 2, EV_FINISH = 3, EV_RELEASE = 4, EV_DEMOTE = 5 };
+enum { EV_PREFILL = 0, EV_EXTEND = 1, EV_CLAIM = 2, EV_FINISH = 3, EV_RELEASE = 4, EV_DEMOTE = 5,
+       EV_RETRY = 7 };
 
 /* Draw the events of pools [first_pool, first_pool + n_pools).
  * desc: 12 int32 per pool; events: n_pools * n_events * 4 int32.
@@ -113,6 +117,10 @@ int64_t rkc_tracegen(const gen_params* g, int64_t first_pool, int32_t n_pools, i
     int32_t n_claims = 0, n_prefill = 0, outstanding = 0;
     for (int32_t t = 0; t < g->n_events; t++) {
       int32_t* e = ev + 4 * (size_t)t;
+      if (g->retry_permille > 0 && uniform_int(&r, 0, 999) < g->retry_permille) {
+        e[0] = EV_RETRY; e[1] = e[2] = e[3] = 0;
+        continue;
+      }
       int32_t u = uniform_int(&r, 0, cum[5] - 1), type = 0;
       while (type < 5 && u >= cum[type]) type++;
       if (type == EV_CLAIM && g->claim_cap > 0 && outstanding >= g->claim_cap) type = EV_RELEASE;
@@ -170,13 +178,13 @@ int64_t rkc_tracegen(const gen_params* g, int64_t first_pool, int32_t n_pools, i
     int32_t* d = desc + 12 * (size_t)i;
     int64_t ev_off = (int64_t)g->n_events * (first_pool + i) - (int64_t)g->n_events * first_pool;
     d[0] = g->usable_blocks;
-    d[1] = (int32_t)(pool % 4);
+    d[1] = g->mode >= 0 ? g->mode : (int32_t)(pool % 4);
     d[2] = g->n_events;
     d[3] = g->chain_pick == 0 ? n_claims : nch;
     d[4] = g->max_live_claims > 0 ? g->max_live_claims : n_claims;
     d[5] = g->max_live_requests > 0 ? g->max_live_requests : n_prefill;
     d[6] = n_claims;
-    d[7] = 0;
+    d[7] = g->defer_limit;
     d[8] = (int32_t)(uint32_t)(uint64_t)ev_off;
     d[9] = (int32_t)((uint64_t)ev_off >> 32);
     d[10] = (int32_t)(uint32_t)(uint64_t)slots;

@@ -16,13 +16,15 @@ GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
 
 MODES = {"lru": 0, "soft": 1, "noadmit": 2, "hard": 3}
 CODES = {"admit": 0, "evict_resident": 1, "refused_claim": 2, "refused_capacity": 3, "matfail": 4,
-         "demoted": 5, "released": 6, "finished": 7, "noop": 8, "invalid": 9}
+         "demoted": 5, "released": 6, "finished": 7, "noop": 8, "invalid": 9, "deferred": 10}
 FLAGS = {"expired": 1, "pred_fail": 2, "harm": 4, "post_release_loss": 8, "evict_unclaimed": 16,
          "noadmit_drop": 32, "lowered": 64, "shadow": 128}
 TEL = {"victims": 10, "resident": 11, "post_release": 12, "dropped": 13, "hits": 14,
        "accepted": 15, "approx": 16, "shadow": 17, "rejected": 18, "harm": 19, "pred_fail": 20,
        "expired": 21, "demoted": 22, "released": 23, "peak_active": 24, "active": 25, "cached": 26,
-       "free": 27, "protected": 28, "live_requests": 29, "live_claims": 30, "status": 31}
+       "free": 27, "protected": 28, "live_requests": 29, "live_claims": 30, "status": 31,
+       "n_deferred": 32, "retry_served": 33, "retry_refused": 34, "queued": 35,
+       "n_admit": 0, "n_refused_claim": 2, "n_refused_capacity": 3}
 DECISIONS = {"none": 0, "accepted": 1, "approx": 2, "shadow": 3, "rejected": 4}
 STATES = {"submitted": 0, "observed": 1, "materialized": 2, "demoted": 3, "expired": 4,
           "released": 5, "harmed": 6, "rejected": 7}
@@ -39,16 +41,20 @@ def _kv(tokens):
 
 
 def parse(path):
+    return parse_text(open(path).read(), os.path.basename(path))
+
+
+def parse_text(text, name):
     pools = []
     cur = None
     section = None
-    for raw in open(path):
+    for raw in text.splitlines():
         line = raw.split("#", 1)[0].rstrip()
         if not line.strip():
             continue
         s = line.strip()
         if s.startswith("[pool"):
-            cur = dict(name=s[5:-1].strip(), events=[], expect=[], file=os.path.basename(path))
+            cur = dict(name=s[5:-1].strip(), events=[], expect=[], file=name)
             pools.append(cur)
             section = None
         elif s == "events:":
@@ -96,10 +102,15 @@ def to_trace(tg, fixtures):
                 evs.append(tg.demote(g("sel")))
             elif kind == "nop":
                 evs.append(tg.nop())
+            elif kind == "retry":
+                evs.append(tg.retry())
             else:
                 raise ValueError(kind)
         pools.append(dict(usable_blocks=int(f["usable"]), mode=MODES[f["mode"]],
-                          n_chains=int(f.get("chains", 0)), events=evs))
+                          n_chains=int(f.get("chains", 0)), events=evs,
+                          defer_limit=int(f.get("defer_limit", 0)),
+                          **({"max_live_requests": int(f["max_requests"])} if "max_requests" in f
+                             else {})))
     return tg.from_pools(pools, "golden")
 
 

@@ -5,14 +5,19 @@ import numpy as np
 
 
 def random_pool(rng: np.random.Generator, U: int, mode: int, n_events: int, n_chains: int = 3,
-                p_malformed: float = 0.03, tight_tables: bool = False) -> dict:
-    """One pool of arbitrary events, including malformed ones and table overflows."""
+                p_malformed: float = 0.03, tight_tables: bool = False, defer_limit: int = 0,
+                p_retry: float = 0.15) -> dict:
+    """One pool of arbitrary events, including malformed ones and table overflows.  With
+    defer_limit > 0 the pool defers blocked prefills and a share p_retry of its events are RETRY
+    (pools without deferral draw exactly the random numbers they always did)."""
     from paper_2605_24259_amd import tracegen as tg
     evs = []
     for _ in range(n_events):
         r = rng.random()
         sel = int(rng.integers(0, 1 << 32))
-        if r < 0.26:
+        if defer_limit > 0 and rng.random() < p_retry:
+            e = tg.retry()
+        elif r < 0.26:
             S = int(rng.integers(1, U + 3))
             if rng.random() < 0.3:
                 c, P = -1, 0
@@ -41,7 +46,7 @@ def random_pool(rng: np.random.Generator, U: int, mode: int, n_events: int, n_ch
             kind = int(rng.integers(0, 6))
             e = list(e)
             if kind == 0:
-                e[0] = (e[0] & ~15) | int(rng.integers(7, 16))    # unknown type
+                e[0] = (e[0] & ~15) | int(rng.integers(7, 16))    # RETRY or an unknown type
             elif kind == 1:
                 e[1] = 0                                           # empty size / footprint
             elif kind == 2 and (e[0] & 15) == 0:
@@ -53,7 +58,7 @@ def random_pool(rng: np.random.Generator, U: int, mode: int, n_events: int, n_ch
             elif kind == 5:
                 e[1] = -5
         evs.append([int(x) for x in e])
-    pool = dict(usable_blocks=U, mode=mode, n_chains=n_chains, events=evs)
+    pool = dict(usable_blocks=U, mode=mode, n_chains=n_chains, events=evs, defer_limit=defer_limit)
     if tight_tables:
         pool["max_live_requests"] = int(rng.integers(1, 4))
         pool["max_live_claims"] = int(rng.integers(1, 4))
@@ -63,9 +68,12 @@ def random_pool(rng: np.random.Generator, U: int, mode: int, n_events: int, n_ch
 
 
 def random_batch(seed: int, n_pools: int, U_range=(2, 9), n_events=(1, 14), n_chains=3,
-                 tight_every: int = 5, p_malformed: float = 0.03, caps=None):
+                 tight_every: int = 5, p_malformed: float = 0.03, caps=None, defer=False,
+                 hard_share: float = 0.0):
     """caps = (live requests, live claims): table capacities of the pools that are not tight
-    (default: one entry per PREFILL / CLAIM event, which never overflows)."""
+    (default: one entry per PREFILL / CLAIM event, which never overflows).  defer: every pool
+    defers, with a defer limit of 1..3.  hard_share: that share of the pools use hard protection
+    (the only policy under which a refusal is attributed to claims), the rest cycle the policies."""
     from paper_2605_24259_amd import tracegen as tg
     rng = np.random.default_rng(seed)
     pools = []
@@ -73,8 +81,14 @@ def random_batch(seed: int, n_pools: int, U_range=(2, 9), n_events=(1, 14), n_ch
         U = int(rng.integers(U_range[0], U_range[1]))
         ne = int(rng.integers(n_events[0], n_events[1] + 1))
         tight = tight_every > 0 and i % tight_every == tight_every - 1
-        pool = random_pool(rng, U, i % 4, ne, n_chains=n_chains, p_malformed=p_malformed,
-                           tight_tables=tight)
+        mode = i % 4
+        dl = 0
+        if defer:
+            dl = int(rng.integers(1, 4))
+            if rng.random() < hard_share:
+                mode = 3
+        pool = random_pool(rng, U, mode, ne, n_chains=n_chains, p_malformed=p_malformed,
+                           tight_tables=tight, defer_limit=dl)
         if caps is not None and not tight:
             pool["max_live_requests"], pool["max_live_claims"] = caps
         pools.append(pool)

@@ -61,7 +61,7 @@ int main(void) {
         lines = subprocess.check_output([exe], text=True).split("\n")
     sizes = [int(x) for x in lines[0].split()]
     offs = [int(x) for x in lines[1].split()]
-    assert sizes == [16, 48, 16, 40, 128, ctypes.sizeof(rkc.Batch)]
+    assert sizes == [16, 48, 16, 40, 256, ctypes.sizeof(rkc.Batch)]
     assert offs == [32, 40, rkc.Batch.d_pools.offset, rkc.Batch.scratch_bytes.offset]
 
 
@@ -91,7 +91,7 @@ def _batch(**kw):
 
 
 def test_version_and_strings(lib):
-    assert lib.rkc_abi_version() == 1
+    assert lib.rkc_abi_version() == 2
     assert lib.rkc_status_string(0) == b"ok"
     assert lib.rkc_status_string(-5).startswith(b"scratch")
     assert lib.rkc_status_string(-99) == b"unknown status"

@@ -9,6 +9,7 @@ the replay is causal, so a prefix of a pool's outcomes is an exact sample).
 import numpy as np
 import pytest
 
+from tests import deferral_cases
 from tests import golden_fixtures as gf
 from tests import randtrace
 from tests.gpu_util import compare_pools, gpu_replay, say
@@ -112,11 +113,12 @@ def _properties(trace, gpu):
     U = trace.field("usable_blocks").astype(np.int64)
     ne = trace.field("n_events")
     assert (pt[:, 31] & ~7 == 0).all(), "internal fault or descriptor status"
-    assert (pt[:, :10].sum(1) == ne).all()
+    assert (pt[:, :10].sum(1) + pt[:, 32] == ne).all()
     assert (pt[:, 25] + pt[:, 26] + pt[:, 27] == U).all()
     assert (pt[:, 24] <= U).all() and (pt[:, 24] >= pt[:, 25]).all()
+    assert (pt[:, 36:] == 0).all()
     code = out[:, 0] & 255
-    ref = (code == 2) | (code == 3)
+    ref = (code == 2) | (code == 3) | (code == 10)
     Ue = np.repeat(U, ne)
     assert (out[ref, 2].astype(np.int64) + out[ref, 3] > Ue[ref]).all()
 
@@ -255,3 +257,88 @@ def test_general_kernel_on_compact_batches(oracle_mod, tg, case):
     compare_pools(trace, gen, ora)
     lean = gpu_replay(trace)
     compare_pools(trace, lean, ora)
+
+
+# ---- active deferral: both kernels ------------------------------------------------------------
+KERNELS = ["compact", "general"]
+
+
+def _kflags(kernel):
+    import paper_2605_24259_amd as rkc
+    return rkc.FLAG_GENERAL_KERNEL if kernel == "general" else 0
+
+
+def _both_kernel(oracle_mod, trace, kernel, pools=None):
+    say(f"case {trace.name} ({kernel} kernel): {trace.n_pools} pools, {trace.n_events} events")
+    gpu = gpu_replay(trace, flags=_kflags(kernel))
+    ora = oracle_mod.replay(trace.desc, trace.events, trace.n_claim_slots, pools=pools,
+                            threads=ORACLE_THREADS)
+    assert not ora[3].any(), "oracle invariant check failed"
+    return gpu, ora
+
+
+@pytest.mark.parametrize("kernel", KERNELS)
+def test_deferral_fixtures(oracle_mod, tg, kernel):
+    """The paper's live scheduler run (defer once, then a terminal refusal) and the hand-derived
+    deferral cases: the expected values and the oracle, on both kernels."""
+    fx = [f for f in gf.all_fixtures() if f["file"].startswith("live_scheduler")]
+    fx += deferral_cases.fixtures()
+    trace = gf.to_trace(tg, fx)
+    gpu, ora = _both_kernel(oracle_mod, trace, kernel)
+    errs = gf.check(fx, trace, *gpu)
+    assert not errs, "\n".join(errs)
+    compare_pools(trace, gpu, ora)
+
+
+@pytest.mark.parametrize("kernel", KERNELS)
+@pytest.mark.parametrize("seed", [51, 52])
+def test_random_deferral_tiny(oracle_mod, kernel, seed):
+    """Deferring pools of <= 12 blocks (mostly hard protection), RETRY events, tight tables
+    (queue rings of 1-3 entries wrap), malformed events."""
+    trace = randtrace.random_batch(seed, 3000, U_range=(1, 13), n_events=(0, 40), n_chains=3,
+                                   defer=True, hard_share=0.8)
+    gpu, ora = _both_kernel(oracle_mod, trace, kernel)
+    compare_pools(trace, gpu, ora)
+    assert gpu[1][:, 32].sum() > 200 and gpu[1][:, 33].sum() > 20
+
+
+@pytest.mark.parametrize("kernel", KERNELS)
+def test_random_deferral_medium(oracle_mod, kernel):
+    """Deferring pools up to 300 blocks and 400 events (several 64-event tiles), tables of 256
+    requests and 64 claims or tighter: retried requests are inserted into long live lists."""
+    trace = randtrace.random_batch(61, 400, U_range=(8, 300), n_events=(1, 400), n_chains=9,
+                                   p_malformed=0.01, tight_every=7, caps=(256, 64), defer=True,
+                                   hard_share=0.8)
+    gpu, ora = _both_kernel(oracle_mod, trace, kernel)
+    compare_pools(trace, gpu, ora)
+    assert gpu[1][:, 33].sum() > 50
+
+
+@pytest.mark.parametrize("variant", ["wide", "wide_global_lists"])
+def test_deferral_storage_layouts(oracle_mod, tg, variant):
+    """Deferral with 32-bit LDS state and with the live lists in global scratch."""
+    import paper_2605_24259_amd as rkc
+    trace = randtrace.random_batch(71, 600, U_range=(2, 200), n_events=(1, 200), n_chains=7,
+                                   tight_every=9, defer=True, hard_share=0.8)
+    lim = dict(trace.limits())
+    lim["max_usable_blocks"] = 40000
+    if variant == "wide_global_lists":
+        lim["max_live_requests"] = 20000
+        lim["max_live_claims"] = 4096
+    say(f"case deferral layouts/{variant}")
+    gpu = rkc.DeviceBatch(trace.desc, trace.events, trace.n_claim_slots, lim).replay().results()
+    ora = oracle_mod.replay(trace.desc, trace.events, trace.n_claim_slots, threads=ORACLE_THREADS)
+    compare_pools(trace, gpu, ora)
+
+
+def test_zipf_defer_full_sampled(oracle_mod, tg):
+    """65,536 hard-protection pools x 2,048 blocks x 1,024 events with deferral and 10% retries,
+    in the benchmark's launch configuration; sampled pools against the oracle."""
+    trace = tg.generate("zipf_defer")
+    pools = _sample(trace.n_pools, 96)
+    gpu, ora = _both(oracle_mod, trace, pools=pools)
+    compare_pools(trace, gpu, ora, pools=pools)
+    _properties(trace, gpu)
+    pt = gpu[1]
+    assert pt[:, 32].sum() > 20 * trace.n_pools
+    assert (pt[:, 35] <= trace.field("max_live_requests")).all()

@@ -139,3 +139,61 @@ def test_bruteforce_exhaustive_pairs(oracle_mod, tg):
                 pools.append(dict(usable_blocks=4, mode=mode, n_chains=3, events=prep + [x, y]))
     trace = tg.from_pools(pools)
     _brute_compare(oracle_mod, trace)
+
+
+@pytest.mark.parametrize("seed", [201, 202, 203])
+def test_bruteforce_random_deferral(oracle_mod, seed):
+    """Oracle == brute-force model on deferring pools (active deferral, §3.5): prefills blocked by
+    hard claims are queued, RETRY events serve, defer again or refuse them, tables overflow."""
+    trace = randtrace.random_batch(seed, 400, U_range=(1, 9), n_events=(8, 30), n_chains=2,
+                                   defer=True, hard_share=0.8)
+    _brute_compare(oracle_mod, trace)
+    _, ptel, _ = _check_clean(oracle_mod, trace)
+    assert ptel[:, 32].sum() > 50 and ptel[:, 33].sum() > 5 and ptel[:, 34].sum() > 5
+
+
+def test_deferral_accounting(oracle_mod):
+    """Identities of the deferral queue on every pool: each deferred request is served, refused or
+    still queued at the end; DEFERRED outcomes appear only in hard-protection pools and carry a
+    valid refusal record; outcome counts (incl. DEFERRED) sum to the event count."""
+    trace = randtrace.random_batch(17, 400, U_range=(4, 60), n_events=(1, 120), n_chains=4,
+                                   defer=True, hard_share=0.7, p_malformed=0.01)
+    out, ptel, _ = _check_clean(oracle_mod, trace)
+    U, ne, eo = trace.field("usable_blocks"), trace.field("n_events"), trace.field("event_offset")
+    assert (ptel[:, :10].sum(1) + ptel[:, 32] == ne).all()
+    assert (ptel[:, 36:] == 0).all()
+    total_queued = 0
+    for i in range(trace.n_pools):
+        o = out[eo[i]: eo[i] + ne[i]]
+        code = o[:, 0] & 255
+        ev = trace.events[eo[i]: eo[i] + ne[i]]
+        typ = ev[:, 0] & 15
+        d = code == 10
+        if d.any():
+            assert trace.field("mode")[i] == 3
+            assert (o[d, 2].astype(np.int64) + o[d, 3] > U[i]).all() and (o[d, 3] <= U[i]).all()
+            assert (o[d, 2] > 0).all() and ((o[d, 0].view(np.uint32) >> 16) >= 1).all()
+        # distinct requests that entered the queue: the PREFILLs whose outcome was DEFERRED
+        entered = int(((typ == 0) & d).sum())
+        assert entered == ptel[i, 33] + ptel[i, 34] + ptel[i, 35]
+        # a RETRY never reports more DEFERRED outcomes for one request than the limit allows
+        assert int(d.sum()) <= entered * int(trace.field("defer_limit")[i])
+        total_queued += entered
+    assert total_queued > 100
+
+
+def test_deferral_off_is_plain_refusal(oracle_mod, tg):
+    """defer_limit 0 reproduces the outputs of a pool without deferral, and RETRY is then a NOOP."""
+    rng = np.random.default_rng(9)
+    pools, plain = [], []
+    for k in range(80):
+        base = randtrace.random_pool(rng, int(rng.integers(4, 40)), 3, 50, n_chains=3,
+                                     defer_limit=2)
+        pools.append(dict(base, defer_limit=0))
+        plain.append(dict(base, defer_limit=0,
+                          events=[e if (e[0] & 15) != 7 else tg.nop() for e in base["events"]]))
+    a = tg.from_pools(pools)
+    b = tg.from_pools(plain)
+    oa, pa, ca = _check_clean(oracle_mod, a)
+    ob, pb, cb = _check_clean(oracle_mod, b)
+    assert np.array_equal(oa, ob) and np.array_equal(pa, pb) and np.array_equal(ca, cb)

@@ -8,6 +8,7 @@
 import numpy as np
 import pytest
 
+from tests import deferral_cases
 from tests import golden_fixtures as gf
 
 MODES = ("lru", "soft", "noadmit", "hard")
@@ -124,3 +125,14 @@ def test_refusal_record_fields(oracle_mod, tg):
                           active_live_blocks_required=70, resident_plus_active_blocks=130,
                           usable_blocks=80, capacity_shortfall_blocks=50)
     assert record["resident_plus_active_blocks"] > record["usable_blocks"]
+
+
+def test_deferral_closed_forms(oracle_mod, tg):
+    """Hand-derived deferral cases (tests/deferral_cases.py)."""
+    fx = deferral_cases.fixtures()
+    trace = gf.to_trace(tg, fx)
+    out, ptel, ctel, chk = oracle_mod.replay(trace.desc, trace.events, trace.n_claim_slots)
+    assert not chk.any(), [oracle_mod.check_names(int(c)) for c in chk]
+    errs = gf.check(fx, trace, out, ptel, ctel)
+    assert not errs, "\n".join(errs)
+
