@@ -33,7 +33,7 @@
 extern "C" {
 #endif
 
-#define RKC_ABI_VERSION 2
+#define RKC_ABI_VERSION 3
 
 /* Hard limits of this implementation (checked on the host and per pool on the device). */
 #define RKC_MAX_USABLE_BLOCKS   (1 << 22) /* U per pool                                        */
@@ -43,7 +43,8 @@ extern "C" {
 /* ----------------------------------------------------------------------------------------------
  * Event: 16 bytes = 4 x int32, pool-major (CSR by rkc_pool_desc.event_offset).
  *
- * w0 = type[0:4] | hard[4] | prio[5:7] | reserved[7:16] | duration[16:32] (u16, 0 = no expiry)
+ * w0 = type[0:4] | hard[4] | prio[5:7] | demotable[7] | best_effort[8] | reserved[9:16]
+ *      | duration[16:32] (u16, 0 = no expiry); bits 4..8 and the duration matter for CLAIM only
  *
  *   PREFILL (0)  active request r = the event's step index.  w1 = S blocks, w2 = shared chain c
  *                (ignored when P = 0), w3 = shared prefix P (0 <= P <= S).  Positions [0,P) are
@@ -56,6 +57,11 @@ extern "C" {
  *                w3 = materialization threshold T (0 <= T <= L), hard/prio/duration from w0.
  *                (§3.1 ResidentClaimInput: footprint, protection mode, optional duration_steps,
  *                materialization predicate "leading contiguous survival >= T".)
+ *                demotable (§3.1 protection modes): the runtime may demote the claim (hard -> soft)
+ *                to serve an active request, in pools with RKC_MODE_RELAX, always before the
+ *                eviction that breaks its predicate.  best_effort (§3.1: telemetry only): the claim
+ *                is observed (decision SHADOW) in every policy, protects nothing, never expires and
+ *                its loss is never harm.
  *   FINISH  (3)  w1 = selector: the request finishes and releases its live KV.
  *   RELEASE (4)  w1 = selector over live claims (ascending id): the claim is released.
  *   DEMOTE  (5)  w1 = selector over materialized hard-requested claims: hard -> soft (§3.1, §3.2).
@@ -87,7 +93,14 @@ enum rkc_pool_mode {
   RKC_MODE_LRU = 0,     /* native eviction: claims are only observed (shadow)                  */
   RKC_MODE_SOFT = 1,    /* soft priority: claims accepted, hard requests lowered (approximate)  */
   RKC_MODE_NOADMIT = 2, /* write no-admit: request KV never becomes reusable; claims observed   */
-  RKC_MODE_HARD = 3     /* hard protected-resident exclusion with scheduler-visible refusal     */
+  RKC_MODE_HARD = 3,    /* hard protected-resident exclusion with scheduler-visible refusal     */
+  /* flag OR'ed into rkc_pool_desc.mode: runtime relaxation (§3.5 mechanism table "relax resident
+   * claim": the active side is served by demoting resident state).  In a hard-protection pool,
+   * before an active PREFILL / EXTEND / RETRY is refused on behalf of claims, the demotable claims
+   * among the blocking ones are demoted, lowest priority first, then lowest id, until the request
+   * fits; none is demoted when even all of them would not make it fit.  No effect under the other
+   * policies (they never refuse on behalf of claims). */
+  RKC_MODE_RELAX = 16
 };
 
 /* ----------------------------------------------------------------------------------------------
@@ -95,7 +108,7 @@ enum rkc_pool_mode {
  * -------------------------------------------------------------------------------------------- */
 typedef struct rkc_pool_desc {
   int32_t usable_blocks;     /* U, 1..RKC_MAX_USABLE_BLOCKS; block size is 16 tokens (§4.1)     */
-  int32_t mode;              /* enum rkc_pool_mode                                               */
+  int32_t mode;              /* enum rkc_pool_mode, optionally | RKC_MODE_RELAX                  */
   int32_t n_events;          /* events of this pool                                              */
   int32_t n_chains;          /* valid shared chain ids are [0, n_chains)                         */
   int32_t max_live_claims;   /* live-claim table capacity; a CLAIM beyond it is INVALID          */
@@ -114,8 +127,9 @@ typedef struct rkc_pool_desc {
  * Outcome: 16 bytes, one per event, at the event's index.   (§3.1 ClaimEvent; §5.4 refusal record)
  *
  * w0 = code[0:8] | flags[8:16] | n16[16:32]
- *   n16 = number of blocking claims for REFUSED_CLAIM, 0 for REFUSED_CAPACITY, otherwise the
- *         number of claims that expired at the start of this step; saturates at 65535.
+ *   n16 = number of blocking claims for REFUSED_CLAIM and DEFERRED, 0 for REFUSED_CAPACITY, the
+ *         number of claims the runtime demoted for RELAXED, otherwise the number of claims that
+ *         expired at the start of this step; saturates at 65535.
  * w1 = id, w2 = a, w3 = b:
  *   ADMIT / EVICT_RESIDENT  after PREFILL: id = request, a = resident victims, b = leading hits h
  *                           after EXTEND : id = request, a = resident victims, b = active blocks after
@@ -128,9 +142,12 @@ typedef struct rkc_pool_desc {
  *   NOOP / INVALID          id = -1, a = 0, b = 0
  *   DEFERRED                the refusal record of REFUSED_CLAIM (id = smallest blocking claim id,
  *                           a = Pr, b = required, n16 = blocking claims): the request is queued
+ *   RELAXED                 served after the runtime demoted claims (RKC_MODE_RELAX): id, a, b as
+ *                           ADMIT for the event (PREFILL, EXTEND or RETRY), n16 = claims demoted
  * RETRY reports the retried request: served -> ADMIT / EVICT_RESIDENT with id = the request (its
  * PREFILL step), a = resident victims, b = leading hits; still blocked -> DEFERRED; refused for good
- * -> REFUSED_CLAIM / REFUSED_CAPACITY; full live-request table -> INVALID (the request stays queued).
+ * -> REFUSED_CLAIM / REFUSED_CAPACITY; full live-request table -> INVALID (the request stays queued);
+ * served after relaxation -> RELAXED.
  * -------------------------------------------------------------------------------------------- */
 typedef struct rkc_outcome {
   int32_t w[4];
@@ -147,7 +164,8 @@ enum rkc_outcome_code {
   RKC_OC_FINISHED = 7,
   RKC_OC_NOOP = 8,
   RKC_OC_INVALID = 9,
-  RKC_OC_DEFERRED = 10
+  RKC_OC_DEFERRED = 10,
+  RKC_OC_RELAXED = 11
 };
 
 enum rkc_outcome_flag {
@@ -165,6 +183,7 @@ enum rkc_outcome_flag {
  * Claim telemetry: 40 bytes = 10 x int32, one slot per CLAIM event in step order.
  *   [0] claim_id (step index; -1 for an unused slot)
  *   [1] packed = decision[0:4] | state[4:8] | hard_req[8] | prio[9:11] | eff_prot[11:13]
+ *                | demotable[13] | best_effort[14] | demoted_by_runtime[15]
  *   [2] accept_step [3] demote_step [4] expire_step [5] release_step [6] pred_fail_step
  *   [7] harm_step   (every step field is -1 when the transition never happened)
  *   [8] blocked_count: active refusals this claim was attributed to
@@ -207,7 +226,8 @@ enum rkc_protection { RKC_PROT_NONE = 0, RKC_PROT_SOFT = 1, RKC_PROT_HARD = 2 };
  *   [29] final live requests [30] final live claims
  *   [31] status: 0, or RKC_PS_* bits
  *   [32] DEFERRED outcomes [33] deferred requests served by RETRY [34] deferred requests refused by
- *   RETRY [35] deferred requests still queued at the end          [36..63] 0 (reserved)
+ *   RETRY [35] deferred requests still queued at the end
+ *   [36] RELAXED outcomes [37] claims demoted by the runtime          [38..63] 0 (reserved)
  * -------------------------------------------------------------------------------------------- */
 typedef struct rkc_pool_telemetry {
   int32_t w[64];

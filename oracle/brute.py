@@ -11,7 +11,9 @@ eight blocks.  Where the C oracle sorts candidates and walks the reuse index, th
   * evaluates a claim's predicate as set containment: positions 0..T-1 of its chain are all present
     in the reuse index (§3.1 useful resident value; §5.4 L6);
   * counts every quantity from explicit sets rather than counters;
-  * keeps deferred requests (active deferral, §3.5) as a plain list whose first element is retried.
+  * keeps deferred requests (active deferral, §3.5) as a plain list whose first element is retried;
+  * relaxes (§3.1 demotable; §3.5 relax resident claim) by trying ever longer prefixes of the
+    demotion order on a copy of the claim states and recounting the available blocks as sets.
 Only meant for tiny inputs: its cost is exponential in the pool size.
 """
 from __future__ import annotations
@@ -25,9 +27,10 @@ STATE_CODE = {"submitted": 0, "observed": 1, "materialized": 2, "demoted": 3, "e
 DEC_CODE = {None: 0, "accepted": 1, "approx": 2, "shadow": 3, "rejected": 4}
 CODES = {"admit": 0, "evict_resident": 1, "refused_claim": 2, "refused_capacity": 3,
          "matfail": 4, "demoted": 5, "released": 6, "finished": 7, "noop": 8, "invalid": 9,
-         "deferred": 10}
+         "deferred": 10, "relaxed": 11}
 TEL_WORD = {name: code for name, code in CODES.items()}
 TEL_WORD["deferred"] = 32
+TEL_WORD["relaxed"] = 36
 LRU, SOFT, NOADMIT, HARD = range(4)
 MAXF = 1 << 24
 
@@ -39,6 +42,8 @@ def _s32(x: int) -> int:
 
 class Pool:
     def __init__(self, U, mode, n_chains, max_claims, max_reqs, n_slots, defer_limit=0):
+        self.relax_on = bool(mode & 16)
+        mode &= ~16
         self.U, self.mode, self.n_chains = U, mode, n_chains
         self.max_claims, self.max_reqs, self.n_slots = max_claims, max_reqs, n_slots
         self.defer_limit = defer_limit
@@ -153,6 +158,37 @@ class Pool:
             return "refused_claim", min(q["id"] for q in blocking), len(prot), req, len(blocking)
         return "refused_capacity", -1, len(prot), req, 0
 
+    def _available(self, hits):
+        free = self.ids(FREE)
+        return len(free) + len({i for i in self.ids(CACHED) - hits if not self.protected(i)})
+
+    def relax(self, t, need, hits):
+        """Demote the shortest prefix of the demotable blocking claims, ordered by (priority, id),
+        that lets `need` blocks be allocated; nothing when no prefix does."""
+        if self.mode != HARD or not self.relax_on or need <= self._available(hits):
+            return 0
+        cands = []
+        for q in self.live_claims():
+            if q["state"] != "materialized" or q["eff"] != 2 or not q["demotable"]:
+                continue
+            blocks = [self.index[(q["chain"], p)] for p in range(q["L"]) if (q["chain"], p) in self.index]
+            if any(self.blocks[i]["state"] == CACHED and i not in hits for i in blocks):
+                cands.append(q)
+        cands.sort(key=lambda q: (q["prio"], q["id"]))
+        for k in range(1, len(cands) + 1):
+            saved = [q["state"] for q in cands[:k]]
+            for q in cands[:k]:
+                q["state"] = "demoted"
+            ok = need <= self._available(hits)
+            for q, st in zip(cands[:k], saved):
+                q["state"] = st
+            if ok:
+                for q in cands[:k]:
+                    q["state"], q["demote"], q["relaxed"] = "demoted", t, 1
+                self.tel[37] += k
+                return k
+        return 0
+
     def live_request_ids(self):
         return sorted(r for r, q in self.reqs.items() if q["live"])
 
@@ -239,6 +275,7 @@ class Pool:
                 rid = live_req[(e[2] & 0xFFFFFFFF) % len(live_req)]
                 rq = self.reqs[rid]
                 need = e[1]
+                relaxed = self.relax(t, need, set())
                 ok, victims, _, _ = self.choose(need, set())
                 if not ok:
                     code, oid, a, b, n16 = self.refusal(need, set())
@@ -249,22 +286,28 @@ class Pool:
                                               pos=rq["len"] + j, reg=False)
                         rq["blocks"].append(i)
                     rq["len"] += need
-                    code = "evict_resident" if st["resident"] else "admit"
+                    code = "relaxed" if relaxed else "evict_resident" if st["resident"] else "admit"
                     oid, a, b = rid, st["resident"], len(self.ids(ACTIVE))
+                    if relaxed:
+                        n16 = relaxed
                     flags |= (8 if st["post"] else 0) | (16 if st["unclaimed"] else 0)
                     self._tel_victims(st)
                     unreg = st["unreg"]
         elif typ == 2:
             L, c, T = e[1], e[2], e[3]
             q = slot
-            q.update(valid=True, chain=c, L=L, T=T, hard=hard, prio=prio, dur=dur,
-                     eff=(2 if hard else 1) if self.mode == HARD else (1 if self.mode == SOFT else 0))
+            demq, beq = (w0 >> 7) & 1, (w0 >> 8) & 1
+            observe = self.mode in (LRU, NOADMIT) or beq
+            q.update(valid=True, chain=c, L=L, T=T, hard=hard, prio=prio, dur=dur, demotable=demq,
+                     best_effort=beq, relaxed=0,
+                     eff=0 if beq else (2 if hard else 1) if self.mode == HARD
+                     else (1 if self.mode == SOFT else 0))
             h = self.prefix_len(c, L)
             hits = {self.index[(c, p)] for p in range(h)}
             need = L - h
             ok, victims, F, E = self.choose(need, hits)
             if not ok:
-                q["decision"] = "shadow" if self.mode in (LRU, NOADMIT) else "rejected"
+                q["decision"] = "shadow" if observe else "rejected"
                 q["state"] = "rejected"
                 code, oid, a, b = "matfail", t, need, F + E
             else:
@@ -275,7 +318,7 @@ class Pool:
                     self.blocks[i] = dict(state=CACHED, ref=0, lu=t, prod=-1, chain=c, pos=h + j,
                                           reg=True)
                     self.index[(c, h + j)] = i
-                if self.mode in (LRU, NOADMIT):
+                if observe:
                     q["decision"], q["state"] = "shadow", "observed"
                     flags |= 128
                 elif self.mode == SOFT and hard:
@@ -361,6 +404,7 @@ class Pool:
         h = self.prefix_len(c, P) if P > 0 else 0
         hits = {self.index[(c, p)] for p in range(h)}
         need = S - h
+        relaxed = self.relax(t, need, hits)
         ok, victims, _, _ = self.choose(need, hits)
         if not ok:
             return False, self.refusal(need, hits), 0, 0
@@ -387,8 +431,8 @@ class Pool:
         self._tel_victims(st)
         self.tel[14] += h
         flags = (8 if st["post"] else 0) | (16 if st["unclaimed"] else 0)
-        code = "evict_resident" if st["resident"] else "admit"
-        return True, (code, rid, st["resident"], h, None), flags, st["unreg"]
+        code = "relaxed" if relaxed else "evict_resident" if st["resident"] else "admit"
+        return True, (code, rid, st["resident"], h, relaxed or None), flags, st["unreg"]
 
     def _tel_victims(self, st):
         self.tel[10] += st["victims"]
@@ -415,7 +459,8 @@ class Pool:
                 slots.append([q["id"], 0, -1, -1, -1, -1, -1, -1, 0, 0])
                 continue
             packed = DEC_CODE[q["decision"]] | (STATE_CODE[q["state"]] << 4) | (q["hard"] << 8) \
-                | (q["prio"] << 9) | (q["eff"] << 11)
+                | (q["prio"] << 9) | (q["eff"] << 11) | (q["demotable"] << 13) \
+                | (q["best_effort"] << 14) | (q["relaxed"] << 15)
             slots.append([q["id"], packed, q["accept"], q["demote"], q["expire"], q["release"],
                           q["pred_fail"], q["harm"], q["blocked"],
                           self.prefix_len(q["chain"], q["L"])])

@@ -14,7 +14,8 @@
  *     protection mode, priority, optional duration) plus decision, state and step telemetry;
  *   - every step runs: expiry, validation, dispatch, predicate sweep, emission;
  *   - a pool that defers (active deferral, §3.5) queues a prefill refused on behalf of resident
- *     claims; RETRY events later serve it, defer it again or refuse it for good.
+ *     claims; RETRY events later serve it, defer it again or refuse it for good;
+ *   - a pool that relaxes demotes demotable hard claims when that lets an active request be served.
  *
  * Nothing here relies on the prefix shape of what survives: hits are the leading registered run,
  * the predicate walks the reuse index from position 0, victims are chosen by sorting every
@@ -31,10 +32,10 @@
 /* ---- this file's copy of the record layouts -------------------------------------------------- */
 enum { EV_PREFILL = 0, EV_EXTEND = 1, EV_CLAIM = 2, EV_FINISH = 3, EV_RELEASE = 4, EV_DEMOTE = 5,
        EV_NOP = 6, EV_RETRY = 7 };
-enum { MODE_LRU = 0, MODE_SOFT = 1, MODE_NOADMIT = 2, MODE_HARD = 3 };
+enum { MODE_LRU = 0, MODE_SOFT = 1, MODE_NOADMIT = 2, MODE_HARD = 3, MODE_RELAX_FLAG = 16 };
 enum { OC_ADMIT = 0, OC_EVICT_RESIDENT = 1, OC_REFUSED_CLAIM = 2, OC_REFUSED_CAPACITY = 3,
        OC_MATFAIL = 4, OC_DEMOTED = 5, OC_RELEASED = 6, OC_FINISHED = 7, OC_NOOP = 8,
-       OC_INVALID = 9, OC_DEFERRED = 10 };
+       OC_INVALID = 9, OC_DEFERRED = 10, OC_RELAXED = 11 };
 enum { FL_EXPIRED = 1, FL_PRED_FAIL = 2, FL_HARM = 4, FL_POST_RELEASE = 8, FL_UNCLAIMED = 16,
        FL_NOADMIT_DROP = 32, FL_LOWERED = 64, FL_SHADOW = 128 };
 enum { DEC_NONE = 0, DEC_ACCEPTED = 1, DEC_APPROX = 2, DEC_SHADOW = 3, DEC_REJECTED = 4 };
@@ -50,7 +51,7 @@ enum { T_VICTIMS = 10, T_RESIDENT = 11, T_POSTREL = 12, T_DROPPED = 13, T_HITS =
        T_PREDFAIL = 20, T_EXPIRED = 21, T_DEMOTED = 22, T_RELEASED = 23, T_PEAK_ACTIVE = 24,
        T_ACTIVE = 25, T_CACHED = 26, T_FREE = 27, T_PROTECTED = 28, T_LIVE_REQ = 29,
        T_LIVE_CLAIMS = 30, T_STATUS = 31, T_DEFERRED = 32, T_RETRY_SERVED = 33,
-       T_RETRY_REFUSED = 34, T_QUEUED = 35, N_TEL = 64 };
+       T_RETRY_REFUSED = 34, T_QUEUED = 35, T_RELAXED = 36, T_RUNTIME_DEMOTED = 37, N_TEL = 64 };
 
 /* invariant check bits (oracle-only diagnostics) */
 enum {
@@ -95,6 +96,9 @@ typedef struct {
   int32_t decision, state, eff;
   int32_t accept, demote, expire, release, pred_fail, harm;
   int32_t blocked;
+  int32_t demotable;   /* the client lets the runtime demote it (§3.1 demotable)               */
+  int32_t best_effort; /* telemetry only (§3.1 best_effort)                                    */
+  int32_t relaxed;     /* demoted by the runtime to serve an active request                     */
 } claim_t;
 
 /* A deferred active request waiting in the scheduler queue (active deferral, §3.5 mechanism table;
@@ -106,6 +110,7 @@ typedef struct {
 
 typedef struct {
   int32_t U, mode, n_events, n_chains, max_claims, max_reqs, n_slots, defer_limit;
+  int32_t relax;   /* the runtime relaxes demotable hard claims before refusing (mode flag 16) */
   block_t* b;
   request_t* req;  /* indexed by request id (= step)           */
   claim_t* cl;     /* indexed by slot                          */
@@ -417,6 +422,69 @@ static int32_t count_active(pool_t* p) {
   return a;
 }
 
+/* FREE blocks plus eviction candidates (CACHED, outside the current hit set, not hard-protected). */
+static int64_t available(pool_t* p) {
+  build_buckets(p);
+  int64_t n = 0;
+  for (int32_t i = 0; i < p->U; i++) {
+    block_t* b = &p->b[i];
+    if (b->state == BLK_FREE) n++;
+    else if (b->state == BLK_CACHED && !b->mark && !block_protected(p, b)) n++;
+  }
+  return n;
+}
+
+/* Runtime relaxation before an active allocation of `need` blocks (hits already marked): §3.1
+ * demotable (the downgrade must come before the predicate-breaking eviction) and §3.5 "relax
+ * resident claim" (the active side is served by demoting resident state).  When the pool relaxes
+ * and hard protection makes the allocation infeasible, the demotable claims among those blocking it
+ * (materialized hard claims covering a cached block outside the hits, as for attribution) are
+ * demoted one at a time, lowest priority first, then lowest id, until the allocation fits.  If
+ * demoting all of them would not make it fit, none is demoted.  Returns the number demoted. */
+static int32_t relax(pool_t* p, int64_t need, int32_t t) {
+  if (p->mode != MODE_HARD || !p->relax) return 0;
+  if (need <= available(p)) return 0;
+  int32_t* order = p->tmp;  /* max(events, U) entries: at least one per claim slot */
+  int32_t n = 0;
+  for (int32_t s = 0; s < p->n_cl; s++) {
+    claim_t* q = &p->cl[s];
+    if (!(claim_live(q) && q->state == ST_MATERIALIZED && q->eff == PROT_HARD && q->demotable)) continue;
+    int blocking = 0;
+    for (int32_t pos = 0; pos < q->L && !blocking; pos++) {
+      int32_t* slot = idx_at(p, q->chain, pos);
+      if (!slot || *slot < 0) continue;
+      block_t* b = &p->b[*slot];
+      if (b->state == BLK_CACHED && !b->mark) blocking = 1;
+    }
+    if (blocking) order[n++] = s;
+  }
+  /* insertion sort by (priority, id) */
+  for (int32_t i = 1; i < n; i++) {
+    int32_t v = order[i], j = i;
+    while (j > 0 && (p->cl[order[j - 1]].prio > p->cl[v].prio ||
+                     (p->cl[order[j - 1]].prio == p->cl[v].prio && p->cl[order[j - 1]].id > p->cl[v].id))) {
+      order[j] = order[j - 1];
+      j--;
+    }
+    order[j] = v;
+  }
+  for (int32_t k = 0; k < n; k++) {
+    p->cl[order[k]].state = ST_DEMOTED;  /* tentative */
+    if (need <= available(p)) {
+      for (int32_t j = 0; j <= k; j++) {
+        claim_t* q = &p->cl[order[j]];
+        q->state = ST_MATERIALIZED;
+        set_state(p, q, ST_DEMOTED);
+        q->demote = t;
+        q->relaxed = 1;
+      }
+      return k + 1;
+    }
+  }
+  for (int32_t k = 0; k < n; k++) p->cl[order[k]].state = ST_MATERIALIZED;
+  return 0;
+}
+
 /* Serve an active prefill of request rid (S blocks, shared chain c, shared prefix P) at step t: the
  * chain's leading registered run below P is hit and the rest allocated (§3.4 feasibility).  Served:
  * returns 1 with o = {code, id, a, b, n16 = -1}; the blocks turn ACTIVE, last used at t, produced by
@@ -427,6 +495,7 @@ static int serve_prefill(pool_t* p, int32_t t, int32_t rid, int32_t S, int32_t c
   int32_t h = Pp > 0 ? leading_hits(p, c, Pp) : 0;
   int64_t need = (int64_t)S - h;
   if (h) mark_hits(p, c, h, 1);
+  int32_t relaxed = relax(p, need, t);
   alloc_t r = alloc_blocks(p, need);
   if (!r.feasible) {
     refusal(p, need, t, o);
@@ -455,8 +524,9 @@ static int serve_prefill(pool_t* p, int32_t t, int32_t rid, int32_t S, int32_t c
     }
     req_push(rq, bid);
   }
-  o[0] = r.resident > 0 ? OC_EVICT_RESIDENT : OC_ADMIT;
-  o[1] = rid; o[2] = r.resident; o[3] = h; o[4] = -1;
+  o[0] = relaxed ? OC_RELAXED : r.resident > 0 ? OC_EVICT_RESIDENT : OC_ADMIT;
+  o[1] = rid; o[2] = r.resident; o[3] = h; o[4] = relaxed ? relaxed : -1;
+  p->tel[T_RUNTIME_DEMOTED] += relaxed;
   if (r.post_release) *flags |= FL_POST_RELEASE;
   if (r.unclaimed) *flags |= FL_UNCLAIMED;
   p->tel[T_VICTIMS] += r.victims; p->tel[T_RESIDENT] += r.resident;
@@ -476,7 +546,8 @@ static void pool_free(pool_t* p) {
 
 static int pool_init(pool_t* p, const int32_t* d, const int32_t* ev) {
   memset(p, 0, sizeof *p);
-  p->U = d[0]; p->mode = d[1]; p->n_events = d[2]; p->n_chains = d[3];
+  p->U = d[0]; p->mode = d[1] & ~MODE_RELAX_FLAG; p->relax = (d[1] & MODE_RELAX_FLAG) != 0;
+  p->n_events = d[2]; p->n_chains = d[3];
   p->max_claims = d[4]; p->max_reqs = d[5]; p->n_slots = d[6]; p->defer_limit = d[7];
   if (p->U < 1 || p->n_events < 0 || p->n_chains < 0 || p->n_slots < 0 || p->defer_limit < 0)
     return -1;
@@ -654,6 +725,7 @@ static int replay_pool(const int32_t* d, const int32_t* ev, int32_t* out, int32_
         int32_t rid = livebuf[(uint32_t)e[2] % (uint32_t)n_live_req];
         request_t* rq = &p->req[rid];
         int64_t need = e[1];
+        int32_t relaxed = relax(p, need, t);
         alloc_t r = alloc_blocks(p, need);
         if (!r.feasible) {
           int32_t o[5];
@@ -668,8 +740,10 @@ static int replay_pool(const int32_t* d, const int32_t* ev, int32_t* out, int32_
             req_push(rq, bid);
           }
           rq->len += (int32_t)need;
-          code = r.resident > 0 ? OC_EVICT_RESIDENT : OC_ADMIT;
+          code = relaxed ? OC_RELAXED : r.resident > 0 ? OC_EVICT_RESIDENT : OC_ADMIT;
           id = rid; a = r.resident; bb = count_active(p);
+          if (relaxed) n16 = relaxed;
+          p->tel[T_RUNTIME_DEMOTED] += relaxed;
           if (r.post_release) flags |= FL_POST_RELEASE;
           if (r.unclaimed) flags |= FL_UNCLAIMED;
           p->tel[T_VICTIMS] += r.victims; p->tel[T_RESIDENT] += r.resident;
@@ -683,7 +757,13 @@ static int replay_pool(const int32_t* d, const int32_t* ev, int32_t* out, int32_
       int32_t L = e[1], c = e[2], T = e[3];
       claim_t* q = slot;
       q->valid = 1; q->chain = c; q->L = L; q->T = T; q->hard = hard; q->prio = prio; q->dur = dur;
-      q->eff = p->mode == MODE_HARD ? (hard ? PROT_HARD : PROT_SOFT)
+      q->demotable = (int32_t)((w0 >> 7) & 1u);
+      q->best_effort = (int32_t)((w0 >> 8) & 1u);
+      /* a best-effort claim carries no preservation obligation: it is observed like a claim in a
+       * pool that does not accept claims (§3.1 best_effort: telemetry only) */
+      const int observe = p->mode == MODE_LRU || p->mode == MODE_NOADMIT || q->best_effort;
+      q->eff = q->best_effort ? PROT_NONE
+             : p->mode == MODE_HARD ? (hard ? PROT_HARD : PROT_SOFT)
              : p->mode == MODE_SOFT ? PROT_SOFT : PROT_NONE;
       int32_t h = leading_hits(p, c, L);
       int64_t need = (int64_t)L - h;
@@ -691,7 +771,7 @@ static int replay_pool(const int32_t* d, const int32_t* ev, int32_t* out, int32_
       alloc_t r = alloc_blocks(p, need);
       if (h) mark_hits(p, c, h, 0);
       if (!r.feasible) {
-        q->decision = (p->mode == MODE_LRU || p->mode == MODE_NOADMIT) ? DEC_SHADOW : DEC_REJECTED;
+        q->decision = observe ? DEC_SHADOW : DEC_REJECTED;
         set_state(p, q, ST_REJECTED);
         code = OC_MATFAIL; id = t; a = (int32_t)need; bb = (int32_t)(r.F + r.E);
       } else {
@@ -703,7 +783,7 @@ static int replay_pool(const int32_t* d, const int32_t* ev, int32_t* out, int32_
           b->chain = c; b->pos = h + (int32_t)j;
           do_register(p, bid, c, b->pos);
         }
-        if (p->mode == MODE_LRU || p->mode == MODE_NOADMIT) {
+        if (observe) {
           q->decision = DEC_SHADOW; set_state(p, q, ST_OBSERVED); flags |= FL_SHADOW;
         } else if (p->mode == MODE_SOFT && hard) {
           q->decision = DEC_APPROX; set_state(p, q, ST_MATERIALIZED); flags |= FL_LOWERED;
@@ -815,7 +895,7 @@ static int replay_pool(const int32_t* d, const int32_t* ev, int32_t* out, int32_
     out[4 * (size_t)t + 1] = id;
     out[4 * (size_t)t + 2] = a;
     out[4 * (size_t)t + 3] = bb;
-    p->tel[code == OC_DEFERRED ? T_DEFERRED : code]++;
+    p->tel[code == OC_DEFERRED ? T_DEFERRED : code == OC_RELAXED ? T_RELAXED : code]++;
     int32_t act = count_active(p);
     if (act > peak) peak = act;
     check_step(p, t);
@@ -845,7 +925,8 @@ static int replay_pool(const int32_t* d, const int32_t* ev, int32_t* out, int32_
     }
     claim_t* q = &p->cl[s];
     w[0] = q->id;
-    w[1] = q->valid ? (q->decision | (q->state << 4) | (q->hard << 8) | (q->prio << 9) | (q->eff << 11)) : 0;
+    w[1] = q->valid ? (q->decision | (q->state << 4) | (q->hard << 8) | (q->prio << 9) | (q->eff << 11) |
+                       (q->demotable << 13) | (q->best_effort << 14) | (q->relaxed << 15)) : 0;
     w[2] = q->accept; w[3] = q->demote; w[4] = q->expire; w[5] = q->release;
     w[6] = q->pred_fail; w[7] = q->harm; w[8] = q->blocked;
     w[9] = q->valid ? imin(lead(p, q->chain), q->L) : 0;

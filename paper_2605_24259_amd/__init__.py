@@ -15,7 +15,7 @@ LIB_PATH = os.path.join(_PKG, "librkc.so")
 _lib = None
 
 # layouts and codes of this binding (rkc.h RKC_ABI_VERSION)
-ABI_VERSION = 2
+ABI_VERSION = 3
 POOL_TEL_WORDS = 64
 
 # rkc_batch.flags: replay with the general kernel even where the compact one applies

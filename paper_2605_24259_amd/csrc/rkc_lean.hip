@@ -59,9 +59,11 @@ enum : u32 { DEC_ACCEPTED = 1, DEC_APPROX = 2, DEC_SHADOW = 3, DEC_REJECTED = 4 
 // pool telemetry words accumulated lane-distributed
 enum : u32 { TW_VICTIMS = 10, TW_RESIDENT = 11, TW_POST = 12, TW_DROPPED = 13, TW_HITS = 14,
              TW_ACCEPTED = 15, TW_HARM = 19, TW_PREDFAIL = 20, TW_EXPIRED = 21, TW_DEMOTED = 22,
-             TW_RELEASED = 23, TW_RETRY_SERVED = 33, TW_RETRY_REFUSED = 34 };
+             TW_RELEASED = 23, TW_RETRY_SERVED = 33, TW_RETRY_REFUSED = 34, TW_RUNTIME_DEMOTED = 37 };
 
 // live-claim meta (low half of qc): state[0:3) eff[3:5) hard[5] prio[6:8) pending[8] decision[9:12)
+// demotable[12] best_effort[13] demoted_by_runtime[14]
+constexpr u32 M_DEMQ = 1u << 12, M_BE = 1u << 13, M_RELAXED = 1u << 14;
 __device__ __forceinline__ u32 m_state(u32 m) { return m & 7u; }
 __device__ __forceinline__ u32 m_eff(u32 m) { return (m >> 3) & 3u; }
 __device__ __forceinline__ u32 m_hard(u32 m) { return (m >> 5) & 1u; }
@@ -69,7 +71,8 @@ __device__ __forceinline__ u32 m_prio(u32 m) { return (m >> 6) & 3u; }
 __device__ __forceinline__ u32 m_pend(u32 m) { return (m >> 8) & 1u; }
 __device__ __forceinline__ u32 m_dec(u32 m) { return (m >> 9) & 7u; }
 __device__ __forceinline__ u32 packed_of(u32 m) {
-  return m_dec(m) | (m_state(m) << 4) | (m_hard(m) << 8) | (m_prio(m) << 9) | (m_eff(m) << 11);
+  return m_dec(m) | (m_state(m) << 4) | (m_hard(m) << 8) | (m_prio(m) << 9) | (m_eff(m) << 11) |
+         (((m >> 12) & 7u) << 13);
 }
 
 __device__ __forceinline__ u32 lo16(u32 v) { return v & 0xFFFFu; }
@@ -119,15 +122,15 @@ struct AllocRes {
 
 // ---- one pool ---------------------------------------------------------------------------------
 // NS: 64-key groups (chains <= 64 NS); MODE: the pool policy, fixed at compile time so that each
-// policy's event loop carries only the logic that policy can reach; DEFER: the pool defers (a
-// hard-protection pool with a defer limit), so its loop carries the deferral ring.
-template <int NS, int MODE, bool DEFER>
+// policy's event loop carries only the logic that policy can reach; EXT: a hard-protection pool that
+// defers or relaxes, whose loop carries the deferral ring and the runtime relaxation.
+template <int NS, int MODE, bool EXT>
 struct Lean {
   static constexpr u32 KC = 64u * NS;  // key slots (chains padded to whole lanes)
   // descriptor: the rarely used limits one per lane of `cst`
   static constexpr u32 mode = MODE;
   u32 cst;  // lane 0 U, 1 chains, 2 live-claim cap, 3 live-request cap, 4 claim slots, 5 node cap,
-            // 6 defer limit
+            // 6 defer limit, 7 relaxation on
   u32 lane;
   __device__ __forceinline__ u32 U() const { return rdl(cst, 0); }
   __device__ __forceinline__ u32 nch() const { return rdl(cst, 1); }
@@ -136,13 +139,15 @@ struct Lean {
   __device__ __forceinline__ u32 nslots() const { return rdl(cst, 4); }
   __device__ __forceinline__ u32 ncap() const { return rdl(cst, 5); }
   __device__ __forceinline__ u32 dlim() const { return rdl(cst, 6); }
+  __device__ __forceinline__ u32 relax_on() const { return rdl(cst, 7); }
   // soft levels and acceptance (soft, hard pools: mode bit 0), hard protection, write no-admit
   __device__ __forceinline__ static constexpr bool softl() { return MODE & 1; }
   __device__ __forceinline__ static constexpr bool shadm() { return !(MODE & 1); }
   __device__ __forceinline__ static constexpr bool hardm() { return MODE == RKC_MODE_HARD; }
   __device__ __forceinline__ static constexpr bool noadm() { return MODE == RKC_MODE_NOADMIT; }
-  // only hard protection attributes refusals to claims, so only hard-protection pools can defer
-  __device__ __forceinline__ static constexpr bool defers() { return MODE == RKC_MODE_HARD && DEFER; }
+  // only hard protection refuses on behalf of claims, so only hard-protection pools can defer or
+  // relax
+  __device__ __forceinline__ static constexpr bool ext() { return MODE == RKC_MODE_HARD && EXT; }
   // memory
   lds_u32* kk;
   lds_u32* hist;  // outcomes per code (16 counters; entry 15 collects the lanes past the end)
@@ -619,9 +624,62 @@ struct Lean {
     cold[C_DQC] = 1;
   }
 
+  // Runtime relaxation (§3.1 demotable: the downgrade comes before the predicate-breaking
+  // eviction; §3.5 "relax resident claim": the active side is served by demoting resident state).
+  // Before an active allocation of `need` blocks that hard protection makes infeasible, the
+  // demotable claims among the blocking ones (materialized hard claims reaching a cached position
+  // outside the hits) are picked lowest priority first, then lowest id, until the allocation would
+  // fit; then the picked claims are demoted.  None is demoted when even all would not make it fit.
+  // Returns the number demoted; ghc (the hit chain's record) is re-read when claims were demoted.
+  __device__ __forceinline__ u32 relax(u32 t, u32 need, i32 hc, u32 h, G0& ghc) {
+    u32 k = 0;
+    if (relax_on() && need > F) {
+      u32 E = Eall + fbl;
+      if (hc >= 0) {
+        const u32 lo = max(ghc.hold, ghc.prot);
+        E -= evictable(ghc.n, lo, 0) - evictable(ghc.n, max(lo, h), 0);
+      }
+      u64 avail = (u64)F + E;
+      if ((u64)need > avail) {
+        const u32 m = lo16(qc), c = hi16(qa), L = lo16(qb);
+        u32 cov = chain_hold(c);
+        if ((i32)c == hc) cov = max(cov, h);
+        const bool hm = lane < ncl && m_state(m) == ST_MATERIALIZED && m_eff(m) == RKC_PROT_HARD;
+        const u32 key = (m_prio(m) << 16) | lo16(qa);
+        u64 left = ballot(hm && (m & M_DEMQ) && L > cov);
+        u64 S = 0;
+        for (u32 guard = 0; left && (u64)need > avail && guard < 64; guard++) {
+          const bool mine = (left >> lane) & 1ull;
+          const u32 kmin = wmin(mine ? key : NEVER);
+          const u32 l = (u32)__builtin_ctzll(ballot(mine && key == kmin));
+          const u32 cq = rdl(c, l);
+          const G0 g = rd0(cq);
+          const u32 base = (i32)cq == hc ? max(g.hold, h) : g.hold;
+          const bool on = hm && c == cq;
+          const u32 before = wmax(on && !((S >> lane) & 1ull) ? L : 0u);
+          S |= 1ull << l;
+          left &= ~(1ull << l);
+          const u32 after = wmax(on && !((S >> lane) & 1ull) ? L : 0u);
+          avail += evictable(g.n, base, after) - evictable(g.n, base, before);
+        }
+        if ((u64)need <= avail) {
+          const bool d = (S >> lane) & 1ull;
+          qc = d ? pk((m & ~7u) | ST_DEMOTED | M_RELAXED, hi16(qc)) : qc;
+          qe = d ? pk(t, hi16(qe)) : qe;
+          recompute_lanes(S);
+          k = (u32)__builtin_popcountll(S);
+          tadd(TW_RUNTIME_DEMOTED, k);
+          if (hc >= 0) ghc = rd0((u32)hc);
+        }
+      }
+    }
+    return k;
+  }
+
   // Serve request rid (S blocks, shared chain cc when P > 0, shared prefix P) at step t; late: a
   // retried request, inserted into the live list by id and taken off the deferral ring (dh, dl).
-  // A refusal on behalf of resident claims defers the request in deferring pools (§3.5 active
+  // In relaxing pools, demotable blocking claims are demoted first when that lets it fit.  A
+  // refusal on behalf of resident claims defers the request in deferring pools (§3.5 active
   // deferral): a new one enters the ring, a retried one is deferred again while its deferrals
   // last, else refused for good (§5.4 live scheduler run).
   __device__ __forceinline__ void admit(u32 t, u32 rid, u32 S, u32 cc, u32 P, bool late, u32 dh, u32 dl,
@@ -636,10 +694,12 @@ struct Lean {
       Hc = h > g.hold ? h - g.hold : 0u;
     }
     const u32 need = S - h;
+    u32 relaxed = 0;
+    if (ext()) relaxed = relax(t, need, hc, h, g);
     const AllocRes r = alloc(need, hc, h, g, o.sweep_due);
     if (!r.ok) {
       refusal(need, hc, h, Hc, g, o);
-      if (defers()) {
+      if (ext()) {
         const bool by_claim = o.code == RKC_OC_REFUSED_CLAIM;
         if (late) {
           const u32 cnt = ufl(cold[C_DQC]);
@@ -650,7 +710,7 @@ struct Lean {
             dq_pop(dh, dl);
             tadd(TW_RETRY_REFUSED, 1);
           }
-        } else if (by_claim) {
+        } else if (by_claim && dlim() > 0) {
           const u32x2 hl = *(lds_u32x2*)(cold + C_DQH);
           const u32 h0 = ufl(hl.x), l0 = ufl(hl.y);
           if (l0 < maxr()) {
@@ -683,6 +743,7 @@ struct Lean {
       o.id = (i32)rid;
       o.b = (i32)h;
       served(r, o);
+      if (relaxed) { o.code = RKC_OC_RELAXED; o.n16 = min(relaxed, 65535u); }
     }
   }
 
@@ -698,7 +759,8 @@ struct Lean {
     }
   }
 
-  // RETRY (deferring pools): the oldest deferred request is served, deferred again or refused.
+  // RETRY (hard-protection pools that defer or relax): the oldest deferred request is served,
+  // deferred again or refused.
   __device__ __forceinline__ void ev_retry(u32 t, Out& o) {
     const u32x2 hl = *(lds_u32x2*)(cold + C_DQH);
     const u32 dh = ufl(hl.x), dl = ufl(hl.y);
@@ -713,13 +775,15 @@ struct Lean {
     }
   }
 
-  __device__ __forceinline__ void ev_extend(u32 w1, u32 w2, Out& o) {
+  __device__ __forceinline__ void ev_extend(u32 t, u32 w1, u32 w2, Out& o) {
     const i32 s1 = (i32)w1;
     if (s1 < 1 || s1 > RKC_MAX_FIELD_BLOCKS) {
       o.code = RKC_OC_INVALID;
     } else if (nreq > 0) {
       const u32 i = w2 % nreq, need = w1;
-      const G0 g = {0, 0, 0, 0, 0, 0, 0, 0};
+      G0 g = {0, 0, 0, 0, 0, 0, 0, 0};
+      u32 relaxed = 0;
+      if (ext()) relaxed = relax(t, need, -1, 0, g);
       const AllocRes r = alloc(need, -1, 0, g, o.sweep_due);
       if (!r.ok) {
         refusal(need, -1, 0, 0, g, o);
@@ -731,6 +795,7 @@ struct Lean {
         o.id = (i32)lo16(e.x);
         o.b = (i32)A;
         served(r, o);
+        if (relaxed) { o.code = RKC_OC_RELAXED; o.n16 = min(relaxed, 65535u); }
       }
     }
   }
@@ -752,13 +817,17 @@ struct Lean {
       } else {
         const u32 L = w1, c = w2, T = w3;
         const u32 hardq = (w0 >> 4) & 1u, prio = (w0 >> 5) & 3u, dur = w0 >> 16;
+        // a best-effort claim is observed in every policy (§3.1 best_effort: telemetry only)
+        const u32 beq = (w0 >> 8) & 1u, req_bits = (w0 & (1u << 7) ? M_DEMQ : 0u) | (beq ? M_BE : 0u);
+        const bool obs = shadm() || beq;
         const G0 g = rd0(c);
         const u32 h = min(L, g.n), need = L - h;
         const AllocRes r = alloc(need, (i32)c, h, g, o.sweep_due);
-        const u32 eff = hardm() ? (hardq ? RKC_PROT_HARD : RKC_PROT_SOFT) : (mode == RKC_MODE_SOFT ? RKC_PROT_SOFT : RKC_PROT_NONE);
+        const u32 eff = beq ? RKC_PROT_NONE : hardm() ? (hardq ? RKC_PROT_HARD : RKC_PROT_SOFT)
+                      : (mode == RKC_MODE_SOFT ? RKC_PROT_SOFT : RKC_PROT_NONE);
         if (!r.ok) {
-          const u32 dec = shadm() ? DEC_SHADOW : DEC_REJECTED;
-          const u32 m = ST_REJECTED | (eff << 3) | (hardq << 5) | (prio << 6) | (dec << 9);
+          const u32 dec = obs ? DEC_SHADOW : DEC_REJECTED;
+          const u32 m = ST_REJECTED | (eff << 3) | (hardq << 5) | (prio << 6) | (dec << 9) | req_bits;
           slotcl[s] = make_uint4(c, L, pk(t, packed_of(m)), 1);
           o.code = RKC_OC_MATFAIL;
           o.id = (i32)t;
@@ -768,11 +837,11 @@ struct Lean {
         } else {
           slotcl[s] = make_uint4(c, L, 0, 0);
           const u32 lowered = (mode == RKC_MODE_SOFT) && hardq;
-          const u32 dec = shadm() ? DEC_SHADOW : lowered ? DEC_APPROX : DEC_ACCEPTED;
-          const u32 st = shadm() ? ST_OBSERVED : ST_MATERIALIZED;
-          o.flags |= shadm() ? (u32)RKC_FL_SHADOW : lowered ? (u32)RKC_FL_LOWERED : 0u;
-          const u32 m = st | (eff << 3) | (hardq << 5) | (prio << 6) | (1u << 8) | (dec << 9);
-          const u32 dur_eff = shadm() ? 0u : dur;  // shadow claims never expire
+          const u32 dec = obs ? DEC_SHADOW : lowered ? DEC_APPROX : DEC_ACCEPTED;
+          const u32 st = obs ? ST_OBSERVED : ST_MATERIALIZED;
+          o.flags |= obs ? (u32)RKC_FL_SHADOW : lowered ? (u32)RKC_FL_LOWERED : 0u;
+          const u32 m = st | (eff << 3) | (hardq << 5) | (prio << 6) | (1u << 8) | (dec << 9) | req_bits;
+          const u32 dur_eff = obs ? 0u : dur;  // shadow claims never expire
           const u32 k = ncl++;
           qa = wrl(qa, pk(t, c), k);
           qb = wrl(qb, pk(L, T), k);
@@ -784,7 +853,7 @@ struct Lean {
           G0 g2 = r.victims ? rd0(c) : g;
           g2.covA = max(g2.covA, L);
           // a materialized hard claim in a hard-protection pool protects [0, L)
-          const u32 pp = (hardm() && hardq) ? max(g2.prot, L) : g2.prot;
+          const u32 pp = eff == RKC_PROT_HARD ? max(g2.prot, L) : g2.prot;
           commit(c, g2, max(g2.n, L), g2.hold, pp, L, t);
           o.id = (i32)t;
           o.b = (i32)need;
@@ -885,11 +954,11 @@ struct Lean {
     Out o = {RKC_OC_NOOP, 0, NEVER, 0, -1, 0, 0};
     if (t >= nexp) expire(t, o.flags, expired);
     if (type == RKC_EV_PREFILL) ev_prefill(t, w1, w2, w3, o);
-    else if (type == RKC_EV_EXTEND) ev_extend(w1, w2, o);
+    else if (type == RKC_EV_EXTEND) ev_extend(t, w1, w2, o);
     else if (type == RKC_EV_CLAIM) ev_claim(t, w0, w1, w2, w3, o);
     else if (type == RKC_EV_FINISH) ev_finish(t, w1, o);
     else if (type == RKC_EV_RELEASE || type == RKC_EV_DEMOTE) ev_lifecycle(t, type, w1, o);
-    else if (defers() && type == RKC_EV_RETRY) ev_retry(t, o);
+    else if (ext() && type == RKC_EV_RETRY) ev_retry(t, o);
     else if ((type & ~1u) != RKC_EV_NOP) o.code = RKC_OC_INVALID;  // NOP, or RETRY with no ring
     static_assert(RKC_EV_NOP == 6 && RKC_EV_RETRY == 7, "NOP and RETRY differ in bit 0 only");
     if (o.sweep_due) o.flags |= sweep(t);
@@ -903,10 +972,10 @@ struct Lean {
 };
 
 // Replay of one pool with policy MODE (the descriptor has been checked by the caller).
-template <int NS, int MODE, bool DEFER>
+template <int NS, int MODE, bool EXT>
 __device__ __forceinline__ void replay_pool(const rkc_lean_args& g, const rkc_pool_desc& d, u32 pool,
                                             unsigned char* lds_raw) {
-  typedef Lean<NS, MODE, DEFER> LP;
+  typedef Lean<NS, MODE, EXT> LP;
   LP P;
   P.lane = __lane_id();
   const i64 ev_off = d.event_offset, slot_off = d.claim_slot_offset;
@@ -915,7 +984,7 @@ __device__ __forceinline__ void replay_pool(const rkc_lean_args& g, const rkc_po
     const u32 l = P.lane;
     P.cst = l == 0 ? (u32)d.usable_blocks : l == 1 ? (u32)d.n_chains : l == 2 ? (u32)d.max_live_claims
           : l == 3 ? (u32)d.max_live_requests : l == 4 ? (u32)d.n_claim_slots : l == 5 ? g.node_cap
-          : (u32)d.defer_limit;
+          : l == 6 ? (u32)d.defer_limit : (u32)((d.mode & RKC_MODE_RELAX) != 0);
   }
   const u32 U = (u32)d.usable_blocks, nch = (u32)d.n_chains, nslots = (u32)d.n_claim_slots;
 
@@ -967,10 +1036,10 @@ __device__ __forceinline__ void replay_pool(const rkc_lean_args& g, const rkc_po
     // outcomes per code; resident victims (a) and leading hits (b of a served prefill)
     const u32 oc = o0 & 255u;
     __hip_atomic_fetch_add(P.hist + (P.lane < cnt ? oc : 15u), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-    const bool srv = P.lane < cnt && oc <= RKC_OC_EVICT_RESIDENT;
+    const bool srv = P.lane < cnt && (oc <= RKC_OC_EVICT_RESIDENT || (LP::ext() && oc == RKC_OC_RELAXED));
     P.tadd(TW_RESIDENT, wsum(srv ? o2 : 0u));
     const u32 ty = e0 & 15u;
-    P.tadd(TW_HITS, wsum(srv && (ty == RKC_EV_PREFILL || (LP::defers() && ty == RKC_EV_RETRY)) ? o3 : 0u));
+    P.tadd(TW_HITS, wsum(srv && (ty == RKC_EV_PREFILL || (LP::ext() && ty == RKC_EV_RETRY)) ? o3 : 0u));
   }
 
   const u32 nslot_used = ufl(P.cold[LP::C_NSLOT]);
@@ -1003,6 +1072,7 @@ __device__ __forceinline__ void replay_pool(const rkc_lean_args& g, const rkc_po
     i32 v = (i32)P.tv;
     if (w < 10) v += (i32)P.hist[w];
     if (w == 32) v += (i32)P.hist[RKC_OC_DEFERRED];
+    if (w == 36) v += (i32)P.hist[RKC_OC_RELAXED];
     if (w == TW_VICTIMS) v = (i32)vic;
     else if (w == TW_POST) v = (i32)post;
     else if (w == 24) v = (i32)P.peak;
@@ -1031,7 +1101,8 @@ __global__ __launch_bounds__(64) void rkc_lean(rkc_lean_args g) {
   const bool ev_ok = d.n_events >= 0 && ev_off >= 0 && ev_off + d.n_events <= g.n_events_total;
   const bool sl_ok = d.n_claim_slots >= 0 && slot_off >= 0 && slot_off + d.n_claim_slots <= g.n_slots_total;
   const bool ok = ev_ok && sl_ok && d.usable_blocks >= 1 && d.usable_blocks <= g.max_usable &&
-                  d.mode >= 0 && d.mode <= 3 && d.n_events <= g.max_events && d.n_chains >= 0 &&
+                  (d.mode & ~RKC_MODE_RELAX) >= 0 && (d.mode & ~RKC_MODE_RELAX) <= 3 &&
+                  d.n_events <= g.max_events && d.n_chains >= 0 &&
                   d.n_chains <= g.max_chains && d.max_live_claims >= 0 && d.max_live_claims <= g.max_claims &&
                   d.max_live_requests >= 0 && d.max_live_requests <= g.max_reqs &&
                   d.n_claim_slots <= g.max_slots && d.defer_limit >= 0;
@@ -1044,12 +1115,12 @@ __global__ __launch_bounds__(64) void rkc_lean(rkc_lean_args g) {
     ptel->w[lane] = lane == 31 ? RKC_PS_DESCRIPTOR : (lane == RKC_OC_INVALID && ev_ok) ? d.n_events : 0;
     return;
   }
-  const u32 mode = (u32)__builtin_amdgcn_readfirstlane(d.mode);
-  const u32 defer = (u32)__builtin_amdgcn_readfirstlane(d.defer_limit) > 0;
+  const u32 mode = (u32)__builtin_amdgcn_readfirstlane(d.mode & ~RKC_MODE_RELAX);
+  const u32 ext = (u32)__builtin_amdgcn_readfirstlane(d.defer_limit) > 0 || (d.mode & RKC_MODE_RELAX);
   if (mode == RKC_MODE_LRU) replay_pool<NS, RKC_MODE_LRU, false>(g, d, pool, lds_raw);
   else if (mode == RKC_MODE_SOFT) replay_pool<NS, RKC_MODE_SOFT, false>(g, d, pool, lds_raw);
   else if (mode == RKC_MODE_NOADMIT) replay_pool<NS, RKC_MODE_NOADMIT, false>(g, d, pool, lds_raw);
-  else if (!defer) replay_pool<NS, RKC_MODE_HARD, false>(g, d, pool, lds_raw);
+  else if (!ext) replay_pool<NS, RKC_MODE_HARD, false>(g, d, pool, lds_raw);
   else replay_pool<NS, RKC_MODE_HARD, true>(g, d, pool, lds_raw);
 }
 

@@ -104,9 +104,11 @@ enum : u32 { RQ_ID = 0, RQ_C, RQ_R, RQ_LEN, RQ_ARRAYS };
 enum : u32 { TW_VICTIMS = 10, TW_RESIDENT = 11, TW_POST = 12, TW_DROPPED = 13, TW_HITS = 14,
              TW_ACCEPTED = 15, TW_HARM = 19, TW_PREDFAIL = 20, TW_EXPIRED = 21, TW_DEMOTED = 22,
              TW_RELEASED = 23, TW_DEFERRED = 32, TW_RETRY_SERVED = 33, TW_RETRY_REFUSED = 34,
-             TW_QUEUED = 35 };
+             TW_QUEUED = 35, TW_RELAXED = 36, TW_RUNTIME_DEMOTED = 37 };
 
 // live-claim meta word: state[0:3) eff[3:5) hard[5] prio[6:8) pending[8] decision[9:12)
+// demotable[12] best_effort[13] demoted_by_runtime[14] picked_for_relaxation[15] (16 bits)
+constexpr u32 M_DEMQ = 1u << 12, M_BE = 1u << 13, M_RELAXED = 1u << 14, M_PICK = 1u << 15;
 __device__ __forceinline__ u32 m_state(u32 m) { return m & 7u; }
 __device__ __forceinline__ u32 m_eff(u32 m) { return (m >> 3) & 3u; }
 __device__ __forceinline__ u32 m_hard(u32 m) { return (m >> 5) & 1u; }
@@ -116,7 +118,8 @@ __device__ __forceinline__ u32 m_dec(u32 m) { return (m >> 9) & 7u; }
 __device__ __forceinline__ u32 m_with_state(u32 m, u32 s) { return (m & ~7u) | s; }
 
 __device__ __forceinline__ u32 packed_of(u32 m) {
-  return m_dec(m) | (m_state(m) << 4) | (m_hard(m) << 8) | (m_prio(m) << 9) | (m_eff(m) << 11);
+  return m_dec(m) | (m_state(m) << 4) | (m_hard(m) << 8) | (m_prio(m) << 9) | (m_eff(m) << 11) |
+         (((m >> 12) & 7u) << 13);
 }
 
 // eviction key of a run of candidates with one (level, last use); steps are below 2^24
@@ -210,6 +213,7 @@ struct Pool {
   static constexpr u32 kWordNil = Store<W>::wnil;
   // descriptor
   i32 U, mode, n_events, n_chains, max_claims, max_reqs, n_slots, defer_limit;
+  u32 relax_on;  // the pool relaxes demotable hard claims (mode flag RKC_MODE_RELAX)
   u32 lane;
   // memory
   lds_w* ch;          // chain records, CF_WORDS words each
@@ -700,6 +704,80 @@ struct Pool {
         : lane == TW_POST ? (u32)r.post : lane == TW_HITS ? hits : 0u;
   }
 
+  // Largest footprint of the materialized hard claims on chain c not picked for relaxation.
+  __device__ __forceinline__ u32 hard_extent(u32 c) {
+    u32 pr = 0;
+    for (u32 i = lane; i < ncl; i += 64) {
+      const u32 m = cla(CL_META)[i];
+      if ((u32)cla(CL_C)[i] == c && m_state(m) == ST_MATERIALIZED && m_eff(m) == RKC_PROT_HARD && !(m & M_PICK))
+        pr = max(pr, (u32)cla(CL_L)[i]);
+    }
+    return wave_max(pr);
+  }
+
+  // Runtime relaxation (§3.1 demotable: the downgrade comes before the predicate-breaking
+  // eviction; §3.5 "relax resident claim": the active side is served by demoting resident state).
+  // Before an active allocation of `need` blocks that hard protection makes infeasible, the
+  // demotable claims among the blocking ones (materialized hard claims reaching a cached position
+  // outside the hits) are picked lowest priority first, then lowest id, until the allocation would
+  // fit; then the picked claims are demoted.  None is demoted when even all would not make it fit.
+  // Returns the number demoted.
+  __device__ __forceinline__ u32 relax(u32 t, i32 need, i32 hc, u32 h) {
+    u32 k = 0;
+    if (relax_on && need > F) {
+      i64 avail = (i64)F + candidates(hc, h);
+      if ((i64)need > avail) {
+        for (u32 guard = 0; (i64)need > avail && guard <= ncl; guard++) {
+          u32 best = 0xFFFFFFFFu, bi = 0;
+          for (u32 i = lane; i < ncl; i += 64) {
+            const u32 m = cla(CL_META)[i];
+            if (m_state(m) != ST_MATERIALIZED || m_eff(m) != RKC_PROT_HARD || !(m & M_DEMQ) || (m & M_PICK)) continue;
+            const u32 c = cla(CL_C)[i];
+            u32 cov = (u32)ch[c * CF_WORDS + CF_HOLD];
+            if ((i32)c == hc) cov = max(cov, h);
+            if ((u32)cla(CL_L)[i] <= cov) continue;  // not blocking: no cached position outside the hits
+            const u32 key = (m_prio(m) << 24) | (u32)cla(CL_ID)[i];
+            if (key < best) { best = key; bi = i; }
+          }
+          const u32 wb = wave_min(best);
+          if (wb == 0xFFFFFFFFu) break;
+          const u64 at = ballot(best == wb);
+          const u32 i = (u32)rdlane((i32)bi, (u32)__builtin_ctzll(at));
+          const u32 c = ufl(cla(CL_C)[i]);
+          const u32 before = hard_extent(c);
+          cla(CL_META)[i] = ufl(cla(CL_META)[i]) | M_PICK;  // every lane, one value
+          lists_fence();
+          const u32 after = hard_extent(c);
+          const uint4 g0 = cg(c, 0);
+          const u32 base = (i32)c == hc ? max(g0.y, h) : g0.y;
+          avail += evictable(g0.x, base, after) - evictable(g0.x, base, before);
+          k++;
+        }
+        const bool fits = (i64)need <= avail;
+        for (u32 i = lane; i < ncl; i += 64) {
+          const u32 m = cla(CL_META)[i];
+          if (!(m & M_PICK)) continue;
+          if (fits) {
+            cla(CL_META)[i] = (m_with_state(m, ST_DEMOTED) & ~M_PICK) | M_RELAXED;
+            cla(CL_DEM)[i] = t;
+            mk[cla(CL_C)[i]] |= MK_RECOMP;
+          } else {
+            cla(CL_META)[i] = m & ~M_PICK;
+          }
+        }
+        lists_fence();
+        if (fits) {
+          __builtin_amdgcn_wave_barrier();
+          recompute_marked(MK_RECOMP);
+          tadd(TW_RUNTIME_DEMOTED, k);
+        } else {
+          k = 0;
+        }
+      }
+    }
+    return k;
+  }
+
   // One event.  Returns the outcome words.
   //
   // Control flow is kept to two switches over a small integer: uniform conditions held in u32
@@ -795,7 +873,9 @@ struct Pool {
       need = w1 - (i32)h;
     }
 
-    // One allocation site for prefill, extend and claim.
+    // One allocation site for prefill, extend and claim; active requests may first relax claims.
+    u32 relaxed = 0;
+    if (mode == RKC_MODE_HARD && (kind == K_PREFILL || kind == K_EXTEND)) relaxed = relax(t, need, hc, h);
     AllocRes r = {1, 0, 0, 0, 0, 0};
     if (kind == K_PREFILL || kind == K_EXTEND || kind == K_CLAIM) r = alloc(need, hc, h, sweep_due);
     if (!r.ok && kind != K_CLAIM) {
@@ -871,13 +951,16 @@ struct Pool {
       case K_CLAIM: {
         const i32 L = w1, T = w3;
         const u32 c = (u32)w2;
-        const u32 eff = mode == RKC_MODE_HARD ? (hardq ? RKC_PROT_HARD : RKC_PROT_SOFT)
+        // a best-effort claim is observed in every policy (§3.1 best_effort: telemetry only)
+        const u32 demq = (uw0 >> 7) & 1u, beq = (uw0 >> 8) & 1u;
+        const u32 eff = beq ? RKC_PROT_NONE : mode == RKC_MODE_HARD ? (hardq ? RKC_PROT_HARD : RKC_PROT_SOFT)
                       : mode == RKC_MODE_SOFT ? RKC_PROT_SOFT : RKC_PROT_NONE;
-        const u32 shadow = (u32)(mode == RKC_MODE_LRU) | (u32)(mode == RKC_MODE_NOADMIT);
+        const u32 shadow = (u32)(mode == RKC_MODE_LRU) | (u32)(mode == RKC_MODE_NOADMIT) | beq;
+        const u32 req_bits = (demq ? M_DEMQ : 0u) | (beq ? M_BE : 0u);
         u32 dec;
         if (!r.ok) {
           dec = shadow ? DEC_SHADOW : DEC_REJECTED;
-          const u32 m = ST_REJECTED | (eff << 3) | (hardq << 5) | (prio << 6) | (dec << 9);
+          const u32 m = ST_REJECTED | (eff << 3) | (hardq << 5) | (prio << 6) | (dec << 9) | req_bits;
           write_record(s, (i32)t, packed_of(m), -1, -1, -1, -1, -1, -1, 0);
           code = RKC_OC_MATFAIL; id = (i32)t; a = need; b = F + r.E;
         } else {
@@ -885,7 +968,7 @@ struct Pool {
           dec = shadow ? DEC_SHADOW : lowered ? DEC_APPROX : DEC_ACCEPTED;
           const u32 st = shadow ? ST_OBSERVED : ST_MATERIALIZED;
           flags |= shadow ? (u32)RKC_FL_SHADOW : lowered ? (u32)RKC_FL_LOWERED : 0u;
-          const u32 m = st | (eff << 3) | (hardq << 5) | (prio << 6) | (1u << 8) | (dec << 9);
+          const u32 m = st | (eff << 3) | (hardq << 5) | (prio << 6) | (1u << 8) | (dec << 9) | req_bits;
           const u32 k = ncl++;
           // only a materialized claim with a duration expires (shadow claims never do)
           const u32 dur_eff = shadow ? 0u : dur;
@@ -904,7 +987,7 @@ struct Pool {
           tn = max(g0.x, (u32)L);
           th = g0.y;
           // a materialized hard claim in a hard-protection pool protects [0, L)
-          tpr = (mode == RKC_MODE_HARD && hardq) ? max(g0.z, (u32)L) : g0.z;
+          tpr = eff == RKC_PROT_HARD ? max(g0.z, (u32)L) : g0.z;
           tx = (u32)L;
           id = (i32)t; b = need;
           count_victims(r, 0);
@@ -1004,7 +1087,8 @@ struct Pool {
         break;
     }
     if (kind == K_PREFILL || kind == K_EXTEND || (kind == K_CLAIM && r.ok)) {
-      code = r.resident > 0 ? RKC_OC_EVICT_RESIDENT : RKC_OC_ADMIT;
+      code = relaxed ? RKC_OC_RELAXED : r.resident > 0 ? RKC_OC_EVICT_RESIDENT : RKC_OC_ADMIT;
+      if (relaxed) n16 = min(relaxed, 65535u);
       a = r.resident;
       flags |= (r.post ? (u32)RKC_FL_POST_RELEASE_LOSS : 0u) | (r.unclaimed ? (u32)RKC_FL_EVICT_UNCLAIMED : 0u);
     }
@@ -1025,7 +1109,7 @@ struct Pool {
     a = quiet ? 0 : a;
     b = quiet ? 0 : b;
     n16 = n16 == NIL ? min(expired, 65535u) : n16;
-    tadd(code == RKC_OC_DEFERRED ? (u32)TW_DEFERRED : (u32)code, 1);
+    tadd(code == RKC_OC_DEFERRED ? (u32)TW_DEFERRED : code == RKC_OC_RELAXED ? (u32)TW_RELAXED : (u32)code, 1);
     peak = max(peak, A);
     return make_int4((i32)((u32)code | (flags << 8) | (n16 << 16)), id, a, b);
   }
@@ -1040,7 +1124,8 @@ __global__ __launch_bounds__(64) void rkc_replay_wave(Args g) {
   Pool<W, kGL> P;
   P.lane = lane_id();
   const rkc_pool_desc d = g.pools[pool];
-  P.U = d.usable_blocks; P.mode = d.mode; P.n_events = d.n_events; P.n_chains = d.n_chains;
+  P.U = d.usable_blocks; P.mode = d.mode & ~RKC_MODE_RELAX; P.n_events = d.n_events; P.n_chains = d.n_chains;
+  P.relax_on = (d.mode & RKC_MODE_RELAX) != 0;
   P.max_claims = d.max_live_claims; P.max_reqs = d.max_live_requests; P.n_slots = d.n_claim_slots;
   const i64 ev_off = d.event_offset, slot_off = d.claim_slot_offset;
   rkc_pool_telemetry* ptel = g.pool_tel + pool;

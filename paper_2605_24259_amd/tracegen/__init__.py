@@ -31,6 +31,7 @@ _lib = None
 SEED0 = 260524259
 
 EV_PREFILL, EV_EXTEND, EV_CLAIM, EV_FINISH, EV_RELEASE, EV_DEMOTE, EV_NOP, EV_RETRY = range(8)
+MODE_RELAX = 16  # pool mode flag: the runtime demotes demotable hard claims to serve active requests
 MODE_LRU, MODE_SOFT, MODE_NOADMIT, MODE_HARD = range(4)
 MODE_NAMES = ("lru", "soft", "noadmit", "hard")
 
@@ -63,6 +64,7 @@ class GenParams(ctypes.Structure):
         ("retry_permille", ctypes.c_int32),
         ("defer_limit", ctypes.c_int32),
         ("mode", ctypes.c_int32),
+        ("demotable_permille", ctypes.c_int32),
         ("zipf_s", ctypes.c_double),
         ("seed0", ctypes.c_uint64),
     ]
@@ -107,6 +109,16 @@ CONFIGS = {
                        claim_thresh=0, hard_permille=500, prio_max=3, dur_min=64, dur_max=512,
                        extend_k=1, claim_cap=0, max_live_claims=64, max_live_requests=256,
                        mode=3, defer_limit=4, retry_permille=100),
+    # The zipf pools under hard protection with runtime relaxation: half of the claims allow
+    # demotion, and the runtime demotes blocking ones (lowest priority first) to serve an active
+    # request before refusing it.
+    "zipf_relax": dict(cfg_id=7, n_pools=65536, usable_blocks=2048, n_events=1024,
+                       mix=(400, 300, 150, 100, 50, 0), prefill_dist=1, prefill_min=4,
+                       prefill_max=1536, chain_pick=1, n_chains=256, chain_len_min=32,
+                       chain_len_max=512, claim_len=0, claim_len_min=0, claim_len_max=0,
+                       claim_thresh=0, hard_permille=500, prio_max=3, dur_min=64, dur_max=512,
+                       extend_k=1, claim_cap=0, max_live_claims=64, max_live_requests=256,
+                       mode=3 | MODE_RELAX, demotable_permille=500),
 }
 
 
@@ -249,9 +261,11 @@ def make_desc(pools: list[dict], n_events: list[int], n_slots: list[int]) -> np.
 
 
 def ev(type_: int, w1: int = 0, w2: int = 0, w3: int = 0, hard: int = 0, prio: int = 0,
-       dur: int = 0) -> list[int]:
-    """Encode one event (w0 = type | hard << 4 | prio << 5 | duration << 16)."""
-    w0 = (type_ & 15) | ((hard & 1) << 4) | ((prio & 3) << 5) | ((dur & 0xFFFF) << 16)
+       dur: int = 0, demotable: int = 0, best_effort: int = 0) -> list[int]:
+    """Encode one event (w0 = type | hard << 4 | prio << 5 | demotable << 7 | best_effort << 8 |
+    duration << 16)."""
+    w0 = ((type_ & 15) | ((hard & 1) << 4) | ((prio & 3) << 5) | ((demotable & 1) << 7)
+          | ((best_effort & 1) << 8) | ((dur & 0xFFFF) << 16))
     if w0 >= 1 << 31:
         w0 -= 1 << 32
     w = [w0, w1, w2, w3]
@@ -266,8 +280,9 @@ def extend(k, sel=0):
     return ev(EV_EXTEND, k, sel)
 
 
-def claim(L, c, T=None, hard=0, prio=0, dur=0):
-    return ev(EV_CLAIM, L, c, L if T is None else T, hard=hard, prio=prio, dur=dur)
+def claim(L, c, T=None, hard=0, prio=0, dur=0, demotable=0, best_effort=0):
+    return ev(EV_CLAIM, L, c, L if T is None else T, hard=hard, prio=prio, dur=dur,
+              demotable=demotable, best_effort=best_effort)
 
 
 def finish(sel=0):

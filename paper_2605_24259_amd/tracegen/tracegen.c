@@ -82,7 +82,8 @@ typedef struct {
   int32_t max_live_claims, max_live_requests; /* <= 0: the pool's own CLAIM / PREFILL count      */
   int32_t retry_permille;  /* > 0: share of RETRY events, drawn before the mix                   */
   int32_t defer_limit;     /* the pools' defer limit (0 = no deferral)                           */
-  int32_t mode;            /* < 0: policy = pool index mod 4; else this policy for every pool    */
+  int32_t mode;            /* < 0: policy = pool index mod 4; else this mode for every pool       */
+  int32_t demotable_permille; /* > 0: share of CLAIM events marked demotable (extra draw only then) */
   double zipf_s;
   uint64_t seed0;
 } gen_params;
@@ -164,8 +165,9 @@ int64_t rkc_tracegen(const gen_params* g, int64_t first_pool, int32_t n_pools, i
         int32_t hard = (int32_t)(uniform_int(&r, 0, 999) < g->hard_permille);
         int32_t prio = uniform_int(&r, 0, g->prio_max);
         int32_t dur = g->dur_max > 0 ? uniform_int(&r, g->dur_min, g->dur_max) : 0;
+        int32_t dem = g->demotable_permille > 0 && uniform_int(&r, 0, 999) < g->demotable_permille;
         e[0] = (int32_t)((uint32_t)EV_CLAIM | ((uint32_t)hard << 4) | ((uint32_t)prio << 5) |
-                         ((uint32_t)dur << 16));
+                         ((uint32_t)dem << 7) | ((uint32_t)dur << 16));
         e[1] = L; e[2] = c; e[3] = T;
         n_claims++;
         outstanding++;

@@ -16,14 +16,16 @@ GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
 
 MODES = {"lru": 0, "soft": 1, "noadmit": 2, "hard": 3}
 CODES = {"admit": 0, "evict_resident": 1, "refused_claim": 2, "refused_capacity": 3, "matfail": 4,
-         "demoted": 5, "released": 6, "finished": 7, "noop": 8, "invalid": 9, "deferred": 10}
+         "demoted": 5, "released": 6, "finished": 7, "noop": 8, "invalid": 9, "deferred": 10,
+         "relaxed": 11}
 FLAGS = {"expired": 1, "pred_fail": 2, "harm": 4, "post_release_loss": 8, "evict_unclaimed": 16,
          "noadmit_drop": 32, "lowered": 64, "shadow": 128}
 TEL = {"victims": 10, "resident": 11, "post_release": 12, "dropped": 13, "hits": 14,
        "accepted": 15, "approx": 16, "shadow": 17, "rejected": 18, "harm": 19, "pred_fail": 20,
        "expired": 21, "demoted": 22, "released": 23, "peak_active": 24, "active": 25, "cached": 26,
        "free": 27, "protected": 28, "live_requests": 29, "live_claims": 30, "status": 31,
-       "n_deferred": 32, "retry_served": 33, "retry_refused": 34, "queued": 35,
+       "n_deferred": 32, "retry_served": 33, "retry_refused": 34, "queued": 35, "n_relaxed": 36,
+       "runtime_demoted": 37,
        "n_admit": 0, "n_refused_claim": 2, "n_refused_capacity": 3}
 DECISIONS = {"none": 0, "accepted": 1, "approx": 2, "shadow": 3, "rejected": 4}
 STATES = {"submitted": 0, "observed": 1, "materialized": 2, "demoted": 3, "expired": 4,
@@ -89,7 +91,8 @@ def to_trace(tg, fixtures):
             g = lambda k, d=0: int(kv.get(k, d))
             if kind == "claim":
                 evs.append(tg.claim(g("L"), g("c"), g("T", g("L")), hard=g("hard"), prio=g("prio"),
-                                    dur=g("dur")))
+                                    dur=g("dur"), demotable=g("demotable"),
+                                    best_effort=g("best_effort")))
             elif kind == "prefill":
                 evs.append(tg.prefill(g("S"), g("c", -1), g("P")))
             elif kind == "extend":
@@ -106,7 +109,8 @@ def to_trace(tg, fixtures):
                 evs.append(tg.retry())
             else:
                 raise ValueError(kind)
-        pools.append(dict(usable_blocks=int(f["usable"]), mode=MODES[f["mode"]],
+        mode = MODES[f["mode"]] | (tg.MODE_RELAX if int(f.get("relax", 0)) else 0)
+        pools.append(dict(usable_blocks=int(f["usable"]), mode=mode,
                           n_chains=int(f.get("chains", 0)), events=evs,
                           defer_limit=int(f.get("defer_limit", 0)),
                           **({"max_live_requests": int(f["max_requests"])} if "max_requests" in f
@@ -152,7 +156,9 @@ def check(fixtures, trace, outcomes, pool_tel, claim_tel):
                 w = claim_tel[so[i] + s]
                 packed = int(w[1])
                 got = dict(decision=packed & 15, state=(packed >> 4) & 15, hard=(packed >> 8) & 1,
-                           prio=(packed >> 9) & 3, eff=(packed >> 11) & 3)
+                           prio=(packed >> 9) & 3, eff=(packed >> 11) & 3,
+                           demotable=(packed >> 13) & 1, best_effort=(packed >> 14) & 1,
+                           relaxed=(packed >> 15) & 1)
                 for k, idx in CLAIM_FIELDS.items():
                     got[k] = int(w[idx])
                 for k, v in kv.items():

@@ -6,10 +6,12 @@ import numpy as np
 
 def random_pool(rng: np.random.Generator, U: int, mode: int, n_events: int, n_chains: int = 3,
                 p_malformed: float = 0.03, tight_tables: bool = False, defer_limit: int = 0,
-                p_retry: float = 0.15) -> dict:
+                p_retry: float = 0.15, relax: bool = False) -> dict:
     """One pool of arbitrary events, including malformed ones and table overflows.  With
     defer_limit > 0 the pool defers blocked prefills and a share p_retry of its events are RETRY
-    (pools without deferral draw exactly the random numbers they always did)."""
+    (pools without deferral draw exactly the random numbers they always did).  With relax, claims
+    are demotable or best-effort at random (extra draws only then); the caller sets the pool's
+    relaxation flag."""
     from paper_2605_24259_amd import tracegen as tg
     evs = []
     for _ in range(n_events):
@@ -32,8 +34,12 @@ def random_pool(rng: np.random.Generator, U: int, mode: int, n_events: int, n_ch
             c = int(rng.integers(0, n_chains))
             T = int(rng.integers(0, L + 1))
             dur = 0 if rng.random() < 0.5 else int(rng.integers(1, 8))
+            dem = be = 0
+            if relax:
+                dem = int(rng.random() < 0.6)
+                be = int(rng.random() < 0.12)
             e = tg.claim(L, c, T, hard=int(rng.integers(0, 2)), prio=int(rng.integers(0, 4)),
-                         dur=dur)
+                         dur=dur, demotable=dem, best_effort=be)
         elif r < 0.76:
             e = tg.finish(sel)
         elif r < 0.85:
@@ -69,11 +75,13 @@ def random_pool(rng: np.random.Generator, U: int, mode: int, n_events: int, n_ch
 
 def random_batch(seed: int, n_pools: int, U_range=(2, 9), n_events=(1, 14), n_chains=3,
                  tight_every: int = 5, p_malformed: float = 0.03, caps=None, defer=False,
-                 hard_share: float = 0.0):
+                 hard_share: float = 0.0, relax=False):
     """caps = (live requests, live claims): table capacities of the pools that are not tight
     (default: one entry per PREFILL / CLAIM event, which never overflows).  defer: every pool
     defers, with a defer limit of 1..3.  hard_share: that share of the pools use hard protection
-    (the only policy under which a refusal is attributed to claims), the rest cycle the policies."""
+    (the only policy under which a refusal is attributed to claims), the rest cycle the policies.
+    relax: every pool relaxes (mode flag) and claims are demotable / best-effort at random; with
+    defer also set, pools both relax and defer."""
     from paper_2605_24259_amd import tracegen as tg
     rng = np.random.default_rng(seed)
     pools = []
@@ -85,10 +93,13 @@ def random_batch(seed: int, n_pools: int, U_range=(2, 9), n_events=(1, 14), n_ch
         dl = 0
         if defer:
             dl = int(rng.integers(1, 4))
+        if defer or relax:
             if rng.random() < hard_share:
                 mode = 3
         pool = random_pool(rng, U, mode, ne, n_chains=n_chains, p_malformed=p_malformed,
-                           tight_tables=tight, defer_limit=dl)
+                           tight_tables=tight, defer_limit=dl, relax=relax)
+        if relax:
+            pool["mode"] = mode | tg.MODE_RELAX
         if caps is not None and not tight:
             pool["max_live_requests"], pool["max_live_claims"] = caps
         pools.append(pool)

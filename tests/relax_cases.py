@@ -1,0 +1,176 @@
+"""Hand-derived cases of runtime relaxation and best-effort claims, in the fixture format of
+tests/golden_fixtures.py.
+
+§3.1 protection modes: a demotable claim may be downgraded before loss, provided the demotion comes
+before the predicate-breaking eviction; a best-effort claim is telemetry only.  §3.5 mechanism
+table, "relax resident claim": the active side is served by demoting resident state.  §5.4 L4: when
+demotion precedes the loss, the 60/70/80 probe loses 50 blocks after release and harms nothing.
+
+Pools with mode flag `relax` demote, before refusing an active request on behalf of claims, the
+demotable claims among the blocking ones, lowest priority first, then lowest id, until the request
+fits; none when even all of them would not make it fit.  Expected values are worked out by hand from
+the feasibility inequality Pr + req <= U (§3.4) and the eviction order (level, last use, position).
+"""
+from tests import golden_fixtures as gf
+
+RELAX_CASES = """
+# The 60/70/80 probe with a demotable hard claim in a relaxing pool: the runtime demotes the claim,
+# then the prefill evicts 50 of its blocks as post-release loss; no harm (§5.4 L4 counts).
+[pool probe_relaxed]
+usable = 80
+mode = hard
+relax = 1
+chains = 2
+events:
+  claim L=60 c=0 T=60 hard=1 prio=3 demotable=1
+  prefill S=70 c=1 P=0
+expect:
+  t0 code=admit b=60 flags=
+  t1 code=relaxed id=1 a=50 b=0 n16=1 flags=pred_fail|post_release_loss
+  tel n_relaxed=1 runtime_demoted=1 resident=50 post_release=50 harm=0 cached=10 active=70
+  tel demoted=0 n_refused_claim=0
+  claim0 state=demoted demote=1 pred_fail=1 harm=-1 lead_end=10 demotable=1 relaxed=1 eff=2
+
+# Without the pool flag the same claim protects as any hard claim: attributed refusal.
+[pool probe_no_relax_flag]
+usable = 80
+mode = hard
+chains = 2
+events:
+  claim L=60 c=0 T=60 hard=1 prio=3 demotable=1
+  prefill S=70 c=1 P=0
+expect:
+  t1 code=refused_claim id=0 a=60 b=70 n16=1
+  claim0 state=materialized demote=-1 relaxed=0 blocked=1
+
+# A relaxing pool never demotes a claim that does not allow it.
+[pool probe_not_demotable]
+usable = 80
+mode = hard
+relax = 1
+chains = 2
+events:
+  claim L=60 c=0 T=60 hard=1 prio=3
+  prefill S=70 c=1 P=0
+expect:
+  t1 code=refused_claim id=0 a=60 b=70 n16=1
+  tel n_relaxed=0 runtime_demoted=0
+
+# Lowest priority first, and only as many as needed: 40 free + 30 from the priority-0 claim cover
+# the 60 blocks; its top 20 positions go (level 1), the priority-1 claim keeps its protection.
+[pool lowest_priority_first]
+usable = 100
+mode = hard
+relax = 1
+chains = 3
+events:
+  claim L=30 c=0 T=30 hard=1 prio=1 demotable=1
+  claim L=30 c=1 T=30 hard=1 prio=0 demotable=1
+  prefill S=60 c=2 P=0
+expect:
+  t2 code=relaxed id=2 a=20 b=0 n16=1 flags=pred_fail|post_release_loss
+  claim0 state=materialized demote=-1 lead_end=30 relaxed=0
+  claim1 state=demoted demote=2 pred_fail=2 lead_end=10 relaxed=1
+  tel runtime_demoted=1 protected=30 cached=40
+
+# Equal priorities: the older claim goes first.
+[pool oldest_first]
+usable = 100
+mode = hard
+relax = 1
+chains = 3
+events:
+  claim L=30 c=0 T=30 hard=1 prio=2 demotable=1
+  claim L=30 c=1 T=30 hard=1 prio=2 demotable=1
+  prefill S=60 c=2 P=0
+expect:
+  t2 code=relaxed id=2 a=20 n16=1
+  claim0 state=demoted demote=2 lead_end=10
+  claim1 state=materialized demote=-1 lead_end=30
+
+# Both demotable claims are needed: 40 free + 30 + 30 >= 90.
+[pool both_needed]
+usable = 100
+mode = hard
+relax = 1
+chains = 3
+events:
+  claim L=30 c=0 T=30 hard=1 prio=1 demotable=1
+  claim L=30 c=1 T=30 hard=1 prio=0 demotable=1
+  prefill S=90 c=2 P=0
+expect:
+  t2 code=relaxed id=2 a=50 n16=2 flags=pred_fail|post_release_loss
+  tel runtime_demoted=2 cached=10 active=90 harm=0
+  claim0 state=demoted demote=2
+  claim1 state=demoted demote=2
+
+# Demoting every demotable blocker would still leave 40 + 30 < 80: nothing is demoted and the
+# refusal names both blockers (Pr 60, required 80).
+[pool insufficient]
+usable = 100
+mode = hard
+relax = 1
+chains = 3
+events:
+  claim L=30 c=0 T=30 hard=1 prio=1
+  claim L=30 c=1 T=30 hard=1 prio=0 demotable=1
+  prefill S=80 c=2 P=0
+expect:
+  t2 code=refused_claim id=0 a=60 b=80 n16=2
+  tel runtime_demoted=0 protected=60
+  claim0 state=materialized blocked=1
+  claim1 state=materialized blocked=1 demote=-1
+
+# Decode growth is relaxed like a prefill: b = active blocks after the extension.
+[pool extend_relaxed]
+usable = 80
+mode = hard
+relax = 1
+chains = 2
+events:
+  claim L=60 c=0 T=60 hard=1 prio=0 demotable=1
+  prefill S=20 c=1 P=0
+  extend k=5 sel=0
+expect:
+  t1 code=admit id=1 b=0
+  t2 code=relaxed id=1 a=5 b=25 n16=1 flags=pred_fail|post_release_loss
+  claim0 state=demoted demote=2 pred_fail=2 lead_end=55
+
+# A best-effort claim carries no obligation in any policy: observed (shadow), never protects, its
+# loss is a predicate failure without harm.
+[pool best_effort_in_hard_pool]
+usable = 80
+mode = hard
+chains = 2
+events:
+  claim L=60 c=0 T=60 hard=1 prio=3 best_effort=1
+  prefill S=70 c=1 P=0
+expect:
+  t0 code=admit b=60 flags=shadow
+  t1 code=evict_resident id=1 a=50 flags=pred_fail
+  tel shadow=1 accepted=0 harm=0 protected=0 resident=50 post_release=0
+  claim0 decision=shadow state=observed eff=0 best_effort=1 pred_fail=1 harm=-1
+
+# Relaxation comes first; a request that no relaxation can serve is still deferred.
+[pool relax_then_defer]
+usable = 68
+mode = hard
+relax = 1
+defer_limit = 1
+chains = 3
+events:
+  claim L=40 c=0 T=40 hard=1 prio=3
+  claim L=10 c=1 T=10 hard=1 prio=0 demotable=1
+  prefill S=46 c=2 P=0
+  prefill S=10 c=2 P=0
+  retry
+expect:
+  t2 code=deferred id=0 a=50 b=46 n16=2
+  t3 code=admit id=3
+  t4 code=refused_claim id=0 a=50 b=56 n16=2
+  tel n_deferred=1 retry_refused=1 runtime_demoted=0
+"""
+
+
+def fixtures():
+    return gf.parse_text(RELAX_CASES, "relaxation closed forms")

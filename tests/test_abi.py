@@ -91,7 +91,7 @@ def _batch(**kw):
 
 
 def test_version_and_strings(lib):
-    assert lib.rkc_abi_version() == 2
+    assert lib.rkc_abi_version() == 3
     assert lib.rkc_status_string(0) == b"ok"
     assert lib.rkc_status_string(-5).startswith(b"scratch")
     assert lib.rkc_status_string(-99) == b"unknown status"

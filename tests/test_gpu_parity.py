@@ -9,7 +9,7 @@ the replay is causal, so a prefix of a pool's outcomes is an exact sample).
 import numpy as np
 import pytest
 
-from tests import deferral_cases
+from tests import deferral_cases, relax_cases
 from tests import golden_fixtures as gf
 from tests import randtrace
 from tests.gpu_util import compare_pools, gpu_replay, say
@@ -113,10 +113,10 @@ def _properties(trace, gpu):
     U = trace.field("usable_blocks").astype(np.int64)
     ne = trace.field("n_events")
     assert (pt[:, 31] & ~7 == 0).all(), "internal fault or descriptor status"
-    assert (pt[:, :10].sum(1) + pt[:, 32] == ne).all()
+    assert (pt[:, :10].sum(1) + pt[:, 32] + pt[:, 36] == ne).all()
     assert (pt[:, 25] + pt[:, 26] + pt[:, 27] == U).all()
     assert (pt[:, 24] <= U).all() and (pt[:, 24] >= pt[:, 25]).all()
-    assert (pt[:, 36:] == 0).all()
+    assert (pt[:, 38:] == 0).all()
     code = out[:, 0] & 255
     ref = (code == 2) | (code == 3) | (code == 10)
     Ue = np.repeat(U, ne)
@@ -316,10 +316,11 @@ def test_random_deferral_medium(oracle_mod, kernel):
 
 @pytest.mark.parametrize("variant", ["wide", "wide_global_lists"])
 def test_deferral_storage_layouts(oracle_mod, tg, variant):
-    """Deferral with 32-bit LDS state and with the live lists in global scratch."""
+    """Deferral and runtime relaxation with 32-bit LDS state and with the live lists in global
+    scratch."""
     import paper_2605_24259_amd as rkc
     trace = randtrace.random_batch(71, 600, U_range=(2, 200), n_events=(1, 200), n_chains=7,
-                                   tight_every=9, defer=True, hard_share=0.8)
+                                   tight_every=9, defer=True, relax=True, hard_share=0.8)
     lim = dict(trace.limits())
     lim["max_usable_blocks"] = 40000
     if variant == "wide_global_lists":
@@ -342,3 +343,52 @@ def test_zipf_defer_full_sampled(oracle_mod, tg):
     pt = gpu[1]
     assert pt[:, 32].sum() > 20 * trace.n_pools
     assert (pt[:, 35] <= trace.field("max_live_requests")).all()
+
+
+# ---- runtime relaxation and best-effort claims: both kernels -----------------------------------
+@pytest.mark.parametrize("kernel", KERNELS)
+def test_relaxation_fixtures(oracle_mod, tg, kernel):
+    """Hand-derived relaxation cases (the 60/70/80 probe relaxed to 50 post-release victims and no
+    harm, lowest priority first, only as many as needed, none when insufficient, decode growth,
+    best-effort claims, relaxation before deferral) on both kernels."""
+    fx = relax_cases.fixtures()
+    trace = gf.to_trace(tg, fx)
+    gpu, ora = _both_kernel(oracle_mod, trace, kernel)
+    errs = gf.check(fx, trace, *gpu)
+    assert not errs, "\n".join(errs)
+    compare_pools(trace, gpu, ora)
+
+
+@pytest.mark.parametrize("kernel", KERNELS)
+@pytest.mark.parametrize("seed,defer", [(81, False), (82, True)])
+def test_random_relaxation_tiny(oracle_mod, kernel, seed, defer):
+    """Relaxing pools of <= 12 blocks with demotable and best-effort claims, with and without
+    deferral, tight tables, malformed events."""
+    trace = randtrace.random_batch(seed, 3000, U_range=(1, 13), n_events=(0, 40), n_chains=3,
+                                   relax=True, defer=defer, hard_share=0.8)
+    gpu, ora = _both_kernel(oracle_mod, trace, kernel)
+    compare_pools(trace, gpu, ora)
+    assert gpu[1][:, 36].sum() > 50
+
+
+@pytest.mark.parametrize("kernel", KERNELS)
+def test_random_relaxation_medium(oracle_mod, kernel):
+    """Relaxing and deferring pools up to 300 blocks and 400 events, up to 64 live claims: the
+    demotion order is a wave-wide minimum over many claim lanes."""
+    trace = randtrace.random_batch(91, 400, U_range=(8, 300), n_events=(1, 400), n_chains=9,
+                                   p_malformed=0.01, tight_every=7, caps=(256, 64), defer=True,
+                                   relax=True, hard_share=0.8)
+    gpu, ora = _both_kernel(oracle_mod, trace, kernel)
+    compare_pools(trace, gpu, ora)
+    assert gpu[1][:, 37].sum() > 50
+
+
+def test_zipf_relax_full_sampled(oracle_mod, tg):
+    """65,536 relaxing hard-protection pools x 2,048 blocks x 1,024 events, half the claims
+    demotable, in the benchmark's launch configuration; sampled pools against the oracle."""
+    trace = tg.generate("zipf_relax")
+    pools = _sample(trace.n_pools, 96)
+    gpu, ora = _both(oracle_mod, trace, pools=pools)
+    compare_pools(trace, gpu, ora, pools=pools)
+    _properties(trace, gpu)
+    assert gpu[1][:, 36].sum() > trace.n_pools

@@ -197,3 +197,40 @@ def test_deferral_off_is_plain_refusal(oracle_mod, tg):
     oa, pa, ca = _check_clean(oracle_mod, a)
     ob, pb, cb = _check_clean(oracle_mod, b)
     assert np.array_equal(oa, ob) and np.array_equal(pa, pb) and np.array_equal(ca, cb)
+
+
+@pytest.mark.parametrize("seed", [301, 302, 303])
+def test_bruteforce_random_relaxation(oracle_mod, seed):
+    """Oracle == brute-force model on relaxing pools (§3.1 demotable / best_effort; §3.5 relax
+    resident claim), alone and together with deferral."""
+    trace = randtrace.random_batch(seed, 500, U_range=(1, 9), n_events=(8, 30), n_chains=2,
+                                   relax=True, defer=seed == 303, hard_share=0.8)
+    _brute_compare(oracle_mod, trace)
+    _, ptel, _ = _check_clean(oracle_mod, trace)
+    assert ptel[:, 36].sum() > 20 and ptel[:, 37].sum() >= ptel[:, 36].sum()
+
+
+def test_relaxation_accounting(oracle_mod):
+    """On relaxing pools: RELAXED outcomes only in hard pools, each demoting at least one claim;
+    runtime demotions are counted in both the outcome and the claim records; no hard claim that is
+    still materialized is ever harmed (I3 holds with relaxation)."""
+    trace = randtrace.random_batch(19, 400, U_range=(4, 60), n_events=(1, 120), n_chains=4,
+                                   relax=True, hard_share=0.7, p_malformed=0.01)
+    out, ptel, ctel = _check_clean(oracle_mod, trace)
+    ne, eo = trace.field("n_events"), trace.field("event_offset")
+    so, ns = trace.field("claim_slot_offset"), trace.field("n_claim_slots")
+    assert (ptel[:, :10].sum(1) + ptel[:, 32] + ptel[:, 36] == ne).all()
+    total = 0
+    for i in range(trace.n_pools):
+        o = out[eo[i]: eo[i] + ne[i]]
+        code = o[:, 0] & 255
+        r = code == 11
+        n16 = o[:, 0].view(np.uint32) >> 16
+        if r.any():
+            assert trace.field("mode")[i] & 15 == 3
+            assert (n16[r] >= 1).all()
+        assert int(n16[r].sum()) == int(ptel[i, 37])
+        packed = ctel[so[i]: so[i] + ns[i], 1]
+        assert int(((packed >> 15) & 1).sum()) == int(ptel[i, 37])
+        total += int(r.sum())
+    assert total > 100

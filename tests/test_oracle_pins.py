@@ -8,7 +8,7 @@
 import numpy as np
 import pytest
 
-from tests import deferral_cases
+from tests import deferral_cases, relax_cases
 from tests import golden_fixtures as gf
 
 MODES = ("lru", "soft", "noadmit", "hard")
@@ -136,3 +136,13 @@ def test_deferral_closed_forms(oracle_mod, tg):
     errs = gf.check(fx, trace, out, ptel, ctel)
     assert not errs, "\n".join(errs)
 
+
+
+def test_relaxation_closed_forms(oracle_mod, tg):
+    """Hand-derived runtime relaxation and best-effort cases (tests/relax_cases.py)."""
+    fx = relax_cases.fixtures()
+    trace = gf.to_trace(tg, fx)
+    out, ptel, ctel, chk = oracle_mod.replay(trace.desc, trace.events, trace.n_claim_slots)
+    assert not chk.any(), [oracle_mod.check_names(int(c)) for c in chk]
+    errs = gf.check(fx, trace, out, ptel, ctel)
+    assert not errs, "\n".join(errs)
