@@ -392,3 +392,38 @@ def test_zipf_relax_full_sampled(oracle_mod, tg):
     compare_pools(trace, gpu, ora, pools=pools)
     _properties(trace, gpu)
     assert gpu[1][:, 36].sum() > trace.n_pools
+
+
+def test_compact_kernel_at_its_limits(oracle_mod, tg):
+    """One batch at the compact kernel's limits: 32,767-block pools, 256 chains, a pool of 65,533
+    events (16-bit ids up to 65,532), live-claim and live-request tables filled to exactly 64 and
+    256 and then overflowed, an empty pool, an all-malformed pool, and a deferring / relaxing pool
+    at full size.  Every outcome, pool word and claim record against the oracle."""
+    import bench
+    rng = np.random.default_rng(2026)
+    big = randtrace.random_pool(rng, 32767, 3, 3000, n_chains=256, p_malformed=0.01)
+    big["max_live_requests"], big["max_live_claims"] = 256, 64
+    long_pool = randtrace.random_pool(rng, 8, 0, 65533, n_chains=1, p_malformed=0.01)
+    long_pool["max_live_requests"], long_pool["max_live_claims"] = 256, 64
+    ext = randtrace.random_pool(rng, 32767, 3, 2000, n_chains=256, p_malformed=0.01, defer_limit=3,
+                                relax=True)
+    ext["mode"] = 3 | tg.MODE_RELAX
+    ext["max_live_requests"], ext["max_live_claims"] = 256, 64
+    tables = dict(usable_blocks=400, mode=1, n_chains=256, max_live_claims=64, max_live_requests=256,
+                  events=[tg.claim(1, c, 1) for c in range(65)] + [tg.prefill(1)] * 257
+                  + [tg.release(0), tg.claim(2, 70, 2), tg.finish(3), tg.prefill(2, 200, 2)])
+    pools = [big, long_pool, ext, tables,
+             dict(usable_blocks=1, mode=2, n_chains=0, events=[]),
+             dict(usable_blocks=32767, mode=3, n_chains=256,
+                  events=[tg.ev(11), tg.prefill(0), tg.claim(5, 256), tg.extend(-1), tg.ev(15)])]
+    trace = tg.from_pools(pools, "compact-limits")
+    lim = trace.limits()
+    assert lim["max_usable_blocks"] == 32767 and lim["max_events"] == 65533
+    assert lim["max_chains"] == 256 and bench.kernel_name(lim) == "rkc_lean"
+    gpu, ora = _both(oracle_mod, trace)
+    compare_pools(trace, gpu, ora)
+    pt = gpu[1]
+    assert pt[3, 31] == 3  # request and claim tables both overflowed (status bits 1 | 2)
+    assert pt[3, 29] == 256 and pt[3, 30] == 64 and pt[3, 9] == 2
+    assert pt[4, 27] == 1 and pt[4, :].sum() == 1  # the empty pool: one FREE block, nothing else
+    assert (pt[5, 9] == 5) and (pt[5, :9] == 0).all()
