@@ -287,8 +287,8 @@ int32_t rkc_abi_version(void);
 /* Device scratch bytes rkc_replay_batch needs for this batch: per pool, the pool state that does not
  * stay on chip (touch-stack nodes beyond the LDS part, the FIFO of finished requests' private runs,
  * one entry per claim slot, a deferral ring of max_live_requests entries, and the live lists when
- * they do not fit in LDS).  Reads only the host-side limits of b; never fails (returns 0 for a NULL
- * b or an empty batch). */
+ * they do not fit in LDS), plus 4 bytes per pool for the launch order of the compact kernel.  Reads
+ * only the host-side limits of b; never fails (returns 0 for a NULL b or an empty batch). */
 size_t rkc_scratch_bytes(const rkc_batch* b);
 
 /* Replay every pool of the batch from empty pools (all U blocks FREE, no claims, no requests).

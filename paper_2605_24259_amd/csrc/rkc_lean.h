@@ -21,6 +21,9 @@ struct rkc_lean_args {
   uint32_t ns, node_cap, nodes_lds;
   uint32_t off_keys, off_hist, off_cold, off_chains, off_reqs, off_nodes, lds_bytes;
   uint64_t scr_pool_bytes, scr_off_nodes, scr_off_fifo, scr_off_slots, scr_off_defer;
+  // after the per-pool regions: the launch order (one u32 pool index per workgroup), each pool's
+  // loop class (one byte) and per-tile class counts of the ordering passes
+  uint64_t scr_off_order, scr_off_cls, scr_off_tiles, scr_total;
 };
 
 // Fill the layout part of g for batch b; false when b is outside the compact kernel's limits

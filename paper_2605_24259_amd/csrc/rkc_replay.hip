@@ -1348,7 +1348,7 @@ int32_t rkc_abi_version(void) { return RKC_ABI_VERSION; }
 size_t rkc_scratch_bytes(const rkc_batch* b) {
   if (!b || b->n_pools <= 0) return 0;
   rkc_lean_args lg;
-  if (use_lean(b, &lg)) return (size_t)(lg.scr_pool_bytes * (u64)b->n_pools);
+  if (use_lean(b, &lg)) return (size_t)lg.scr_total;
   Layout L;
   if (!choose_layout(b, &L)) return 0;
   return (size_t)(L.scr_pool_bytes * (u64)b->n_pools);
@@ -1360,7 +1360,7 @@ rkc_status rkc_replay_batch(const rkc_batch* b, void* s) {
   if (b->n_pools == 0) return RKC_OK;
   rkc_lean_args lg;
   if (use_lean(b, &lg)) {
-    const u64 need = lg.scr_pool_bytes * (u64)b->n_pools;
+    const u64 need = lg.scr_total;
     if (!b->d_scratch || b->scratch_bytes < need) return RKC_E_SCRATCH;
     lg.pools = b->d_pools; lg.events = b->d_events; lg.outcomes = b->d_outcomes;
     lg.pool_tel = b->d_pool_tel; lg.claim_tel = b->d_claim_tel; lg.scratch = b->d_scratch;

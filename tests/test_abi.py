@@ -124,7 +124,8 @@ def test_scratch_grows_with_limits(lib):
     small = lib.rkc_scratch_bytes(ctypes.byref(_batch()))
     big = lib.rkc_scratch_bytes(ctypes.byref(_batch(max_events=4096)))
     many = lib.rkc_scratch_bytes(ctypes.byref(_batch(n_pools=20)))
-    assert big > small and many == 10 * small
+    # per-pool regions, plus the launch order, class bytes and tile counts (256 bytes each here)
+    assert big > small and many - 768 == 10 * (small - 768)
 
 
 @pytest.mark.parametrize("max_events", [0, 1, 13, 63, 64, 65, 1024])
