@@ -24,7 +24,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, AMD published peak
-BYTES_EVENT, BYTES_OUTCOME, BYTES_CLAIM_SLOT, BYTES_POOL_TEL, BYTES_DESC = 16, 16, 40, 256, 48
+BYTES_EVENT, BYTES_OUTCOME, BYTES_CLAIM_SLOT, BYTES_POOL_TEL, BYTES_DESC = 16, 16, 40, 256, 64
 COPY_BYTES = 1 << 30
 METRIC = "replayed allocator events/sec (1 GPU) + % of HBM peak; bit-exact vs oracle"
 

@@ -33,7 +33,7 @@
 extern "C" {
 #endif
 
-#define RKC_ABI_VERSION 3
+#define RKC_ABI_VERSION 4
 
 /* Hard limits of this implementation (checked on the host and per pool on the device). */
 #define RKC_MAX_USABLE_BLOCKS   (1 << 22) /* U per pool                                        */
@@ -104,7 +104,7 @@ enum rkc_pool_mode {
 };
 
 /* ----------------------------------------------------------------------------------------------
- * Pool descriptor: 48 bytes.
+ * Pool descriptor: 64 bytes.
  * -------------------------------------------------------------------------------------------- */
 typedef struct rkc_pool_desc {
   int32_t usable_blocks;     /* U, 1..RKC_MAX_USABLE_BLOCKS; block size is 16 tokens (§4.1)     */
@@ -119,6 +119,8 @@ typedef struct rkc_pool_desc {
                                 at most max_live_requests deep); a queued request receives at most
                                 defer_limit DEFERRED outcomes before a RETRY that still finds it
                                 blocked refuses it                                               */
+  int32_t offload_blocks;    /* second-tier capacity in blocks (0 = no second tier)              */
+  int32_t reserved[3];       /* must be 0                                                        */
   int64_t event_offset;      /* index of the pool's first event in the event (and outcome) array */
   int64_t claim_slot_offset; /* index of the pool's first slot in the claim telemetry array      */
 } rkc_pool_desc;

@@ -77,12 +77,12 @@ def replay(desc: np.ndarray, events: np.ndarray, n_claim_slots_total: int, pools
            threads: int = 1):
     """Replay pools of a batch on the CPU.
 
-    desc: int32 [P, 12] (48-byte pool descriptors), events: int32 [E, 4].
+    desc: int32 [P, 16] (64-byte pool descriptors), events: int32 [E, 4].
     pools: iterable of pool indices to replay (default: all); other pools' outputs stay zero.
     Returns (outcomes int32 [E,4], pool_tel int32 [P,64], claim_tel int32 [C,10], check int32 [P]).
     """
     lib = _load()
-    desc = np.ascontiguousarray(desc, dtype=np.int32).reshape(-1, 12)
+    desc = np.ascontiguousarray(desc, dtype=np.int32).reshape(-1, 16)
     events = np.ascontiguousarray(events, dtype=np.int32).reshape(-1, 4)
     n_pools = desc.shape[0]
     out = np.zeros((events.shape[0], 4), np.int32)

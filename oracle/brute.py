@@ -468,7 +468,7 @@ class Pool:
 
 
 def replay_pool(desc_row, events):
-    """Replay one pool: desc_row = 12 int32 descriptor words, events = list of 4-int lists."""
+    """Replay one pool: desc_row = 16 int32 descriptor words, events = list of 4-int lists."""
     U, mode, n_ev, n_chains, max_claims, max_reqs, n_slots, defer_limit = \
         [int(x) for x in desc_row[:8]]
     if U > 12:

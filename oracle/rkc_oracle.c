@@ -938,16 +938,16 @@ static int replay_pool(const int32_t* d, const int32_t* ev, int32_t* out, int32_
 }
 
 /* Batch entry: pools [first, first + count) of a batch laid out like the device ABI.
- * desc: 12 int32 per pool (48-byte records); events/outcomes: 4 int32 per event; pool_tel: 64 int32
+ * desc: 16 int32 per pool (64-byte records); events/outcomes: 4 int32 per event; pool_tel: 64 int32
  * per pool; claim_tel: 10 int32 per slot; check: one int32 per pool (invariant violation bits,
  * -1 when the pool could not be set up).  Returns the number of pools with a non-zero check. */
 int rkc_oracle_replay(const int32_t* desc, int32_t first, int32_t count, const int32_t* events,
                       int32_t* outcomes, int32_t* pool_tel, int32_t* claim_tel, int32_t* check) {
   int bad = 0;
   for (int32_t i = first; i < first + count; i++) {
-    const int32_t* d = desc + 12 * (size_t)i;
-    int64_t ev_off = (int64_t)(uint32_t)d[8] | ((int64_t)d[9] << 32);
-    int64_t cl_off = (int64_t)(uint32_t)d[10] | ((int64_t)d[11] << 32);
+    const int32_t* d = desc + 16 * (size_t)i;
+    int64_t ev_off = (int64_t)(uint32_t)d[12] | ((int64_t)d[13] << 32);
+    int64_t cl_off = (int64_t)(uint32_t)d[14] | ((int64_t)d[15] << 32);
     int rc = replay_pool(d, events + 4 * ev_off, outcomes + 4 * ev_off, pool_tel + N_TEL * (size_t)i,
                          claim_tel + 10 * cl_off, &check[i]);
     if (rc != 0) check[i] = -1;

@@ -15,7 +15,7 @@ LIB_PATH = os.path.join(_PKG, "librkc.so")
 _lib = None
 
 # layouts and codes of this binding (rkc.h RKC_ABI_VERSION)
-ABI_VERSION = 3
+ABI_VERSION = 4
 POOL_TEL_WORDS = 64
 
 # rkc_batch.flags: replay with the general kernel even where the compact one applies
@@ -102,7 +102,7 @@ class DeviceBatch:
             raise RuntimeError("no GPU: the replay runs only in the HIP kernels")
         lib = load()
         self.device = torch.device(device)
-        self.desc = torch.as_tensor(desc, dtype=torch.int32).reshape(-1, 12).to(self.device).contiguous()
+        self.desc = torch.as_tensor(desc, dtype=torch.int32).reshape(-1, 16).to(self.device).contiguous()
         self.events = torch.as_tensor(events, dtype=torch.int32).reshape(-1, 4).to(self.device).contiguous()
         n_pools = int(self.desc.shape[0])
         n_ev = int(self.events.shape[0])

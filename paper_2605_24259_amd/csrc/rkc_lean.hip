@@ -399,7 +399,7 @@ struct Lean {
     const u64 hm = ballot(hit);
     nexp = wmin(cand && !hit ? ex : NEVER);
     expired = (u32)__builtin_popcountll(hm);
-    if (hm) {
+    if (__builtin_expect(hm != 0, 0)) {
       recompute_lanes(hm);
       flags |= RKC_FL_EXPIRED;
       tadd(TW_EXPIRED, expired);
@@ -418,7 +418,7 @@ struct Lean {
     qf = fail ? pk(t, harm ? t : hi16(qf)) : qf;
     const u64 fm = ballot(fail), hmk = ballot(harm);
     u32 fl = 0;
-    if (fm) {
+    if (__builtin_expect(fm != 0, 0)) {
       const u32 pf = (u32)__builtin_popcountll(fm), hc = (u32)__builtin_popcountll(hmk);
       tadd(TW_PREDFAIL, pf);
       tadd(TW_HARM, hc);
@@ -522,7 +522,7 @@ struct Lean {
             set_status(0x80000000u);  // cannot happen: feasibility was checked
             K = 0;
           }
-          if (guard > 0x10000u) { set_status(0x80000000u); K = 0; }
+          if (__builtin_expect(guard > 0x10000u, 0)) { set_status(0x80000000u); K = 0; }
         }
         cold_fifo_out();
         cold_nodes_out();
@@ -952,7 +952,7 @@ struct Lean {
     const u32 type = w0 & 15u;
     u32 expired = 0;
     Out o = {RKC_OC_NOOP, 0, NEVER, 0, -1, 0, 0};
-    if (t >= nexp) expire(t, o.flags, expired);
+    if (__builtin_expect(t >= nexp, 0)) expire(t, o.flags, expired);
     if (type == RKC_EV_PREFILL) ev_prefill(t, w1, w2, w3, o);
     else if (type == RKC_EV_EXTEND) ev_extend(t, w1, w2, o);
     else if (type == RKC_EV_CLAIM) ev_claim(t, w0, w1, w2, w3, o);
@@ -961,7 +961,7 @@ struct Lean {
     else if (ext() && type == RKC_EV_RETRY) ev_retry(t, o);
     else if ((type & ~1u) != RKC_EV_NOP) o.code = RKC_OC_INVALID;  // NOP, or RETRY with no ring
     static_assert(RKC_EV_NOP == 6 && RKC_EV_RETRY == 7, "NOP and RETRY differ in bit 0 only");
-    if (o.sweep_due) o.flags |= sweep(t);
+    if (__builtin_expect(o.sweep_due != 0, 0)) o.flags |= sweep(t);
     const bool quiet = o.code == RKC_OC_NOOP || o.code == RKC_OC_INVALID;
     o0 = o.code | (o.flags << 8) | ((o.n16 == NEVER ? min(expired, 65535u) : o.n16) << 16);
     o1 = quiet ? -1 : o.id;
@@ -1170,7 +1170,8 @@ __global__ __launch_bounds__(64) void rkc_lean(rkc_lean_args g) {
                   d.n_events <= g.max_events && d.n_chains >= 0 &&
                   d.n_chains <= g.max_chains && d.max_live_claims >= 0 && d.max_live_claims <= g.max_claims &&
                   d.max_live_requests >= 0 && d.max_live_requests <= g.max_reqs &&
-                  d.n_claim_slots <= g.max_slots && d.defer_limit >= 0;
+                  d.n_claim_slots <= g.max_slots && d.defer_limit >= 0 && d.offload_blocks == 0 &&
+                  d.reserved[0] == 0 && d.reserved[1] == 0 && d.reserved[2] == 0;
   if (!ok) {
     if (ev_ok)
       for (i32 i = (i32)lane; i < d.n_events; i += 64) g.outcomes[ev_off + i] = rkc_outcome{{RKC_OC_INVALID, -1, 0, 0}};

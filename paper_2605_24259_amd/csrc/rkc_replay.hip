@@ -1137,7 +1137,8 @@ __global__ __launch_bounds__(64) void rkc_replay_wave(Args g) {
                   P.mode >= 0 && P.mode <= 3 && P.n_events <= g.max_events && P.n_chains >= 0 &&
                   P.n_chains <= g.max_chains && P.max_claims >= 0 && P.max_claims <= g.max_claims &&
                   P.max_reqs >= 0 && P.max_reqs <= g.max_reqs && P.n_slots <= g.max_slots &&
-                  d.defer_limit >= 0;
+                  d.defer_limit >= 0 && d.offload_blocks == 0 && d.reserved[0] == 0 &&
+                  d.reserved[1] == 0 && d.reserved[2] == 0;
   if (!ok) {
     if (ev_ok)
       for (i32 i = (i32)P.lane; i < P.n_events; i += 64)

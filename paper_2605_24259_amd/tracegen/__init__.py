@@ -32,6 +32,7 @@ SEED0 = 260524259
 
 EV_PREFILL, EV_EXTEND, EV_CLAIM, EV_FINISH, EV_RELEASE, EV_DEMOTE, EV_NOP, EV_RETRY = range(8)
 MODE_RELAX = 16  # pool mode flag: the runtime demotes demotable hard claims to serve active requests
+DESC_WORDS = 16  # int32 words per pool descriptor (64 bytes): event offset at 12:14, slot offset at 14:16
 MODE_LRU, MODE_SOFT, MODE_NOADMIT, MODE_HARD = range(4)
 MODE_NAMES = ("lru", "soft", "noadmit", "hard")
 
@@ -148,7 +149,7 @@ def _load():
 
 @dataclass
 class Trace:
-    """A batch of pools: 48-byte descriptors (int32 [P,12]) and 16-byte events (int32 [E,4])."""
+    """A batch of pools: 64-byte descriptors (int32 [P,16]) and 16-byte events (int32 [E,4])."""
     desc: np.ndarray
     events: np.ndarray
     n_claim_slots: int
@@ -165,13 +166,14 @@ class Trace:
 
     def field(self, name: str) -> np.ndarray:
         cols = {"usable_blocks": 0, "mode": 1, "n_events": 2, "n_chains": 3, "max_live_claims": 4,
-                "max_live_requests": 5, "n_claim_slots": 6, "defer_limit": 7}
+                "max_live_requests": 5, "n_claim_slots": 6, "defer_limit": 7,
+                "offload_blocks": 8}
         if name in cols:
             return self.desc[:, cols[name]]
         if name == "event_offset":
-            return self.desc[:, 8:10].copy().view(np.int64)[:, 0]
+            return self.desc[:, 12:14].copy().view(np.int64)[:, 0]
         if name == "claim_slot_offset":
-            return self.desc[:, 10:12].copy().view(np.int64)[:, 0]
+            return self.desc[:, 14:16].copy().view(np.int64)[:, 0]
         raise KeyError(name)
 
     def limits(self) -> dict:
@@ -197,12 +199,12 @@ class Trace:
         for p in pools:
             row = self.desc[p].copy()
             evs.append(self.events[eo[p]: eo[p] + ne[p]])
-            row[8:10] = np.array([e_acc], np.int64).view(np.int32)
-            row[10:12] = np.array([s_acc], np.int64).view(np.int32)
+            row[12:14] = np.array([e_acc], np.int64).view(np.int32)
+            row[14:16] = np.array([s_acc], np.int64).view(np.int32)
             rows.append(row)
             e_acc += int(ne[p])
             s_acc += int(ns[p])
-        desc = np.stack(rows) if rows else np.zeros((0, 12), np.int32)
+        desc = np.stack(rows) if rows else np.zeros((0, DESC_WORDS), np.int32)
         events = np.concatenate(evs) if evs else np.zeros((0, 4), np.int32)
         t = Trace(desc, np.ascontiguousarray(events), s_acc, self.name + "[subset]", dict(self.meta))
         t.meta["source_pools"] = pools
@@ -224,13 +226,13 @@ class Trace:
             n_sl = int(np.sum((ev[:, 0] & 15) == EV_CLAIM))
             row[2] = k
             row[6] = n_sl
-            row[8:10] = np.array([e_acc], np.int64).view(np.int32)
-            row[10:12] = np.array([s_acc], np.int64).view(np.int32)
+            row[12:14] = np.array([e_acc], np.int64).view(np.int32)
+            row[14:16] = np.array([s_acc], np.int64).view(np.int32)
             rows.append(row)
             evs.append(ev)
             e_acc += k
             s_acc += n_sl
-        desc = np.stack(rows) if rows else np.zeros((0, 12), np.int32)
+        desc = np.stack(rows) if rows else np.zeros((0, DESC_WORDS), np.int32)
         events = np.concatenate(evs) if evs else np.zeros((0, 4), np.int32)
         return Trace(desc, np.ascontiguousarray(events), s_acc, self.name + "[prefix]", dict(sub.meta))
 
@@ -242,7 +244,7 @@ class Trace:
 
 
 def make_desc(pools: list[dict], n_events: list[int], n_slots: list[int]) -> np.ndarray:
-    desc = np.zeros((len(pools), 12), np.int32)
+    desc = np.zeros((len(pools), DESC_WORDS), np.int32)
     e_acc = s_acc = 0
     for i, p in enumerate(pools):
         desc[i, 0] = p["usable_blocks"]
@@ -253,8 +255,9 @@ def make_desc(pools: list[dict], n_events: list[int], n_slots: list[int]) -> np.
         desc[i, 5] = p.get("max_live_requests", max(n_events[i], 1))
         desc[i, 6] = p.get("n_claim_slots", n_slots[i])
         desc[i, 7] = p.get("defer_limit", 0)
-        desc[i, 8:10] = np.array([e_acc], np.int64).view(np.int32)
-        desc[i, 10:12] = np.array([s_acc], np.int64).view(np.int32)
+        desc[i, 8] = p.get("offload_blocks", 0)
+        desc[i, 12:14] = np.array([e_acc], np.int64).view(np.int32)
+        desc[i, 14:16] = np.array([s_acc], np.int64).view(np.int32)
         e_acc += n_events[i]
         s_acc += int(desc[i, 6])
     return desc
@@ -339,7 +342,7 @@ def sweep(residents=SWEEP_GRID["residents"], actives=SWEEP_GRID["actives"], usab
                              np.asarray(usables), indexing="ij")
     m, r, a, u = (x.reshape(-1).astype(np.int64) for x in (m, r, a, u))
     n = m.size
-    desc = np.zeros((n, 12), np.int32)
+    desc = np.zeros((n, DESC_WORDS), np.int32)
     desc[:, 0] = u
     desc[:, 1] = m
     desc[:, 2] = 2
@@ -348,8 +351,8 @@ def sweep(residents=SWEEP_GRID["residents"], actives=SWEEP_GRID["actives"], usab
     desc[:, 5] = 1
     desc[:, 6] = 1
     idx = np.arange(n, dtype=np.int64)
-    desc[:, 8:10] = (2 * idx).view(np.int32).reshape(n, 2)
-    desc[:, 10:12] = idx.view(np.int32).reshape(n, 2)
+    desc[:, 12:14] = (2 * idx).view(np.int32).reshape(n, 2)
+    desc[:, 14:16] = idx.view(np.int32).reshape(n, 2)
     ev = np.zeros((n, 2, 4), np.int64)
     ev[:, 0, 0] = EV_CLAIM | (1 << 4) | (3 << 5)
     ev[:, 0, 1] = r
@@ -388,7 +391,7 @@ def generate(name: str, n_pools: int | None = None, first_pool: int = 0, **overr
     g.zipf_s = 1.1
     g.seed0 = SEED0
     lib = _load()
-    desc = np.zeros((n_pools, 12), np.int32)
+    desc = np.zeros((n_pools, DESC_WORDS), np.int32)
     events = np.empty((n_pools * cfg["n_events"], 4), np.int32)
     slots = lib.rkc_tracegen(ctypes.byref(g), first_pool, n_pools, ctypes.c_void_p(desc.ctypes.data),
                              ctypes.c_void_p(events.ctypes.data))

@@ -92,7 +92,7 @@ enum { EV_PREFILL = 0, EV_EXTEND = 1, EV_CLAIM = 2, EV_FINISH = 3, EV_RELEASE = 
        EV_RETRY = 7 };
 
 /* Draw the events of pools [first_pool, first_pool + n_pools).
- * desc: 12 int32 per pool; events: n_pools * n_events * 4 int32.
+ * desc: 16 int32 per pool; events: n_pools * n_events * 4 int32.
  * Returns the total number of claim slots (CLAIM events), or -1 on bad parameters. */
 int64_t rkc_tracegen(const gen_params* g, int64_t first_pool, int32_t n_pools, int32_t* desc,
                      int32_t* events) {
@@ -177,7 +177,7 @@ int64_t rkc_tracegen(const gen_params* g, int64_t first_pool, int32_t n_pools, i
         if (type == EV_RELEASE && outstanding > 0) outstanding--;
       }
     }
-    int32_t* d = desc + 12 * (size_t)i;
+    int32_t* d = desc + 16 * (size_t)i;
     int64_t ev_off = (int64_t)g->n_events * (first_pool + i) - (int64_t)g->n_events * first_pool;
     d[0] = g->usable_blocks;
     d[1] = g->mode >= 0 ? g->mode : (int32_t)(pool % 4);
@@ -187,10 +187,11 @@ int64_t rkc_tracegen(const gen_params* g, int64_t first_pool, int32_t n_pools, i
     d[5] = g->max_live_requests > 0 ? g->max_live_requests : n_prefill;
     d[6] = n_claims;
     d[7] = g->defer_limit;
-    d[8] = (int32_t)(uint32_t)(uint64_t)ev_off;
-    d[9] = (int32_t)((uint64_t)ev_off >> 32);
-    d[10] = (int32_t)(uint32_t)(uint64_t)slots;
-    d[11] = (int32_t)((uint64_t)slots >> 32);
+    d[8] = d[9] = d[10] = d[11] = 0;
+    d[12] = (int32_t)(uint32_t)(uint64_t)ev_off;
+    d[13] = (int32_t)((uint64_t)ev_off >> 32);
+    d[14] = (int32_t)(uint32_t)(uint64_t)slots;
+    d[15] = (int32_t)((uint64_t)slots >> 32);
     slots += n_claims;
   }
   free(zcdf);

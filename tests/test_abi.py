@@ -61,8 +61,8 @@ int main(void) {
         lines = subprocess.check_output([exe], text=True).split("\n")
     sizes = [int(x) for x in lines[0].split()]
     offs = [int(x) for x in lines[1].split()]
-    assert sizes == [16, 48, 16, 40, 256, ctypes.sizeof(rkc.Batch)]
-    assert offs == [32, 40, rkc.Batch.d_pools.offset, rkc.Batch.scratch_bytes.offset]
+    assert sizes == [16, 64, 16, 40, 256, ctypes.sizeof(rkc.Batch)]
+    assert offs == [48, 56, rkc.Batch.d_pools.offset, rkc.Batch.scratch_bytes.offset]
 
 
 def _batch(**kw):
@@ -91,7 +91,7 @@ def _batch(**kw):
 
 
 def test_version_and_strings(lib):
-    assert lib.rkc_abi_version() == 3
+    assert lib.rkc_abi_version() == 4
     assert lib.rkc_status_string(0) == b"ok"
     assert lib.rkc_status_string(-5).startswith(b"scratch")
     assert lib.rkc_status_string(-99) == b"unknown status"

@@ -143,7 +143,8 @@ def test_nested_full_sampled(oracle_mod, tg):
 
 def test_huge_full_prefix_sampled(oracle_mod, tg):
     """64 pools x 262,144 blocks x 65,536 events; the oracle replays the first 1,500 events of
-    sampled pools and their outcomes must equal the GPU's first 1,500 outcomes."""
+    sampled pools and their outcomes must equal the GPU's first 1,500 outcomes; four whole pools
+    must equal the oracle's stored digests."""
     trace = tg.generate("huge")
     say(f"case huge: {trace.n_pools} pools, {trace.n_events} events")
     gpu = gpu_replay(trace)
@@ -155,7 +156,7 @@ def test_huge_full_prefix_sampled(oracle_mod, tg):
     evs = []
     for j in range(len(pools)):
         d[j, 2] = pre
-        d[j, 8:10] = np.array([j * pre], np.int64).view(np.int32)
+        d[j, 12:14] = np.array([j * pre], np.int64).view(np.int32)
         evs.append(sub.events[j * 65536: j * 65536 + pre])
     ora = oracle_mod.replay(d, np.concatenate(evs), sub.n_claim_slots, threads=4)
     assert not ora[3].any()
@@ -164,6 +165,24 @@ def test_huge_full_prefix_sampled(oracle_mod, tg):
         a = gpu[0][eo[p]: eo[p] + pre]
         b = ora[0][j * pre: (j + 1) * pre]
         assert np.array_equal(a, b), (p, int(np.nonzero((a != b).any(1))[0][0]))
+    # whole pools: the oracle's outputs for all 65,536 events of four pools, stored as digests by
+    # tests/golden/make_huge_digests.py (minutes of oracle time per pool)
+    import hashlib
+    import json
+    import os
+
+    def sha(x):
+        return hashlib.sha256(np.ascontiguousarray(x, dtype=np.int32).tobytes()).hexdigest()
+
+    doc = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "huge_digests.json")))
+    ne, so, ns = trace.field("n_events"), trace.field("claim_slot_offset"), trace.field("n_claim_slots")
+    for key, dg in doc["pools"].items():
+        p = int(key)
+        assert sha(trace.events[eo[p]: eo[p] + ne[p]]) == dg["events_sha256"], \
+            "the generator changed: re-run tests/golden/make_huge_digests.py"
+        assert gpu[1][p].tolist() == dg["pool_tel"], p
+        assert sha(gpu[0][eo[p]: eo[p] + ne[p]]) == dg["outcomes_sha256"], p
+        assert sha(gpu[2][so[p]: so[p] + ns[p]]) == dg["claim_tel_sha256"], p
 
 
 def test_batch_order_independent(oracle_mod, tg):
