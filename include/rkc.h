@@ -43,8 +43,9 @@ extern "C" {
 /* ----------------------------------------------------------------------------------------------
  * Event: 16 bytes = 4 x int32, pool-major (CSR by rkc_pool_desc.event_offset).
  *
- * w0 = type[0:4] | hard[4] | prio[5:7] | demotable[7] | best_effort[8] | reserved[9:16]
- *      | duration[16:32] (u16, 0 = no expiry); bits 4..8 and the duration matter for CLAIM only
+ * w0 = type[0:4] | hard[4] | prio[5:7] | demotable[7] | best_effort[8] | offloadable[9]
+ *      | reserved[10:16] | duration[16:32] (u16, 0 = no expiry); bits 4..9 and the duration matter
+ *      for CLAIM only
  *
  *   PREFILL (0)  active request r = the event's step index.  w1 = S blocks, w2 = shared chain c
  *                (ignored when P = 0), w3 = shared prefix P (0 <= P <= S).  Positions [0,P) are
@@ -61,7 +62,10 @@ extern "C" {
  *                to serve an active request, in pools with RKC_MODE_RELAX, always before the
  *                eviction that breaks its predicate.  best_effort (§3.1: telemetry only): the claim
  *                is observed (decision SHADOW) in every policy, protects nothing, never expires and
- *                its loss is never harm.
+ *                its loss is never harm.  offloadable (§3.1 protection modes): the runtime may move
+ *                the claim's content to the pool's second tier (offload_blocks) to serve an active
+ *                request, in pools with RKC_MODE_RELAX, as long as its predicate stays restorable;
+ *                an offloaded claim keeps state MATERIALIZED with effective protection OFFLOADED.
  *   FINISH  (3)  w1 = selector: the request finishes and releases its live KV.
  *   RELEASE (4)  w1 = selector over live claims (ascending id): the claim is released.
  *   DEMOTE  (5)  w1 = selector over materialized hard-requested claims: hard -> soft (§3.1, §3.2).
@@ -96,9 +100,17 @@ enum rkc_pool_mode {
   RKC_MODE_HARD = 3,    /* hard protected-resident exclusion with scheduler-visible refusal     */
   /* flag OR'ed into rkc_pool_desc.mode: runtime relaxation (§3.5 mechanism table "relax resident
    * claim": the active side is served by demoting resident state).  In a hard-protection pool,
-   * before an active PREFILL / EXTEND / RETRY is refused on behalf of claims, the demotable claims
-   * among the blocking ones are demoted, lowest priority first, then lowest id, until the request
-   * fits; none is demoted when even all of them would not make it fit.  No effect under the other
+   * before an active PREFILL / EXTEND / RETRY is refused on behalf of claims, the blocking claims
+   * that are offloadable or demotable are taken lowest priority first, then lowest id: each is
+   * offloaded when it is offloadable and its footprint L fits the second tier's free room
+   * (offload_blocks minus the blocks offloaded claims hold), else demoted when it is demotable,
+   * else left alone, until the request fits; no claim changes when even all of them would not make
+   * it fit (§3.5 mechanism table "relax resident claim", "offload resident").  An offloaded claim
+   * protects nothing, ranks nothing, its victims count as unclaimed and its predicate never fails;
+   * its copy (L blocks of the second tier) is dropped when it expires or is released, and DEMOTE
+   * never selects it.  A served PREFILL / RETRY with shared prefix P past its hits h counts
+   * min(P, largest footprint of an offloaded claim on its chain) - h blocks as restored from the
+   * second tier (pool telemetry [40]); they still take new GPU blocks.  No effect under the other
    * policies (they never refuse on behalf of claims). */
   RKC_MODE_RELAX = 16
 };
@@ -119,7 +131,8 @@ typedef struct rkc_pool_desc {
                                 at most max_live_requests deep); a queued request receives at most
                                 defer_limit DEFERRED outcomes before a RETRY that still finds it
                                 blocked refuses it                                               */
-  int32_t offload_blocks;    /* second-tier capacity in blocks (0 = no second tier)              */
+  int32_t offload_blocks;    /* second-tier capacity in blocks, >= 0 (0 = no second tier); used
+                                by relaxing hard-protection pools only                           */
   int32_t reserved[3];       /* must be 0                                                        */
   int64_t event_offset;      /* index of the pool's first event in the event (and outcome) array */
   int64_t claim_slot_offset; /* index of the pool's first slot in the claim telemetry array      */
@@ -130,7 +143,7 @@ typedef struct rkc_pool_desc {
  *
  * w0 = code[0:8] | flags[8:16] | n16[16:32]
  *   n16 = number of blocking claims for REFUSED_CLAIM and DEFERRED, 0 for REFUSED_CAPACITY, the
- *         number of claims the runtime demoted for RELAXED, otherwise the number of claims that
+ *         number of claims the runtime demoted or offloaded for RELAXED, otherwise the number of claims that
  *         expired at the start of this step; saturates at 65535.
  * w1 = id, w2 = a, w3 = b:
  *   ADMIT / EVICT_RESIDENT  after PREFILL: id = request, a = resident victims, b = leading hits h
@@ -144,8 +157,9 @@ typedef struct rkc_pool_desc {
  *   NOOP / INVALID          id = -1, a = 0, b = 0
  *   DEFERRED                the refusal record of REFUSED_CLAIM (id = smallest blocking claim id,
  *                           a = Pr, b = required, n16 = blocking claims): the request is queued
- *   RELAXED                 served after the runtime demoted claims (RKC_MODE_RELAX): id, a, b as
- *                           ADMIT for the event (PREFILL, EXTEND or RETRY), n16 = claims demoted
+ *   RELAXED                 served after the runtime demoted or offloaded claims (RKC_MODE_RELAX):
+ *                           id, a, b as ADMIT for the event (PREFILL, EXTEND or RETRY), n16 = claims
+ *                           demoted + claims offloaded
  * RETRY reports the retried request: served -> ADMIT / EVICT_RESIDENT with id = the request (its
  * PREFILL step), a = resident victims, b = leading hits; still blocked -> DEFERRED; refused for good
  * -> REFUSED_CLAIM / REFUSED_CAPACITY; full live-request table -> INVALID (the request stays queued);
@@ -185,7 +199,8 @@ enum rkc_outcome_flag {
  * Claim telemetry: 40 bytes = 10 x int32, one slot per CLAIM event in step order.
  *   [0] claim_id (step index; -1 for an unused slot)
  *   [1] packed = decision[0:4] | state[4:8] | hard_req[8] | prio[9:11] | eff_prot[11:13]
- *                | demotable[13] | best_effort[14] | demoted_by_runtime[15]
+ *                | demotable[13] | best_effort[14] | relaxed_by_runtime[15] | offloadable[16]
+ *       (eff_prot 3 = OFFLOADED: the claim holds a second-tier copy)
  *   [2] accept_step [3] demote_step [4] expire_step [5] release_step [6] pred_fail_step
  *   [7] harm_step   (every step field is -1 when the transition never happened)
  *   [8] blocked_count: active refusals this claim was attributed to
@@ -215,7 +230,7 @@ enum rkc_claim_state { /* §3.1 ResidentClaimState */
   RKC_ST_REJECTED = 7
 };
 
-enum rkc_protection { RKC_PROT_NONE = 0, RKC_PROT_SOFT = 1, RKC_PROT_HARD = 2 };
+enum rkc_protection { RKC_PROT_NONE = 0, RKC_PROT_SOFT = 1, RKC_PROT_HARD = 2, RKC_PROT_OFFLOADED = 3 };
 
 /* ----------------------------------------------------------------------------------------------
  * Pool telemetry: 256 bytes = 64 x int32.
@@ -229,7 +244,9 @@ enum rkc_protection { RKC_PROT_NONE = 0, RKC_PROT_SOFT = 1, RKC_PROT_HARD = 2 };
  *   [31] status: 0, or RKC_PS_* bits
  *   [32] DEFERRED outcomes [33] deferred requests served by RETRY [34] deferred requests refused by
  *   RETRY [35] deferred requests still queued at the end
- *   [36] RELAXED outcomes [37] claims demoted by the runtime          [38..63] 0 (reserved)
+ *   [36] RELAXED outcomes [37] claims demoted by the runtime
+ *   [38] claims offloaded [39] blocks offloaded [40] blocks restored from the second tier
+ *   [41] peak second-tier blocks held                                  [42..63] 0 (reserved)
  * -------------------------------------------------------------------------------------------- */
 typedef struct rkc_pool_telemetry {
   int32_t w[64];

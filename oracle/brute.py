@@ -41,8 +41,9 @@ def _s32(x: int) -> int:
 
 
 class Pool:
-    def __init__(self, U, mode, n_chains, max_claims, max_reqs, n_slots, defer_limit=0):
+    def __init__(self, U, mode, n_chains, max_claims, max_reqs, n_slots, defer_limit=0, U2=0):
         self.relax_on = bool(mode & 16)
+        self.U2, self.t2_used = U2, 0
         mode &= ~16
         self.U, self.mode, self.n_chains = U, mode, n_chains
         self.max_claims, self.max_reqs, self.n_slots = max_claims, max_reqs, n_slots
@@ -125,7 +126,7 @@ class Pool:
         out = free[: min(need, len(free))] + list(victims)
         stats = dict(victims=len(victims), resident=0, post=0, unclaimed=0, unreg=0)
         for i in victims:
-            cov = self.covering(i)
+            cov = [q for q in self.covering(i) if not q.get("offloaded")]
             if cov:
                 stats["resident"] += 1
                 if all(q["state"] in ("demoted", "expired") for q in cov):
@@ -163,31 +164,61 @@ class Pool:
         return len(free) + len({i for i in self.ids(CACHED) - hits if not self.protected(i)})
 
     def relax(self, t, need, hits):
-        """Demote the shortest prefix of the demotable blocking claims, ordered by (priority, id),
-        that lets `need` blocks be allocated; nothing when no prefix does."""
+        """Relax the shortest prefix of the blocking claims that allow demotion or offload, ordered
+        by (priority, id), that lets `need` blocks be allocated: in that prefix a claim is offloaded
+        when it allows it and its footprint fits the second tier's free room, else demoted when it
+        allows it, else left alone.  Nothing changes when no prefix suffices."""
         if self.mode != HARD or not self.relax_on or need <= self._available(hits):
             return 0
         cands = []
         for q in self.live_claims():
-            if q["state"] != "materialized" or q["eff"] != 2 or not q["demotable"]:
+            if q["state"] != "materialized" or q["eff"] != 2 or not (q["demotable"] or q["offloadable"]):
                 continue
             blocks = [self.index[(q["chain"], p)] for p in range(q["L"]) if (q["chain"], p) in self.index]
             if any(self.blocks[i]["state"] == CACHED and i not in hits for i in blocks):
                 cands.append(q)
         cands.sort(key=lambda q: (q["prio"], q["id"]))
-        for k in range(1, len(cands) + 1):
-            saved = [q["state"] for q in cands[:k]]
+
+        def actions(k):
+            room, acts = self.U2 - self.t2_used, []
             for q in cands[:k]:
-                q["state"] = "demoted"
+                if q["offloadable"] and q["L"] <= room:
+                    acts.append((q, "offload"))
+                    room -= q["L"]
+                elif q["demotable"]:
+                    acts.append((q, "demote"))
+            return acts
+
+        for k in range(1, len(cands) + 1):
+            acts = actions(k)
+            saved = [(q["state"], q["eff"]) for q, _ in acts]
+            for q, a in acts:
+                if a == "offload":
+                    q["eff"] = 3
+                else:
+                    q["state"] = "demoted"
             ok = need <= self._available(hits)
-            for q, st in zip(cands[:k], saved):
-                q["state"] = st
+            for (q, _), (st, eff) in zip(acts, saved):
+                q["state"], q["eff"] = st, eff
             if ok:
-                for q in cands[:k]:
-                    q["state"], q["demote"], q["relaxed"] = "demoted", t, 1
-                self.tel[37] += k
-                return k
+                for q, a in acts:
+                    q["relaxed"] = 1
+                    if a == "offload":
+                        q["eff"], q["offloaded"] = 3, 1
+                        self.t2_used += q["L"]
+                        self.tel[38] += 1
+                        self.tel[39] += q["L"]
+                    else:
+                        q["state"], q["demote"] = "demoted", t
+                        self.tel[37] += 1
+                self.tel[41] = max(self.tel[41], self.t2_used)
+                return len(acts)
         return 0
+
+    def _restorable(self, c, h, P):
+        e = max([q["L"] for q in self.live_claims() if q.get("offloaded") and q["chain"] == c],
+                default=0)
+        return max(0, min(P, e) - h)
 
     def live_request_ids(self):
         return sorted(r for r, q in self.reqs.items() if q["live"])
@@ -204,6 +235,14 @@ class Pool:
                     and q["accept"] + q["dur"] <= t:
                 q["state"], q["expire"] = "expired", t
                 expired += 1
+                if q.get("offloaded"):
+                    self.t2_used -= q["L"]
+                    q["offloaded"], q["eff"] = 0, 0
+                    # the predicate held only through the dropped copy
+                    if q["pred_fail"] < 0 and not self.pred(q):
+                        q["pred_fail"] = t
+                        flags |= 2
+                        self.tel[20] += 1
         if expired:
             flags |= 1
             self.tel[21] += expired
@@ -296,10 +335,10 @@ class Pool:
         elif typ == 2:
             L, c, T = e[1], e[2], e[3]
             q = slot
-            demq, beq = (w0 >> 7) & 1, (w0 >> 8) & 1
+            demq, beq, offq = (w0 >> 7) & 1, (w0 >> 8) & 1, (w0 >> 9) & 1
             observe = self.mode in (LRU, NOADMIT) or beq
             q.update(valid=True, chain=c, L=L, T=T, hard=hard, prio=prio, dur=dur, demotable=demq,
-                     best_effort=beq, relaxed=0,
+                     best_effort=beq, offloadable=offq, offloaded=0, relaxed=0,
                      eff=0 if beq else (2 if hard else 1) if self.mode == HARD
                      else (1 if self.mode == SOFT else 0))
             h = self.prefix_len(c, L)
@@ -363,12 +402,15 @@ class Pool:
             else:
                 q = live[(e[1] & 0xFFFFFFFF) % len(live)]
                 q["state"], q["release"] = "released", t
+                if q.get("offloaded"):
+                    self.t2_used -= q["L"]
+                    q["offloaded"] = 0
                 code, oid = "released", q["id"]
                 a, b = self.prefix_len(q["chain"], q["L"]), q["T"]
                 self.tel[23] += 1
         elif typ == 5:
             cands = [q for q in self.claims if q.get("valid") and q["state"] == "materialized"
-                     and q["hard"]] if self.mode in (SOFT, HARD) else []
+                     and q["hard"] and not q.get("offloaded")] if self.mode in (SOFT, HARD) else []
             if not cands:
                 code = "noop"
             else:
@@ -381,7 +423,7 @@ class Pool:
             for q in self.claims:
                 if q.get("valid") and q["pred_fail"] < 0 and \
                         q["state"] in ("observed", "materialized", "demoted", "expired") \
-                        and not self.pred(q):
+                        and not q.get("offloaded") and not self.pred(q):
                     q["pred_fail"] = t
                     flags |= 2
                     self.tel[20] += 1
@@ -430,6 +472,8 @@ class Pool:
         self.reqs[rid] = dict(live=True, blocks=blks, len=S)
         self._tel_victims(st)
         self.tel[14] += h
+        if P > h:
+            self.tel[40] += self._restorable(c, h, P)
         flags = (8 if st["post"] else 0) | (16 if st["unclaimed"] else 0)
         code = "relaxed" if relaxed else "evict_resident" if st["resident"] else "admit"
         return True, (code, rid, st["resident"], h, relaxed or None), flags, st["unreg"]
@@ -460,7 +504,7 @@ class Pool:
                 continue
             packed = DEC_CODE[q["decision"]] | (STATE_CODE[q["state"]] << 4) | (q["hard"] << 8) \
                 | (q["prio"] << 9) | (q["eff"] << 11) | (q["demotable"] << 13) \
-                | (q["best_effort"] << 14) | (q["relaxed"] << 15)
+                | (q["best_effort"] << 14) | (q["relaxed"] << 15) | (q["offloadable"] << 16)
             slots.append([q["id"], packed, q["accept"], q["demote"], q["expire"], q["release"],
                           q["pred_fail"], q["harm"], q["blocked"],
                           self.prefix_len(q["chain"], q["L"])])
@@ -469,11 +513,11 @@ class Pool:
 
 def replay_pool(desc_row, events):
     """Replay one pool: desc_row = 16 int32 descriptor words, events = list of 4-int lists."""
-    U, mode, n_ev, n_chains, max_claims, max_reqs, n_slots, defer_limit = \
-        [int(x) for x in desc_row[:8]]
+    U, mode, n_ev, n_chains, max_claims, max_reqs, n_slots, defer_limit, U2 = \
+        [int(x) for x in desc_row[:9]]
     if U > 12:
         raise ValueError("the brute-force model enumerates subsets; use it on pools of <= 12 blocks")
-    p = Pool(U, mode, n_chains, max_claims, max_reqs, n_slots, defer_limit)
+    p = Pool(U, mode, n_chains, max_claims, max_reqs, n_slots, defer_limit, U2)
     outs = [p.step(t, [int(x) for x in events[t]]) for t in range(n_ev)]
     tel, slots = p.finish_telemetry()
     return outs, tel, slots

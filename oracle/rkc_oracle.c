@@ -41,7 +41,7 @@ enum { FL_EXPIRED = 1, FL_PRED_FAIL = 2, FL_HARM = 4, FL_POST_RELEASE = 8, FL_UN
 enum { DEC_NONE = 0, DEC_ACCEPTED = 1, DEC_APPROX = 2, DEC_SHADOW = 3, DEC_REJECTED = 4 };
 enum { ST_SUBMITTED = 0, ST_OBSERVED = 1, ST_MATERIALIZED = 2, ST_DEMOTED = 3, ST_EXPIRED = 4,
        ST_RELEASED = 5, ST_HARMED = 6, ST_REJECTED = 7 };
-enum { PROT_NONE = 0, PROT_SOFT = 1, PROT_HARD = 2 };
+enum { PROT_NONE = 0, PROT_SOFT = 1, PROT_HARD = 2, PROT_OFFLOADED = 3 };
 enum { PS_REQ_TABLE = 1, PS_CLAIM_TABLE = 2, PS_SLOT_TABLE = 4 };
 enum { BLK_FREE = 0, BLK_ACTIVE = 1, BLK_CACHED = 2 };
 
@@ -51,7 +51,8 @@ enum { T_VICTIMS = 10, T_RESIDENT = 11, T_POSTREL = 12, T_DROPPED = 13, T_HITS =
        T_PREDFAIL = 20, T_EXPIRED = 21, T_DEMOTED = 22, T_RELEASED = 23, T_PEAK_ACTIVE = 24,
        T_ACTIVE = 25, T_CACHED = 26, T_FREE = 27, T_PROTECTED = 28, T_LIVE_REQ = 29,
        T_LIVE_CLAIMS = 30, T_STATUS = 31, T_DEFERRED = 32, T_RETRY_SERVED = 33,
-       T_RETRY_REFUSED = 34, T_QUEUED = 35, T_RELAXED = 36, T_RUNTIME_DEMOTED = 37, N_TEL = 64 };
+       T_RETRY_REFUSED = 34, T_QUEUED = 35, T_RELAXED = 36, T_RUNTIME_DEMOTED = 37, T_OFF_CLAIMS = 38,
+       T_OFF_BLOCKS = 39, T_RESTORED = 40, T_T2_PEAK = 41, N_TEL = 64 };
 
 /* invariant check bits (oracle-only diagnostics) */
 enum {
@@ -98,7 +99,9 @@ typedef struct {
   int32_t blocked;
   int32_t demotable;   /* the client lets the runtime demote it (§3.1 demotable)               */
   int32_t best_effort; /* telemetry only (§3.1 best_effort)                                    */
-  int32_t relaxed;     /* demoted by the runtime to serve an active request                     */
+  int32_t relaxed;     /* demoted or offloaded by the runtime to serve an active request        */
+  int32_t offloadable; /* its content may move to the second tier (§3.1 offloadable)           */
+  int32_t offloaded;   /* holds a second-tier copy: effective protection OFFLOADED              */
 } claim_t;
 
 /* A deferred active request waiting in the scheduler queue (active deferral, §3.5 mechanism table;
@@ -111,6 +114,8 @@ typedef struct {
 typedef struct {
   int32_t U, mode, n_events, n_chains, max_claims, max_reqs, n_slots, defer_limit;
   int32_t relax;   /* the runtime relaxes demotable hard claims before refusing (mode flag 16) */
+  int32_t U2;      /* second-tier capacity in blocks                                        */
+  int64_t t2_used; /* second-tier blocks held by offloaded claims                           */
   block_t* b;
   request_t* req;  /* indexed by request id (= step)           */
   claim_t* cl;     /* indexed by slot                          */
@@ -323,7 +328,7 @@ static alloc_t alloc_blocks(pool_t* p, int64_t need) {
       if (b->registered && b->chain >= 0) {
         for (int32_t s = p->bucket_head[b->chain]; s >= 0; s = p->bucket_next[s]) {
           claim_t* q = &p->cl[s];
-          if (!covers(q, b)) continue;
+          if (!covers(q, b) || q->offloaded) continue;
           covered = 1;
           if (q->state != ST_DEMOTED && q->state != ST_EXPIRED) covered_strict = 1;
           if (p->mode == MODE_HARD && q->state == ST_MATERIALIZED && q->eff == PROT_HARD) covered_hard = 1;
@@ -435,12 +440,15 @@ static int64_t available(pool_t* p) {
 }
 
 /* Runtime relaxation before an active allocation of `need` blocks (hits already marked): §3.1
- * demotable (the downgrade must come before the predicate-breaking eviction) and §3.5 "relax
- * resident claim" (the active side is served by demoting resident state).  When the pool relaxes
- * and hard protection makes the allocation infeasible, the demotable claims among those blocking it
- * (materialized hard claims covering a cached block outside the hits, as for attribution) are
- * demoted one at a time, lowest priority first, then lowest id, until the allocation fits.  If
- * demoting all of them would not make it fit, none is demoted.  Returns the number demoted. */
+ * demotable (the downgrade must come before the predicate-breaking eviction) and offloadable (the
+ * content may leave GPU memory if the predicate stays restorable); §3.5 "relax resident claim" and
+ * "offload resident" (the active side is served by demoting or offloading resident state, the
+ * latter subject to restore cost).  When the pool relaxes and hard protection makes the allocation
+ * infeasible, the claims blocking it (materialized hard claims covering a cached block outside the
+ * hits, as for attribution) that allow demotion or offload are taken lowest priority first, then
+ * lowest id: each is offloaded when it allows it and its footprint fits the second tier's free
+ * capacity, else demoted when it allows it, else left alone, until the allocation fits.  If it never
+ * fits, nothing changes.  Returns the number of claims relaxed. */
 static int32_t relax(pool_t* p, int64_t need, int32_t t) {
   if (p->mode != MODE_HARD || !p->relax) return 0;
   if (need <= available(p)) return 0;
@@ -448,7 +456,8 @@ static int32_t relax(pool_t* p, int64_t need, int32_t t) {
   int32_t n = 0;
   for (int32_t s = 0; s < p->n_cl; s++) {
     claim_t* q = &p->cl[s];
-    if (!(claim_live(q) && q->state == ST_MATERIALIZED && q->eff == PROT_HARD && q->demotable)) continue;
+    if (!(claim_live(q) && q->state == ST_MATERIALIZED && q->eff == PROT_HARD &&
+          (q->demotable || q->offloadable))) continue;
     int blocking = 0;
     for (int32_t pos = 0; pos < q->L && !blocking; pos++) {
       int32_t* slot = idx_at(p, q->chain, pos);
@@ -468,21 +477,64 @@ static int32_t relax(pool_t* p, int64_t need, int32_t t) {
     }
     order[j] = v;
   }
-  for (int32_t k = 0; k < n; k++) {
-    p->cl[order[k]].state = ST_DEMOTED;  /* tentative */
-    if (need <= available(p)) {
-      for (int32_t j = 0; j <= k; j++) {
-        claim_t* q = &p->cl[order[j]];
-        q->state = ST_MATERIALIZED;
-        set_state(p, q, ST_DEMOTED);
-        q->demote = t;
-        q->relaxed = 1;
+  /* tentative picks: 1 offload, 2 demote, 0 left alone */
+  int32_t* pick = (int32_t*)malloc((size_t)(n > 0 ? n : 1) * sizeof(int32_t));
+  int64_t room = (int64_t)p->U2 - p->t2_used;
+  int fits = 0;
+  int32_t k = 0;
+  for (; k < n && !fits; k++) {
+    claim_t* q = &p->cl[order[k]];
+    pick[k] = 0;
+    if (q->offloadable && q->L <= room) {
+      pick[k] = 1;
+      q->eff = PROT_OFFLOADED;
+      room -= q->L;
+    } else if (q->demotable) {
+      pick[k] = 2;
+      q->state = ST_DEMOTED;
+    } else {
+      continue;
+    }
+    fits = need <= available(p);
+  }
+  int32_t relaxed = 0;
+  for (int32_t j = 0; j < k; j++) {
+    claim_t* q = &p->cl[order[j]];
+    if (pick[j] == 1) {
+      if (fits) {
+        q->offloaded = 1; q->relaxed = 1;
+        p->t2_used += q->L;
+        p->tel[T_OFF_CLAIMS]++; p->tel[T_OFF_BLOCKS] += q->L;
+        relaxed++;
+      } else {
+        q->eff = PROT_HARD;
       }
-      return k + 1;
+    } else if (pick[j] == 2) {
+      q->state = ST_MATERIALIZED;
+      if (fits) {
+        set_state(p, q, ST_DEMOTED);
+        q->demote = t; q->relaxed = 1;
+        p->tel[T_RUNTIME_DEMOTED]++;
+        relaxed++;
+      }
     }
   }
-  for (int32_t k = 0; k < n; k++) p->cl[order[k]].state = ST_MATERIALIZED;
-  return 0;
+  if (p->t2_used > p->tel[T_T2_PEAK]) p->tel[T_T2_PEAK] = (int32_t)p->t2_used;
+  free(pick);
+  return relaxed;
+}
+
+/* Positions [h, P) of chain c that a claim holding a second-tier copy covers: a served prefill
+ * takes them from the second tier instead of recomputing them (the restore cost, §3.5 "offload
+ * resident"); they still take new GPU blocks like any position past the hits. */
+static int32_t restorable(pool_t* p, int32_t c, int32_t h, int32_t Pp) {
+  int32_t e = 0;
+  for (int32_t s = 0; s < p->n_cl; s++) {
+    claim_t* q = &p->cl[s];
+    if (claim_live(q) && q->offloaded && q->chain == c && q->L > e) e = q->L;
+  }
+  int32_t top = imin(Pp, e);
+  return top > h ? top - h : 0;
 }
 
 /* Serve an active prefill of request rid (S blocks, shared chain c, shared prefix P) at step t: the
@@ -526,7 +578,7 @@ static int serve_prefill(pool_t* p, int32_t t, int32_t rid, int32_t S, int32_t c
   }
   o[0] = relaxed ? OC_RELAXED : r.resident > 0 ? OC_EVICT_RESIDENT : OC_ADMIT;
   o[1] = rid; o[2] = r.resident; o[3] = h; o[4] = relaxed ? relaxed : -1;
-  p->tel[T_RUNTIME_DEMOTED] += relaxed;
+  if (Pp > h) p->tel[T_RESTORED] += restorable(p, c, h, Pp);
   if (r.post_release) *flags |= FL_POST_RELEASE;
   if (r.unclaimed) *flags |= FL_UNCLAIMED;
   p->tel[T_VICTIMS] += r.victims; p->tel[T_RESIDENT] += r.resident;
@@ -547,6 +599,8 @@ static void pool_free(pool_t* p) {
 static int pool_init(pool_t* p, const int32_t* d, const int32_t* ev) {
   memset(p, 0, sizeof *p);
   p->U = d[0]; p->mode = d[1] & ~MODE_RELAX_FLAG; p->relax = (d[1] & MODE_RELAX_FLAG) != 0;
+  p->U2 = d[8];
+  if (p->U2 < 0 || d[9] != 0 || d[10] != 0 || d[11] != 0) return -1;
   p->n_events = d[2]; p->n_chains = d[3];
   p->max_claims = d[4]; p->max_reqs = d[5]; p->n_slots = d[6]; p->defer_limit = d[7];
   if (p->U < 1 || p->n_events < 0 || p->n_chains < 0 || p->n_slots < 0 || p->defer_limit < 0)
@@ -644,6 +698,16 @@ static int replay_pool(const int32_t* d, const int32_t* ev, int32_t* out, int32_
         set_state(p, q, ST_EXPIRED);
         q->expire = t;
         expired++;
+        if (q->offloaded) {  /* responsibility ends: the second-tier copy is dropped */
+          p->t2_used -= q->L; q->offloaded = 0; q->eff = PROT_NONE;
+          /* its predicate held only through the copy: without it, a chain already shorter than
+           * T fails the predicate now (§3.1 offloadable: only while it stays restorable) */
+          if (q->pred_fail < 0 && !pred_holds(p, q)) {
+            q->pred_fail = t;
+            flags |= FL_PRED_FAIL;
+            p->tel[T_PREDFAIL]++;
+          }
+        }
       }
     }
     if (expired) { flags |= FL_EXPIRED; p->tel[T_EXPIRED] += expired; }
@@ -743,7 +807,6 @@ static int replay_pool(const int32_t* d, const int32_t* ev, int32_t* out, int32_
           code = relaxed ? OC_RELAXED : r.resident > 0 ? OC_EVICT_RESIDENT : OC_ADMIT;
           id = rid; a = r.resident; bb = count_active(p);
           if (relaxed) n16 = relaxed;
-          p->tel[T_RUNTIME_DEMOTED] += relaxed;
           if (r.post_release) flags |= FL_POST_RELEASE;
           if (r.unclaimed) flags |= FL_UNCLAIMED;
           p->tel[T_VICTIMS] += r.victims; p->tel[T_RESIDENT] += r.resident;
@@ -758,6 +821,7 @@ static int replay_pool(const int32_t* d, const int32_t* ev, int32_t* out, int32_
       claim_t* q = slot;
       q->valid = 1; q->chain = c; q->L = L; q->T = T; q->hard = hard; q->prio = prio; q->dur = dur;
       q->demotable = (int32_t)((w0 >> 7) & 1u);
+      q->offloadable = (int32_t)((w0 >> 9) & 1u);
       q->best_effort = (int32_t)((w0 >> 8) & 1u);
       /* a best-effort claim carries no preservation obligation: it is observed like a claim in a
        * pool that does not accept claims (§3.1 best_effort: telemetry only) */
@@ -842,6 +906,7 @@ static int replay_pool(const int32_t* d, const int32_t* ev, int32_t* out, int32_
         claim_t* q = &p->cl[livebuf[(uint32_t)e[1] % (uint32_t)n]];
         set_state(p, q, ST_RELEASED);
         q->release = t;
+        if (q->offloaded) { p->t2_used -= q->L; q->offloaded = 0; }
         code = OC_RELEASED; id = q->id; a = imin(lead(p, q->chain), q->L); bb = q->T;
         p->tel[T_RELEASED]++;
       }
@@ -851,7 +916,7 @@ static int replay_pool(const int32_t* d, const int32_t* ev, int32_t* out, int32_
       if (p->mode == MODE_SOFT || p->mode == MODE_HARD)
         for (int32_t s = 0; s < p->n_cl; s++) {
           claim_t* q = &p->cl[s];
-          if (q->valid && q->state == ST_MATERIALIZED && q->hard) livebuf[n++] = s;
+          if (q->valid && q->state == ST_MATERIALIZED && q->hard && !q->offloaded) livebuf[n++] = s;
         }
       if (n == 0) {
         code = OC_NOOP;
@@ -875,7 +940,7 @@ static int replay_pool(const int32_t* d, const int32_t* ev, int32_t* out, int32_
         if (!q->valid || q->pred_fail >= 0) continue;
         if (!(q->state == ST_OBSERVED || q->state == ST_MATERIALIZED || q->state == ST_DEMOTED ||
               q->state == ST_EXPIRED)) continue;
-        if (pred_holds(p, q)) continue;
+        if (q->offloaded || pred_holds(p, q)) continue;
         q->pred_fail = t;
         flags |= FL_PRED_FAIL;
         p->tel[T_PREDFAIL]++;
@@ -926,7 +991,8 @@ static int replay_pool(const int32_t* d, const int32_t* ev, int32_t* out, int32_
     claim_t* q = &p->cl[s];
     w[0] = q->id;
     w[1] = q->valid ? (q->decision | (q->state << 4) | (q->hard << 8) | (q->prio << 9) | (q->eff << 11) |
-                       (q->demotable << 13) | (q->best_effort << 14) | (q->relaxed << 15)) : 0;
+                       (q->demotable << 13) | (q->best_effort << 14) | (q->relaxed << 15) |
+                       (q->offloadable << 16)) : 0;
     w[2] = q->accept; w[3] = q->demote; w[4] = q->expire; w[5] = q->release;
     w[6] = q->pred_fail; w[7] = q->harm; w[8] = q->blocked;
     w[9] = q->valid ? imin(lead(p, q->chain), q->L) : 0;

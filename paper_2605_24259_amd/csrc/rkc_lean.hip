@@ -59,11 +59,12 @@ enum : u32 { DEC_ACCEPTED = 1, DEC_APPROX = 2, DEC_SHADOW = 3, DEC_REJECTED = 4 
 // pool telemetry words accumulated lane-distributed
 enum : u32 { TW_VICTIMS = 10, TW_RESIDENT = 11, TW_POST = 12, TW_DROPPED = 13, TW_HITS = 14,
              TW_ACCEPTED = 15, TW_HARM = 19, TW_PREDFAIL = 20, TW_EXPIRED = 21, TW_DEMOTED = 22,
-             TW_RELEASED = 23, TW_RETRY_SERVED = 33, TW_RETRY_REFUSED = 34, TW_RUNTIME_DEMOTED = 37 };
+             TW_RELEASED = 23, TW_RETRY_SERVED = 33, TW_RETRY_REFUSED = 34, TW_RUNTIME_DEMOTED = 37,
+             TW_OFF_CLAIMS = 38, TW_OFF_BLOCKS = 39, TW_RESTORED = 40 };
 
 // live-claim meta (low half of qc): state[0:3) eff[3:5) hard[5] prio[6:8) pending[8] decision[9:12)
-// demotable[12] best_effort[13] demoted_by_runtime[14]
-constexpr u32 M_DEMQ = 1u << 12, M_BE = 1u << 13, M_RELAXED = 1u << 14;
+// demotable[12] best_effort[13] relaxed_by_runtime[14] offloadable[15]
+constexpr u32 M_DEMQ = 1u << 12, M_BE = 1u << 13, M_RELAXED = 1u << 14, M_OFFQ = 1u << 15;
 __device__ __forceinline__ u32 m_state(u32 m) { return m & 7u; }
 __device__ __forceinline__ u32 m_eff(u32 m) { return (m >> 3) & 3u; }
 __device__ __forceinline__ u32 m_hard(u32 m) { return (m >> 5) & 1u; }
@@ -72,7 +73,7 @@ __device__ __forceinline__ u32 m_pend(u32 m) { return (m >> 8) & 1u; }
 __device__ __forceinline__ u32 m_dec(u32 m) { return (m >> 9) & 7u; }
 __device__ __forceinline__ u32 packed_of(u32 m) {
   return m_dec(m) | (m_state(m) << 4) | (m_hard(m) << 8) | (m_prio(m) << 9) | (m_eff(m) << 11) |
-         (((m >> 12) & 7u) << 13);
+         (((m >> 12) & 15u) << 13);
 }
 
 __device__ __forceinline__ u32 lo16(u32 v) { return v & 0xFFFFu; }
@@ -83,6 +84,8 @@ __device__ __forceinline__ i32 st16(u32 v) { return v == NIL ? -1 : (i32)v; }  /
 // ---- wave primitives (all 64 lanes active) ----------------------------------------------------
 __device__ __forceinline__ u32 ufl(u32 v) { return (u32)__builtin_amdgcn_readfirstlane((int)v); }
 __device__ __forceinline__ u32 rdl(u32 v, u32 l) { return (u32)__builtin_amdgcn_readlane((int)v, (int)l); }
+// a - b, or 0 when b exceeds a
+__device__ __forceinline__ u32 sub0(u32 a, u32 b) { return a > b ? a - b : 0u; }
 // lane l of `old` replaced by the uniform value v
 __device__ __forceinline__ u32 wrl(u32 old, u32 v, u32 l) { return __lane_id() == l ? v : old; }
 __device__ __forceinline__ u64 ballot(bool p) { return __ballot(p); }
@@ -130,7 +133,7 @@ struct Lean {
   // descriptor: the rarely used limits one per lane of `cst`
   static constexpr u32 mode = MODE;
   u32 cst;  // lane 0 U, 1 chains, 2 live-claim cap, 3 live-request cap, 4 claim slots, 5 node cap,
-            // 6 defer limit, 7 relaxation on
+            // 6 defer limit, 7 relaxation on, 8 second-tier capacity
   u32 lane;
   __device__ __forceinline__ u32 U() const { return rdl(cst, 0); }
   __device__ __forceinline__ u32 nch() const { return rdl(cst, 1); }
@@ -140,6 +143,7 @@ struct Lean {
   __device__ __forceinline__ u32 ncap() const { return rdl(cst, 5); }
   __device__ __forceinline__ u32 dlim() const { return rdl(cst, 6); }
   __device__ __forceinline__ u32 relax_on() const { return rdl(cst, 7); }
+  __device__ __forceinline__ u32 t2cap() const { return rdl(cst, 8); }
   // soft levels and acceptance (soft, hard pools: mode bit 0), hard protection, write no-admit
   __device__ __forceinline__ static constexpr bool softl() { return MODE & 1; }
   __device__ __forceinline__ static constexpr bool shadm() { return !(MODE & 1); }
@@ -185,7 +189,7 @@ struct Lean {
   // (QH..FLO is one 16-byte group, VIC, POST and DQH, DQL 8-byte groups: keep their word offsets
   // aligned)
   enum : u32 { C_QH = 0, C_QT, C_FT, C_FLO, C_FTOP, C_FNODE, C_BUMP, C_NSLOT, C_VIC, C_POST, C_STATUS,
-               C_DQC, C_DQH, C_DQL, C_WORDS };
+               C_DQC, C_DQH, C_DQL, C_T2, C_T2PK, C_WORDS };
   static_assert(C_QH % 4 == 0 && C_VIC % 2 == 0 && C_DQH % 2 == 0 && C_WORDS <= 16, "cold block layout");
   u32 fnode, bump;              // valid between cold_nodes_in() and cold_nodes_out()
   u32 qh, qt, ft, flo, ftop;    // valid between cold_fifo_in() and cold_fifo_out()
@@ -364,7 +368,7 @@ struct Lean {
     const bool on = on_chain(c);
     const u32 pp = wmax((on && hardm() && m_state(m) == ST_MATERIALIZED && m_eff(m) == RKC_PROT_HARD) ? L : 0u);
     G0 g = rd0(c);
-    g.covA = wmax(on ? L : 0u);
+    g.covA = wmax(on && m_eff(m) != RKC_PROT_OFFLOADED ? L : 0u);
     commit(c, g, g.n, g.hold, pp, 0, 0);
   }
   // recompute every chain named by a claim lane in `mask`
@@ -394,7 +398,24 @@ struct Lean {
     const bool cand = lane < ncl && (st == ST_MATERIALIZED || st == ST_DEMOTED) && dur != 0;
     const u32 ex = lo16(qa) + dur;
     const bool hit = cand && ex <= t;
-    qc = hit ? pk((m & ~7u) | ST_EXPIRED, hi16(qc)) : qc;
+    if (ext()) {
+      // responsibility ends: an offloaded claim's second-tier copy is dropped
+      const bool off = hit && m_eff(m) == RKC_PROT_OFFLOADED;
+      if (__builtin_expect(ballot(off) != 0, 0)) {
+        cold[C_T2] = ufl(cold[C_T2]) - wsum(off ? lo16(qb) : 0u);
+        // its predicate held only through the dropped copy: a chain already shorter than T fails
+        // it now (no harm: the claim is expired)
+        const bool fail = off && m_pend(m) && chain_n(hi16(qa)) < hi16(qb);
+        qc = off ? pk(m & ~(3u << 3) & ~(fail ? 1u << 8 : 0u), hi16(qc)) : qc;
+        qf = fail ? pk(t, hi16(qf)) : qf;
+        const u32 nf = (u32)__builtin_popcountll(ballot(fail));
+        if (nf) {
+          flags |= RKC_FL_PRED_FAIL;
+          tadd(TW_PREDFAIL, nf);
+        }
+      }
+    }
+    qc = hit ? pk((lo16(qc) & ~7u) | ST_EXPIRED, hi16(qc)) : qc;
     qe = hit ? pk(lo16(qe), t) : qe;
     const u64 hm = ballot(hit);
     nexp = wmin(cand && !hit ? ex : NEVER);
@@ -411,7 +432,7 @@ struct Lean {
   __device__ __forceinline__ u32 sweep(u32 t) {
     const u32 m = lo16(qc), T = hi16(qb), c = hi16(qa);
     const u32 nc = chain_n(c);
-    const bool fail = lane < ncl && m_pend(m) && nc < T;
+    const bool fail = lane < ncl && m_pend(m) && nc < T && m_eff(m) != RKC_PROT_OFFLOADED;
     const bool harm = fail && m_state(m) == ST_MATERIALIZED;
     const u32 m2 = (m & ~(1u << 8) & ~(harm ? 7u : 0u)) | (harm ? ST_HARMED : 0u);
     qc = fail ? pk(m2, hi16(qc)) : qc;
@@ -501,11 +522,12 @@ struct Lean {
               // victims inside live claims: resident; inside only demoted / expired ones: post-release
               const u32 st = m_state(lo16(qc));
               const bool on = on_chain(c);
-              const u32 covS = wmax((on && (st == ST_OBSERVED || st == ST_MATERIALIZED || st == ST_HARMED)) ? lo16(qb) : 0u);
+              const bool off = m_eff(lo16(qc)) == RKC_PROT_OFFLOADED;
+              const u32 covS = wmax((on && !off && (st == ST_OBSERVED || st == ST_MATERIALIZED || st == ST_HARMED)) ? lo16(qb) : 0u);
               rs = min(nn, g.covA) - nw;
               sc = min(nn, covS) > nw ? min(nn, covS) - nw : 0u;
               // a claim whose predicate still holds needs more than nw leading blocks
-              if (ballot(on && m_pend(lo16(qc)) && hi16(qb) > nw)) sweep_due = 1;
+              if (ballot(on && !off && m_pend(lo16(qc)) && hi16(qb) > nw)) sweep_due = 1;
             }
             r.victims += m;
             r.resident += rs;
@@ -625,12 +647,14 @@ struct Lean {
   }
 
   // Runtime relaxation (§3.1 demotable: the downgrade comes before the predicate-breaking
-  // eviction; §3.5 "relax resident claim": the active side is served by demoting resident state).
-  // Before an active allocation of `need` blocks that hard protection makes infeasible, the
-  // demotable claims among the blocking ones (materialized hard claims reaching a cached position
-  // outside the hits) are picked lowest priority first, then lowest id, until the allocation would
-  // fit; then the picked claims are demoted.  None is demoted when even all would not make it fit.
-  // Returns the number demoted; ghc (the hit chain's record) is re-read when claims were demoted.
+  // eviction; offloadable: the content may leave GPU memory if the predicate stays restorable; §3.5
+  // "relax resident claim" and "offload resident").  Before an active allocation of `need` blocks
+  // that hard protection makes infeasible, the blocking claims (materialized hard claims reaching a
+  // cached position outside the hits) that allow demotion or offload are taken lowest priority
+  // first, then lowest id: each is offloaded when it allows it and its footprint fits the second
+  // tier's free room, else demoted when it allows it, else left alone, until the allocation would
+  // fit; only then do the picked claims change.  Nothing changes when it never fits.  Returns the
+  // number of claims relaxed; ghc (the hit chain's record) is re-read when claims changed.
   __device__ __forceinline__ u32 relax(u32 t, u32 need, i32 hc, u32 h, G0& ghc) {
     u32 k = 0;
     if (relax_on() && need > F) {
@@ -646,29 +670,44 @@ struct Lean {
         if ((i32)c == hc) cov = max(cov, h);
         const bool hm = lane < ncl && m_state(m) == ST_MATERIALIZED && m_eff(m) == RKC_PROT_HARD;
         const u32 key = (m_prio(m) << 16) | lo16(qa);
-        u64 left = ballot(hm && (m & M_DEMQ) && L > cov);
-        u64 S = 0;
+        u64 left = ballot(hm && (m & (M_DEMQ | M_OFFQ)) && L > cov);
+        u64 S = 0, O = 0;  // picked; picked for offload (the rest of S is demoted)
+        u32 room = sub0(t2cap(), ufl(cold[C_T2])), moved = 0;
         for (u32 guard = 0; left && (u64)need > avail && guard < 64; guard++) {
           const bool mine = (left >> lane) & 1ull;
           const u32 kmin = wmin(mine ? key : NEVER);
           const u32 l = (u32)__builtin_ctzll(ballot(mine && key == kmin));
-          const u32 cq = rdl(c, l);
-          const G0 g = rd0(cq);
-          const u32 base = (i32)cq == hc ? max(g.hold, h) : g.hold;
-          const bool on = hm && c == cq;
-          const u32 before = wmax(on && !((S >> lane) & 1ull) ? L : 0u);
-          S |= 1ull << l;
           left &= ~(1ull << l);
-          const u32 after = wmax(on && !((S >> lane) & 1ull) ? L : 0u);
-          avail += evictable(g.n, base, after) - evictable(g.n, base, before);
+          const u32 ml = rdl(m, l), Ll = rdl(L, l);
+          const bool off = (ml & M_OFFQ) && Ll <= room;
+          if (off || (ml & M_DEMQ)) {
+            if (off) { O |= 1ull << l; room -= Ll; moved += Ll; }
+            const u32 cq = rdl(c, l);
+            const G0 g = rd0(cq);
+            const u32 base = (i32)cq == hc ? max(g.hold, h) : g.hold;
+            const bool on = hm && c == cq;
+            const u32 before = wmax(on && !((S >> lane) & 1ull) ? L : 0u);
+            S |= 1ull << l;
+            const u32 after = wmax(on && !((S >> lane) & 1ull) ? L : 0u);
+            avail += evictable(g.n, base, after) - evictable(g.n, base, before);
+          }
         }
         if ((u64)need <= avail) {
-          const bool d = (S >> lane) & 1ull;
+          const bool o = (O >> lane) & 1ull, d = ((S & ~O) >> lane) & 1ull;
           qc = d ? pk((m & ~7u) | ST_DEMOTED | M_RELAXED, hi16(qc)) : qc;
+          qc = o ? pk((m & ~(3u << 3)) | (RKC_PROT_OFFLOADED << 3) | M_RELAXED, hi16(qc)) : qc;
           qe = d ? pk(t, hi16(qe)) : qe;
           recompute_lanes(S);
           k = (u32)__builtin_popcountll(S);
-          tadd(TW_RUNTIME_DEMOTED, k);
+          const u32 no = (u32)__builtin_popcountll(O);
+          tadd(TW_RUNTIME_DEMOTED, k - no);
+          if (no) {
+            const u32 used = ufl(cold[C_T2]) + moved;
+            cold[C_T2] = used;
+            cold[C_T2PK] = max(ufl(cold[C_T2PK]), used);
+            tadd(TW_OFF_CLAIMS, no);
+            tadd(TW_OFF_BLOCKS, moved);
+          }
           if (hc >= 0) ghc = rd0((u32)hc);
         }
       }
@@ -744,6 +783,12 @@ struct Lean {
       o.b = (i32)h;
       served(r, o);
       if (relaxed) { o.code = RKC_OC_RELAXED; o.n16 = min(relaxed, 65535u); }
+      if (ext() && P > h && t2cap() > 0) {
+        // positions past the hits that a claim holding a second-tier copy covers are restored
+        // from the second tier (restore cost), still on new GPU blocks
+        const u32 e = wmax(on_chain(cc) && m_eff(lo16(qc)) == RKC_PROT_OFFLOADED ? lo16(qb) : 0u);
+        tadd(TW_RESTORED, sub0(min(P, e), h));
+      }
     }
   }
 
@@ -818,7 +863,8 @@ struct Lean {
         const u32 L = w1, c = w2, T = w3;
         const u32 hardq = (w0 >> 4) & 1u, prio = (w0 >> 5) & 3u, dur = w0 >> 16;
         // a best-effort claim is observed in every policy (§3.1 best_effort: telemetry only)
-        const u32 beq = (w0 >> 8) & 1u, req_bits = (w0 & (1u << 7) ? M_DEMQ : 0u) | (beq ? M_BE : 0u);
+        const u32 beq = (w0 >> 8) & 1u;
+        const u32 req_bits = (w0 & (1u << 7) ? M_DEMQ : 0u) | (beq ? M_BE : 0u) | (w0 & (1u << 9) ? M_OFFQ : 0u);
         const bool obs = shadm() || beq;
         const G0 g = rd0(c);
         const u32 h = min(L, g.n), need = L - h;
@@ -828,7 +874,8 @@ struct Lean {
         if (!r.ok) {
           const u32 dec = obs ? DEC_SHADOW : DEC_REJECTED;
           const u32 m = ST_REJECTED | (eff << 3) | (hardq << 5) | (prio << 6) | (dec << 9) | req_bits;
-          slotcl[s] = make_uint4(c, L, pk(t, packed_of(m)), 1);
+          const u32 pw = packed_of(m);
+          slotcl[s] = make_uint4(c, L, pk(t, pw & 0xFFFFu), 1u | ((pw >> 16) << 1));
           o.code = RKC_OC_MATFAIL;
           o.id = (i32)t;
           o.a = (i32)need;
@@ -911,7 +958,7 @@ struct Lean {
       if (ncl > 0) i = w1 % ncl;
     } else if (softl()) {
       const u32 m = lo16(qc);
-      const u64 cm = ballot(lane < ncl && m_state(m) == ST_MATERIALIZED && m_hard(m));
+      const u64 cm = ballot(lane < ncl && m_state(m) == ST_MATERIALIZED && m_hard(m) && m_eff(m) != RKC_PROT_OFFLOADED);
       const u32 cnt = (u32)__builtin_popcountll(cm);
       if (cnt > 0) {
         const u32 k = w1 % cnt;
@@ -924,6 +971,7 @@ struct Lean {
       const u32 qbv = rdl(qb, i);
       if (type == RKC_EV_RELEASE) {
         if (lane == i) write_own_record(ST_RELEASED, (i32)t);
+        if (ext() && m_eff(lo16(rdl(qc, i))) == RKC_PROT_OFFLOADED) cold[C_T2] = ufl(cold[C_T2]) - lo16(qbv);
         // close the gap: lanes >= i take their upper neighbour's claim
         const bool up = lane >= i;
         qa = up ? shift_down(qa) : qa; qb = up ? shift_down(qb) : qb; qc = up ? shift_down(qc) : qc;
@@ -984,7 +1032,8 @@ __device__ __forceinline__ void replay_pool(const rkc_lean_args& g, const rkc_po
     const u32 l = P.lane;
     P.cst = l == 0 ? (u32)d.usable_blocks : l == 1 ? (u32)d.n_chains : l == 2 ? (u32)d.max_live_claims
           : l == 3 ? (u32)d.max_live_requests : l == 4 ? (u32)d.n_claim_slots : l == 5 ? g.node_cap
-          : l == 6 ? (u32)d.defer_limit : (u32)((d.mode & RKC_MODE_RELAX) != 0);
+          : l == 6 ? (u32)d.defer_limit : l == 7 ? (u32)((d.mode & RKC_MODE_RELAX) != 0)
+          : (u32)d.offload_blocks;
   }
   const u32 U = (u32)d.usable_blocks, nch = (u32)d.n_chains, nslots = (u32)d.n_claim_slots;
 
@@ -1045,6 +1094,7 @@ __device__ __forceinline__ void replay_pool(const rkc_lean_args& g, const rkc_po
   const u32 nslot_used = ufl(P.cold[LP::C_NSLOT]);
   const u32 vic = ufl(P.cold[LP::C_VIC]), post = ufl(P.cold[LP::C_POST]);
   const u32 status = ufl(P.cold[LP::C_STATUS]), queued = ufl(P.cold[LP::C_DQL]);
+  const u32 t2peak = ufl(P.cold[LP::C_T2PK]);
   // Final records of the claims still live (each lane writes its own) ...
   if (P.lane < P.ncl) P.write_own_record(m_state(lo16(P.qc)), -1);
   __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
@@ -1057,7 +1107,7 @@ __device__ __forceinline__ void replay_pool(const rkc_lean_args& g, const rkc_po
       if (cl.x != NEVER) le = min(P.chain_n(cl.x), cl.y);
       if (cl.w) {
         // rejected or malformed claim: no step ever happened to it
-        const i32 id = (i32)lo16(cl.z), packed = (i32)hi16(cl.z);
+        const i32 id = (i32)lo16(cl.z), packed = (i32)(hi16(cl.z) | ((cl.w >> 1) << 16));
         P.rec[s] = rkc_claim_telemetry{{id, packed, -1, -1, -1, -1, -1, -1, 0, (i32)le}};
       } else {
         P.rec[s].w[9] = (i32)le;
@@ -1073,6 +1123,7 @@ __device__ __forceinline__ void replay_pool(const rkc_lean_args& g, const rkc_po
     if (w < 10) v += (i32)P.hist[w];
     if (w == 32) v += (i32)P.hist[RKC_OC_DEFERRED];
     if (w == 36) v += (i32)P.hist[RKC_OC_RELAXED];
+    if (w == 41) v = (i32)t2peak;
     if (w == TW_VICTIMS) v = (i32)vic;
     else if (w == TW_POST) v = (i32)post;
     else if (w == 24) v = (i32)P.peak;
@@ -1170,7 +1221,7 @@ __global__ __launch_bounds__(64) void rkc_lean(rkc_lean_args g) {
                   d.n_events <= g.max_events && d.n_chains >= 0 &&
                   d.n_chains <= g.max_chains && d.max_live_claims >= 0 && d.max_live_claims <= g.max_claims &&
                   d.max_live_requests >= 0 && d.max_live_requests <= g.max_reqs &&
-                  d.n_claim_slots <= g.max_slots && d.defer_limit >= 0 && d.offload_blocks == 0 &&
+                  d.n_claim_slots <= g.max_slots && d.defer_limit >= 0 && d.offload_blocks >= 0 &&
                   d.reserved[0] == 0 && d.reserved[1] == 0 && d.reserved[2] == 0;
   if (!ok) {
     if (ev_ok)

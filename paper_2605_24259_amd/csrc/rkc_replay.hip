@@ -104,11 +104,13 @@ enum : u32 { RQ_ID = 0, RQ_C, RQ_R, RQ_LEN, RQ_ARRAYS };
 enum : u32 { TW_VICTIMS = 10, TW_RESIDENT = 11, TW_POST = 12, TW_DROPPED = 13, TW_HITS = 14,
              TW_ACCEPTED = 15, TW_HARM = 19, TW_PREDFAIL = 20, TW_EXPIRED = 21, TW_DEMOTED = 22,
              TW_RELEASED = 23, TW_DEFERRED = 32, TW_RETRY_SERVED = 33, TW_RETRY_REFUSED = 34,
-             TW_QUEUED = 35, TW_RELAXED = 36, TW_RUNTIME_DEMOTED = 37 };
+             TW_QUEUED = 35, TW_RELAXED = 36, TW_RUNTIME_DEMOTED = 37, TW_OFF_CLAIMS = 38,
+             TW_OFF_BLOCKS = 39, TW_RESTORED = 40, TW_T2_PEAK = 41 };
 
 // live-claim meta word: state[0:3) eff[3:5) hard[5] prio[6:8) pending[8] decision[9:12)
-// demotable[12] best_effort[13] demoted_by_runtime[14] picked_for_relaxation[15] (16 bits)
-constexpr u32 M_DEMQ = 1u << 12, M_BE = 1u << 13, M_RELAXED = 1u << 14, M_PICK = 1u << 15;
+// demotable[12] best_effort[13] relaxed_by_runtime[14] offloadable[15] (16 bits)
+constexpr u32 M_DEMQ = 1u << 12, M_BE = 1u << 13, M_RELAXED = 1u << 14, M_OFFQ = 1u << 15;
+__device__ __forceinline__ u32 m_with_eff(u32 m, u32 e) { return (m & ~(3u << 3)) | (e << 3); }
 __device__ __forceinline__ u32 m_state(u32 m) { return m & 7u; }
 __device__ __forceinline__ u32 m_eff(u32 m) { return (m >> 3) & 3u; }
 __device__ __forceinline__ u32 m_hard(u32 m) { return (m >> 5) & 1u; }
@@ -119,7 +121,7 @@ __device__ __forceinline__ u32 m_with_state(u32 m, u32 s) { return (m & ~7u) | s
 
 __device__ __forceinline__ u32 packed_of(u32 m) {
   return m_dec(m) | (m_state(m) << 4) | (m_hard(m) << 8) | (m_prio(m) << 9) | (m_eff(m) << 11) |
-         (((m >> 12) & 7u) << 13);
+         (((m >> 12) & 15u) << 13);
 }
 
 // eviction key of a run of candidates with one (level, last use); steps are below 2^24
@@ -214,6 +216,7 @@ struct Pool {
   // descriptor
   i32 U, mode, n_events, n_chains, max_claims, max_reqs, n_slots, defer_limit;
   u32 relax_on;  // the pool relaxes demotable hard claims (mode flag RKC_MODE_RELAX)
+  u32 t2cap, t2used, t2peak;  // second tier: capacity, blocks held by offloaded claims, peak
   u32 lane;
   // memory
   lds_w* ch;          // chain records, CF_WORDS words each
@@ -419,6 +422,8 @@ struct Pool {
     for (u32 i = lane; i < ncl; i += 64) {
       if (cla(CL_C)[i] != c) continue;
       const u32 m = cla(CL_META)[i], L = cla(CL_L)[i], st = m_state(m);
+      // an offloaded claim's victims are not resident and its predicate never fails
+      if (m_eff(m) == RKC_PROT_OFFLOADED) continue;
       ca = max(ca, L);
       if (st == ST_OBSERVED || st == ST_MATERIALIZED || st == ST_HARMED) cso = max(cso, L);
       if (hardm && st == ST_MATERIALIZED && m_eff(m) == RKC_PROT_HARD) pr = max(pr, L);
@@ -560,7 +565,7 @@ struct Pool {
       if (!(mk[c] & MK_SWEEP)) continue;
       u32 m = cla(CL_META)[i];
       const u32 st = m_state(m);
-      if (!m_pending(m)) continue;
+      if (!m_pending(m) || m_eff(m) == RKC_PROT_OFFLOADED) continue;
       if (ch[c * CF_WORDS + CF_N] >= cla(CL_T)[i]) continue;
       m &= ~(1u << 8);
       pf++;
@@ -673,13 +678,27 @@ struct Pool {
   }
 
   __device__ __forceinline__ void expire(u32 t, u32& flags, u32& expired) {
-    u32 cnt = 0, nx = EXP_NEVER;
+    u32 cnt = 0, nx = EXP_NEVER, drop = 0, pf = 0;
     for (u32 i = lane; i < ncl; i += 64) {
       const u32 m = cla(CL_META)[i], st = m_state(m), dur = cla(CL_EXP)[i];
       if ((st != ST_MATERIALIZED && st != ST_DEMOTED) || dur == 0) continue;
       const u32 ex = (u32)cla(CL_ID)[i] + dur;
       if (ex <= t) {
-        cla(CL_META)[i] = m_with_state(m, ST_EXPIRED);
+        // responsibility ends: an offloaded claim's second-tier copy is dropped
+        const bool off = m_eff(m) == RKC_PROT_OFFLOADED;
+        u32 m2 = m;
+        if (off) {
+          drop += cla(CL_L)[i];
+          m2 = m_with_eff(m2, RKC_PROT_NONE);
+          // its predicate held only through the dropped copy: a chain already shorter than T
+          // fails it now (no harm: the claim is expired)
+          if (m_pending(m) && (u32)ch[(u32)cla(CL_C)[i] * CF_WORDS + CF_N] < (u32)cla(CL_T)[i]) {
+            m2 &= ~(1u << 8);
+            cla(CL_PF)[i] = t;
+            pf++;
+          }
+        }
+        cla(CL_META)[i] = m_with_state(m2, ST_EXPIRED);
         cla(CL_EXST)[i] = t;
         mk[cla(CL_C)[i]] |= MK_RECOMP;
         cnt++;
@@ -689,6 +708,12 @@ struct Pool {
     }
     lists_fence();
     cnt = wave_sum(cnt);
+    t2used -= wave_sum(drop);
+    pf = wave_sum(pf);
+    if (pf) {
+      flags |= RKC_FL_PRED_FAIL;
+      tadd(TW_PREDFAIL, pf);
+    }
     next_exp = wave_min(nx);
     if (cnt) {
       __builtin_amdgcn_wave_barrier();
@@ -704,72 +729,94 @@ struct Pool {
         : lane == TW_POST ? (u32)r.post : lane == TW_HITS ? hits : 0u;
   }
 
-  // Largest footprint of the materialized hard claims on chain c not picked for relaxation.
+  // Largest footprint of the materialized hard claims on chain c (tentative picks of the
+  // relaxation have left that state already).
   __device__ __forceinline__ u32 hard_extent(u32 c) {
     u32 pr = 0;
     for (u32 i = lane; i < ncl; i += 64) {
       const u32 m = cla(CL_META)[i];
-      if ((u32)cla(CL_C)[i] == c && m_state(m) == ST_MATERIALIZED && m_eff(m) == RKC_PROT_HARD && !(m & M_PICK))
+      if ((u32)cla(CL_C)[i] == c && m_state(m) == ST_MATERIALIZED && m_eff(m) == RKC_PROT_HARD)
         pr = max(pr, (u32)cla(CL_L)[i]);
     }
     return wave_max(pr);
   }
 
   // Runtime relaxation (§3.1 demotable: the downgrade comes before the predicate-breaking
-  // eviction; §3.5 "relax resident claim": the active side is served by demoting resident state).
-  // Before an active allocation of `need` blocks that hard protection makes infeasible, the
-  // demotable claims among the blocking ones (materialized hard claims reaching a cached position
-  // outside the hits) are picked lowest priority first, then lowest id, until the allocation would
-  // fit; then the picked claims are demoted.  None is demoted when even all would not make it fit.
-  // Returns the number demoted.
+  // eviction; offloadable: the content may leave GPU memory if the predicate stays restorable; §3.5
+  // "relax resident claim" and "offload resident").  Before an active allocation of `need` blocks
+  // that hard protection makes infeasible, the blocking claims (materialized hard claims reaching a
+  // cached position outside the hits) that allow demotion or offload are visited lowest priority
+  // first, then lowest id: each is offloaded when it allows it and its footprint fits the second
+  // tier's free room, else demoted when it allows it, else left alone, until the allocation would
+  // fit.  The picks change the claims tentatively (offload: effective protection OFFLOADED; demote:
+  // state DEMOTED), marked by a demotion step equal to t, which no other claim can carry at t; they
+  // are kept when the allocation fits and undone otherwise.  Returns the number of claims relaxed.
   __device__ __forceinline__ u32 relax(u32 t, i32 need, i32 hc, u32 h) {
     u32 k = 0;
     if (relax_on && need > F) {
       i64 avail = (i64)F + candidates(hc, h);
       if ((i64)need > avail) {
+        u32 room = t2cap > t2used ? t2cap - t2used : 0u, moved = 0, no = 0, lo = 0;
         for (u32 guard = 0; (i64)need > avail && guard <= ncl; guard++) {
           u32 best = 0xFFFFFFFFu, bi = 0;
           for (u32 i = lane; i < ncl; i += 64) {
             const u32 m = cla(CL_META)[i];
-            if (m_state(m) != ST_MATERIALIZED || m_eff(m) != RKC_PROT_HARD || !(m & M_DEMQ) || (m & M_PICK)) continue;
+            if (m_state(m) != ST_MATERIALIZED || m_eff(m) != RKC_PROT_HARD || !(m & (M_DEMQ | M_OFFQ))) continue;
             const u32 c = cla(CL_C)[i];
             u32 cov = (u32)ch[c * CF_WORDS + CF_HOLD];
             if ((i32)c == hc) cov = max(cov, h);
             if ((u32)cla(CL_L)[i] <= cov) continue;  // not blocking: no cached position outside the hits
             const u32 key = (m_prio(m) << 24) | (u32)cla(CL_ID)[i];
-            if (key < best) { best = key; bi = i; }
+            if (key >= lo && key < best) { best = key; bi = i; }
           }
           const u32 wb = wave_min(best);
           if (wb == 0xFFFFFFFFu) break;
+          lo = wb + 1;  // visited: a claim left alone is not visited again
           const u64 at = ballot(best == wb);
           const u32 i = (u32)rdlane((i32)bi, (u32)__builtin_ctzll(at));
+          const u32 m = ufl(cla(CL_META)[i]), L = ufl(cla(CL_L)[i]);
+          const bool off = (m & M_OFFQ) && L <= room;
+          if (!off && !(m & M_DEMQ)) continue;
           const u32 c = ufl(cla(CL_C)[i]);
           const u32 before = hard_extent(c);
-          cla(CL_META)[i] = ufl(cla(CL_META)[i]) | M_PICK;  // every lane, one value
+          // every lane, one value
+          cla(CL_META)[i] = off ? m_with_eff(m, RKC_PROT_OFFLOADED) : m_with_state(m, ST_DEMOTED);
+          cla(CL_DEM)[i] = t;
           lists_fence();
           const u32 after = hard_extent(c);
           const uint4 g0 = cg(c, 0);
           const u32 base = (i32)c == hc ? max(g0.y, h) : g0.y;
           avail += evictable(g0.x, base, after) - evictable(g0.x, base, before);
+          if (off) { room -= L; moved += L; no++; }
           k++;
         }
         const bool fits = (i64)need <= avail;
-        for (u32 i = lane; i < ncl; i += 64) {
-          const u32 m = cla(CL_META)[i];
-          if (!(m & M_PICK)) continue;
-          if (fits) {
-            cla(CL_META)[i] = (m_with_state(m, ST_DEMOTED) & ~M_PICK) | M_RELAXED;
-            cla(CL_DEM)[i] = t;
-            mk[cla(CL_C)[i]] |= MK_RECOMP;
-          } else {
-            cla(CL_META)[i] = m & ~M_PICK;
+        if (k) {
+          for (u32 i = lane; i < ncl; i += 64) {
+            if (lnil((u32)cla(CL_DEM)[i]) != t) continue;
+            const u32 m = cla(CL_META)[i];
+            const bool off = m_eff(m) == RKC_PROT_OFFLOADED;
+            if (fits) {
+              cla(CL_META)[i] = m | M_RELAXED;
+              if (off) cla(CL_DEM)[i] = kListNil;  // an offloaded claim records no demotion
+              mk[cla(CL_C)[i]] |= MK_RECOMP;
+            } else {
+              cla(CL_META)[i] = off ? m_with_eff(m, RKC_PROT_HARD) : m_with_state(m, ST_MATERIALIZED);
+              cla(CL_DEM)[i] = kListNil;
+            }
           }
+          lists_fence();
         }
-        lists_fence();
         if (fits) {
           __builtin_amdgcn_wave_barrier();
           recompute_marked(MK_RECOMP);
-          tadd(TW_RUNTIME_DEMOTED, k);
+          tadd(TW_RUNTIME_DEMOTED, k - no);
+          if (no) {
+            t2used += moved;
+            t2peak = max(t2peak, t2used);
+            tadd(TW_OFF_CLAIMS, no);
+            tadd(TW_OFF_BLOCKS, moved);
+          }
         } else {
           k = 0;
         }
@@ -940,6 +987,15 @@ struct Pool {
         lists_fence();
         id = (i32)rid; b = (i32)h;
         count_victims(r, h);
+        if (hc >= 0 && (u32)w3 > h && t2cap > 0) {
+          // positions past the hits that a claim holding a second-tier copy covers are restored
+          // from the second tier (restore cost), still on new GPU blocks
+          u32 e = 0;
+          for (u32 i = lane; i < ncl; i += 64)
+            if ((u32)cla(CL_C)[i] == (u32)hc && m_eff(cla(CL_META)[i]) == RKC_PROT_OFFLOADED) e = max(e, (u32)cla(CL_L)[i]);
+          const u32 top = min((u32)w3, wave_max(e));
+          if (top > h) tadd(TW_RESTORED, top - h);
+        }
         break;
       }
       case K_EXTEND:
@@ -956,7 +1012,7 @@ struct Pool {
         const u32 eff = beq ? RKC_PROT_NONE : mode == RKC_MODE_HARD ? (hardq ? RKC_PROT_HARD : RKC_PROT_SOFT)
                       : mode == RKC_MODE_SOFT ? RKC_PROT_SOFT : RKC_PROT_NONE;
         const u32 shadow = (u32)(mode == RKC_MODE_LRU) | (u32)(mode == RKC_MODE_NOADMIT) | beq;
-        const u32 req_bits = (demq ? M_DEMQ : 0u) | (beq ? M_BE : 0u);
+        const u32 req_bits = (demq ? M_DEMQ : 0u) | (beq ? M_BE : 0u) | ((uw0 >> 9) & 1u ? M_OFFQ : 0u);
         u32 dec;
         if (!r.ok) {
           dec = shadow ? DEC_SHADOW : DEC_REJECTED;
@@ -1039,14 +1095,16 @@ struct Pool {
           u32 cnt = 0;
           for (u32 base = 0; base < ncl; base += 64) {
             const u32 j = base + lane;
-            const bool cand = j < ncl && m_state(cla(CL_META)[j]) == ST_MATERIALIZED && m_hard(cla(CL_META)[j]);
+            const u32 m = j < ncl ? (u32)cla(CL_META)[j] : 0u;
+            const bool cand = j < ncl && m_state(m) == ST_MATERIALIZED && m_hard(m) && m_eff(m) != RKC_PROT_OFFLOADED;
             cnt += (u32)__builtin_popcountll(ballot(cand));
           }
           if (cnt > 0) {
             u32 k = (u32)w1 % cnt;
             for (u32 base = 0; base < ncl && i == NIL; base += 64) {
               const u32 j = base + lane;
-              const bool cand = j < ncl && m_state(cla(CL_META)[j]) == ST_MATERIALIZED && m_hard(cla(CL_META)[j]);
+              const u32 m = j < ncl ? (u32)cla(CL_META)[j] : 0u;
+              const bool cand = j < ncl && m_state(m) == ST_MATERIALIZED && m_hard(m) && m_eff(m) != RKC_PROT_OFFLOADED;
               const u64 bl = ballot(cand);
               const u32 pc = (u32)__builtin_popcountll(bl);
               if (k < pc) {
@@ -1064,6 +1122,7 @@ struct Pool {
           const u32 T = ufl(cla(CL_T)[i]);
           if (kind == K_RELEASE) {
             write_live_record(i, ST_RELEASED, (i32)t);
+            if (m_eff(ufl(cla(CL_META)[i])) == RKC_PROT_OFFLOADED) t2used -= L;  // the copy is dropped
             __builtin_amdgcn_wave_barrier();
             list_remove(cl, cl_cap, CL_ARRAYS, ncl, i);
             ncl--;
@@ -1126,6 +1185,7 @@ __global__ __launch_bounds__(64) void rkc_replay_wave(Args g) {
   const rkc_pool_desc d = g.pools[pool];
   P.U = d.usable_blocks; P.mode = d.mode & ~RKC_MODE_RELAX; P.n_events = d.n_events; P.n_chains = d.n_chains;
   P.relax_on = (d.mode & RKC_MODE_RELAX) != 0;
+  P.t2cap = (u32)d.offload_blocks; P.t2used = 0; P.t2peak = 0;
   P.max_claims = d.max_live_claims; P.max_reqs = d.max_live_requests; P.n_slots = d.n_claim_slots;
   const i64 ev_off = d.event_offset, slot_off = d.claim_slot_offset;
   rkc_pool_telemetry* ptel = g.pool_tel + pool;
@@ -1137,7 +1197,7 @@ __global__ __launch_bounds__(64) void rkc_replay_wave(Args g) {
                   P.mode >= 0 && P.mode <= 3 && P.n_events <= g.max_events && P.n_chains >= 0 &&
                   P.n_chains <= g.max_chains && P.max_claims >= 0 && P.max_claims <= g.max_claims &&
                   P.max_reqs >= 0 && P.max_reqs <= g.max_reqs && P.n_slots <= g.max_slots &&
-                  d.defer_limit >= 0 && d.offload_blocks == 0 && d.reserved[0] == 0 &&
+                  d.defer_limit >= 0 && d.offload_blocks >= 0 && d.reserved[0] == 0 &&
                   d.reserved[1] == 0 && d.reserved[2] == 0;
   if (!ok) {
     if (ev_ok)
@@ -1240,6 +1300,7 @@ __global__ __launch_bounds__(64) void rkc_replay_wave(Args g) {
     else if (w == 30) v = (i32)P.ncl;
     else if (w == 31) v = (i32)P.status;
     else if (w == TW_QUEUED) v = (i32)P.dq_len;
+    else if (w == TW_T2_PEAK) v = (i32)P.t2peak;
     ptel->w[w] = v;
   }
 }

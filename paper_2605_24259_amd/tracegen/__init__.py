@@ -264,11 +264,11 @@ def make_desc(pools: list[dict], n_events: list[int], n_slots: list[int]) -> np.
 
 
 def ev(type_: int, w1: int = 0, w2: int = 0, w3: int = 0, hard: int = 0, prio: int = 0,
-       dur: int = 0, demotable: int = 0, best_effort: int = 0) -> list[int]:
+       dur: int = 0, demotable: int = 0, best_effort: int = 0, offloadable: int = 0) -> list[int]:
     """Encode one event (w0 = type | hard << 4 | prio << 5 | demotable << 7 | best_effort << 8 |
-    duration << 16)."""
+    offloadable << 9 | duration << 16)."""
     w0 = ((type_ & 15) | ((hard & 1) << 4) | ((prio & 3) << 5) | ((demotable & 1) << 7)
-          | ((best_effort & 1) << 8) | ((dur & 0xFFFF) << 16))
+          | ((best_effort & 1) << 8) | ((offloadable & 1) << 9) | ((dur & 0xFFFF) << 16))
     if w0 >= 1 << 31:
         w0 -= 1 << 32
     w = [w0, w1, w2, w3]
@@ -283,9 +283,9 @@ def extend(k, sel=0):
     return ev(EV_EXTEND, k, sel)
 
 
-def claim(L, c, T=None, hard=0, prio=0, dur=0, demotable=0, best_effort=0):
+def claim(L, c, T=None, hard=0, prio=0, dur=0, demotable=0, best_effort=0, offloadable=0):
     return ev(EV_CLAIM, L, c, L if T is None else T, hard=hard, prio=prio, dur=dur,
-              demotable=demotable, best_effort=best_effort)
+              demotable=demotable, best_effort=best_effort, offloadable=offloadable)
 
 
 def finish(sel=0):
@@ -310,7 +310,8 @@ def retry():
 
 def from_pools(pools: list[dict], name: str = "handmade") -> Trace:
     """Batch from explicit pools: each dict has usable_blocks, mode, events (list of 4-int lists),
-    optional n_chains / max_live_claims / max_live_requests / n_claim_slots / defer_limit."""
+    optional n_chains / max_live_claims / max_live_requests / n_claim_slots / defer_limit /
+    offload_blocks."""
     evs = [np.asarray(p["events"], np.int64).reshape(-1, 4) for p in pools]
     n_ev = [int(e.shape[0]) for e in evs]
     n_sl = [int(np.sum((e[:, 0] & 15) == EV_CLAIM)) if e.size else 0 for e in evs]

@@ -25,7 +25,7 @@ TEL = {"victims": 10, "resident": 11, "post_release": 12, "dropped": 13, "hits":
        "expired": 21, "demoted": 22, "released": 23, "peak_active": 24, "active": 25, "cached": 26,
        "free": 27, "protected": 28, "live_requests": 29, "live_claims": 30, "status": 31,
        "n_deferred": 32, "retry_served": 33, "retry_refused": 34, "queued": 35, "n_relaxed": 36,
-       "runtime_demoted": 37,
+       "runtime_demoted": 37, "off_claims": 38, "off_blocks": 39, "restored": 40, "t2_peak": 41,
        "n_admit": 0, "n_refused_claim": 2, "n_refused_capacity": 3}
 DECISIONS = {"none": 0, "accepted": 1, "approx": 2, "shadow": 3, "rejected": 4}
 STATES = {"submitted": 0, "observed": 1, "materialized": 2, "demoted": 3, "expired": 4,
@@ -92,7 +92,7 @@ def to_trace(tg, fixtures):
             if kind == "claim":
                 evs.append(tg.claim(g("L"), g("c"), g("T", g("L")), hard=g("hard"), prio=g("prio"),
                                     dur=g("dur"), demotable=g("demotable"),
-                                    best_effort=g("best_effort")))
+                                    best_effort=g("best_effort"), offloadable=g("offloadable")))
             elif kind == "prefill":
                 evs.append(tg.prefill(g("S"), g("c", -1), g("P")))
             elif kind == "extend":
@@ -113,6 +113,7 @@ def to_trace(tg, fixtures):
         pools.append(dict(usable_blocks=int(f["usable"]), mode=mode,
                           n_chains=int(f.get("chains", 0)), events=evs,
                           defer_limit=int(f.get("defer_limit", 0)),
+                          offload_blocks=int(f.get("offload", 0)),
                           **({"max_live_requests": int(f["max_requests"])} if "max_requests" in f
                              else {})))
     return tg.from_pools(pools, "golden")
@@ -158,7 +159,7 @@ def check(fixtures, trace, outcomes, pool_tel, claim_tel):
                 got = dict(decision=packed & 15, state=(packed >> 4) & 15, hard=(packed >> 8) & 1,
                            prio=(packed >> 9) & 3, eff=(packed >> 11) & 3,
                            demotable=(packed >> 13) & 1, best_effort=(packed >> 14) & 1,
-                           relaxed=(packed >> 15) & 1)
+                           relaxed=(packed >> 15) & 1, offloadable=(packed >> 16) & 1)
                 for k, idx in CLAIM_FIELDS.items():
                     got[k] = int(w[idx])
                 for k, v in kv.items():

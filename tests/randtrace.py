@@ -6,7 +6,7 @@ import numpy as np
 
 def random_pool(rng: np.random.Generator, U: int, mode: int, n_events: int, n_chains: int = 3,
                 p_malformed: float = 0.03, tight_tables: bool = False, defer_limit: int = 0,
-                p_retry: float = 0.15, relax: bool = False) -> dict:
+                p_retry: float = 0.15, relax: bool = False, offload: bool = False) -> dict:
     """One pool of arbitrary events, including malformed ones and table overflows.  With
     defer_limit > 0 the pool defers blocked prefills and a share p_retry of its events are RETRY
     (pools without deferral draw exactly the random numbers they always did).  With relax, claims
@@ -34,12 +34,14 @@ def random_pool(rng: np.random.Generator, U: int, mode: int, n_events: int, n_ch
             c = int(rng.integers(0, n_chains))
             T = int(rng.integers(0, L + 1))
             dur = 0 if rng.random() < 0.5 else int(rng.integers(1, 8))
-            dem = be = 0
+            dem = be = off = 0
             if relax:
                 dem = int(rng.random() < 0.6)
                 be = int(rng.random() < 0.12)
+            if offload:
+                off = int(rng.random() < 0.6)
             e = tg.claim(L, c, T, hard=int(rng.integers(0, 2)), prio=int(rng.integers(0, 4)),
-                         dur=dur, demotable=dem, best_effort=be)
+                         dur=dur, demotable=dem, best_effort=be, offloadable=off)
         elif r < 0.76:
             e = tg.finish(sel)
         elif r < 0.85:
@@ -75,13 +77,14 @@ def random_pool(rng: np.random.Generator, U: int, mode: int, n_events: int, n_ch
 
 def random_batch(seed: int, n_pools: int, U_range=(2, 9), n_events=(1, 14), n_chains=3,
                  tight_every: int = 5, p_malformed: float = 0.03, caps=None, defer=False,
-                 hard_share: float = 0.0, relax=False):
+                 hard_share: float = 0.0, relax=False, offload=False):
     """caps = (live requests, live claims): table capacities of the pools that are not tight
     (default: one entry per PREFILL / CLAIM event, which never overflows).  defer: every pool
     defers, with a defer limit of 1..3.  hard_share: that share of the pools use hard protection
     (the only policy under which a refusal is attributed to claims), the rest cycle the policies.
     relax: every pool relaxes (mode flag) and claims are demotable / best-effort at random; with
-    defer also set, pools both relax and defer."""
+    defer also set, pools both relax and defer.  offload: claims are offloadable at random and each
+    pool gets a second tier of 0..U blocks."""
     from paper_2605_24259_amd import tracegen as tg
     rng = np.random.default_rng(seed)
     pools = []
@@ -97,9 +100,11 @@ def random_batch(seed: int, n_pools: int, U_range=(2, 9), n_events=(1, 14), n_ch
             if rng.random() < hard_share:
                 mode = 3
         pool = random_pool(rng, U, mode, ne, n_chains=n_chains, p_malformed=p_malformed,
-                           tight_tables=tight, defer_limit=dl, relax=relax)
+                           tight_tables=tight, defer_limit=dl, relax=relax, offload=offload)
         if relax:
             pool["mode"] = mode | tg.MODE_RELAX
+        if offload:
+            pool["offload_blocks"] = int(rng.integers(0, U + 1))
         if caps is not None and not tight:
             pool["max_live_requests"], pool["max_live_claims"] = caps
         pools.append(pool)

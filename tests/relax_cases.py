@@ -172,5 +172,151 @@ expect:
 """
 
 
+# Offload to a second tier (§3.1 offloadable: the content may leave GPU memory only if the
+# predicate stays restorable; §3.5 "offload resident": the resident survives and the active side is
+# served, subject to restore cost).  Pools with a second tier of `offload` blocks offload a blocking
+# claim that allows it when its footprint fits the free room; its predicate then never fails, its
+# GPU blocks are ordinary cache (victims it covers are not resident loss), and a later prefill that
+# reaches past its leading GPU hits into the claim's footprint counts those positions as restored.
+OFFLOAD_CASES = """
+# The 60/70/80 probe with an offloadable claim and a 60-block second tier: the claim is offloaded,
+# 50 of its GPU blocks are taken without loss (unclaimed victims), no predicate failure, no harm.
+[pool probe_offloaded]
+usable = 80
+mode = hard
+relax = 1
+offload = 60
+chains = 2
+events:
+  claim L=60 c=0 T=60 hard=1 prio=3 offloadable=1
+  prefill S=70 c=1 P=0
+expect:
+  t1 code=relaxed id=1 a=0 b=0 n16=1 flags=evict_unclaimed
+  tel n_relaxed=1 off_claims=1 off_blocks=60 t2_peak=60 runtime_demoted=0 resident=0 victims=50
+  tel pred_fail=0 harm=0 cached=10 protected=0
+  claim0 state=materialized eff=3 relaxed=1 offloadable=1 pred_fail=-1 harm=-1 lead_end=10
+
+# Too little room (50 < 60): an offloadable-only claim cannot be relaxed, the refusal stands; a
+# claim that also allows demotion is demoted instead.
+[pool no_room]
+usable = 80
+mode = hard
+relax = 1
+offload = 50
+chains = 3
+events:
+  claim L=60 c=0 T=60 hard=1 prio=3 offloadable=1
+  prefill S=70 c=1 P=0
+expect:
+  t1 code=refused_claim id=0 a=60 b=70 n16=1
+  tel off_claims=0 t2_peak=0
+  claim0 state=materialized eff=2 relaxed=0 blocked=1
+
+[pool no_room_demoted]
+usable = 80
+mode = hard
+relax = 1
+offload = 50
+chains = 3
+events:
+  claim L=60 c=0 T=60 hard=1 prio=3 offloadable=1 demotable=1
+  prefill S=70 c=1 P=0
+expect:
+  t1 code=relaxed id=1 a=50 n16=1 flags=pred_fail|post_release_loss
+  tel off_claims=0 runtime_demoted=1
+  claim0 state=demoted eff=2 relaxed=1 demote=1 pred_fail=1 harm=-1
+
+# Restore: after the offload, the request finishes and a prefill of 40 on the claim's chain hits the
+# 10 GPU-resident positions and restores 30 from the second tier (it still takes 30 GPU blocks, the
+# oldest cached ones of the finished request's private run).
+[pool restore]
+usable = 80
+mode = hard
+relax = 1
+offload = 60
+chains = 2
+events:
+  claim L=60 c=0 T=60 hard=1 prio=3 offloadable=1
+  prefill S=70 c=1 P=0
+  finish sel=0
+  prefill S=40 c=0 P=40
+expect:
+  t3 code=admit id=3 a=0 b=10 flags=evict_unclaimed
+  tel restored=30 off_claims=1 live_requests=1
+  claim0 state=materialized eff=3 lead_end=40
+
+# DEMOTE never selects an offloaded claim; RELEASE drops its copy, so the next offload fits.
+[pool release_frees_room]
+usable = 100
+mode = hard
+relax = 1
+offload = 60
+chains = 3
+events:
+  claim L=60 c=0 T=60 hard=1 offloadable=1
+  prefill S=90 c=2 P=0
+  demote sel=0
+  finish sel=0
+  release sel=0
+  claim L=60 c=1 T=60 hard=1 offloadable=1
+  prefill S=90 c=2 P=0
+expect:
+  t1 code=relaxed id=1 n16=1
+  t2 code=noop
+  t6 code=relaxed id=6 n16=1
+  tel off_claims=2 off_blocks=120 t2_peak=60
+  claim0 state=released eff=3
+  claim1 state=materialized eff=3
+
+# Expiry ends the runtime's responsibility: the copy is dropped and the claim, now expired, loses
+# its protection class (effective protection none).  Its predicate held only through the copy: the
+# chain keeps 10 < T = 60 leading blocks, so it fails at the expiry step, without harm (the claim is
+# expired).  The next prefill of 75 takes the chain's 10 GPU blocks first (last used at step 0,
+# before the finished run's step 4): resident, post-release loss.
+[pool expiry_drops_copy]
+usable = 80
+mode = hard
+relax = 1
+offload = 60
+chains = 3
+events:
+  claim L=60 c=0 T=60 hard=1 offloadable=1 dur=3
+  prefill S=70 c=1 P=0
+  nop
+  nop
+  finish sel=0
+  prefill S=75 c=2 P=0
+expect:
+  t1 code=relaxed id=1 n16=1
+  t3 code=noop n16=1 flags=expired|pred_fail
+  t5 code=evict_resident id=5 a=10 flags=post_release_loss|evict_unclaimed
+  tel expired=1 off_claims=1 t2_peak=60 harm=0 pred_fail=1
+  claim0 state=expired eff=0 expire=3 pred_fail=3 harm=-1
+
+# The same with T = 10: the 10 leading blocks left on the GPU still satisfy the predicate when the
+# copy is dropped, so nothing fails.
+[pool expiry_keeps_predicate]
+usable = 80
+mode = hard
+relax = 1
+offload = 60
+chains = 3
+events:
+  claim L=60 c=0 T=10 hard=1 offloadable=1 dur=3
+  prefill S=70 c=1 P=0
+  nop
+  nop
+expect:
+  t1 code=relaxed id=1 n16=1
+  t3 code=noop n16=1 flags=expired
+  tel expired=1 off_claims=1 pred_fail=0 harm=0
+  claim0 state=expired eff=0 expire=3 pred_fail=-1 lead_end=10
+"""
+
+
 def fixtures():
     return gf.parse_text(RELAX_CASES, "relaxation closed forms")
+
+
+def offload_fixtures():
+    return gf.parse_text(OFFLOAD_CASES, "offload closed forms")

@@ -333,19 +333,21 @@ def test_random_deferral_medium(oracle_mod, kernel):
     assert gpu[1][:, 33].sum() > 50
 
 
+@pytest.mark.parametrize("offload", [False, True])
 @pytest.mark.parametrize("variant", ["wide", "wide_global_lists"])
-def test_deferral_storage_layouts(oracle_mod, tg, variant):
-    """Deferral and runtime relaxation with 32-bit LDS state and with the live lists in global
-    scratch."""
+def test_deferral_storage_layouts(oracle_mod, tg, variant, offload):
+    """Deferral and runtime relaxation (with and without a second tier) with 32-bit LDS state and
+    with the live lists in global scratch."""
     import paper_2605_24259_amd as rkc
     trace = randtrace.random_batch(71, 600, U_range=(2, 200), n_events=(1, 200), n_chains=7,
-                                   tight_every=9, defer=True, relax=True, hard_share=0.8)
+                                   tight_every=9, defer=True, relax=True, hard_share=0.8,
+                                   offload=offload)
     lim = dict(trace.limits())
     lim["max_usable_blocks"] = 40000
     if variant == "wide_global_lists":
         lim["max_live_requests"] = 20000
         lim["max_live_claims"] = 4096
-    say(f"case deferral layouts/{variant}")
+    say(f"case deferral layouts/{variant} offload={offload}")
     gpu = rkc.DeviceBatch(trace.desc, trace.events, trace.n_claim_slots, lim).replay().results()
     ora = oracle_mod.replay(trace.desc, trace.events, trace.n_claim_slots, threads=ORACLE_THREADS)
     compare_pools(trace, gpu, ora)
@@ -400,6 +402,45 @@ def test_random_relaxation_medium(oracle_mod, kernel):
     gpu, ora = _both_kernel(oracle_mod, trace, kernel)
     compare_pools(trace, gpu, ora)
     assert gpu[1][:, 37].sum() > 50
+
+
+# ---- offload to a second tier: both kernels --------------------------------------------------
+@pytest.mark.parametrize("kernel", KERNELS)
+def test_offload_fixtures(oracle_mod, tg, kernel):
+    """Hand-derived offload cases (offload before demotion, a footprint larger than the free room
+    falls back to demotion, restore accounting on a later prefill, expiry and release drop the
+    copy, offloaded claims never harmed, peak second-tier use) on both kernels."""
+    fx = relax_cases.offload_fixtures()
+    trace = gf.to_trace(tg, fx)
+    gpu, ora = _both_kernel(oracle_mod, trace, kernel)
+    errs = gf.check(fx, trace, *gpu)
+    assert not errs, "\n".join(errs)
+    compare_pools(trace, gpu, ora)
+
+
+@pytest.mark.parametrize("kernel", KERNELS)
+@pytest.mark.parametrize("seed,defer", [(401, False), (402, True)])
+def test_random_offload_tiny(oracle_mod, kernel, seed, defer):
+    """Relaxing pools of <= 12 blocks with a second tier of random capacity, offloadable and
+    demotable claims, with and without deferral."""
+    trace = randtrace.random_batch(seed, 3000, U_range=(1, 13), n_events=(0, 40), n_chains=3,
+                                   relax=True, offload=True, defer=defer, hard_share=0.8)
+    gpu, ora = _both_kernel(oracle_mod, trace, kernel)
+    compare_pools(trace, gpu, ora)
+    assert gpu[1][:, 38].sum() > 50
+
+
+@pytest.mark.parametrize("kernel", KERNELS)
+def test_random_offload_medium(oracle_mod, kernel):
+    """Offloading pools up to 300 blocks and 400 events, up to 64 live claims, deferral mixed in:
+    the offload order is a wave-wide minimum over many claim lanes and the room runs out."""
+    trace = randtrace.random_batch(411, 400, U_range=(8, 300), n_events=(1, 400), n_chains=9,
+                                   p_malformed=0.01, tight_every=7, caps=(256, 64), defer=True,
+                                   relax=True, offload=True, hard_share=0.8)
+    gpu, ora = _both_kernel(oracle_mod, trace, kernel)
+    compare_pools(trace, gpu, ora)
+    pt = gpu[1]
+    assert pt[:, 38].sum() > 50 and pt[:, 40].sum() > 0
 
 
 def test_zipf_relax_full_sampled(oracle_mod, tg):

@@ -234,3 +234,41 @@ def test_relaxation_accounting(oracle_mod):
         assert int(((packed >> 15) & 1).sum()) == int(ptel[i, 37])
         total += int(r.sum())
     assert total > 100
+
+
+@pytest.mark.parametrize("seed", [401, 402, 403])
+def test_bruteforce_random_offload(oracle_mod, seed):
+    """Oracle == brute-force model on relaxing pools with a second tier and offloadable claims
+    (§3.1 offloadable; §3.5 offload resident), with demotable claims and deferral mixed in."""
+    trace = randtrace.random_batch(seed, 500, U_range=(1, 9), n_events=(8, 30), n_chains=2,
+                                   relax=True, offload=True, defer=seed == 403, hard_share=0.8)
+    _brute_compare(oracle_mod, trace)
+    _, ptel, _ = _check_clean(oracle_mod, trace)
+    assert ptel[:, 38].sum() > 20 and ptel[:, 40].sum() > 0
+
+
+def test_offload_accounting(oracle_mod):
+    """On pools with a second tier: offloaded claims never fail their predicate while offloaded,
+    second-tier use never exceeds the capacity, and relaxation counts add up."""
+    trace = randtrace.random_batch(23, 400, U_range=(4, 60), n_events=(1, 120), n_chains=4,
+                                   relax=True, offload=True, hard_share=0.7, p_malformed=0.01)
+    out, ptel, ctel = _check_clean(oracle_mod, trace)
+    U2 = trace.field("offload_blocks")
+    assert (ptel[:, 41] <= U2).all()
+    so, ns = trace.field("claim_slot_offset"), trace.field("n_claim_slots")
+    eo, ne = trace.field("event_offset"), trace.field("n_events")
+    for i in range(trace.n_pools):
+        rec = ctel[so[i]: so[i] + ns[i]]
+        packed = rec[:, 1]
+        relaxed = int(((packed >> 15) & 1).sum())
+        assert relaxed == int(ptel[i, 37] + ptel[i, 38])
+        # claims still holding a copy at the end: offloadable, relaxed, never failed or harmed, and
+        # no more of them than were offloaded
+        held = ((packed >> 11) & 3) == 3
+        assert (((packed[held] >> 16) & 1) == 1).all() and (((packed[held] >> 15) & 1) == 1).all()
+        assert (rec[held, 6] == -1).all() and (rec[held, 7] == -1).all()
+        assert int(held.sum()) <= int(ptel[i, 38])
+        o = out[eo[i]: eo[i] + ne[i]]
+        r = (o[:, 0] & 255) == 11
+        assert int((o[r, 0].view(np.uint32) >> 16).sum()) == relaxed
+    assert ptel[:, 38].sum() > 50

@@ -146,3 +146,13 @@ def test_relaxation_closed_forms(oracle_mod, tg):
     assert not chk.any(), [oracle_mod.check_names(int(c)) for c in chk]
     errs = gf.check(fx, trace, out, ptel, ctel)
     assert not errs, "\n".join(errs)
+
+
+def test_offload_closed_forms(oracle_mod, tg):
+    """Hand-derived second-tier offload and restore cases (tests/relax_cases.py)."""
+    fx = relax_cases.offload_fixtures()
+    trace = gf.to_trace(tg, fx)
+    out, ptel, ctel, chk = oracle_mod.replay(trace.desc, trace.events, trace.n_claim_slots)
+    assert not chk.any(), [oracle_mod.check_names(int(c)) for c in chk]
+    errs = gf.check(fx, trace, out, ptel, ctel)
+    assert not errs, "\n".join(errs)
