@@ -125,7 +125,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--workload", default="zipf", choices=["small", "zipf", "nested", "huge", "sweep", "zipf_defer", "zipf_relax"])
+    ap.add_argument("--workload", default="zipf", choices=["small", "zipf", "nested", "huge", "sweep", "zipf_defer", "zipf_relax", "zipf_offload"])
     ap.add_argument("--mode", default="replay", choices=["replay", "copy"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-parity", action="store_true")

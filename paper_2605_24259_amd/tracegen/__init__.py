@@ -66,6 +66,8 @@ class GenParams(ctypes.Structure):
         ("defer_limit", ctypes.c_int32),
         ("mode", ctypes.c_int32),
         ("demotable_permille", ctypes.c_int32),
+        ("offloadable_permille", ctypes.c_int32),
+        ("offload_blocks", ctypes.c_int32),
         ("zipf_s", ctypes.c_double),
         ("seed0", ctypes.c_uint64),
     ]
@@ -120,6 +122,17 @@ CONFIGS = {
                        claim_thresh=0, hard_permille=500, prio_max=3, dur_min=64, dur_max=512,
                        extend_k=1, claim_cap=0, max_live_claims=64, max_live_requests=256,
                        mode=3 | MODE_RELAX, demotable_permille=500),
+    # The same pools with a second tier of 1,024 blocks (half the GPU pool): half of the claims
+    # allow offload and a quarter allow demotion; a blocking claim is offloaded when it allows it
+    # and fits the tier's free room, else demoted when it allows it.
+    "zipf_offload": dict(cfg_id=8, n_pools=65536, usable_blocks=2048, n_events=1024,
+                         mix=(400, 300, 150, 100, 50, 0), prefill_dist=1, prefill_min=4,
+                         prefill_max=1536, chain_pick=1, n_chains=256, chain_len_min=32,
+                         chain_len_max=512, claim_len=0, claim_len_min=0, claim_len_max=0,
+                         claim_thresh=0, hard_permille=500, prio_max=3, dur_min=64, dur_max=512,
+                         extend_k=1, claim_cap=0, max_live_claims=64, max_live_requests=256,
+                         mode=3 | MODE_RELAX, demotable_permille=250, offloadable_permille=500,
+                         offload_blocks=1024),
 }
 
 

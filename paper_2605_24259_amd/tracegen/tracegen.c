@@ -84,6 +84,9 @@ typedef struct {
   int32_t defer_limit;     /* the pools' defer limit (0 = no deferral)                           */
   int32_t mode;            /* < 0: policy = pool index mod 4; else this mode for every pool       */
   int32_t demotable_permille; /* > 0: share of CLAIM events marked demotable (extra draw only then) */
+  int32_t offloadable_permille; /* > 0: share of CLAIM events marked offloadable (extra draw only
+                                   then)                                                         */
+  int32_t offload_blocks;  /* the pools' second-tier capacity in blocks (0 = none)              */
   double zipf_s;
   uint64_t seed0;
 } gen_params;
@@ -166,8 +169,9 @@ int64_t rkc_tracegen(const gen_params* g, int64_t first_pool, int32_t n_pools, i
         int32_t prio = uniform_int(&r, 0, g->prio_max);
         int32_t dur = g->dur_max > 0 ? uniform_int(&r, g->dur_min, g->dur_max) : 0;
         int32_t dem = g->demotable_permille > 0 && uniform_int(&r, 0, 999) < g->demotable_permille;
+        int32_t off = g->offloadable_permille > 0 && uniform_int(&r, 0, 999) < g->offloadable_permille;
         e[0] = (int32_t)((uint32_t)EV_CLAIM | ((uint32_t)hard << 4) | ((uint32_t)prio << 5) |
-                         ((uint32_t)dem << 7) | ((uint32_t)dur << 16));
+                         ((uint32_t)dem << 7) | ((uint32_t)off << 9) | ((uint32_t)dur << 16));
         e[1] = L; e[2] = c; e[3] = T;
         n_claims++;
         outstanding++;
@@ -187,7 +191,8 @@ int64_t rkc_tracegen(const gen_params* g, int64_t first_pool, int32_t n_pools, i
     d[5] = g->max_live_requests > 0 ? g->max_live_requests : n_prefill;
     d[6] = n_claims;
     d[7] = g->defer_limit;
-    d[8] = d[9] = d[10] = d[11] = 0;
+    d[8] = g->offload_blocks;
+    d[9] = d[10] = d[11] = 0;
     d[12] = (int32_t)(uint32_t)(uint64_t)ev_off;
     d[13] = (int32_t)((uint64_t)ev_off >> 32);
     d[14] = (int32_t)(uint32_t)(uint64_t)slots;

@@ -116,7 +116,7 @@ def _properties(trace, gpu):
     assert (pt[:, :10].sum(1) + pt[:, 32] + pt[:, 36] == ne).all()
     assert (pt[:, 25] + pt[:, 26] + pt[:, 27] == U).all()
     assert (pt[:, 24] <= U).all() and (pt[:, 24] >= pt[:, 25]).all()
-    assert (pt[:, 38:] == 0).all()
+    assert (pt[:, 42:] == 0).all()
     code = out[:, 0] & 255
     ref = (code == 2) | (code == 3) | (code == 10)
     Ue = np.repeat(U, ne)
@@ -452,6 +452,20 @@ def test_zipf_relax_full_sampled(oracle_mod, tg):
     compare_pools(trace, gpu, ora, pools=pools)
     _properties(trace, gpu)
     assert gpu[1][:, 36].sum() > trace.n_pools
+
+
+def test_zipf_offload_full_sampled(oracle_mod, tg):
+    """65,536 relaxing hard-protection pools x 2,048 blocks x 1,024 events with a 1,024-block second
+    tier, half the claims offloadable and a quarter demotable, in the benchmark's launch
+    configuration; sampled pools against the oracle."""
+    trace = tg.generate("zipf_offload")
+    pools = _sample(trace.n_pools, 96)
+    gpu, ora = _both(oracle_mod, trace, pools=pools)
+    compare_pools(trace, gpu, ora, pools=pools)
+    _properties(trace, gpu)
+    pt = gpu[1]
+    assert pt[:, 38].sum() > trace.n_pools and pt[:, 40].sum() > 0
+    assert (pt[:, 41] <= 1024).all()
 
 
 def test_compact_kernel_at_its_limits(oracle_mod, tg):
