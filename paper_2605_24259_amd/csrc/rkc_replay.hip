@@ -91,7 +91,7 @@ enum : u32 { DEC_ACCEPTED = 1, DEC_APPROX = 2, DEC_SHADOW = 3, DEC_REJECTED = 4 
 enum : u32 { CF_N = 0, CF_HOLD = 1, CF_PROT = 2, CF_BT = 3,          // group 0
              CF_NX = 4, CF_COVA = 5, CF_COVS = 6, CF_TPEND = 7,      // group 1
              CF_LV = 8,                                              // group 2: lv[0..3]
-             CF_STOP = 12, CF_SBOT = 13,                             // group 3
+             CF_STOP = 12, CF_SBOT = 13, CF_HCNT = 14,               // group 3
              CF_WORDS = 16 };
 
 // live-claim list arrays (struct of arrays, capacity cl_cap each)
@@ -641,38 +641,66 @@ struct Pool {
                  (i32)ufl(cla(CL_BLK)[i]));
   }
 
-  // Remove entry i of a struct-of-arrays list (narr arrays of capacity cap) by shifting the tail
-  // down one place; lanes read their source entries before any lane writes.
-  __device__ __forceinline__ void list_remove(lword* base0, u32 cap, u32 narr, u32 len, u32 i) {
-    for (u32 base = i; base + 1 < len; base += 64) {
-      const u32 j = base + lane;
-      const bool act = j + 1 < len;
-      for (u32 k = 0; k < narr; k++) {
-        lword* a = base0 + k * cap;
-        const u32 v = act ? (u32)a[j + 1] : 0u;
-        __builtin_amdgcn_wave_barrier();
-        if (act) a[j] = v;
-        __builtin_amdgcn_wave_barrier();
+  // Remove entry i of a struct-of-arrays list (NARR arrays of capacity cap) by shifting the tail
+  // down one place.  Each round loads KU chunks of 64 entries of every array before it stores any,
+  // so KU * NARR loads are in flight together (the lists of large pools live in global scratch,
+  // where one dependent round trip per chunk and array would dominate).  A round's stores land
+  // below the entries its later chunks and the next rounds read, and every load a store could
+  // overwrite has completed before that store issues.
+  template <u32 NARR, u32 KU>
+  __device__ __forceinline__ void list_remove(lword* base0, u32 cap, u32 len, u32 i) {
+    for (u32 base = i; base + 1 < len; base += 64 * KU) {
+      u32 v[KU][NARR];
+#pragma unroll
+      for (u32 u = 0; u < KU; u++) {
+        const u32 j = base + 64 * u + lane;
+#pragma unroll
+        for (u32 k = 0; k < NARR; k++) v[u][k] = j + 1 < len ? (u32)base0[k * cap + j + 1] : 0u;
       }
+      __builtin_amdgcn_wave_barrier();
+#pragma unroll
+      for (u32 u = 0; u < KU; u++) {
+        const u32 j = base + 64 * u + lane;
+        if (j + 1 < len) {
+#pragma unroll
+          for (u32 k = 0; k < NARR; k++) base0[k * cap + j] = (lword)v[u][k];
+        }
+      }
+      __builtin_amdgcn_wave_barrier();
     }
     lists_fence();
   }
 
   // Open a gap at entry i of a struct-of-arrays list of len entries (len < cap) by shifting
-  // [i, len) up one place, highest chunk first; lanes read their entries before any lane writes.
-  __device__ __forceinline__ void list_open(lword* base0, u32 cap, u32 narr, u32 len, u32 i) {
+  // [i, len) up one place, highest chunks first, KU chunks of every array loaded per round before
+  // any store (the mirror image of list_remove).
+  template <u32 NARR, u32 KU>
+  __device__ __forceinline__ void list_open(lword* base0, u32 cap, u32 len, u32 i) {
     for (u32 top = len; top > i;) {
-      const u32 base = top - i > 64 ? top - 64 : i;
-      const u32 j = base + lane;
-      const bool act = j < top;
-      for (u32 k = 0; k < narr; k++) {
-        lword* a = base0 + k * cap;
-        const u32 v = act ? (u32)a[j] : 0u;
-        __builtin_amdgcn_wave_barrier();
-        if (act) a[j + 1] = v;
-        __builtin_amdgcn_wave_barrier();
+      u32 v[KU][NARR];
+      u32 lo = top;
+#pragma unroll
+      for (u32 u = 0; u < KU; u++) {
+        const u32 hi = lo;
+        lo = hi > i + 64 ? hi - 64 : i;
+        const u32 j = lo + lane;
+#pragma unroll
+        for (u32 k = 0; k < NARR; k++) v[u][k] = j < hi ? (u32)base0[k * cap + j] : 0u;
       }
-      top = base;
+      __builtin_amdgcn_wave_barrier();
+      u32 lo2 = top;
+#pragma unroll
+      for (u32 u = 0; u < KU; u++) {
+        const u32 hi = lo2;
+        lo2 = hi > i + 64 ? hi - 64 : i;
+        const u32 j = lo2 + lane;
+        if (j < hi) {
+#pragma unroll
+          for (u32 k = 0; k < NARR; k++) base0[k * cap + j + 1] = (lword)v[u][k];
+        }
+      }
+      __builtin_amdgcn_wave_barrier();
+      top = lo;
     }
     lists_fence();
   }
@@ -968,6 +996,9 @@ struct Pool {
           th = max(g0.y, R);
           tpr = g0.z;
           tx = R;
+          // the chain's hold is the largest R of its live requests; CF_HCNT counts the requests
+          // holding exactly that much, so a finish rarely has to look for the next largest
+          if (R > 0 && R >= g0.y) cs((u32)hc, CF_HCNT, R > g0.y ? 1u : cf((u32)hc, CF_HCNT) + 1u);
         }
         // the live list stays in id order: a retried request goes before the later ids
         u32 k = nreq;
@@ -975,7 +1006,7 @@ struct Pool {
           u32 below = 0;
           for (u32 j = lane; j < nreq; j += 64) below += (u32)((u32)rqa(RQ_ID)[j] < rid);
           k = wave_sum(below);
-          list_open(rq, rq_cap, RQ_ARRAYS, nreq, k);
+          list_open<RQ_ARRAYS, kGL ? 8 : 1>(rq, rq_cap, nreq, k);
           dq_head = dq_head + 1 == (u32)max_reqs ? 0u : dq_head + 1;
           dq_len--;
           dq_cnt = 1;
@@ -1055,16 +1086,44 @@ struct Pool {
         const u32 i = (u32)w1 % nreq;
         const u32 rid = ufl(rqa(RQ_ID)[i]), c = lnil(ufl(rqa(RQ_C)[i])), R = ufl(rqa(RQ_R)[i]);
         const u32 len = ufl(rqa(RQ_LEN)[i]);
-        list_remove(rq, rq_cap, RQ_ARRAYS, nreq, i);
+        list_remove<RQ_ARRAYS, kGL ? 8 : 1>(rq, rq_cap, nreq, i);
         nreq--;
         i32 turned = 0;
         if (c != NIL) {
-          u32 hn = 0;
-          for (u32 j = lane; j < nreq; j += 64)
-            if ((u32)rqa(RQ_C)[j] == c) hn = max(hn, (u32)rqa(RQ_R)[j]);
-          hn = wave_max(hn);
-          turned += max(0, (i32)R - (i32)hn);
+          // the new hold of the chain is the largest R of the requests still on it: unchanged
+          // unless this request was the only one holding the current hold
           const uint4 g0 = cg(c, 0);
+          u32 hn = g0.y;
+          if (R > 0 && R == g0.y) {
+            const u32 hk = cf(c, CF_HCNT);
+            if (hk > 1) {
+              cs(c, CF_HCNT, hk - 1);
+            } else {
+              // scan the live list (in global scratch: 8 chunks per round, their loads in flight
+              // together) for the largest R on the chain and how many requests hold it
+              constexpr u32 KU = kGL ? 8 : 1;
+              u32 m = 0, k = 0;
+              for (u32 base = 0; base < nreq; base += 64 * KU) {
+                u32 cc[KU], rr[KU];
+#pragma unroll
+                for (u32 u = 0; u < KU; u++) {
+                  const u32 j = base + 64 * u + lane;
+                  cc[u] = j < nreq ? (u32)rqa(RQ_C)[j] : kListNil;
+                  rr[u] = j < nreq ? (u32)rqa(RQ_R)[j] : 0u;
+                }
+#pragma unroll
+                for (u32 u = 0; u < KU; u++) {
+                  if (cc[u] == c && rr[u] >= m) {
+                    k = rr[u] > m ? 1u : k + 1u;
+                    m = rr[u];
+                  }
+                }
+              }
+              hn = wave_max(m);
+              cs(c, CF_HCNT, wave_sum(m == hn ? k : 0u));
+            }
+          }
+          turned += max(0, (i32)R - (i32)hn);
           tc = c; tn = g0.x; th = hn; tpr = g0.z; tx = R;
         }
         // write no-admit drops the request's own blocks; otherwise they become a private run
@@ -1124,7 +1183,7 @@ struct Pool {
             write_live_record(i, ST_RELEASED, (i32)t);
             if (m_eff(ufl(cla(CL_META)[i])) == RKC_PROT_OFFLOADED) t2used -= L;  // the copy is dropped
             __builtin_amdgcn_wave_barrier();
-            list_remove(cl, cl_cap, CL_ARRAYS, ncl, i);
+            list_remove<CL_ARRAYS, kGL ? 4 : 1>(cl, cl_cap, ncl, i);
             ncl--;
             code = RKC_OC_RELEASED;
             tadd(TW_RELEASED, 1);
