@@ -222,9 +222,12 @@ struct Pool {
   lds_w* ch;          // chain records, CF_WORDS words each
   lds_u32* mk;        // per-chain mark bits
   lds_u32* tk;        // top keys of chains >= kRegChains
-  lword* rq;          // live requests, RQ_ARRAYS arrays of rq_cap
+  lword* rq;          // live requests, RQ_ARRAYS arrays of rq_cap (stride)
   lword* cl;          // live claims, CL_ARRAYS arrays of cl_cap
   u32 rq_cap, cl_cap;
+  // Lists in global scratch: entry 0 of the live-request list sits at rq_head, with twice the
+  // table's capacity allocated, so a finish can close its gap from whichever side is shorter.
+  u32 rq_head;
   lds_w4* node_lds;   // nodes [0, nl)
   glb_uint4* node_glb;  // nodes [nl, node_cap), 32-bit words
   u32 nl, node_cap;
@@ -268,7 +271,7 @@ struct Pool {
 
   // -- lists --
   __device__ __forceinline__ lword* cla(u32 k) { return cl + k * cl_cap; }
-  __device__ __forceinline__ lword* rqa(u32 k) { return rq + k * rq_cap; }
+  __device__ __forceinline__ lword* rqa(u32 k) { return rq + k * rq_cap + (kGL ? rq_head : 0u); }
   __device__ __forceinline__ static u32 lnil(u32 v) { return v == kListNil ? NIL : v; }
   __device__ __forceinline__ void lists_fence() {
     if (kGL) __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
@@ -705,6 +708,32 @@ struct Pool {
     lists_fence();
   }
 
+  // Move entries [d, d + len) of every array down to [0, len), KU chunks of every array loaded per
+  // round before any store (ascending rounds: a round stores below what later rounds read).
+  template <u32 NARR, u32 KU>
+  __device__ __forceinline__ void list_compact(lword* base0, u32 cap, u32 len, u32 d) {
+    for (u32 base = 0; base < len; base += 64 * KU) {
+      u32 v[KU][NARR];
+#pragma unroll
+      for (u32 u = 0; u < KU; u++) {
+        const u32 j = base + 64 * u + lane;
+#pragma unroll
+        for (u32 k = 0; k < NARR; k++) v[u][k] = j < len ? (u32)base0[k * cap + j + d] : 0u;
+      }
+      __builtin_amdgcn_wave_barrier();
+#pragma unroll
+      for (u32 u = 0; u < KU; u++) {
+        const u32 j = base + 64 * u + lane;
+        if (j < len) {
+#pragma unroll
+          for (u32 k = 0; k < NARR; k++) base0[k * cap + j] = (lword)v[u][k];
+        }
+      }
+      __builtin_amdgcn_wave_barrier();
+    }
+    lists_fence();
+  }
+
   __device__ __forceinline__ void expire(u32 t, u32& flags, u32& expired) {
     u32 cnt = 0, nx = EXP_NEVER, drop = 0, pf = 0;
     for (u32 i = lane; i < ncl; i += 64) {
@@ -1001,12 +1030,17 @@ struct Pool {
           if (R > 0 && R >= g0.y) cs((u32)hc, CF_HCNT, R > g0.y ? 1u : cf((u32)hc, CF_HCNT) + 1u);
         }
         // the live list stays in id order: a retried request goes before the later ids
+        if (kGL && rq_head + nreq >= rq_cap) {
+          // no room above the list: move it back to the start of its arrays
+          list_compact<RQ_ARRAYS, 8>(rq, rq_cap, nreq, rq_head);
+          rq_head = 0;
+        }
         u32 k = nreq;
         if (retry) {
           u32 below = 0;
           for (u32 j = lane; j < nreq; j += 64) below += (u32)((u32)rqa(RQ_ID)[j] < rid);
           k = wave_sum(below);
-          list_open<RQ_ARRAYS, kGL ? 8 : 1>(rq, rq_cap, nreq, k);
+          list_open<RQ_ARRAYS, kGL ? 8 : 1>(rqa(0), rq_cap, nreq, k);
           dq_head = dq_head + 1 == (u32)max_reqs ? 0u : dq_head + 1;
           dq_len--;
           dq_cnt = 1;
@@ -1086,7 +1120,13 @@ struct Pool {
         const u32 i = (u32)w1 % nreq;
         const u32 rid = ufl(rqa(RQ_ID)[i]), c = lnil(ufl(rqa(RQ_C)[i])), R = ufl(rqa(RQ_R)[i]);
         const u32 len = ufl(rqa(RQ_LEN)[i]);
-        list_remove<RQ_ARRAYS, kGL ? 8 : 1>(rq, rq_cap, nreq, i);
+        if (kGL && 2 * i + 1 < nreq) {
+          // fewer entries below the gap than above it: move those up one place
+          list_open<RQ_ARRAYS, 8>(rqa(0), rq_cap, i, 0);
+          rq_head++;
+        } else {
+          list_remove<RQ_ARRAYS, kGL ? 8 : 1>(rqa(0), rq_cap, nreq, i);
+        }
         nreq--;
         i32 turned = 0;
         if (c != NIL) {
@@ -1285,7 +1325,8 @@ __global__ __launch_bounds__(64) void rkc_replay_wave(Args g) {
     P.rq = (lword*)(lds + L.off_rq / 4);
     P.cl = (lword*)(lds + L.off_cl / 4);
   }
-  P.rq_cap = L.reqs;
+  P.rq_cap = L.global_lists ? 2 * L.reqs : L.reqs;
+  P.rq_head = 0;
   P.cl_cap = L.claims;
   P.node_lds = (lds_w4*)(lds + L.off_node / 4);
   P.node_glb = (glb_uint4*)(scr + L.scr_off_node);
@@ -1411,7 +1452,7 @@ bool make_layout(const rkc_batch* b, Layout* L, bool narrow, bool global_lists) 
   s = align_up(s, 256);
   L->scr_off_dq = s; s += 16ull * L->reqs; s = align_up(s, 256);  // deferred requests (ring)
   if (global_lists) {
-    L->scr_off_rq = s; s += 4ull * RQ_ARRAYS * L->reqs; s = align_up(s, 256);
+    L->scr_off_rq = s; s += 4ull * RQ_ARRAYS * 2 * L->reqs; s = align_up(s, 256);  // two-sided
     L->scr_off_cl = s; s += 4ull * CL_ARRAYS * L->claims;
   }
   L->scr_pool_bytes = align_up(s, 256);

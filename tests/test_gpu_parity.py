@@ -239,13 +239,18 @@ def test_descriptor_outside_batch_limits(tg):
     assert db.query_telemetry(1, 0)[0] == -7
 
 
-@pytest.mark.parametrize("variant", ["narrow", "wide", "wide_global_lists"])
+@pytest.mark.parametrize("variant", ["narrow", "wide", "wide_global_lists",
+                                     "global_lists_small_request_table"])
 def test_storage_layouts_agree(oracle_mod, tg, variant):
     """The same pools replayed with 16-bit LDS state, 32-bit LDS state and 32-bit state with the
-    lists in global scratch (chosen by the batch's declared limits) match the oracle exactly."""
+    lists in global scratch (chosen by the batch's declared limits) match the oracle exactly.  The
+    last variant keeps the lists in global scratch with a live-request table of at most 6 entries,
+    so the request list's gap closing from both sides wraps back to the start of its arrays."""
     import paper_2605_24259_amd as rkc
     trace = randtrace.random_batch(41, 600, U_range=(2, 200), n_events=(1, 200), n_chains=7,
                                    tight_every=9)
+    if variant == "global_lists_small_request_table":
+        _small_request_tables(trace)
     lim = dict(trace.limits())
     if variant == "wide":
         lim["max_usable_blocks"] = 40000          # above the 16-bit bound
@@ -253,10 +258,18 @@ def test_storage_layouts_agree(oracle_mod, tg, variant):
         lim["max_usable_blocks"] = 40000
         lim["max_live_requests"] = 20000          # lists no longer fit in LDS
         lim["max_live_claims"] = 4096
+    else:
+        lim["max_usable_blocks"] = 40000
+        lim["max_live_claims"] = 8192             # the claim list no longer fits in LDS
     say(f"case layouts/{variant}")
     gpu = rkc.DeviceBatch(trace.desc, trace.events, trace.n_claim_slots, lim).replay().results()
     ora = oracle_mod.replay(trace.desc, trace.events, trace.n_claim_slots, threads=ORACLE_THREADS)
     compare_pools(trace, gpu, ora)
+
+
+def _small_request_tables(trace):
+    """Cap every pool's live-request table at 6 entries (descriptor field 5)."""
+    trace.desc[:, 5] = np.minimum(trace.desc[:, 5], 6)
 
 
 @pytest.mark.parametrize("case", ["small", "random"])
@@ -334,19 +347,24 @@ def test_random_deferral_medium(oracle_mod, kernel):
 
 
 @pytest.mark.parametrize("offload", [False, True])
-@pytest.mark.parametrize("variant", ["wide", "wide_global_lists"])
+@pytest.mark.parametrize("variant", ["wide", "wide_global_lists", "global_lists_small_request_table"])
 def test_deferral_storage_layouts(oracle_mod, tg, variant, offload):
     """Deferral and runtime relaxation (with and without a second tier) with 32-bit LDS state and
-    with the live lists in global scratch."""
+    with the live lists in global scratch (also with live-request tables of at most 6 entries:
+    retried requests enter a list that wraps back to the start of its arrays)."""
     import paper_2605_24259_amd as rkc
     trace = randtrace.random_batch(71, 600, U_range=(2, 200), n_events=(1, 200), n_chains=7,
                                    tight_every=9, defer=True, relax=True, hard_share=0.8,
                                    offload=offload)
+    if variant == "global_lists_small_request_table":
+        _small_request_tables(trace)
     lim = dict(trace.limits())
     lim["max_usable_blocks"] = 40000
     if variant == "wide_global_lists":
         lim["max_live_requests"] = 20000
         lim["max_live_claims"] = 4096
+    elif variant == "global_lists_small_request_table":
+        lim["max_live_claims"] = 8192
     say(f"case deferral layouts/{variant} offload={offload}")
     gpu = rkc.DeviceBatch(trace.desc, trace.events, trace.n_claim_slots, lim).replay().results()
     ora = oracle_mod.replay(trace.desc, trace.events, trace.n_claim_slots, threads=ORACLE_THREADS)
