@@ -111,12 +111,20 @@ def kernel_name(lim):
     return "rkc_lean" if fits else "rkc_replay_wave"
 
 
-def kernel_source_sha():
-    """SHA-256 over the HIP sources of both replay kernels (the counters describe one build)."""
+KERNEL_SOURCES = {
+    "rkc_lean": ("paper_2605_24259_amd/csrc/rkc_lean.hip", "paper_2605_24259_amd/csrc/rkc_lean.h",
+                 "include/rkc.h"),
+    "rkc_replay_wave": ("paper_2605_24259_amd/csrc/rkc_replay.hip", "include/rkc.h"),
+}
+
+
+def kernel_source_sha(kernel="rkc_lean"):
+    """SHA-256 over the sources that define one replay kernel and its launch (the counters
+    describe the build of those sources)."""
     import hashlib
     h = hashlib.sha256()
-    for f in ("rkc_replay.hip", "rkc_lean.hip"):
-        h.update(open(os.path.join(ROOT, "paper_2605_24259_amd", "csrc", f), "rb").read())
+    for f in KERNEL_SOURCES[kernel]:
+        h.update(open(os.path.join(ROOT, f), "rb").read())
     return h.hexdigest()
 
 
@@ -216,7 +224,8 @@ def main():
         "roofline": {
             "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBPS, 4),
-            "traffic": traffic_from_profiles(kernel_name(lim), args.workload, kernel_source_sha()),
+            "traffic": traffic_from_profiles(kernel_name(lim), args.workload,
+                                             kernel_source_sha(kernel_name(lim))),
             "credited_bytes_per_launch": cbytes,
             "copy_ceiling_gbps": round(ceiling, 1),
             "frac_of_copy_ceiling": round(achieved / ceiling, 4),
