@@ -1411,6 +1411,7 @@ u64 align_up(u64 v, u64 a) { return (v + a - 1) / a * a; }
 constexpr u32 kNodesLdsNarrow = 128, kNodesLdsWide = 64;
 
 constexpr u64 kLdsBudget = 160 * 1024;
+constexpr u32 kCUs = 256;  // compute units of one MI355X
 
 // 16-bit storage holds every stored value of the batch below 0xFFFF
 bool narrow_ok(const rkc_batch* b) {
@@ -1438,6 +1439,13 @@ bool make_layout(const rkc_batch* b, Layout* L, bool narrow, bool global_lists) 
   if (!global_lists) {
     L->off_rq = take(ws * RQ_ARRAYS * L->reqs, 16);
     L->off_cl = take(ws * CL_ARRAYS * L->claims, 16);
+  }
+  if (b->n_pools <= (i32)kCUs) {
+    // at most one pool per CU: the node pool takes the LDS the other regions leave
+    const u64 left = align_up(o, 16) < kLdsBudget ? kLdsBudget - align_up(o, 16) : 0;
+    const u64 fit = left / (4 * ws);
+    L->nodes_lds = (u32)(fit < L->node_cap ? fit : L->node_cap);
+    if (L->nodes_lds < nlds && L->nodes_lds < L->node_cap) L->nodes_lds = L->node_cap < nlds ? L->node_cap : nlds;
   }
   L->off_node = take(4 * ws * L->nodes_lds, 16);
   o = align_up(o, 16);
