@@ -490,7 +490,7 @@ def test_compact_kernel_at_its_limits(oracle_mod, tg):
     """One batch at the compact kernel's limits: 32,767-block pools, 256 chains, a pool of 65,533
     events (16-bit ids up to 65,532), live-claim and live-request tables filled to exactly 64 and
     256 and then overflowed, an empty pool, an all-malformed pool, and a deferring / relaxing pool
-    at full size.  Every outcome, pool word and claim record against the oracle."""
+    and an offloading one at full size.  Every outcome, pool word and claim record against the oracle."""
     import bench
     rng = np.random.default_rng(2026)
     big = randtrace.random_pool(rng, 32767, 3, 3000, n_chains=256, p_malformed=0.01)
@@ -501,13 +501,18 @@ def test_compact_kernel_at_its_limits(oracle_mod, tg):
                                 relax=True)
     ext["mode"] = 3 | tg.MODE_RELAX
     ext["max_live_requests"], ext["max_live_claims"] = 256, 64
+    off = randtrace.random_pool(rng, 32767, 3, 2000, n_chains=256, p_malformed=0.01, defer_limit=3,
+                                relax=True, offload=True)
+    off["mode"] = 3 | tg.MODE_RELAX
+    off["max_live_requests"], off["max_live_claims"], off["offload_blocks"] = 256, 64, 16000
     tables = dict(usable_blocks=400, mode=1, n_chains=256, max_live_claims=64, max_live_requests=256,
                   events=[tg.claim(1, c, 1) for c in range(65)] + [tg.prefill(1)] * 257
                   + [tg.release(0), tg.claim(2, 70, 2), tg.finish(3), tg.prefill(2, 200, 2)])
     pools = [big, long_pool, ext, tables,
              dict(usable_blocks=1, mode=2, n_chains=0, events=[]),
              dict(usable_blocks=32767, mode=3, n_chains=256,
-                  events=[tg.ev(11), tg.prefill(0), tg.claim(5, 256), tg.extend(-1), tg.ev(15)])]
+                  events=[tg.ev(11), tg.prefill(0), tg.claim(5, 256), tg.extend(-1), tg.ev(15)]),
+             off]
     trace = tg.from_pools(pools, "compact-limits")
     lim = trace.limits()
     assert lim["max_usable_blocks"] == 32767 and lim["max_events"] == 65533
@@ -519,3 +524,4 @@ def test_compact_kernel_at_its_limits(oracle_mod, tg):
     assert pt[3, 29] == 256 and pt[3, 30] == 64 and pt[3, 9] == 2
     assert pt[4, 27] == 1 and pt[4, :].sum() == 1  # the empty pool: one FREE block, nothing else
     assert (pt[5, 9] == 5) and (pt[5, :9] == 0).all()
+    assert pt[6, 38] > 0 and pt[6, 41] <= 16000
