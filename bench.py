@@ -90,16 +90,21 @@ def cpu_baseline(trace, seconds_budget=12.0):
                        f"{threads} threads, {wall:.1f} s wall")
 
 
-def traffic_from_profiles(kernel, workload, kernel_sha):
-    """HBM bytes per launch from the committed rocprofv3 counter summary of this kernel and
-    workload, if it was taken on the current kernel sources; else None."""
+def profile_record(kernel, workload, kernel_sha):
+    """The committed rocprofv3 counter summary of this kernel and workload (HBM bytes and scalar
+    instructions per launch), if it was taken on the current kernel sources; else {}."""
     path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_traffic.json")
     if not os.path.exists(path):
-        return None
+        return {}
     d = json.load(open(path))
     if d.get("kernel_source_sha256") != kernel_sha:
-        return None
-    return d.get("traffic_bytes_per_launch")
+        return {}
+    return d
+
+
+# Scalar issue ceiling: one scalar instruction per CU per cycle, 256 CUs at the 2.4 GHz peak
+# engine clock, in G instructions/s.
+SCALAR_ISSUE_PEAK = 256 * 2.4
 
 
 def kernel_name(lim):
@@ -200,6 +205,8 @@ def main():
     ceiling = copy_ceiling(torch)
     base = None if args.no_cpu_baseline else cpu_baseline(trace)
     lim = trace.limits()
+    prof = profile_record(kernel_name(lim), args.workload, kernel_source_sha(kernel_name(lim)))
+    salu = prof.get("sq_insts_salu_per_launch")
     line = {
         "metric": METRIC,
         "value": round(value, 1),
@@ -224,11 +231,15 @@ def main():
         "roofline": {
             "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBPS, 4),
-            "traffic": traffic_from_profiles(kernel_name(lim), args.workload,
-                                             kernel_source_sha(kernel_name(lim))),
+            "traffic": prof.get("traffic_bytes_per_launch"),
             "credited_bytes_per_launch": cbytes,
             "copy_ceiling_gbps": round(ceiling, 1),
             "frac_of_copy_ceiling": round(achieved / ceiling, 4),
+            # what actually bounds the replay: the scalar instructions the counters saw per launch
+            # over this launch time, against the scalar issue ceiling
+            "scalar_issue": None if salu is None else {
+                "achieved": round(salu / (ms_per_step * 1e-3) / 1e9, 1), "peak": SCALAR_ISSUE_PEAK,
+                "unit": "G scalar instr/s", "frac": round(salu / (ms_per_step * 1e-3) / 1e9 / SCALAR_ISSUE_PEAK, 4)},
         },
         "cpu_baseline": base,
         "parity": parity,
