@@ -472,6 +472,21 @@ def test_zipf_relax_full_sampled(oracle_mod, tg):
     assert gpu[1][:, 36].sum() > trace.n_pools
 
 
+@pytest.mark.parametrize("kernel", KERNELS)
+def test_random_all_features(oracle_mod, kernel):
+    """Every pool defers and carries the relaxation flag (ignored outside hard protection), claims
+    are demotable, best-effort and offloadable at random, half the pools are hard, the rest cycle
+    the policies; pools up to 400 blocks and 300 events, tight and overflowing tables, malformed
+    events.  Every word of both kernels against the oracle."""
+    trace = randtrace.random_batch(501, 2000, U_range=(1, 400), n_events=(0, 300), n_chains=12,
+                                   p_malformed=0.02, tight_every=6, caps=(256, 64), defer=True,
+                                   relax=True, offload=True, hard_share=0.5)
+    gpu, ora = _both_kernel(oracle_mod, trace, kernel)
+    compare_pools(trace, gpu, ora)
+    pt = gpu[1]
+    assert pt[:, 32].sum() > 100 and pt[:, 37].sum() > 100 and pt[:, 38].sum() > 100
+
+
 def test_zipf_offload_full_sampled(oracle_mod, tg):
     """65,536 relaxing hard-protection pools x 2,048 blocks x 1,024 events with a 1,024-block second
     tier, half the claims offloadable and a quarter demotable, in the benchmark's launch
