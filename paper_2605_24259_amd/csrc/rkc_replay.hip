@@ -95,8 +95,11 @@ enum : u32 { CF_N = 0, CF_HOLD = 1, CF_PROT = 2, CF_BT = 3,          // group 0
              CF_WORDS = 16 };
 
 // live-claim list arrays (struct of arrays, capacity cl_cap each)
-enum : u32 { CL_ID = 0, CL_C, CL_L, CL_T, CL_META, CL_EXP, CL_SLOT, CL_BLK, CL_DEM, CL_EXST, CL_PF,
-             CL_HARM, CL_ARRAYS };
+// (the demotion, expiry, predicate-failure and harm steps go straight into the claim's record in
+// the caller's telemetry buffer when they happen: they are never read on the event path)
+enum : u32 { CL_ID = 0, CL_C, CL_L, CL_T, CL_META, CL_EXP, CL_SLOT, CL_BLK, CL_ARRAYS };
+// words of a claim record written when the step happens
+enum : u32 { RW_DEM = 3, RW_EXST = 4, RW_PF = 6, RW_HARM = 7 };
 // live-request list arrays
 enum : u32 { RQ_ID = 0, RQ_C, RQ_R, RQ_LEN, RQ_ARRAYS };
 
@@ -572,11 +575,12 @@ struct Pool {
       if (ch[c * CF_WORDS + CF_N] >= cla(CL_T)[i]) continue;
       m &= ~(1u << 8);
       pf++;
-      cla(CL_PF)[i] = t;
+      rkc_claim_telemetry* r = rec + (u32)cla(CL_SLOT)[i];
+      r->w[RW_PF] = (i32)t;
       if (st == ST_MATERIALIZED) {
         m = m_with_state(m, ST_HARMED);
         hm++;
-        cla(CL_HARM)[i] = t;
+        r->w[RW_HARM] = (i32)t;
       }
       cla(CL_META)[i] = m;
     }
@@ -624,9 +628,10 @@ struct Pool {
     b = (i32)req;
   }
 
-  // Claim records: words 0..8 are written exactly once (lane k writes word k), when the claim is
-  // final (rejected at birth, released, or live at the end); word 9 (lead_end) is written by the
-  // final pass.
+  // Claim records: a rejected claim's words 0..8 are written at birth (lane k writes word k); a
+  // live claim's step words 3, 4, 6, 7 start at -1 at birth and take their step when it happens,
+  // and its words 0, 1, 2, 5, 8 are written once, when it is released or at the end; word 9
+  // (lead_end) is written by the final pass.
   __device__ __forceinline__ void write_record(u32 slot, i32 id, u32 packed, i32 accept, i32 dem,
                                                i32 exst, i32 rel, i32 pf, i32 harm, i32 blk) {
     if (lane < 9) {
@@ -635,14 +640,19 @@ struct Pool {
       rec[slot].w[lane] = v;
     }
   }
-  __device__ __forceinline__ static i32 step_or_none(u32 v) { return v == NIL ? -1 : (i32)v; }
-  __device__ __forceinline__ void write_live_record(u32 i, u32 state, i32 rel) {
-    const u32 id = ufl(cla(CL_ID)[i]);
-    write_record(ufl(cla(CL_SLOT)[i]), (i32)id, packed_of(m_with_state(ufl(cla(CL_META)[i]), state)),
-                 (i32)id, step_or_none(lnil(ufl(cla(CL_DEM)[i]))), step_or_none(lnil(ufl(cla(CL_EXST)[i]))),
-                 rel, step_or_none(lnil(ufl(cla(CL_PF)[i]))), step_or_none(lnil(ufl(cla(CL_HARM)[i]))),
-                 (i32)ufl(cla(CL_BLK)[i]));
+  __device__ __forceinline__ void write_birth_record(u32 slot) {
+    if (lane == RW_DEM || lane == RW_EXST || lane == RW_PF || lane == RW_HARM) rec[slot].w[lane] = -1;
   }
+  __device__ __forceinline__ void write_live_record(u32 i, u32 state, i32 rel) {
+    const u32 id = ufl(cla(CL_ID)[i]), slot = ufl(cla(CL_SLOT)[i]);
+    const u32 packed = packed_of(m_with_state(ufl(cla(CL_META)[i]), state)), blk = ufl(cla(CL_BLK)[i]);
+    if (lane == 0 || lane == 1 || lane == 2 || lane == 5 || lane == 8) {
+      const i32 v = lane == 0 || lane == 2 ? (i32)id : lane == 1 ? (i32)packed : lane == 5 ? rel : (i32)blk;
+      rec[slot].w[lane] = v;
+    }
+  }
+  // the step word w of live claim i's record (every lane, one value)
+  __device__ __forceinline__ void record_step(u32 i, u32 w, i32 v) { rec[ufl(cla(CL_SLOT)[i])].w[w] = v; }
 
   // Remove entry i of a struct-of-arrays list (NARR arrays of capacity cap) by shifting the tail
   // down one place.  Each round loads KU chunks of 64 entries of every array before it stores any,
@@ -751,12 +761,12 @@ struct Pool {
           // fails it now (no harm: the claim is expired)
           if (m_pending(m) && (u32)ch[(u32)cla(CL_C)[i] * CF_WORDS + CF_N] < (u32)cla(CL_T)[i]) {
             m2 &= ~(1u << 8);
-            cla(CL_PF)[i] = t;
+            rec[(u32)cla(CL_SLOT)[i]].w[RW_PF] = (i32)t;
             pf++;
           }
         }
         cla(CL_META)[i] = m_with_state(m2, ST_EXPIRED);
-        cla(CL_EXST)[i] = t;
+        rec[(u32)cla(CL_SLOT)[i]].w[RW_EXST] = (i32)t;
         mk[cla(CL_C)[i]] |= MK_RECOMP;
         cnt++;
       } else {
@@ -806,8 +816,8 @@ struct Pool {
   // first, then lowest id: each is offloaded when it allows it and its footprint fits the second
   // tier's free room, else demoted when it allows it, else left alone, until the allocation would
   // fit.  The picks change the claims tentatively (offload: effective protection OFFLOADED; demote:
-  // state DEMOTED), marked by a demotion step equal to t, which no other claim can carry at t; they
-  // are kept when the allocation fits and undone otherwise.  Returns the number of claims relaxed.
+  // state DEMOTED), marked by the demotion step t in the claim's record, which no other claim can
+  // carry at t; they are kept when the allocation fits and undone otherwise.  Returns the number of claims relaxed.
   __device__ __forceinline__ u32 relax(u32 t, i32 need, i32 hc, u32 h) {
     u32 k = 0;
     if (relax_on && need > F) {
@@ -838,7 +848,7 @@ struct Pool {
           const u32 before = hard_extent(c);
           // every lane, one value
           cla(CL_META)[i] = off ? m_with_eff(m, RKC_PROT_OFFLOADED) : m_with_state(m, ST_DEMOTED);
-          cla(CL_DEM)[i] = t;
+          record_step(i, RW_DEM, (i32)t);
           lists_fence();
           const u32 after = hard_extent(c);
           const uint4 g0 = cg(c, 0);
@@ -849,17 +859,19 @@ struct Pool {
         }
         const bool fits = (i64)need <= avail;
         if (k) {
+          __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");  // the marks reach the scan
           for (u32 i = lane; i < ncl; i += 64) {
-            if (lnil((u32)cla(CL_DEM)[i]) != t) continue;
+            i32* dem = &rec[(u32)cla(CL_SLOT)[i]].w[RW_DEM];
+            if (*dem != (i32)t) continue;
             const u32 m = cla(CL_META)[i];
             const bool off = m_eff(m) == RKC_PROT_OFFLOADED;
             if (fits) {
               cla(CL_META)[i] = m | M_RELAXED;
-              if (off) cla(CL_DEM)[i] = kListNil;  // an offloaded claim records no demotion
+              if (off) *dem = -1;  // an offloaded claim records no demotion
               mk[cla(CL_C)[i]] |= MK_RECOMP;
             } else {
               cla(CL_META)[i] = off ? m_with_eff(m, RKC_PROT_HARD) : m_with_state(m, ST_MATERIALIZED);
-              cla(CL_DEM)[i] = kListNil;
+              *dem = -1;
             }
           }
           lists_fence();
@@ -1095,8 +1107,7 @@ struct Pool {
           const u32 dur_eff = shadow ? 0u : dur;
           cla(CL_ID)[k] = t; cla(CL_C)[k] = c; cla(CL_L)[k] = (u32)L; cla(CL_T)[k] = (u32)T;
           cla(CL_META)[k] = m; cla(CL_EXP)[k] = dur_eff; cla(CL_SLOT)[k] = s; cla(CL_BLK)[k] = 0;
-          cla(CL_DEM)[k] = kListNil; cla(CL_EXST)[k] = kListNil; cla(CL_PF)[k] = kListNil;
-          cla(CL_HARM)[k] = kListNil;
+          write_birth_record(s);
           // a new live claim only raises the chain's maxima
           const uint4 g1 = cg(c, 1);
           cgs(c, 1, make_uint4(g1.x, max(g1.y, (u32)L), max(g1.z, (u32)L), max(g1.w, (u32)T)));
@@ -1229,7 +1240,7 @@ struct Pool {
             tadd(TW_RELEASED, 1);
           } else {
             cla(CL_META)[i] = m_with_state(ufl(cla(CL_META)[i]), ST_DEMOTED);
-            cla(CL_DEM)[i] = t;
+            record_step(i, RW_DEM, (i32)t);
             __builtin_amdgcn_wave_barrier();
             code = RKC_OC_DEMOTED;
             tadd(TW_DEMOTED, 1);
