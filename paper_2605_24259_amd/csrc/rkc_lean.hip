@@ -78,7 +78,12 @@ __device__ __forceinline__ u32 packed_of(u32 m) {
 
 __device__ __forceinline__ u32 lo16(u32 v) { return v & 0xFFFFu; }
 __device__ __forceinline__ u32 hi16(u32 v) { return v >> 16; }
-__device__ __forceinline__ u32 pk(u32 lo, u32 hi) { return (lo & 0xFFFFu) | (hi << 16); }
+// two 16-bit halves as one vector, so that uniform operands pack in one scalar instruction
+typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ u32 pk(u32 lo, u32 hi) {
+  const u16x2 v = {(unsigned short)lo, (unsigned short)hi};
+  return __builtin_bit_cast(u32, v);
+}
 __device__ __forceinline__ i32 st16(u32 v) { return v == NIL ? -1 : (i32)v; }  // step field
 
 // ---- wave primitives (all 64 lanes active) ----------------------------------------------------
