@@ -144,7 +144,7 @@ def main():
     ap.add_argument("--no-parity", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py: this build replays on one GPU only (pools are independent; a multi-GPU "
+        print("bench.py: the replay runs on one GPU only (pools are independent; a multi-GPU "
               "run would split the pool range across ranks, which is not implemented)", flush=True)
         sys.exit(2)
 
