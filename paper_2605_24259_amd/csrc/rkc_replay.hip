@@ -425,20 +425,22 @@ struct Pool {
   __device__ __forceinline__ u32 claim_maxima(u32 c) {
     u32 pr = 0, l1 = 0, l2 = 0, l3 = 0, l4 = 0, ca = 0, cso = 0, tp = 0;
     const bool hardm = mode == RKC_MODE_HARD, softl = soft_levels();
-    for (u32 i = lane; i < ncl; i += 64) {
-      if (cla(CL_C)[i] != c) continue;
-      const u32 m = cla(CL_META)[i], L = cla(CL_L)[i], st = m_state(m);
+    // uniform chunks, every lane reading a valid entry and selecting, so that no lane mask is
+    // saved and restored per condition
+    for (u32 base = 0; base < ncl; base += 64) {
+      const u32 i = base + lane, j = i < ncl ? i : base;
+      const u32 m = cla(CL_META)[j], L = cla(CL_L)[j], T = cla(CL_T)[j], st = m_state(m);
       // an offloaded claim's victims are not resident and its predicate never fails
-      if (m_eff(m) == RKC_PROT_OFFLOADED) continue;
-      ca = max(ca, L);
-      if (st == ST_OBSERVED || st == ST_MATERIALIZED || st == ST_HARMED) cso = max(cso, L);
-      if (hardm && st == ST_MATERIALIZED && m_eff(m) == RKC_PROT_HARD) pr = max(pr, L);
-      if (softl && ((st == ST_MATERIALIZED && m_eff(m) == RKC_PROT_SOFT) || st == ST_DEMOTED)) {
-        const u32 p = m_prio(m);
-        if (p == 0) l1 = max(l1, L); else if (p == 1) l2 = max(l2, L);
-        else if (p == 2) l3 = max(l3, L); else l4 = max(l4, L);
-      }
-      if (m_pending(m)) tp = max(tp, cla(CL_T)[i]);
+      const bool on = i < ncl && (u32)cla(CL_C)[j] == c && m_eff(m) != RKC_PROT_OFFLOADED;
+      const u32 x = on ? L : 0u;
+      ca = max(ca, x);
+      cso = max(cso, (st == ST_OBSERVED || st == ST_MATERIALIZED || st == ST_HARMED) ? x : 0u);
+      pr = max(pr, (hardm && st == ST_MATERIALIZED && m_eff(m) == RKC_PROT_HARD) ? x : 0u);
+      const u32 p = m_prio(m);
+      const u32 sx = (softl && ((st == ST_MATERIALIZED && m_eff(m) == RKC_PROT_SOFT) || st == ST_DEMOTED)) ? x : 0u;
+      l1 = max(l1, p == 0 ? sx : 0u); l2 = max(l2, p == 1 ? sx : 0u);
+      l3 = max(l3, p == 2 ? sx : 0u); l4 = max(l4, p == 3 ? sx : 0u);
+      tp = max(tp, on && m_pending(m) ? T : 0u);
     }
     pr = wave_max(pr); l1 = wave_max(l1); l2 = wave_max(l2); l3 = wave_max(l3); l4 = wave_max(l4);
     ca = wave_max(ca); cso = wave_max(cso); tp = wave_max(tp);
