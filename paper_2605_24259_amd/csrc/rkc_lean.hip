@@ -1208,6 +1208,12 @@ __global__ __launch_bounds__(1024) void rkc_lean_order_scatter(i32 n_pools, cons
   }
 }
 
+// Batch order (pools of a few events: grouping them by event loop does not pay for its passes).
+__global__ __launch_bounds__(1024) void rkc_lean_order_identity(i32 n_pools, u32* order) {
+  const i32 p = (i32)(blockIdx.x * kOrderTile + threadIdx.x);
+  if (p < n_pools) order[p] = (u32)p;
+}
+
 // One wavefront per pool, in the launch order above; the pool's policy selects its specialized
 // event loop once.
 template <int NS>
@@ -1296,11 +1302,17 @@ rkc_status launch_ns(const rkc_lean_args* g, hipStream_t s) {
     return RKC_E_HIP;
   unsigned char* scr = (unsigned char*)g->scratch;
   const unsigned tiles = (unsigned)(((u64)g->n_pools + kOrderTile - 1) / kOrderTile);
-  hipLaunchKernelGGL(rkc_lean_order_count, dim3(tiles), dim3(kOrderTile), 0, s, g->pools, (i32)g->n_pools,
-                     scr + g->scr_off_cls, (u32*)(scr + g->scr_off_tiles));
-  hipLaunchKernelGGL(rkc_lean_order_scatter, dim3(tiles), dim3(kOrderTile), 0, s, (i32)g->n_pools,
-                     (const unsigned char*)(scr + g->scr_off_cls), (const u32*)(scr + g->scr_off_tiles),
-                     (u32*)(scr + g->scr_off_order));
+  if (g->max_events >= 64) {
+    // long event loops: group the pools by loop so that a CU's resident pools share one loop
+    hipLaunchKernelGGL(rkc_lean_order_count, dim3(tiles), dim3(kOrderTile), 0, s, g->pools, (i32)g->n_pools,
+                       scr + g->scr_off_cls, (u32*)(scr + g->scr_off_tiles));
+    hipLaunchKernelGGL(rkc_lean_order_scatter, dim3(tiles), dim3(kOrderTile), 0, s, (i32)g->n_pools,
+                       (const unsigned char*)(scr + g->scr_off_cls), (const u32*)(scr + g->scr_off_tiles),
+                       (u32*)(scr + g->scr_off_order));
+  } else {
+    hipLaunchKernelGGL(rkc_lean_order_identity, dim3(tiles), dim3(kOrderTile), 0, s, (i32)g->n_pools,
+                       (u32*)(scr + g->scr_off_order));
+  }
   if (hipGetLastError() != hipSuccess) return RKC_E_HIP;
   hipLaunchKernelGGL((rkc_lean<NS>), dim3((unsigned)g->n_pools), dim3(64), g->lds_bytes, s, *g);
   return hipGetLastError() == hipSuccess ? RKC_OK : RKC_E_HIP;
