@@ -442,7 +442,10 @@ struct Pool {
       l3 = max(l3, p == 2 ? sx : 0u); l4 = max(l4, p == 3 ? sx : 0u);
       tp = max(tp, on && m_pending(m) ? T : 0u);
     }
-    pr = wave_max(pr); l1 = wave_max(l1); l2 = wave_max(l2); l3 = wave_max(l3); l4 = wave_max(l4);
+    // (the soft levels are zero in every lane outside soft levels, the hard extent outside hard
+    // protection: those reductions are skipped)
+    if (hardm) pr = wave_max(pr);
+    if (softl) { l1 = wave_max(l1); l2 = wave_max(l2); l3 = wave_max(l3); l4 = wave_max(l4); }
     ca = wave_max(ca); cso = wave_max(cso); tp = wave_max(tp);
     cgs(c, 2, make_uint4(l1, l2, l3, l4));
     cs(c, CF_COVA, ca); cs(c, CF_COVS, cso); cs(c, CF_TPEND, tp);
