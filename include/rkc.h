@@ -256,8 +256,13 @@ enum rkc_pool_status {
   RKC_PS_REQUEST_TABLE = 1, /* a PREFILL found the live-request table full                   */
   RKC_PS_CLAIM_TABLE = 2,   /* a CLAIM found the live-claim table full                         */
   RKC_PS_SLOT_TABLE = 4,    /* more CLAIM events than n_claim_slots                            */
-  RKC_PS_DESCRIPTOR = 256   /* descriptor outside the batch limits; the pool was not replayed,
+  RKC_PS_DESCRIPTOR = 256,  /* descriptor outside the batch limits; the pool was not replayed,
                                every outcome is INVALID (an ABI fault, not a contract outcome) */
+  RKC_PS_INTERNAL = (int32_t)0x80000000u /* a kernel's own consistency guard fired (an allocation
+                               that feasibility said must succeed found no block, a touch-stack
+                               node beyond its bound, a runaway loop); the pool's outputs from
+                               that step on are unreliable.  Never set on a correct build: the
+                               parity tests require it to be clear on every pool */
 };
 
 /* ----------------------------------------------------------------------------------------------
@@ -300,10 +305,11 @@ typedef enum rkc_status {
   RKC_E_POOL_STATUS = -7  /* query succeeded, but the pool's status word is non-zero           */
 } rkc_status;
 
-/* ABI version (RKC_ABI_VERSION). */
+/* ABI version (RKC_ABI_VERSION).  Implementation detail, no passage of the paper. */
 int32_t rkc_abi_version(void);
 
-/* Device scratch bytes rkc_replay_batch needs for this batch: per pool, the pool state that does not
+/* Device scratch bytes rkc_replay_batch needs for this batch (an implementation detail: the paper
+ * defines no storage, only the contract the replay follows): per pool, the pool state that does not
  * stay on chip (touch-stack nodes beyond the LDS part, the FIFO of finished requests' private runs,
  * one entry per claim slot, a deferral ring of max_live_requests entries, and the live lists when
  * they do not fit in LDS), plus 4 bytes per pool for the launch order of the compact kernel.  Reads
@@ -311,26 +317,42 @@ int32_t rkc_abi_version(void);
 size_t rkc_scratch_bytes(const rkc_batch* b);
 
 /* Replay every pool of the batch from empty pools (all U blocks FREE, no claims, no requests).
- * Asynchronous: validates the host struct, then only enqueues kernels on stream s (NULL = the
- * default stream).  Pool i is replayed by its own wavefront or workgroup; pools are independent,
- * so results do not depend on batch composition or order.  Returns RKC_OK or a negative status;
- * on a negative status nothing was enqueued. */
+ * What each event does is the contract of the paper: the claim input schema and the ClaimEvent
+ * surface (§3.1 minimal conformance schema; protection-mode table), decisions and the lifecycle
+ * (§3.1 decision and state rows; §3.2 harm semantics; §3.3), the feasibility boundary
+ * protected_resident + active_live <= usable (§3.4), the policies and runtime actions (§3.5
+ * mechanism table) and scheduler-visible refusal with its record (§5.4 refusal record).
+ * Arguments: b describes device buffers laid out as above (the host struct itself is read during
+ * the call only); s is a hipStream_t of the current device (NULL = the default stream).
+ * Asynchronous: validates the host struct, then only enqueues kernels on s.  Pool i is replayed by
+ * its own wavefront or workgroup; pools are independent, so results do not depend on batch
+ * composition or order.  Returns RKC_OK or a negative status; on a negative status nothing was
+ * enqueued.  Outcomes, pool telemetry and claim telemetry are written in full; scratch contents are
+ * undefined afterwards. */
 rkc_status rkc_replay_batch(const rkc_batch* b, void* s /* hipStream_t */);
 
-/* Copy outcomes [first, first + count) of pool `pool` into host_dst after synchronizing s.
+/* Copy outcomes [first, first + count) of pool `pool` into host_dst (caller-owned, count records)
+ * after synchronizing s.  One outcome per input event: the ClaimEvent stream of §3.1 (event type,
+ * claim or request id, step = index, predicate / capacity fields), with refusals carrying the §5.4
+ * refusal record (blocking claim id, protected resident, active required; shortfall = a + b - U).
  * Also reads the pool descriptor back to locate the events.  Returns RKC_E_RANGE when the range
- * leaves the pool, RKC_E_POOL_STATUS (data still copied) when the pool's status is non-zero. */
+ * leaves the pool or the descriptor's event offset does not fit the batch (nothing copied),
+ * RKC_E_POOL_STATUS (data still copied) when the pool's status is non-zero. */
 rkc_status rkc_query_outcomes(const rkc_batch* b, int32_t pool, int32_t first, int32_t count,
                               rkc_outcome* host_dst, void* s);
 
 /* Copy pool telemetry of `pool` (if host_pool != NULL) and up to max_claims of its claim
  * telemetry slots (if host_claims != NULL; *n_claims receives the pool's slot count) after
- * synchronizing s.  Returns RKC_E_POOL_STATUS (data still copied) for a non-zero pool status. */
+ * synchronizing s.  The claim records are the claim-level telemetry of the §7 runtime-surface table
+ * (accepted, refused, demoted, evicted, offloaded or harmed) over the §3.1 decision and state rows
+ * and the §3.2 harm table.  Returns RKC_E_RANGE when the descriptor's slot range does not fit the
+ * batch (claim records not copied), RKC_E_POOL_STATUS (data still copied) for a non-zero pool
+ * status. */
 rkc_status rkc_query_telemetry(const rkc_batch* b, int32_t pool, rkc_pool_telemetry* host_pool,
                                rkc_claim_telemetry* host_claims, int32_t max_claims,
                                int32_t* n_claims, void* s);
 
-/* Static, human-readable name of a status. */
+/* Static, human-readable name of a status.  Implementation detail, no passage of the paper. */
 const char* rkc_status_string(rkc_status st);
 
 #ifdef __cplusplus

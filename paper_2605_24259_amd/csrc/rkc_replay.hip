@@ -1540,7 +1540,7 @@ size_t rkc_scratch_bytes(const rkc_batch* b) {
   return (size_t)(L.scr_pool_bytes * (u64)b->n_pools);
 }
 
-rkc_status rkc_replay_batch(const rkc_batch* b, void* s) {
+static rkc_status replay(const rkc_batch* b, void* s) {
   rkc_status st = check_batch(b);
   if (st != RKC_OK) return st;
   if (b->n_pools == 0) return RKC_OK;
@@ -1572,6 +1572,8 @@ rkc_status rkc_replay_batch(const rkc_batch* b, void* s) {
   return launch<u32, false>(g, (unsigned)b->n_pools, (hipStream_t)s);
 }
 
+rkc_status rkc_replay_batch(const rkc_batch* b, void* s) { return replay(b, s); }
+
 static rkc_status read_desc(const rkc_batch* b, int32_t pool, rkc_pool_desc* d, void* s) {
   if (!b) return RKC_E_NULL;
   if (pool < 0 || pool >= b->n_pools) return RKC_E_RANGE;
@@ -1593,6 +1595,10 @@ rkc_status rkc_query_outcomes(const rkc_batch* b, int32_t pool, int32_t first, i
   rkc_status st = read_desc(b, pool, &d, s);
   if (st != RKC_OK) return st;
   if (first < 0 || count < 0 || (int64_t)first + count > d.n_events) return RKC_E_RANGE;
+  // the descriptor is caller data: never copy from outside the batch's outcome array
+  if (d.event_offset < 0 || d.event_offset > b->n_events_total ||
+      (int64_t)first + count > b->n_events_total - d.event_offset)
+    return RKC_E_RANGE;
   if (count > 0 && hipMemcpy(host_dst, b->d_outcomes + d.event_offset + first,
                              (size_t)count * sizeof(rkc_outcome), hipMemcpyDeviceToHost) != hipSuccess)
     return RKC_E_HIP;
@@ -1611,6 +1617,10 @@ rkc_status rkc_query_telemetry(const rkc_batch* b, int32_t pool, rkc_pool_teleme
     return RKC_E_HIP;
   if (host_claims && max_claims > 0) {
     int32_t k = d.n_claim_slots < max_claims ? d.n_claim_slots : max_claims;
+    // the descriptor is caller data: never copy from outside the batch's claim telemetry array
+    if (k > 0 && (d.claim_slot_offset < 0 || d.claim_slot_offset > b->n_claim_slots_total ||
+                  k > b->n_claim_slots_total - d.claim_slot_offset))
+      return RKC_E_RANGE;
     if (k > 0 && hipMemcpy(host_claims, b->d_claim_tel + d.claim_slot_offset,
                            (size_t)k * sizeof(rkc_claim_telemetry), hipMemcpyDeviceToHost) != hipSuccess)
       return RKC_E_HIP;

@@ -239,6 +239,29 @@ def test_descriptor_outside_batch_limits(tg):
     assert db.query_telemetry(1, 0)[0] == -7
 
 
+@pytest.mark.parametrize("flags", [0, 1], ids=["compact", "general"])
+def test_descriptor_offsets_outside_batch(tg, flags):
+    """A descriptor whose event or claim-slot offset leaves the batch's arrays: the kernel writes
+    nothing of that pool but its telemetry (descriptor status), and the queries refuse to copy
+    from outside the arrays instead of reading past them."""
+    import paper_2605_24259_amd as rkc
+    ev = [tg.claim(10, 0, 10), tg.prefill(5), tg.finish()]
+    trace = tg.from_pools([dict(usable_blocks=80, mode=3, n_chains=2, events=ev),
+                           dict(usable_blocks=80, mode=3, n_chains=2, events=ev),
+                           dict(usable_blocks=80, mode=3, n_chains=2, events=ev)])
+    lim = trace.limits()
+    trace.desc[1, 12:14] = np.array([trace.n_events + 1000], np.int64).view(np.int32)
+    trace.desc[2, 14:16] = np.array([trace.n_claim_slots + 7], np.int64).view(np.int32)
+    db = rkc.DeviceBatch(trace.desc, trace.events, trace.n_claim_slots, lim, flags=flags).replay()
+    out, pt, ct = db.results()
+    assert pt[0, 31] == 0 and pt[1, 31] == 256 and pt[2, 31] == 256
+    assert db.query_outcomes(0, 0, 3)[0] == 0
+    assert db.query_outcomes(1, 0, 1)[0] == -3
+    assert db.query_outcomes(2, 0, 3)[0] == -7  # events in range, status set
+    assert db.query_telemetry(1, 1)[0] == -7     # slots in range, status set
+    assert db.query_telemetry(2, 1)[0] == -3
+
+
 @pytest.mark.parametrize("variant", ["narrow", "wide", "wide_global_lists",
                                      "global_lists_small_request_table"])
 def test_storage_layouts_agree(oracle_mod, tg, variant):
