@@ -17,8 +17,9 @@
  * return a negative status.
  *
  * Ownership.  The caller owns every buffer (in practice torch tensors in device memory).  The
- * library allocates no device memory, keeps no mutable global state and is re-entrant for disjoint
- * buffers on different streams.  Every output buffer is fully overwritten by a replay, so callers
+ * library allocates no device memory and is re-entrant for disjoint buffers on different streams;
+ * its one piece of global state is the built-in scratch of rkc_replay_batch_noalloc (a fixed
+ * per-device array, see there).  Every output buffer is fully overwritten by a replay, so callers
  * need not clear them.  Buffers must stay alive until the stream has finished the replay.
  *
  * All integers are little-endian.  Device pointers are HIP device addresses of the current device.
@@ -33,12 +34,14 @@
 extern "C" {
 #endif
 
-#define RKC_ABI_VERSION 4
+#define RKC_ABI_VERSION 5
 
 /* Hard limits of this implementation (checked on the host and per pool on the device). */
 #define RKC_MAX_USABLE_BLOCKS   (1 << 22) /* U per pool                                        */
 #define RKC_MAX_EVENTS_PER_POOL (1 << 24) /* events per pool; request/claim ids are < this     */
 #define RKC_MAX_FIELD_BLOCKS    (1 << 24) /* S, k, L, P, T above this make an event malformed  */
+/* Size of the built-in device scratch that rkc_replay_batch_noalloc uses instead of a caller buffer. */
+#define RKC_NOALLOC_SCRATCH_BYTES (64u << 20)
 
 /* ----------------------------------------------------------------------------------------------
  * Event: 16 bytes = 4 x int32, pool-major (CSR by rkc_pool_desc.event_offset).
@@ -302,7 +305,9 @@ typedef enum rkc_status {
   RKC_E_UNSUPPORTED = -4, /* a limit beyond what this implementation supports                  */
   RKC_E_SCRATCH = -5,     /* scratch buffer missing or too small                               */
   RKC_E_HIP = -6,         /* a HIP runtime call failed (launch, copy, synchronize)             */
-  RKC_E_POOL_STATUS = -7  /* query succeeded, but the pool's status word is non-zero           */
+  RKC_E_POOL_STATUS = -7, /* query succeeded, but the pool's status word is non-zero           */
+  RKC_E_SCRATCH_LIMIT = -8 /* rkc_replay_batch_noalloc: the batch needs more scratch than
+                              RKC_NOALLOC_SCRATCH_BYTES                                          */
 } rkc_status;
 
 /* ABI version (RKC_ABI_VERSION).  Implementation detail, no passage of the paper. */
@@ -330,6 +335,18 @@ size_t rkc_scratch_bytes(const rkc_batch* b);
  * enqueued.  Outcomes, pool telemetry and claim telemetry are written in full; scratch contents are
  * undefined afterwards. */
 rkc_status rkc_replay_batch(const rkc_batch* b, void* s /* hipStream_t */);
+
+/* For callers that cannot allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc): rkc_replay_batch with the library's built-in scratch instead of
+ * b->d_scratch (b->d_scratch and b->scratch_bytes are ignored and may be NULL / 0).  Same outputs,
+ * same asynchrony, same statuses, plus RKC_E_SCRATCH_LIMIT when rkc_scratch_bytes(b) exceeds
+ * RKC_NOALLOC_SCRATCH_BYTES (64 MiB: e.g. 4,096 pools of 80 blocks x 256 events, or 2,048 pools of
+ * 2,048 blocks x 1,024 events).  It calls no hipMalloc / hipFree: the scratch is a static device array
+ * of the library, one per device, looked up on the first call made with that device current and
+ * held until the process ends.  Every call on one device shares that array, so calls that overlap
+ * on one device (different streams, or threads) race and give undefined results: serialize them.
+ * Nothing in the array needs clearing between calls. */
+rkc_status rkc_replay_batch_noalloc(const rkc_batch* b, void* s /* hipStream_t */);
 
 /* Copy outcomes [first, first + count) of pool `pool` into host_dst (caller-owned, count records)
  * after synchronizing s.  One outcome per input event: the ClaimEvent stream of §3.1 (event type,

@@ -15,7 +15,7 @@ LIB_PATH = os.path.join(_PKG, "librkc.so")
 _lib = None
 
 # layouts and codes of this binding (rkc.h RKC_ABI_VERSION)
-ABI_VERSION = 4
+ABI_VERSION = 5
 POOL_TEL_WORDS = 64
 
 # rkc_batch.flags: replay with the general kernel even where the compact one applies
@@ -24,7 +24,11 @@ FLAG_GENERAL_KERNEL = 1
 # status codes (rkc_status)
 STATUS = {0: "ok", -1: "null pointer", -2: "misaligned pointer", -3: "argument out of range",
           -4: "unsupported size or mode", -5: "scratch buffer missing or too small",
-          -6: "HIP runtime error", -7: "pool status is non-zero"}
+          -6: "HIP runtime error", -7: "pool status is non-zero",
+          -8: "batch needs more scratch than the built-in buffer holds"}
+
+# size of the built-in scratch of rkc_replay_batch_noalloc (RKC_NOALLOC_SCRATCH_BYTES)
+NOALLOC_SCRATCH_BYTES = 64 << 20
 
 
 class RkcError(RuntimeError):
@@ -70,6 +74,8 @@ def load():
         lib.rkc_scratch_bytes.restype = ctypes.c_size_t
         lib.rkc_replay_batch.argtypes = [bp, vp]
         lib.rkc_replay_batch.restype = ctypes.c_int
+        lib.rkc_replay_batch_noalloc.argtypes = [bp, vp]
+        lib.rkc_replay_batch_noalloc.restype = ctypes.c_int
         lib.rkc_query_outcomes.argtypes = [bp, i32, i32, i32, vp, vp]
         lib.rkc_query_outcomes.restype = ctypes.c_int
         lib.rkc_query_telemetry.argtypes = [bp, i32, vp, vp, i32, ctypes.POINTER(i32), vp]
@@ -83,8 +89,8 @@ def load():
     return _lib
 
 
-EXPORTS = ("rkc_abi_version", "rkc_scratch_bytes", "rkc_replay_batch", "rkc_query_outcomes",
-           "rkc_query_telemetry", "rkc_status_string")
+EXPORTS = ("rkc_abi_version", "rkc_scratch_bytes", "rkc_replay_batch", "rkc_replay_batch_noalloc",
+           "rkc_query_outcomes", "rkc_query_telemetry", "rkc_status_string")
 
 
 def _stream_ptr(stream):
@@ -96,7 +102,8 @@ def _stream_ptr(stream):
 class DeviceBatch:
     """Device-resident inputs, outputs and scratch of one replay launch (torch tensors)."""
 
-    def __init__(self, desc, events, n_claim_slots: int, limits: dict, device="cuda", flags: int = 0):
+    def __init__(self, desc, events, n_claim_slots: int, limits: dict, device="cuda", flags: int = 0,
+                 scratch: bool = True):
         import torch
         if not torch.cuda.is_available():
             raise RuntimeError("no GPU: the replay runs only in the HIP kernels")
@@ -124,23 +131,36 @@ class DeviceBatch:
         b.d_outcomes = self.outcomes.data_ptr()
         b.d_pool_tel = self.pool_tel.data_ptr()
         b.d_claim_tel = self.claim_tel.data_ptr()
-        nbytes = int(lib.rkc_scratch_bytes(ctypes.byref(b)))
-        self.scratch = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=self.device)
-        b.d_scratch = self.scratch.data_ptr()
-        b.scratch_bytes = int(self.scratch.numel())
+        self.scratch_needed = int(lib.rkc_scratch_bytes(ctypes.byref(b)))
+        if scratch:
+            self.scratch = torch.empty(max(self.scratch_needed, 256), dtype=torch.uint8, device=self.device)
+            b.d_scratch = self.scratch.data_ptr()
+            b.scratch_bytes = int(self.scratch.numel())
+        else:  # only for replay_noalloc, which brings its own
+            self.scratch = None
+            b.d_scratch = None
+            b.scratch_bytes = 0
         self.batch = b
         self.n_pools = n_pools
         self.n_events = n_ev
 
     @classmethod
-    def from_trace(cls, trace, device="cuda", flags: int = 0):
-        return cls(trace.desc, trace.events, trace.n_claim_slots, trace.limits(), device, flags)
+    def from_trace(cls, trace, device="cuda", flags: int = 0, scratch: bool = True):
+        return cls(trace.desc, trace.events, trace.n_claim_slots, trace.limits(), device, flags, scratch)
 
     def replay(self, stream=None):
         """Enqueue the replay on `stream` (default: torch's current stream)."""
         st = load().rkc_replay_batch(ctypes.byref(self.batch), _stream_ptr(stream))
         if st != 0:
             raise RkcError(st, "rkc_replay_batch")
+        return self
+
+    def replay_noalloc(self, stream=None):
+        """Enqueue the replay through rkc_replay_batch_noalloc (the library's built-in scratch; no
+        device allocation in the call)."""
+        st = load().rkc_replay_batch_noalloc(ctypes.byref(self.batch), _stream_ptr(stream))
+        if st != 0:
+            raise RkcError(st, "rkc_replay_batch_noalloc")
         return self
 
     def results(self):

@@ -39,8 +39,15 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <mutex>
+
 #include "rkc.h"
 #include "rkc_lean.h"
+
+// Built-in device scratch of rkc_replay_batch_noalloc, for callers that cannot allocate.  Each device
+// the library runs on holds its own copy until the process ends.  Host code never passes this name to
+// a kernel or a copy: it is a host-side stand-in; the device address comes from hipGetSymbolAddress.
+static __device__ __align__(256) unsigned char scratch[RKC_NOALLOC_SCRATCH_BYTES];
 
 namespace {
 
@@ -1574,6 +1581,38 @@ static rkc_status replay(const rkc_batch* b, void* s) {
 
 rkc_status rkc_replay_batch(const rkc_batch* b, void* s) { return replay(b, s); }
 
+// Device address of the built-in scratch on the current device, looked up once per device.
+static void* noalloc_scratch(void) {
+  enum { kMaxDevices = 64 };
+  static std::mutex mu;
+  static void* addr[kMaxDevices];
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return nullptr;
+    addr[dev] = p;
+  }
+  return addr[dev];
+}
+
+rkc_status rkc_replay_batch_noalloc(const rkc_batch* b, void* s) {
+  if (!b) return RKC_E_NULL;
+  rkc_batch nb = *b;
+  nb.d_scratch = nullptr;
+  nb.scratch_bytes = 0;
+  rkc_status st = check_batch(&nb);
+  if (st != RKC_OK) return st;
+  if (nb.n_pools == 0) return RKC_OK;
+  if (rkc_scratch_bytes(&nb) > (size_t)RKC_NOALLOC_SCRATCH_BYTES) return RKC_E_SCRATCH_LIMIT;
+  void* p = noalloc_scratch();
+  if (!p) return RKC_E_HIP;
+  nb.d_scratch = p;
+  nb.scratch_bytes = (size_t)RKC_NOALLOC_SCRATCH_BYTES;
+  return replay(&nb, s);
+}
+
 static rkc_status read_desc(const rkc_batch* b, int32_t pool, rkc_pool_desc* d, void* s) {
   if (!b) return RKC_E_NULL;
   if (pool < 0 || pool >= b->n_pools) return RKC_E_RANGE;
@@ -1638,6 +1677,7 @@ const char* rkc_status_string(rkc_status st) {
     case RKC_E_SCRATCH: return "scratch buffer missing or too small";
     case RKC_E_HIP: return "HIP runtime error";
     case RKC_E_POOL_STATUS: return "pool status is non-zero";
+    case RKC_E_SCRATCH_LIMIT: return "batch needs more scratch than the built-in buffer holds";
   }
   return "unknown status";
 }

@@ -91,9 +91,10 @@ def _batch(**kw):
 
 
 def test_version_and_strings(lib):
-    assert lib.rkc_abi_version() == 4
+    assert lib.rkc_abi_version() == 5
     assert lib.rkc_status_string(0) == b"ok"
     assert lib.rkc_status_string(-5).startswith(b"scratch")
+    assert b"built-in" in lib.rkc_status_string(-8)
     assert lib.rkc_status_string(-99) == b"unknown status"
 
 
@@ -118,6 +119,21 @@ def test_host_argument_checks(lib):
     # an empty batch is a valid no-op
     assert lib.rkc_replay_batch(ctypes.byref(_batch(n_pools=0)), None) == 0
     assert lib.rkc_scratch_bytes(null) == 0
+
+
+def test_noalloc_host_checks(lib):
+    """The no-allocation entry point checks the batch like rkc_replay_batch (it ignores the scratch
+    fields) and refuses, before any HIP call, a batch whose scratch exceeds its built-in 64 MiB."""
+    import paper_2605_24259_amd as rkc
+    null = ctypes.POINTER(type(_batch()))()
+    assert lib.rkc_replay_batch_noalloc(null, None) == -1
+    assert lib.rkc_replay_batch_noalloc(ctypes.byref(_batch(d_events=0)), None) == -1
+    assert lib.rkc_replay_batch_noalloc(ctypes.byref(_batch(d_outcomes=0x30008)), None) == -2
+    assert lib.rkc_replay_batch_noalloc(ctypes.byref(_batch(n_pools=-1)), None) == -3
+    assert lib.rkc_replay_batch_noalloc(ctypes.byref(_batch(n_pools=0, d_scratch=0)), None) == 0
+    big = _batch(n_pools=4096, max_events=4096, d_scratch=0)
+    assert lib.rkc_scratch_bytes(ctypes.byref(big)) > rkc.NOALLOC_SCRATCH_BYTES
+    assert lib.rkc_replay_batch_noalloc(ctypes.byref(big), None) == -8
 
 
 def test_scratch_grows_with_limits(lib):
