@@ -11,7 +11,8 @@ import ctypes
 import os
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_PKG, "librkc.so")
+# RKC_LIBRARY may name another build of the same sources (the uniformity-checking build)
+LIB_PATH = os.environ.get("RKC_LIBRARY") or os.path.join(_PKG, "librkc.so")
 _lib = None
 
 # layouts and codes of this binding (rkc.h RKC_ABI_VERSION)

@@ -24,15 +24,22 @@ def hipcc() -> str:
     return os.path.join(rocm, "bin", "hipcc")
 
 
-def build(verbose: bool = False) -> str:
-    tmp = LIB + ".tmp%d" % os.getpid()
-    cmd = [hipcc(), *HIPCC_FLAGS, *SRCS, "-o", tmp]
+# checking build: every readfirstlane also verifies that the active lanes agree (slower; used to
+# run the GPU parity suite once against the uniformity assumptions of both kernels)
+CHECK_LIB = os.path.join(PKG, "librkc_check.so")
+
+
+def build(verbose: bool = False, check_uniform: bool = False) -> str:
+    out = CHECK_LIB if check_uniform else LIB
+    tmp = out + ".tmp%d" % os.getpid()
+    cmd = [hipcc(), *HIPCC_FLAGS, *(["-DRKC_CHECK_UNIFORM"] if check_uniform else []), *SRCS, "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.check_call(cmd)
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, out)
+    return out
 
 
 if __name__ == "__main__":
-    print(build(verbose=True))
+    import sys
+    print(build(verbose=True, check_uniform="--check-uniform" in sys.argv))

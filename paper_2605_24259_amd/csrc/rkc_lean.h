@@ -33,4 +33,9 @@ bool rkc_lean_layout(const rkc_batch* b, rkc_lean_args* g);
 // Launch the compact kernel (one 64-lane workgroup per pool) on stream s.
 rkc_status rkc_lean_launch(const rkc_lean_args* g, hipStream_t s);
 
+#ifdef RKC_CHECK_UNIFORM
+// checking build only: calls of the compact kernel's readfirstlane whose active lanes disagreed
+unsigned rkc_lean_uniform_violations(void);
+#endif
+
 #endif

@@ -87,7 +87,20 @@ __device__ __forceinline__ u32 pk(u32 lo, u32 hi) {
 __device__ __forceinline__ i32 st16(u32 v) { return v == NIL ? -1 : (i32)v; }  // step field
 
 // ---- wave primitives (all 64 lanes active) ----------------------------------------------------
+// A value every lane holds identically, moved to a scalar register.  Built with RKC_CHECK_UNIFORM
+// (a checking build, never the product one), every call also verifies that the active lanes agree
+// and counts the calls where they do not.
+#ifdef RKC_CHECK_UNIFORM
+__device__ unsigned int g_lean_uniform_violations;
+__device__ __forceinline__ u32 ufl(u32 v) {
+  const u32 f = (u32)__builtin_amdgcn_readfirstlane((int)v);
+  if (__ballot(v != f) != 0 && __lane_id() == (u32)__builtin_ctzll(__ballot(true)))
+    atomicAdd(&g_lean_uniform_violations, 1u);
+  return f;
+}
+#else
 __device__ __forceinline__ u32 ufl(u32 v) { return (u32)__builtin_amdgcn_readfirstlane((int)v); }
+#endif
 __device__ __forceinline__ u32 rdl(u32 v, u32 l) { return (u32)__builtin_amdgcn_readlane((int)v, (int)l); }
 // a - b, or 0 when b exceeds a
 __device__ __forceinline__ u32 sub0(u32 a, u32 b) { return a > b ? a - b : 0u; }
@@ -1293,6 +1306,14 @@ bool rkc_lean_layout(const rkc_batch* b, rkc_lean_args* g) {
   g->scr_total = g->scr_off_tiles + align_up(4ull * kClasses * tiles, 256);
   return true;
 }
+
+#ifdef RKC_CHECK_UNIFORM
+unsigned rkc_lean_uniform_violations(void) {
+  unsigned v = 0;
+  if (hipMemcpyFromSymbol(&v, HIP_SYMBOL(g_lean_uniform_violations), sizeof v) != hipSuccess) return ~0u;
+  return v;
+}
+#endif
 
 template <int NS>
 rkc_status launch_ns(const rkc_lean_args* g, hipStream_t s) {

@@ -141,8 +141,20 @@ __device__ __forceinline__ u32 make_key(u32 level, u32 lu) { return (level << 28
 __device__ __forceinline__ u32 lane_id() { return __lane_id(); }
 __device__ __forceinline__ u64 ballot(bool p) { return __ballot(p); }
 __device__ __forceinline__ i32 rdlane(i32 v, u32 l) { return __builtin_amdgcn_readlane(v, (int)l); }
-// a value every lane holds identically, moved to a scalar register
+// A value every lane holds identically, moved to a scalar register.  Built with RKC_CHECK_UNIFORM
+// (a checking build, never the product one), every call also verifies that the active lanes agree
+// and counts the calls where they do not.
+#ifdef RKC_CHECK_UNIFORM
+__device__ unsigned int g_wave_uniform_violations;
+__device__ __forceinline__ u32 ufl(u32 v) {
+  const u32 f = (u32)__builtin_amdgcn_readfirstlane((int)v);
+  if (__ballot(v != f) != 0 && __lane_id() == (u32)__builtin_ctzll(__ballot(true)))
+    atomicAdd(&g_wave_uniform_violations, 1u);
+  return f;
+}
+#else
 __device__ __forceinline__ u32 ufl(u32 v) { return (u32)__builtin_amdgcn_readfirstlane((int)v); }
+#endif
 __device__ __forceinline__ uint4 ufl4(uint4 v) { return make_uint4(ufl(v.x), ufl(v.y), ufl(v.z), ufl(v.w)); }
 
 // Cross-lane reductions with DPP row permutes (no LDS round trip): within each 16-lane row,
@@ -1666,6 +1678,17 @@ rkc_status rkc_query_telemetry(const rkc_batch* b, int32_t pool, rkc_pool_teleme
   }
   return pool_status(b, pool, RKC_OK);
 }
+
+#ifdef RKC_CHECK_UNIFORM
+// Checking build only (not part of the ABI): readfirstlane calls of either kernel whose active lanes
+// held different values, since the library was loaded.
+uint32_t rkc_debug_uniform_violations(void) {
+  unsigned v = 0;
+  if (hipMemcpyFromSymbol(&v, HIP_SYMBOL(g_wave_uniform_violations), sizeof v) != hipSuccess) return ~0u;
+  const unsigned w = rkc_lean_uniform_violations();
+  return w == ~0u ? ~0u : v + w;
+}
+#endif
 
 const char* rkc_status_string(rkc_status st) {
   switch (st) {
