@@ -369,6 +369,25 @@ def test_random_deferral_medium(oracle_mod, kernel):
     assert gpu[1][:, 33].sum() > 50
 
 
+def test_regression_capacity_refusal_record_in_deferring_pools(oracle_mod):
+    """Regression guard for a wrong record once produced by builds of the compact kernel: in
+    deferring hard-protection pools, capacity refusals came out with b (active live required) equal
+    to the hit count of the served-prefill record instead of A + cached hits + need.  Every refusal
+    must satisfy the feasibility identity a + b > U (protected resident plus required exceeds the
+    usable pool, §3.4) and equal the oracle."""
+    trace = randtrace.random_batch(61, 400, U_range=(8, 300), n_events=(1, 400), n_chains=9,
+                                   p_malformed=0.01, tight_every=7, caps=(256, 64), defer=True,
+                                   hard_share=0.8)
+    gpu, ora = _both_kernel(oracle_mod, trace, "compact")
+    out = gpu[0]
+    code = out[:, 0] & 255
+    ref = (code == 2) | (code == 3) | (code == 10)
+    Ue = np.repeat(trace.field("usable_blocks").astype(np.int64), trace.field("n_events"))
+    assert ref.sum() > 1000
+    assert (out[ref, 2].astype(np.int64) + out[ref, 3] > Ue[ref]).all()
+    compare_pools(trace, gpu, ora)
+
+
 @pytest.mark.parametrize("offload", [False, True])
 @pytest.mark.parametrize("variant", ["wide", "wide_global_lists", "global_lists_small_request_table"])
 def test_deferral_storage_layouts(oracle_mod, tg, variant, offload):
