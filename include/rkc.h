@@ -279,7 +279,7 @@ typedef struct rkc_batch {
   int32_t max_live_requests; /* >= every pool's max_live_requests                                */
   int32_t max_live_claims;   /* >= every pool's max_live_claims                                  */
   int32_t max_claim_slots;   /* >= every pool's n_claim_slots                                    */
-  int32_t flags;             /* 0, or RKC_FLAG_GENERAL_KERNEL; other bits are an error           */
+  int32_t flags;             /* RKC_FLAG_* bits (below); other bits are an error                  */
   int64_t n_events_total;    /* length of the event and outcome arrays                           */
   int64_t n_claim_slots_total; /* length of the claim telemetry array                            */
   const rkc_pool_desc* d_pools;     /* [n_pools], 16-byte aligned                               */
@@ -296,6 +296,11 @@ typedef struct rkc_batch {
  * claims <= 64 and live requests <= 256).  Both give identical outputs; the flag exists so the
  * general kernel can be checked on the same inputs. */
 #define RKC_FLAG_GENERAL_KERNEL 1
+/* rkc_batch.flags: one wavefront per pool everywhere.  Without it, a batch of at most 256 pools (one
+ * per compute unit) whose live lists do not fit in LDS is replayed by a workgroup of 8 wavefronts
+ * per pool (wave 0 runs the pool's event loop; the others share the scans and moves of its long
+ * lists).  Both give identical outputs; the flag exists so both can be checked on the same inputs. */
+#define RKC_FLAG_ONE_WAVE_PER_POOL 2
 
 typedef enum rkc_status {
   RKC_OK = 0,

@@ -21,6 +21,8 @@ POOL_TEL_WORDS = 64
 
 # rkc_batch.flags: replay with the general kernel even where the compact one applies
 FLAG_GENERAL_KERNEL = 1
+# rkc_batch.flags: one wavefront per pool even where a workgroup per pool applies
+FLAG_ONE_WAVE_PER_POOL = 2
 
 # status codes (rkc_status)
 STATUS = {0: "ok", -1: "null pointer", -2: "misaligned pointer", -3: "argument out of range",

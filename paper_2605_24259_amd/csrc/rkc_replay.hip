@@ -191,11 +191,12 @@ __device__ __forceinline__ u32 wave_sum(u32 v) { return wave_reduce<OpAdd>(v); }
 // ---- launch geometry (computed on the host) ---------------------------------------------------
 struct Layout {
   u32 chains, reqs, claims, nodes_lds;
-  u32 off_chain, off_mark, off_key, off_rq, off_cl, off_node;
+  u32 off_chain, off_mark, off_key, off_rq, off_cl, off_node, off_job;
   u32 lds_bytes;
   u64 scr_pool_bytes, scr_off_node, scr_off_fifo, scr_off_slot, scr_off_dq, scr_off_rq, scr_off_cl;
   u32 fifo_cap, node_cap;
   u32 global_lists, narrow;
+  u32 waves;  // waves per pool (1, or kGroupWaves for the workgroup-per-pool kernel)
 };
 
 struct Args {
@@ -211,6 +212,15 @@ struct Args {
 };
 
 enum : u32 { MK_SWEEP = 1, MK_RECOMP = 2 };
+
+// Workgroup per pool (NW > 1 waves): wave 0 runs the per-event state machine; the other waves wait
+// on the workgroup barrier and join the scans that cover a pool's live lists.  Wave 0 posts a job
+// (a word and its arguments on the LDS job board) and passes a barrier; every wave then takes its
+// share of the scan (entries wave * 64 + lane, stepping 64 * NW), reduces it across its lanes and
+// leaves up to 8 partial results on the board; a second barrier, and wave 0 combines them.
+enum : u32 { J_EXIT = 0, J_MAXIMA, J_EXPIRE, J_SWEEP, J_ATTRIB, J_HOLD, J_MOVE };
+constexpr u32 JB_ARGS = 16;   // board words before the partials (job word + arguments)
+constexpr u32 kGroupWaves = 8; // waves per pool in the workgroup-per-pool kernel
 // internal-consistency fault bit in the pool status word: set only if a structural bound that
 // the algorithm guarantees is ever violated; loops stop instead of running on.
 constexpr u32 kFault = 0x80000000u;
@@ -227,8 +237,10 @@ struct AllocRes {
 // kGL: the live-request and live-claim lists live in global scratch instead of LDS (pools whose
 // lists do not fit on chip).  Lane-parallel writes to them are then followed by a workgroup fence
 // before any other lane reads them.
-template <typename W, bool kGL>
+template <typename W, bool kGL, int NW>
 struct Pool {
+  static_assert(NW >= 1 && 8 * NW <= 64, "at most 8 waves per pool");
+  static constexpr u32 kSpan = 64u * NW;  // entries one pass of the workgroup covers
   typedef typename ListMem<W, kGL>::word lword;
   typedef typename Store<W>::lds_w lds_w;
   typedef typename Store<W>::w4 w4;
@@ -240,6 +252,8 @@ struct Pool {
   u32 relax_on;  // the pool relaxes demotable hard claims (mode flag RKC_MODE_RELAX)
   u32 t2cap, t2used, t2peak;  // second tier: capacity, blocks held by offloaded claims, peak
   u32 lane;
+  u32 wave;           // wave index in the workgroup (wave 0 runs the state machine)
+  lds_u32* jb;        // job board (NW > 1)
   // memory
   lds_w* ch;          // chain records, CF_WORDS words each
   lds_u32* mk;        // per-chain mark bits
@@ -297,6 +311,47 @@ struct Pool {
   __device__ __forceinline__ static u32 lnil(u32 v) { return v == kListNil ? NIL : v; }
   __device__ __forceinline__ void lists_fence() {
     if (kGL) __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
+  }
+
+  // -- cooperative scans --
+  __device__ __forceinline__ u32 first() const { return wave * 64u + lane; }
+  // wave 0: post a job and its arguments, and release the other waves into it
+  __device__ __forceinline__ void post(u32 job, u32 a0 = 0, u32 a1 = 0, u32 a2 = 0, u32 a3 = 0, u32 a4 = 0) {
+    if (NW > 1) {
+      if (lane < 6)
+        jb[lane] = lane == 0 ? job : lane == 1 ? a0 : lane == 2 ? a1 : lane == 3 ? a2 : lane == 4 ? a3 : a4;
+      __syncthreads();
+    }
+  }
+  __device__ __forceinline__ u32 arg(u32 k) { return ufl(jb[1 + k]); }
+  // Publish this wave's partial results p[0..NP) and, on wave 0, combine the waves' partials: slot k
+  // takes the maximum where bit k of maxs is set, the minimum where bit k of mins is set, else the sum.
+  template <u32 NP>
+  __device__ __forceinline__ void exchange(u32 (&p)[NP], u32 maxs, u32 mins) {
+    if (NW > 1) {
+      u32 v = 0;
+#pragma unroll
+      for (u32 k = 0; k < NP; k++) v = lane == k ? p[k] : v;
+      if (lane < NP) jb[JB_ARGS + 8 * wave + lane] = v;
+      __syncthreads();
+      if (wave == 0) {
+        const u32 x = lane < 8 * NW ? (u32)jb[JB_ARGS + lane] : 0u;
+#pragma unroll
+        for (u32 k = 0; k < NP; k++) {
+          u32 r = (u32)rdlane((i32)x, k);
+#pragma unroll
+          for (u32 w = 1; w < (u32)NW; w++) {
+            const u32 y = (u32)rdlane((i32)x, 8 * w + k);
+            r = ((maxs >> k) & 1u) ? max(r, y) : ((mins >> k) & 1u) ? min(r, y) : r + y;
+          }
+          p[k] = r;
+        }
+      }
+    }
+  }
+  __device__ __forceinline__ void mark_or(u32 c, u32 bit) {
+    if (NW > 1) __hip_atomic_fetch_or(mk + c, bit, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    else mk[c] |= bit;
   }
 
   // -- nodes (x = extent, y = step, z = up (newer), w = down (older)); the first nl live in LDS,
@@ -442,11 +497,22 @@ struct Pool {
   // Recompute chain c's claim maxima from the live-claim list; returns the new hard protection
   // (the caller applies it through chain_update).
   __device__ __forceinline__ u32 claim_maxima(u32 c) {
+    post(J_MAXIMA, c, ncl);
+    u32 q[8];
+    maxima_slice(c, ncl, q);
+    cgs(c, 2, make_uint4(q[1], q[2], q[3], q[4]));
+    cs(c, CF_COVA, q[5]); cs(c, CF_COVS, q[6]); cs(c, CF_TPEND, q[7]);
+    return q[0];
+  }
+  // This wave's share of the claim maxima of chain c over the n live claims (all waves: the
+  // combined maxima in q on wave 0): hard protection, soft levels 1..4, coverage of live claims,
+  // of live claims not demoted / expired, and the largest pending threshold.
+  __device__ __forceinline__ void maxima_slice(u32 c, u32 ncl, u32 (&q)[8]) {
     u32 pr = 0, l1 = 0, l2 = 0, l3 = 0, l4 = 0, ca = 0, cso = 0, tp = 0;
     const bool hardm = mode == RKC_MODE_HARD, softl = soft_levels();
     // uniform chunks, every lane reading a valid entry and selecting, so that no lane mask is
     // saved and restored per condition
-    for (u32 base = 0; base < ncl; base += 64) {
+    for (u32 base = wave * 64u; base < ncl; base += kSpan) {
       const u32 i = base + lane, j = i < ncl ? i : base;
       const u32 m = cla(CL_META)[j], L = cla(CL_L)[j], T = cla(CL_T)[j], st = m_state(m);
       // an offloaded claim's victims are not resident and its predicate never fails
@@ -466,9 +532,8 @@ struct Pool {
     if (hardm) pr = wave_max(pr);
     if (softl) { l1 = wave_max(l1); l2 = wave_max(l2); l3 = wave_max(l3); l4 = wave_max(l4); }
     ca = wave_max(ca); cso = wave_max(cso); tp = wave_max(tp);
-    cgs(c, 2, make_uint4(l1, l2, l3, l4));
-    cs(c, CF_COVA, ca); cs(c, CF_COVS, cso); cs(c, CF_TPEND, tp);
-    return pr;
+    q[0] = pr; q[1] = l1; q[2] = l2; q[3] = l3; q[4] = l4; q[5] = ca; q[6] = cso; q[7] = tp;
+    exchange(q, 0xFFu, 0u);
   }
   __device__ __forceinline__ void recompute(u32 c) {
     const u32 pr = claim_maxima(c);
@@ -589,8 +654,19 @@ struct Pool {
 
   // Predicate sweep over claims on chains that shrank below a pending threshold (§3.2 harm).
   __device__ __forceinline__ u32 sweep(u32 t) {
+    post(J_SWEEP, t, ncl);
+    u32 q[2];
+    sweep_slice(t, ncl, q);
+    const u32 pf = q[0], hm = q[1];
+    tadd(TW_PREDFAIL, pf);
+    tadd(TW_HARM, hm);
+    recompute_marked(MK_SWEEP);
+    return (pf ? (u32)RKC_FL_PRED_FAIL : 0u) | (hm ? (u32)RKC_FL_HARM : 0u);
+  }
+  // this wave's share of the sweep (q: predicate failures, harms; combined on wave 0)
+  __device__ __forceinline__ void sweep_slice(u32 t, u32 ncl, u32 (&q)[2]) {
     u32 pf = 0, hm = 0;
-    for (u32 i = lane; i < ncl; i += 64) {
+    for (u32 i = first(); i < ncl; i += kSpan) {
       const u32 c = cla(CL_C)[i];
       if (!(mk[c] & MK_SWEEP)) continue;
       u32 m = cla(CL_META)[i];
@@ -609,12 +685,9 @@ struct Pool {
       cla(CL_META)[i] = m;
     }
     lists_fence();
-    pf = wave_sum(pf);
-    hm = wave_sum(hm);
-    tadd(TW_PREDFAIL, pf);
-    tadd(TW_HARM, hm);
-    recompute_marked(MK_SWEEP);
-    return (pf ? (u32)RKC_FL_PRED_FAIL : 0u) | (hm ? (u32)RKC_FL_HARM : 0u);
+    q[0] = wave_sum(pf);
+    q[1] = wave_sum(hm);
+    exchange(q, 0u, 0u);
   }
 
   // Refusal record of an active event that cannot be served (§3.4; §5.4 refusal record).
@@ -628,21 +701,11 @@ struct Pool {
     const i64 req = (i64)A + Hc + need;
     if (Pr > 0 && req <= U) {
       code = RKC_OC_REFUSED_CLAIM;
-      u32 mn = NIL, cnt = 0;
-      for (u32 i = lane; i < ncl; i += 64) {
-        const u32 m = cla(CL_META)[i];
-        if (m_state(m) != ST_MATERIALIZED || m_eff(m) != RKC_PROT_HARD) continue;
-        const u32 c = cla(CL_C)[i];
-        u32 cov = ch[c * CF_WORDS + CF_HOLD];
-        if ((i32)c == hc) cov = max(cov, h);
-        if (cla(CL_L)[i] <= cov) continue;
-        cla(CL_BLK)[i] += 1;
-        cnt++;
-        mn = min(mn, (u32)cla(CL_ID)[i]);
-      }
-      lists_fence();
-      id = (i32)wave_min(mn);
-      n16 = min(wave_sum(cnt), 65535u);
+      post(J_ATTRIB, (u32)hc, h, ncl);
+      u32 q[2];
+      attrib_slice(hc, h, ncl, q);
+      id = (i32)q[0];
+      n16 = min(q[1], 65535u);
     } else {
       code = RKC_OC_REFUSED_CAPACITY;
       id = -1;
@@ -650,6 +713,28 @@ struct Pool {
     }
     a = Pr;
     b = (i32)req;
+  }
+
+  // This wave's share of the attribution of a refusal (§5.4 blocking_claim_ids): every
+  // materialized hard claim reaching a cached position outside the hits (h leading positions of
+  // chain hc) counts it; q = smallest blocking id, number of blocking claims (combined on wave 0).
+  __device__ __forceinline__ void attrib_slice(i32 hc, u32 h, u32 ncl, u32 (&q)[2]) {
+    u32 mn = NIL, cnt = 0;
+    for (u32 i = first(); i < ncl; i += kSpan) {
+      const u32 m = cla(CL_META)[i];
+      if (m_state(m) != ST_MATERIALIZED || m_eff(m) != RKC_PROT_HARD) continue;
+      const u32 c = cla(CL_C)[i];
+      u32 cov = ch[c * CF_WORDS + CF_HOLD];
+      if ((i32)c == hc) cov = max(cov, h);
+      if (cla(CL_L)[i] <= cov) continue;
+      cla(CL_BLK)[i] += 1;
+      cnt++;
+      mn = min(mn, (u32)cla(CL_ID)[i]);
+    }
+    lists_fence();
+    q[0] = wave_min(mn);
+    q[1] = wave_sum(cnt);
+    exchange(q, 0u, 1u);
   }
 
   // Claim records: a rejected claim's words 0..8 are written at birth (lane k writes word k); a
@@ -768,9 +853,138 @@ struct Pool {
     lists_fence();
   }
 
+  // Workgroup version of the list moves (NW > 1): entries [src, src + len) of every array move to
+  // [dst, dst + len), in rounds of KU chunks of 64 entries per wave; each round loads its share,
+  // passes a workgroup barrier and only then stores, and the rounds run away from the destination
+  // (ascending when moving down, descending when moving up), so no store of a round lands on an
+  // entry a later round still has to load.
+  template <u32 NARR, u32 KU>
+  __device__ __forceinline__ void move_slice(lword* base0, u32 cap, u32 src, u32 dst, u32 len) {
+    constexpr u32 S = kSpan * KU;
+    const bool down = dst < src;
+    const u32 rounds = (len + S - 1) / S;
+    for (u32 r = 0; r < rounds; r++) {
+      const u32 r0 = down ? r * S : (len > (r + 1) * S ? len - (r + 1) * S : 0u);
+      const u32 r1 = down ? min(len, r0 + S) : len - r * S;
+      u32 v[KU][NARR];
+#pragma unroll
+      for (u32 u = 0; u < KU; u++) {
+        const u32 j = r0 + (wave * KU + u) * 64u + lane;
+#pragma unroll
+        for (u32 k = 0; k < NARR; k++) v[u][k] = j < r1 ? (u32)base0[k * cap + src + j] : 0u;
+      }
+      __syncthreads();
+#pragma unroll
+      for (u32 u = 0; u < KU; u++) {
+        const u32 j = r0 + (wave * KU + u) * 64u + lane;
+        if (j < r1) {
+#pragma unroll
+          for (u32 k = 0; k < NARR; k++) base0[k * cap + dst + j] = (lword)v[u][k];
+        }
+      }
+    }
+    __syncthreads();
+  }
+  // list 0: the live requests (indices relative to the arrays' start), 1: the live claims
+  __device__ __forceinline__ void list_move(u32 list, u32 src, u32 dst, u32 len) {
+    post(J_MOVE, list, src, dst, len);
+    move_any(list, src, dst, len);
+  }
+  __device__ __forceinline__ void move_any(u32 list, u32 src, u32 dst, u32 len) {
+    if (list == 0) move_slice<RQ_ARRAYS, 4>(rq, rq_cap, src, dst, len);
+    else move_slice<CL_ARRAYS, 2>(cl, cl_cap, src, dst, len);
+  }
+
+  // This wave's share of the hold rescan of chain c over the n live requests: the largest R on
+  // the chain and how many requests hold it (wave 0 receives the combination).
+  __device__ __forceinline__ void hold_slice(u32 c, u32 n, u32& hm, u32& hk) {
+    constexpr u32 KU = kGL ? 2 : 1;
+    u32 m = 0, k = 0;
+    for (u32 base = wave * 64u * KU; base < n; base += kSpan * KU) {
+      u32 cc[KU], rr[KU];
+#pragma unroll
+      for (u32 u = 0; u < KU; u++) {
+        const u32 j = base + 64 * u + lane;
+        cc[u] = j < n ? (u32)rqa(RQ_C)[j] : kListNil;
+        rr[u] = j < n ? (u32)rqa(RQ_R)[j] : 0u;
+      }
+#pragma unroll
+      for (u32 u = 0; u < KU; u++) {
+        if (cc[u] == c && rr[u] >= m) {
+          k = rr[u] > m ? 1u : k + 1u;
+          m = rr[u];
+        }
+      }
+    }
+    u32 q[2];
+    q[0] = wave_max(m);
+    q[1] = wave_sum(m == q[0] ? k : 0u);
+    hm = q[0];
+    hk = q[1];
+    if (NW > 1) {
+      if (lane < 2) jb[JB_ARGS + 8 * wave + lane] = lane == 0 ? q[0] : q[1];
+      __syncthreads();
+      if (wave == 0) {
+        hm = 0;
+        for (u32 w = 0; w < (u32)NW; w++) hm = max(hm, ufl(jb[JB_ARGS + 8 * w]));
+        hk = 0;
+        for (u32 w = 0; w < (u32)NW; w++)
+          hk += ufl(jb[JB_ARGS + 8 * w]) == hm ? ufl(jb[JB_ARGS + 8 * w + 1]) : 0u;
+      }
+    }
+  }
+
+  // Waves 1..NW-1: run the jobs wave 0 posts until it posts J_EXIT.
+  __device__ __forceinline__ void serve() {
+    for (;;) {
+      __syncthreads();
+      const u32 job = ufl(jb[0]);
+      if (job == J_EXIT) break;
+      if (job == J_MAXIMA) {
+        u32 q[8];
+        maxima_slice(arg(0), arg(1), q);
+      } else if (job == J_EXPIRE) {
+        u32 q[4];
+        expire_slice(arg(0), arg(1), q);
+      } else if (job == J_SWEEP) {
+        u32 q[2];
+        sweep_slice(arg(0), arg(1), q);
+      } else if (job == J_ATTRIB) {
+        u32 q[2];
+        attrib_slice((i32)arg(0), arg(1), arg(2), q);
+      } else if (job == J_HOLD) {
+        rq_head = arg(2);
+        u32 hm, hk;
+        hold_slice(arg(0), arg(1), hm, hk);
+      } else {
+        move_any(arg(0), arg(1), arg(2), arg(3));
+      }
+    }
+  }
+
   __device__ __forceinline__ void expire(u32 t, u32& flags, u32& expired) {
+    post(J_EXPIRE, t, ncl);
+    u32 q[4];
+    expire_slice(t, ncl, q);
+    const u32 cnt = q[0], pf = q[3];
+    t2used -= q[2];
+    if (pf) {
+      flags |= RKC_FL_PRED_FAIL;
+      tadd(TW_PREDFAIL, pf);
+    }
+    next_exp = q[1];
+    if (cnt) {
+      recompute_marked(MK_RECOMP);
+      flags |= RKC_FL_EXPIRED;
+      tadd(TW_EXPIRED, cnt);
+    }
+    expired = cnt;
+  }
+  // This wave's share of the expiry at the start of step t (q: claims expired, next expiry step,
+  // second-tier blocks dropped, predicate failures; combined on wave 0).
+  __device__ __forceinline__ void expire_slice(u32 t, u32 ncl, u32 (&q)[4]) {
     u32 cnt = 0, nx = EXP_NEVER, drop = 0, pf = 0;
-    for (u32 i = lane; i < ncl; i += 64) {
+    for (u32 i = first(); i < ncl; i += kSpan) {
       const u32 m = cla(CL_META)[i], st = m_state(m), dur = cla(CL_EXP)[i];
       if ((st != ST_MATERIALIZED && st != ST_DEMOTED) || dur == 0) continue;
       const u32 ex = (u32)cla(CL_ID)[i] + dur;
@@ -791,28 +1005,19 @@ struct Pool {
         }
         cla(CL_META)[i] = m_with_state(m2, ST_EXPIRED);
         rec[(u32)cla(CL_SLOT)[i]].w[RW_EXST] = (i32)t;
-        mk[cla(CL_C)[i]] |= MK_RECOMP;
+        mark_or(cla(CL_C)[i], MK_RECOMP);
         cnt++;
       } else {
         nx = min(nx, ex);
       }
     }
     lists_fence();
-    cnt = wave_sum(cnt);
-    t2used -= wave_sum(drop);
-    pf = wave_sum(pf);
-    if (pf) {
-      flags |= RKC_FL_PRED_FAIL;
-      tadd(TW_PREDFAIL, pf);
-    }
-    next_exp = wave_min(nx);
-    if (cnt) {
-      __builtin_amdgcn_wave_barrier();
-      recompute_marked(MK_RECOMP);
-      flags |= RKC_FL_EXPIRED;
-      tadd(TW_EXPIRED, cnt);
-    }
-    expired = cnt;
+    q[0] = wave_sum(cnt);
+    q[1] = wave_min(nx);
+    q[2] = wave_sum(drop);
+    q[3] = wave_sum(pf);
+    __builtin_amdgcn_wave_barrier();
+    exchange(q, 0u, 2u);
   }
 
   __device__ __forceinline__ void count_victims(const AllocRes& r, u32 hits) {
@@ -1068,7 +1273,8 @@ struct Pool {
         // the live list stays in id order: a retried request goes before the later ids
         if (kGL && rq_head + nreq >= rq_cap) {
           // no room above the list: move it back to the start of its arrays
-          list_compact<RQ_ARRAYS, 8>(rq, rq_cap, nreq, rq_head);
+          if (NW > 1) list_move(0, rq_head, 0, nreq);
+          else list_compact<RQ_ARRAYS, 8>(rq, rq_cap, nreq, rq_head);
           rq_head = 0;
         }
         u32 k = nreq;
@@ -1076,7 +1282,8 @@ struct Pool {
           u32 below = 0;
           for (u32 j = lane; j < nreq; j += 64) below += (u32)((u32)rqa(RQ_ID)[j] < rid);
           k = wave_sum(below);
-          list_open<RQ_ARRAYS, kGL ? 8 : 1>(rqa(0), rq_cap, nreq, k);
+          if (NW > 1) list_move(0, rq_head + k, rq_head + k + 1, nreq - k);
+          else list_open<RQ_ARRAYS, kGL ? 8 : 1>(rqa(0), rq_cap, nreq, k);
           dq_head = dq_head + 1 == (u32)max_reqs ? 0u : dq_head + 1;
           dq_len--;
           dq_cnt = 1;
@@ -1157,8 +1364,11 @@ struct Pool {
         const u32 len = ufl(rqa(RQ_LEN)[i]);
         if (kGL && 2 * i + 1 < nreq) {
           // fewer entries below the gap than above it: move those up one place
-          list_open<RQ_ARRAYS, 8>(rqa(0), rq_cap, i, 0);
+          if (NW > 1) list_move(0, rq_head, rq_head + 1, i);
+          else list_open<RQ_ARRAYS, 8>(rqa(0), rq_cap, i, 0);
           rq_head++;
+        } else if (NW > 1) {
+          list_move(0, rq_head + i + 1, rq_head + i, nreq - i - 1);
         } else {
           list_remove<RQ_ARRAYS, kGL ? 8 : 1>(rqa(0), rq_cap, nreq, i);
         }
@@ -1174,28 +1384,35 @@ struct Pool {
             if (hk > 1) {
               cs(c, CF_HCNT, hk - 1);
             } else {
-              // scan the live list (in global scratch: 8 chunks per round, their loads in flight
-              // together) for the largest R on the chain and how many requests hold it
-              constexpr u32 KU = kGL ? 8 : 1;
-              u32 m = 0, k = 0;
-              for (u32 base = 0; base < nreq; base += 64 * KU) {
-                u32 cc[KU], rr[KU];
+              // scan the live list for the largest R on the chain and how many requests hold it
+              if (NW > 1) {
+                post(J_HOLD, c, nreq, rq_head);
+                u32 hk2;
+                hold_slice(c, nreq, hn, hk2);
+                cs(c, CF_HCNT, hk2);
+              } else {
+                // (in global scratch: 8 chunks per round, their loads in flight together)
+                constexpr u32 KU = kGL ? 8 : 1;
+                u32 m = 0, k = 0;
+                for (u32 base = 0; base < nreq; base += 64 * KU) {
+                  u32 cc[KU], rr[KU];
 #pragma unroll
-                for (u32 u = 0; u < KU; u++) {
-                  const u32 j = base + 64 * u + lane;
-                  cc[u] = j < nreq ? (u32)rqa(RQ_C)[j] : kListNil;
-                  rr[u] = j < nreq ? (u32)rqa(RQ_R)[j] : 0u;
-                }
+                  for (u32 u = 0; u < KU; u++) {
+                    const u32 j = base + 64 * u + lane;
+                    cc[u] = j < nreq ? (u32)rqa(RQ_C)[j] : kListNil;
+                    rr[u] = j < nreq ? (u32)rqa(RQ_R)[j] : 0u;
+                  }
 #pragma unroll
-                for (u32 u = 0; u < KU; u++) {
-                  if (cc[u] == c && rr[u] >= m) {
-                    k = rr[u] > m ? 1u : k + 1u;
-                    m = rr[u];
+                  for (u32 u = 0; u < KU; u++) {
+                    if (cc[u] == c && rr[u] >= m) {
+                      k = rr[u] > m ? 1u : k + 1u;
+                      m = rr[u];
+                    }
                   }
                 }
+                hn = wave_max(m);
+                cs(c, CF_HCNT, wave_sum(m == hn ? k : 0u));
               }
-              hn = wave_max(m);
-              cs(c, CF_HCNT, wave_sum(m == hn ? k : 0u));
             }
           }
           turned += max(0, (i32)R - (i32)hn);
@@ -1258,7 +1475,8 @@ struct Pool {
             write_live_record(i, ST_RELEASED, (i32)t);
             if (m_eff(ufl(cla(CL_META)[i])) == RKC_PROT_OFFLOADED) t2used -= L;  // the copy is dropped
             __builtin_amdgcn_wave_barrier();
-            list_remove<CL_ARRAYS, kGL ? 4 : 1>(cl, cl_cap, ncl, i);
+            if (NW > 1) list_move(1, i + 1, i, ncl - i - 1);
+            else list_remove<CL_ARRAYS, kGL ? 4 : 1>(cl, cl_cap, ncl, i);
             ncl--;
             code = RKC_OC_RELEASED;
             tadd(TW_RELEASED, 1);
@@ -1308,14 +1526,15 @@ struct Pool {
   }
 };
 
-template <typename W, bool kGL>
-__global__ __launch_bounds__(64) void rkc_replay_wave(Args g) {
+template <typename W, bool kGL, int NW>
+__global__ __launch_bounds__(64 * NW) void rkc_replay_wave(Args g) {
   extern __shared__ __align__(16) unsigned char lds_raw[];
   const u32 pool = blockIdx.x;
   if ((i32)pool >= g.n_pools) return;
   const Layout& L = g.L;
-  Pool<W, kGL> P;
+  Pool<W, kGL, NW> P;
   P.lane = lane_id();
+  P.wave = NW > 1 ? (u32)__builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6)) : 0u;
   const rkc_pool_desc d = g.pools[pool];
   P.U = d.usable_blocks; P.mode = d.mode & ~RKC_MODE_RELAX; P.n_events = d.n_events; P.n_chains = d.n_chains;
   P.relax_on = (d.mode & RKC_MODE_RELAX) != 0;
@@ -1334,24 +1553,28 @@ __global__ __launch_bounds__(64) void rkc_replay_wave(Args g) {
                   d.defer_limit >= 0 && d.offload_blocks >= 0 && d.reserved[0] == 0 &&
                   d.reserved[1] == 0 && d.reserved[2] == 0;
   if (!ok) {
-    if (ev_ok)
-      for (i32 i = (i32)P.lane; i < P.n_events; i += 64)
-        g.outcomes[ev_off + i] = rkc_outcome{{RKC_OC_INVALID, -1, 0, 0}};
-    if (sl_ok)
-      for (i32 i = (i32)P.lane; i < P.n_slots; i += 64)
-        g.claim_tel[slot_off + i] = rkc_claim_telemetry{{-1, 0, -1, -1, -1, -1, -1, -1, 0, 0}};
-    ptel->w[P.lane] = P.lane == 31 ? RKC_PS_DESCRIPTOR : (P.lane == RKC_OC_INVALID && ev_ok) ? P.n_events : 0;
+    // (every wave of the workgroup returns here; wave 0 writes)
+    if (P.wave == 0) {
+      if (ev_ok)
+        for (i32 i = (i32)P.lane; i < P.n_events; i += 64)
+          g.outcomes[ev_off + i] = rkc_outcome{{RKC_OC_INVALID, -1, 0, 0}};
+      if (sl_ok)
+        for (i32 i = (i32)P.lane; i < P.n_slots; i += 64)
+          g.claim_tel[slot_off + i] = rkc_claim_telemetry{{-1, 0, -1, -1, -1, -1, -1, -1, 0, 0}};
+      ptel->w[P.lane] = P.lane == 31 ? RKC_PS_DESCRIPTOR : (P.lane == RKC_OC_INVALID && ev_ok) ? P.n_events : 0;
+    }
     return;
   }
 
   // memory carve-up
-  typedef typename Pool<W, kGL>::lword lword;
-  typedef typename Pool<W, kGL>::lds_w lds_w;
-  typedef typename Pool<W, kGL>::lds_w4 lds_w4;
+  typedef typename Pool<W, kGL, NW>::lword lword;
+  typedef typename Pool<W, kGL, NW>::lds_w lds_w;
+  typedef typename Pool<W, kGL, NW>::lds_w4 lds_w4;
   lds_u32* lds = (lds_u32*)lds_raw;
   P.ch = (lds_w*)(lds + L.off_chain / 4);
   P.mk = lds + L.off_mark / 4;
   P.tk = lds + L.off_key / 4;
+  P.jb = lds + L.off_job / 4;
   unsigned char* scr = g.scratch + (u64)pool * L.scr_pool_bytes;
   if (kGL) {
     P.rq = (lword*)(scr + L.scr_off_rq);
@@ -1373,7 +1596,7 @@ __global__ __launch_bounds__(64) void rkc_replay_wave(Args g) {
   P.defer_limit = d.defer_limit;
   P.rec = g.claim_tel + slot_off;
 
-  for (i32 c = (i32)P.lane; c < P.n_chains; c += 64) {
+  for (i32 c = (i32)P.first(); c < P.n_chains; c += (i32)P.kSpan) {
     P.cgs((u32)c, 0, make_uint4(0, 0, 0, 0));
     P.cgs((u32)c, 1, make_uint4(0, 0, 0, 0));
     P.cgs((u32)c, 2, make_uint4(0, 0, 0, 0));
@@ -1390,6 +1613,10 @@ __global__ __launch_bounds__(64) void rkc_replay_wave(Args g) {
   P.status = 0;
   P.dq_head = 0; P.dq_len = 0; P.dq_cnt = 1;
   __syncthreads();
+  if (NW > 1 && P.wave != 0) {
+    P.serve();
+    return;
+  }
 
   const rkc_event* ev = g.events + ev_off;
   rkc_outcome* out = g.outcomes + ev_off;
@@ -1408,6 +1635,7 @@ __global__ __launch_bounds__(64) void rkc_replay_wave(Args g) {
     }
     if ((i32)P.lane < cnt) out[base + P.lane] = rkc_outcome{{mine.x, mine.y, mine.z, mine.w}};
   }
+  P.post(J_EXIT);  // the other waves leave
 
   // Final claim records of the claims still live ...
   for (u32 i = 0; i < P.ncl; i++) P.write_live_record(i, m_state(ufl((u32)P.cla(CL_META)[i])), -1);
@@ -1458,6 +1686,9 @@ bool make_layout(const rkc_batch* b, Layout* L, bool narrow, bool global_lists) 
   memset(L, 0, sizeof *L);
   L->narrow = narrow;
   L->global_lists = global_lists;
+  // Batches of at most one pool per CU whose lists live in global scratch get a workgroup of
+  // several waves per pool: the other waves share the scans of the long lists.
+  L->waves = (global_lists && b->n_pools <= (i32)kCUs && !(b->flags & RKC_FLAG_ONE_WAVE_PER_POOL)) ? kGroupWaves : 1;
   const u64 ws = narrow ? 2 : 4;
   L->chains = (u32)(b->max_chains > 0 ? b->max_chains : 1);
   L->reqs = (u32)(b->max_live_requests > 0 ? b->max_live_requests : 1);
@@ -1471,6 +1702,7 @@ bool make_layout(const rkc_batch* b, Layout* L, bool narrow, bool global_lists) 
   L->off_chain = take(ws * CF_WORDS * C, 16);
   L->off_key = take(4 * (C > kRegChains ? C : 1), 16);
   L->off_mark = take(4 * C, 16);
+  L->off_job = take(L->waves > 1 ? 4ull * (JB_ARGS + 8 * L->waves) : 0, 16);
   if (!global_lists) {
     L->off_rq = take(ws * RQ_ARRAYS * L->reqs, 16);
     L->off_cl = take(ws * CL_ARRAYS * L->claims, 16);
@@ -1513,7 +1745,8 @@ rkc_status check_batch(const rkc_batch* b) {
   if (!b) return RKC_E_NULL;
   if (b->n_pools < 0 || b->max_usable_blocks < 0 || b->max_events < 0 || b->max_chains < 0 ||
       b->max_live_requests < 0 || b->max_live_claims < 0 || b->max_claim_slots < 0 ||
-      b->n_events_total < 0 || b->n_claim_slots_total < 0 || (b->flags & ~RKC_FLAG_GENERAL_KERNEL) != 0)
+      b->n_events_total < 0 || b->n_claim_slots_total < 0 ||
+      (b->flags & ~(RKC_FLAG_GENERAL_KERNEL | RKC_FLAG_ONE_WAVE_PER_POOL)) != 0)
     return RKC_E_RANGE;
   if (b->max_usable_blocks > RKC_MAX_USABLE_BLOCKS || b->max_events > RKC_MAX_EVENTS_PER_POOL)
     return RKC_E_UNSUPPORTED;
@@ -1527,13 +1760,13 @@ rkc_status check_batch(const rkc_batch* b) {
   return RKC_OK;
 }
 
-template <typename W, bool kGL>
+template <typename W, bool kGL, int NW>
 rkc_status launch(const Args& g, unsigned n_pools, hipStream_t s) {
-  const void* fn = (const void*)rkc_replay_wave<W, kGL>;
+  const void* fn = (const void*)rkc_replay_wave<W, kGL, NW>;
   if (g.L.lds_bytes > 64 * 1024 &&
       hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)g.L.lds_bytes) != hipSuccess)
     return RKC_E_HIP;
-  hipLaunchKernelGGL((rkc_replay_wave<W, kGL>), dim3(n_pools), dim3(64), g.L.lds_bytes, s, g);
+  hipLaunchKernelGGL((rkc_replay_wave<W, kGL, NW>), dim3(n_pools), dim3(64 * NW), g.L.lds_bytes, s, g);
   return hipGetLastError() == hipSuccess ? RKC_OK : RKC_E_HIP;
 }
 
@@ -1586,9 +1819,11 @@ static rkc_status replay(const rkc_batch* b, void* s) {
   g.n_pools = b->n_pools; g.max_usable = b->max_usable_blocks; g.max_events = b->max_events;
   g.max_chains = b->max_chains; g.max_reqs = b->max_live_requests; g.max_claims = b->max_live_claims;
   g.max_slots = b->max_claim_slots;
-  if (g.L.narrow) return launch<uint16_t, false>(g, (unsigned)b->n_pools, (hipStream_t)s);
-  if (g.L.global_lists) return launch<u32, true>(g, (unsigned)b->n_pools, (hipStream_t)s);
-  return launch<u32, false>(g, (unsigned)b->n_pools, (hipStream_t)s);
+  if (g.L.narrow) return launch<uint16_t, false, 1>(g, (unsigned)b->n_pools, (hipStream_t)s);
+  if (g.L.global_lists && g.L.waves > 1)
+    return launch<u32, true, kGroupWaves>(g, (unsigned)b->n_pools, (hipStream_t)s);
+  if (g.L.global_lists) return launch<u32, true, 1>(g, (unsigned)b->n_pools, (hipStream_t)s);
+  return launch<u32, false, 1>(g, (unsigned)b->n_pools, (hipStream_t)s);
 }
 
 rkc_status rkc_replay_batch(const rkc_batch* b, void* s) { return replay(b, s); }

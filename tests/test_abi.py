@@ -105,7 +105,7 @@ def test_host_argument_checks(lib):
     assert lib.rkc_replay_batch(ctypes.byref(_batch(d_outcomes=0x30008)), None) == -2
     assert lib.rkc_replay_batch(ctypes.byref(_batch(d_scratch=0x60010)), None) == -2
     assert lib.rkc_replay_batch(ctypes.byref(_batch(n_pools=-1)), None) == -3
-    assert lib.rkc_replay_batch(ctypes.byref(_batch(flags=2)), None) == -3
+    assert lib.rkc_replay_batch(ctypes.byref(_batch(flags=4)), None) == -3
     assert lib.rkc_replay_batch(ctypes.byref(_batch(max_usable_blocks=(1 << 22) + 1)), None) == -4
     # scratch too small (the batch needs > 0 bytes)
     b = _batch()
