@@ -18,7 +18,7 @@ struct rkc_lean_args {
   int64_t n_events_total, n_slots_total;
   int32_t n_pools, max_usable, max_events, max_chains, max_reqs, max_claims, max_slots;
   // layout: LDS byte offsets, node split, per-pool scratch regions
-  uint32_t ns, node_cap, nodes_lds;
+  uint32_t ns, nq, node_cap, nodes_lds;  // 64-chain key groups, 64-claim sets, node split
   uint32_t off_keys, off_hist, off_cold, off_chains, off_reqs, off_nodes, lds_bytes;
   uint64_t scr_pool_bytes, scr_off_nodes, scr_off_fifo, scr_off_slots, scr_off_defer;
   // after the per-pool regions: the launch order (one u32 pool index per workgroup), each pool's
@@ -27,7 +27,8 @@ struct rkc_lean_args {
 };
 
 // Fill the layout part of g for batch b; false when b is outside the compact kernel's limits
-// (usable blocks <= 32,767, events <= 65,533, chains <= 256, live claims <= 64, live requests <= 256).
+// (usable blocks <= 32,767, events <= 65,533, live requests <= 256, and live claims <= 64 with
+// chains <= 256 or live claims <= 256 with chains <= 64).
 bool rkc_lean_layout(const rkc_batch* b, rkc_lean_args* g);
 
 // Launch the compact kernel (one 64-lane workgroup per pool) on stream s.

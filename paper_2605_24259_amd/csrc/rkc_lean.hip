@@ -142,10 +142,11 @@ struct AllocRes {
 };
 
 // ---- one pool ---------------------------------------------------------------------------------
-// NS: 64-key groups (chains <= 64 NS); MODE: the pool policy, fixed at compile time so that each
-// policy's event loop carries only the logic that policy can reach; EXT: a hard-protection pool that
-// defers or relaxes, whose loop carries the deferral ring and the runtime relaxation.
-template <int NS, int MODE, bool EXT>
+// NS: 64-key groups (chains <= 64 NS); NQ: 64-claim sets (live claims <= 64 NQ; claim j sits in lane
+// j mod 64 of set j / 64); MODE: the pool policy, fixed at compile time so that each policy's event
+// loop carries only the logic that policy can reach; EXT: a hard-protection pool that defers or
+// relaxes, whose loop carries the deferral ring and the runtime relaxation.
+template <int NS, int NQ, int MODE, bool EXT>
 struct Lean {
   static constexpr u32 KC = 64u * NS;  // key slots (chains padded to whole lanes)
   // descriptor: the rarely used limits one per lane of `cst`
@@ -187,13 +188,13 @@ struct Lean {
   // released claim's record is written by its own lane
   uint4* slotcl;
   rkc_claim_telemetry* rec;
-  // live claims, one per lane
-  u32 qa;  // id | chain
-  u32 qb;  // L | T
-  u32 qc;  // meta | slot
-  u32 qd;  // duration | blocked count
-  u32 qe;  // demote step | expire step
-  u32 qf;  // predicate-failure step | harm step
+  // live claims, one per lane of each set
+  u32 qa[NQ];  // id | chain
+  u32 qb[NQ];  // L | T
+  u32 qc[NQ];  // meta | slot
+  u32 qd[NQ];  // duration | blocked count
+  u32 qe[NQ];  // demote step | expire step
+  u32 qf[NQ];  // predicate-failure step | harm step
   u32 tv;  // pool telemetry word `lane`
   // scalars
   u32 F, A, PR, peak, Eall, fbl;
@@ -280,22 +281,30 @@ struct Lean {
   __device__ __forceinline__ static u32 protd(u32 hold, u32 prot) { return prot > hold ? prot - hold : 0u; }
 
   // -- what the claims on a chain imply, computed from the claim lanes when it matters --
-  // this lane's claim is live on chain c
-  __device__ __forceinline__ bool on_chain(u32 c) const { return lane < ncl && hi16(qa) == c; }
+  // this lane's claim of set q is live (claim index 64 q + lane below the live count)
+  __device__ __forceinline__ bool live(u32 q) const { return q * 64u + lane < ncl; }
+  // ... and on chain c
+  __device__ __forceinline__ bool on_chain(u32 c, u32 q) const { return live(q) && hi16(qa[q]) == c; }
   // ... and ranks victims at soft level prio + 1 (accepted soft or lowered claims still
   // materialized, and demoted claims; §3.1 soft priority, demotion to soft)
-  __device__ __forceinline__ bool leveled(u32 c) const {
-    const u32 m = lo16(qc), st = m_state(m);
-    return on_chain(c) && ((st == ST_MATERIALIZED && m_eff(m) == RKC_PROT_SOFT) || st == ST_DEMOTED);
+  __device__ __forceinline__ bool leveled(u32 c, u32 q) const {
+    const u32 m = lo16(qc[q]), st = m_state(m);
+    return on_chain(c, q) && ((st == ST_MATERIALIZED && m_eff(m) == RKC_PROT_SOFT) || st == ST_DEMOTED);
   }
   // soft level of position p of chain c
   __device__ __forceinline__ u32 level_of(u32 c, u32 p) const {
-    return wmax(leveled(c) && lo16(qb) > p ? m_prio(lo16(qc)) + 1u : 0u);
+    u32 v = 0;
+#pragma unroll
+    for (u32 q = 0; q < NQ; q++) v = max(v, leveled(c, q) && lo16(qb[q]) > p ? m_prio(lo16(qc[q])) + 1u : 0u);
+    return wmax(v);
   }
   // positions at or above the result have a level <= lvl: the largest footprint of the claims
   // ranking above lvl (they all end at or below the position where level lvl starts)
   __device__ __forceinline__ u32 level_floor(u32 c, u32 lvl) const {
-    return wmax(leveled(c) && m_prio(lo16(qc)) + 1u > lvl ? lo16(qb) : 0u);
+    u32 v = 0;
+#pragma unroll
+    for (u32 q = 0; q < NQ; q++) v = max(v, leveled(c, q) && m_prio(lo16(qc[q])) + 1u > lvl ? lo16(qb[q]) : 0u);
+    return wmax(v);
   }
 
   // Key of chain c's top run; advances a stale stack bottom (the node above it reaches n).
@@ -382,63 +391,79 @@ struct Lean {
   // After a lifecycle change of claims on chain c: the extent of its live claims, its hard
   // protection extent (hard-protection pools), and its key (soft levels may have changed).
   __device__ __forceinline__ void recompute(u32 c) {
-    const u32 L = lo16(qb), m = lo16(qc);
-    const bool on = on_chain(c);
-    const u32 pp = wmax((on && hardm() && m_state(m) == ST_MATERIALIZED && m_eff(m) == RKC_PROT_HARD) ? L : 0u);
+    u32 pv = 0, cv = 0;
+#pragma unroll
+    for (u32 q = 0; q < NQ; q++) {
+      const u32 L = lo16(qb[q]), m = lo16(qc[q]);
+      const bool on = on_chain(c, q);
+      pv = max(pv, (on && hardm() && m_state(m) == ST_MATERIALIZED && m_eff(m) == RKC_PROT_HARD) ? L : 0u);
+      cv = max(cv, on && m_eff(m) != RKC_PROT_OFFLOADED ? L : 0u);
+    }
+    const u32 pp = wmax(pv);
     G0 g = rd0(c);
-    g.covA = wmax(on && m_eff(m) != RKC_PROT_OFFLOADED ? L : 0u);
+    g.covA = wmax(cv);
     commit(c, g, g.n, g.hold, pp, 0, 0);
   }
-  // recompute every chain named by a claim lane in `mask`
-  __device__ __forceinline__ void recompute_lanes(u64 mask) {
-    const u32 cl = hi16(qa);
-    for (u32 guard = 0; mask && guard < 64; guard++) {
-      const u32 l = (u32)__builtin_ctzll(mask);
-      const u32 c = rdl(cl, l);
-      recompute(c);
-      mask &= ~ballot(cl == c);
+  // recompute every chain named by a claim lane in `mask` (one lane mask per claim set)
+  __device__ __forceinline__ void recompute_lanes(u64 (&mask)[NQ]) {
+#pragma unroll
+    for (u32 q = 0; q < NQ; q++) {
+      for (u32 guard = 0; mask[q] && guard < 64; guard++) {
+        const u32 l = (u32)__builtin_ctzll(mask[q]);
+        const u32 c = rdl(hi16(qa[q]), l);
+        recompute(c);
+#pragma unroll
+        for (u32 q2 = q; q2 < NQ; q2++) mask[q2] &= ~ballot(hi16(qa[q2]) == c);
+      }
     }
   }
 
-  // Record of the live claim in this lane (the caller selects the lanes).
-  __device__ __forceinline__ void write_own_record(u32 state, i32 rel) {
-    const u32 id = lo16(qa), m = lo16(qc);
+  // Record of the live claim in this lane of set q (the caller selects the lanes).
+  __device__ __forceinline__ void write_own_record(u32 q, u32 state, i32 rel) {
+    const u32 id = lo16(qa[q]), m = lo16(qc[q]);
     const u32 mm = (m & ~7u) | state;
-    rkc_claim_telemetry* r = rec + hi16(qc);
+    rkc_claim_telemetry* r = rec + hi16(qc[q]);
     r->w[0] = (i32)id; r->w[1] = (i32)packed_of(mm); r->w[2] = (i32)id;
-    r->w[3] = st16(lo16(qe)); r->w[4] = st16(hi16(qe)); r->w[5] = rel;
-    r->w[6] = st16(lo16(qf)); r->w[7] = st16(hi16(qf)); r->w[8] = (i32)hi16(qd);
+    r->w[3] = st16(lo16(qe[q])); r->w[4] = st16(hi16(qe[q])); r->w[5] = rel;
+    r->w[6] = st16(lo16(qf[q])); r->w[7] = st16(hi16(qf[q])); r->w[8] = (i32)hi16(qd[q]);
   }
 
   // Expiry at the start of step t (claims materialized or demoted with a duration).
   __device__ __forceinline__ void expire(u32 t, u32& flags, u32& expired) {
-    const u32 m = lo16(qc), st = m_state(m), dur = lo16(qd);
-    const bool cand = lane < ncl && (st == ST_MATERIALIZED || st == ST_DEMOTED) && dur != 0;
-    const u32 ex = lo16(qa) + dur;
-    const bool hit = cand && ex <= t;
-    if (ext()) {
-      // responsibility ends: an offloaded claim's second-tier copy is dropped
-      const bool off = hit && m_eff(m) == RKC_PROT_OFFLOADED;
-      if (__builtin_expect(ballot(off) != 0, 0)) {
-        cold[C_T2] = ufl(cold[C_T2]) - wsum(off ? lo16(qb) : 0u);
-        // its predicate held only through the dropped copy: a chain already shorter than T fails
-        // it now (no harm: the claim is expired)
-        const bool fail = off && m_pend(m) && chain_n(hi16(qa)) < hi16(qb);
-        qc = off ? pk(m & ~(3u << 3) & ~(fail ? 1u << 8 : 0u), hi16(qc)) : qc;
-        qf = fail ? pk(t, hi16(qf)) : qf;
-        const u32 nf = (u32)__builtin_popcountll(ballot(fail));
-        if (nf) {
-          flags |= RKC_FL_PRED_FAIL;
-          tadd(TW_PREDFAIL, nf);
+    u64 hm[NQ];
+    u32 nx = NEVER;
+    expired = 0;
+#pragma unroll
+    for (u32 q = 0; q < NQ; q++) {
+      const u32 m = lo16(qc[q]), st = m_state(m), dur = lo16(qd[q]);
+      const bool cand = live(q) && (st == ST_MATERIALIZED || st == ST_DEMOTED) && dur != 0;
+      const u32 ex = lo16(qa[q]) + dur;
+      const bool hit = cand && ex <= t;
+      if (ext()) {
+        // responsibility ends: an offloaded claim's second-tier copy is dropped
+        const bool off = hit && m_eff(m) == RKC_PROT_OFFLOADED;
+        if (__builtin_expect(ballot(off) != 0, 0)) {
+          cold[C_T2] = ufl(cold[C_T2]) - wsum(off ? lo16(qb[q]) : 0u);
+          // its predicate held only through the dropped copy: a chain already shorter than T
+          // fails it now (no harm: the claim is expired)
+          const bool fail = off && m_pend(m) && chain_n(hi16(qa[q])) < hi16(qb[q]);
+          qc[q] = off ? pk(m & ~(3u << 3) & ~(fail ? 1u << 8 : 0u), hi16(qc[q])) : qc[q];
+          qf[q] = fail ? pk(t, hi16(qf[q])) : qf[q];
+          const u32 nf = (u32)__builtin_popcountll(ballot(fail));
+          if (nf) {
+            flags |= RKC_FL_PRED_FAIL;
+            tadd(TW_PREDFAIL, nf);
+          }
         }
       }
+      qc[q] = hit ? pk((lo16(qc[q]) & ~7u) | ST_EXPIRED, hi16(qc[q])) : qc[q];
+      qe[q] = hit ? pk(lo16(qe[q]), t) : qe[q];
+      hm[q] = ballot(hit);
+      nx = min(nx, cand && !hit ? ex : NEVER);
+      expired += (u32)__builtin_popcountll(hm[q]);
     }
-    qc = hit ? pk((lo16(qc) & ~7u) | ST_EXPIRED, hi16(qc)) : qc;
-    qe = hit ? pk(lo16(qe), t) : qe;
-    const u64 hm = ballot(hit);
-    nexp = wmin(cand && !hit ? ex : NEVER);
-    expired = (u32)__builtin_popcountll(hm);
-    if (__builtin_expect(hm != 0, 0)) {
+    nexp = wmin(nx);
+    if (__builtin_expect(expired != 0, 0)) {
       recompute_lanes(hm);
       flags |= RKC_FL_EXPIRED;
       tadd(TW_EXPIRED, expired);
@@ -448,17 +473,23 @@ struct Lean {
   // Predicate sweep after evictions: a claim whose chain now holds fewer than T leading blocks
   // fails for the first time; a materialized (accepted) claim is harmed (§3.2).
   __device__ __forceinline__ u32 sweep(u32 t) {
-    const u32 m = lo16(qc), T = hi16(qb), c = hi16(qa);
-    const u32 nc = chain_n(c);
-    const bool fail = lane < ncl && m_pend(m) && nc < T && m_eff(m) != RKC_PROT_OFFLOADED;
-    const bool harm = fail && m_state(m) == ST_MATERIALIZED;
-    const u32 m2 = (m & ~(1u << 8) & ~(harm ? 7u : 0u)) | (harm ? ST_HARMED : 0u);
-    qc = fail ? pk(m2, hi16(qc)) : qc;
-    qf = fail ? pk(t, harm ? t : hi16(qf)) : qf;
-    const u64 fm = ballot(fail), hmk = ballot(harm);
+    u64 fm[NQ];
+    u32 pf = 0, hc = 0;
+#pragma unroll
+    for (u32 q = 0; q < NQ; q++) {
+      const u32 m = lo16(qc[q]), T = hi16(qb[q]), c = hi16(qa[q]);
+      const u32 nc = chain_n(c);
+      const bool fail = live(q) && m_pend(m) && nc < T && m_eff(m) != RKC_PROT_OFFLOADED;
+      const bool harm = fail && m_state(m) == ST_MATERIALIZED;
+      const u32 m2 = (m & ~(1u << 8) & ~(harm ? 7u : 0u)) | (harm ? ST_HARMED : 0u);
+      qc[q] = fail ? pk(m2, hi16(qc[q])) : qc[q];
+      qf[q] = fail ? pk(t, harm ? t : hi16(qf[q])) : qf[q];
+      fm[q] = ballot(fail);
+      pf += (u32)__builtin_popcountll(fm[q]);
+      hc += (u32)__builtin_popcountll(ballot(harm));
+    }
     u32 fl = 0;
-    if (__builtin_expect(fm != 0, 0)) {
-      const u32 pf = (u32)__builtin_popcountll(fm), hc = (u32)__builtin_popcountll(hmk);
+    if (__builtin_expect(pf != 0, 0)) {
       tadd(TW_PREDFAIL, pf);
       tadd(TW_HARM, hc);
       recompute_lanes(fm);
@@ -538,14 +569,21 @@ struct Lean {
             u32 rs = 0, sc = 0;
             if (g.covA > nw) {
               // victims inside live claims: resident; inside only demoted / expired ones: post-release
-              const u32 st = m_state(lo16(qc));
-              const bool on = on_chain(c);
-              const bool off = m_eff(lo16(qc)) == RKC_PROT_OFFLOADED;
-              const u32 covS = wmax((on && !off && (st == ST_OBSERVED || st == ST_MATERIALIZED || st == ST_HARMED)) ? lo16(qb) : 0u);
+              u32 cv = 0;
+              bool due = false;
+#pragma unroll
+              for (u32 q = 0; q < NQ; q++) {
+                const u32 st = m_state(lo16(qc[q]));
+                const bool on = on_chain(c, q);
+                const bool off = m_eff(lo16(qc[q])) == RKC_PROT_OFFLOADED;
+                cv = max(cv, (on && !off && (st == ST_OBSERVED || st == ST_MATERIALIZED || st == ST_HARMED)) ? lo16(qb[q]) : 0u);
+                // a claim whose predicate still holds needs more than nw leading blocks
+                due = due || (on && !off && m_pend(lo16(qc[q])) && hi16(qb[q]) > nw);
+              }
+              const u32 covS = wmax(cv);
               rs = min(nn, g.covA) - nw;
               sc = min(nn, covS) > nw ? min(nn, covS) - nw : 0u;
-              // a claim whose predicate still holds needs more than nw leading blocks
-              if (ballot(on && !off && m_pend(lo16(qc)) && hi16(qb) > nw)) sweep_due = 1;
+              if (ballot(due)) sweep_due = 1;
             }
             r.victims += m;
             r.resident += rs;
@@ -582,15 +620,20 @@ struct Lean {
     const u64 req = (u64)A + Hc + need;
     if (Pr > 0 && req <= U()) {
       o.code = RKC_OC_REFUSED_CLAIM;
-      const u32 m = lo16(qc), c = hi16(qa);
-      u32 cov = chain_hold(c);
-      if ((i32)c == hc) cov = max(cov, h);
-      const bool blk = lane < ncl && m_state(m) == ST_MATERIALIZED && m_eff(m) == RKC_PROT_HARD &&
-                       lo16(qb) > cov;
-      qd += blk ? (1u << 16) : 0u;
-      const u64 bm = ballot(blk);
-      o.id = (i32)wmin(blk ? lo16(qa) : NEVER);
-      o.n16 = min((u32)__builtin_popcountll(bm), 65535u);
+      u32 mn = NEVER, nb = 0;
+#pragma unroll
+      for (u32 q = 0; q < NQ; q++) {
+        const u32 m = lo16(qc[q]), c = hi16(qa[q]);
+        u32 cov = chain_hold(c);
+        if ((i32)c == hc) cov = max(cov, h);
+        const bool blk = live(q) && m_state(m) == ST_MATERIALIZED && m_eff(m) == RKC_PROT_HARD &&
+                         lo16(qb[q]) > cov;
+        qd[q] += blk ? (1u << 16) : 0u;
+        nb += (u32)__builtin_popcountll(ballot(blk));
+        mn = min(mn, blk ? lo16(qa[q]) : NEVER);
+      }
+      o.id = (i32)wmin(mn);
+      o.n16 = min(nb, 65535u);
     } else {
       o.code = RKC_OC_REFUSED_CAPACITY;
       o.id = -1;
@@ -683,41 +726,72 @@ struct Lean {
       }
       u64 avail = (u64)F + E;
       if ((u64)need > avail) {
-        const u32 m = lo16(qc), c = hi16(qa), L = lo16(qb);
-        u32 cov = chain_hold(c);
-        if ((i32)c == hc) cov = max(cov, h);
-        const bool hm = lane < ncl && m_state(m) == ST_MATERIALIZED && m_eff(m) == RKC_PROT_HARD;
-        const u32 key = (m_prio(m) << 16) | lo16(qa);
-        u64 left = ballot(hm && (m & (M_DEMQ | M_OFFQ)) && L > cov);
-        u64 S = 0, O = 0;  // picked; picked for offload (the rest of S is demoted)
+        u32 m[NQ], c[NQ], L[NQ], key[NQ];
+        bool hm[NQ];
+        u64 left[NQ], S[NQ], O[NQ];  // candidates not visited; picked; picked for offload
+        u32 nleft = 0;
+#pragma unroll
+        for (u32 q = 0; q < NQ; q++) {
+          m[q] = lo16(qc[q]); c[q] = hi16(qa[q]); L[q] = lo16(qb[q]);
+          u32 cov = chain_hold(c[q]);
+          if ((i32)c[q] == hc) cov = max(cov, h);
+          hm[q] = live(q) && m_state(m[q]) == ST_MATERIALIZED && m_eff(m[q]) == RKC_PROT_HARD;
+          key[q] = (m_prio(m[q]) << 16) | lo16(qa[q]);
+          left[q] = ballot(hm[q] && (m[q] & (M_DEMQ | M_OFFQ)) && L[q] > cov);
+          S[q] = 0; O[q] = 0;
+          nleft += (u32)__builtin_popcountll(left[q]);
+        }
         u32 room = sub0(t2cap(), ufl(cold[C_T2])), moved = 0;
-        for (u32 guard = 0; left && (u64)need > avail && guard < 64; guard++) {
-          const bool mine = (left >> lane) & 1ull;
-          const u32 kmin = wmin(mine ? key : NEVER);
-          const u32 l = (u32)__builtin_ctzll(ballot(mine && key == kmin));
-          left &= ~(1ull << l);
-          const u32 ml = rdl(m, l), Ll = rdl(L, l);
+        for (u32 guard = 0; nleft > 0 && (u64)need > avail && guard < 64u * NQ; guard++) {
+          u32 kv = NEVER;
+#pragma unroll
+          for (u32 q = 0; q < NQ; q++) kv = min(kv, ((left[q] >> lane) & 1ull) ? key[q] : NEVER);
+          const u32 kmin = wmin(kv);
+          // the claim with the smallest (priority, id): set lq, lane l (keys are distinct)
+          u32 lq = 0, l = 0, ml = 0, Ll = 0, cq = 0;
+#pragma unroll
+          for (u32 q = 0; q < NQ; q++) {
+            const u64 b = ballot(((left[q] >> lane) & 1ull) && key[q] == kmin);
+            if (b) {
+              lq = q;
+              l = (u32)__builtin_ctzll(b);
+              ml = rdl(m[q], l); Ll = rdl(L[q], l); cq = rdl(c[q], l);
+              left[q] &= ~(1ull << l);
+            }
+          }
+          nleft--;
           const bool off = (ml & M_OFFQ) && Ll <= room;
           if (off || (ml & M_DEMQ)) {
-            if (off) { O |= 1ull << l; room -= Ll; moved += Ll; }
-            const u32 cq = rdl(c, l);
+            if (off) { room -= Ll; moved += Ll; }
             const G0 g = rd0(cq);
             const u32 base = (i32)cq == hc ? max(g.hold, h) : g.hold;
-            const bool on = hm && c == cq;
-            const u32 before = wmax(on && !((S >> lane) & 1ull) ? L : 0u);
-            S |= 1ull << l;
-            const u32 after = wmax(on && !((S >> lane) & 1ull) ? L : 0u);
+            u32 bv = 0, av = 0;
+#pragma unroll
+            for (u32 q = 0; q < NQ; q++) {
+              const bool on = hm[q] && c[q] == cq;
+              bv = max(bv, on && !((S[q] >> lane) & 1ull) ? L[q] : 0u);
+              if (q == lq) {
+                S[q] |= 1ull << l;
+                if (off) O[q] |= 1ull << l;
+              }
+              av = max(av, on && !((S[q] >> lane) & 1ull) ? L[q] : 0u);
+            }
+            const u32 before = wmax(bv), after = wmax(av);
             avail += evictable(g.n, base, after) - evictable(g.n, base, before);
           }
         }
         if ((u64)need <= avail) {
-          const bool o = (O >> lane) & 1ull, d = ((S & ~O) >> lane) & 1ull;
-          qc = d ? pk((m & ~7u) | ST_DEMOTED | M_RELAXED, hi16(qc)) : qc;
-          qc = o ? pk((m & ~(3u << 3)) | (RKC_PROT_OFFLOADED << 3) | M_RELAXED, hi16(qc)) : qc;
-          qe = d ? pk(t, hi16(qe)) : qe;
+          u32 no = 0;
+#pragma unroll
+          for (u32 q = 0; q < NQ; q++) {
+            const bool o = (O[q] >> lane) & 1ull, d = ((S[q] & ~O[q]) >> lane) & 1ull;
+            qc[q] = d ? pk((m[q] & ~7u) | ST_DEMOTED | M_RELAXED, hi16(qc[q])) : qc[q];
+            qc[q] = o ? pk((m[q] & ~(3u << 3)) | (RKC_PROT_OFFLOADED << 3) | M_RELAXED, hi16(qc[q])) : qc[q];
+            qe[q] = d ? pk(t, hi16(qe[q])) : qe[q];
+            k += (u32)__builtin_popcountll(S[q]);
+            no += (u32)__builtin_popcountll(O[q]);
+          }
           recompute_lanes(S);
-          k = (u32)__builtin_popcountll(S);
-          const u32 no = (u32)__builtin_popcountll(O);
           tadd(TW_RUNTIME_DEMOTED, k - no);
           if (no) {
             const u32 used = ufl(cold[C_T2]) + moved;
@@ -804,7 +878,11 @@ struct Lean {
       if (ext() && P > h && t2cap() > 0) {
         // positions past the hits that a claim holding a second-tier copy covers are restored
         // from the second tier (restore cost), still on new GPU blocks
-        const u32 e = wmax(on_chain(cc) && m_eff(lo16(qc)) == RKC_PROT_OFFLOADED ? lo16(qb) : 0u);
+        u32 ev = 0;
+#pragma unroll
+        for (u32 q = 0; q < NQ; q++)
+          ev = max(ev, on_chain(cc, q) && m_eff(lo16(qc[q])) == RKC_PROT_OFFLOADED ? lo16(qb[q]) : 0u);
+        const u32 e = wmax(ev);
         tadd(TW_RESTORED, sub0(min(P, e), h));
       }
     }
@@ -907,13 +985,18 @@ struct Lean {
           o.flags |= obs ? (u32)RKC_FL_SHADOW : lowered ? (u32)RKC_FL_LOWERED : 0u;
           const u32 m = st | (eff << 3) | (hardq << 5) | (prio << 6) | (1u << 8) | (dec << 9) | req_bits;
           const u32 dur_eff = obs ? 0u : dur;  // shadow claims never expire
-          const u32 k = ncl++;
-          qa = wrl(qa, pk(t, c), k);
-          qb = wrl(qb, pk(L, T), k);
-          qc = wrl(qc, pk(m, s), k);
-          qd = wrl(qd, dur_eff, k);
-          qe = wrl(qe, 0xFFFFFFFFu, k);
-          qf = wrl(qf, 0xFFFFFFFFu, k);
+          const u32 k = ncl++, kq = k >> 6, kl = k & 63u;
+#pragma unroll
+          for (u32 q = 0; q < NQ; q++) {
+            if (NQ == 1 || q == kq) {
+              qa[q] = wrl(qa[q], pk(t, c), kl);
+              qb[q] = wrl(qb[q], pk(L, T), kl);
+              qc[q] = wrl(qc[q], pk(m, s), kl);
+              qd[q] = wrl(qd[q], dur_eff, kl);
+              qe[q] = wrl(qe[q], 0xFFFFFFFFu, kl);
+              qf[q] = wrl(qf[q], 0xFFFFFFFFu, kl);
+            }
+          }
           if (dur_eff > 0) nexp = min(nexp, t + dur_eff);
           G0 g2 = r.victims ? rd0(c) : g;
           g2.covA = max(g2.covA, L);
@@ -975,32 +1058,68 @@ struct Lean {
     if (type == RKC_EV_RELEASE) {
       if (ncl > 0) i = w1 % ncl;
     } else if (softl()) {
-      const u32 m = lo16(qc);
-      const u64 cm = ballot(lane < ncl && m_state(m) == ST_MATERIALIZED && m_hard(m) && m_eff(m) != RKC_PROT_OFFLOADED);
-      const u32 cnt = (u32)__builtin_popcountll(cm);
+      // the (w1 mod count)-th demotable claim in id order (claims sit in id order, set by set)
+      u64 cm[NQ];
+      u32 cnt = 0;
+#pragma unroll
+      for (u32 q = 0; q < NQ; q++) {
+        const u32 m = lo16(qc[q]);
+        cm[q] = ballot(live(q) && m_state(m) == ST_MATERIALIZED && m_hard(m) && m_eff(m) != RKC_PROT_OFFLOADED);
+        cnt += (u32)__builtin_popcountll(cm[q]);
+      }
       if (cnt > 0) {
-        const u32 k = w1 % cnt;
-        const u32 rank = __builtin_amdgcn_mbcnt_hi((u32)(cm >> 32), __builtin_amdgcn_mbcnt_lo((u32)cm, 0u));
-        i = (u32)__builtin_ctzll(ballot(((cm >> lane) & 1ull) && rank == k));
+        u32 k = w1 % cnt;
+#pragma unroll
+        for (u32 q = 0; q < NQ; q++) {
+          const u32 pc = (u32)__builtin_popcountll(cm[q]);
+          if (i == NEVER && k < pc) {
+            const u32 rank = __builtin_amdgcn_mbcnt_hi((u32)(cm[q] >> 32), __builtin_amdgcn_mbcnt_lo((u32)cm[q], 0u));
+            i = 64u * q + (u32)__builtin_ctzll(ballot(((cm[q] >> lane) & 1ull) && rank == k));
+          } else if (i == NEVER) {
+            k -= pc;
+          }
+        }
       }
     }
     if (i != NEVER) {
-      const u32 qid = lo16(rdl(qa, i)), c = hi16(rdl(qa, i));
-      const u32 qbv = rdl(qb, i);
+      const u32 iq = i >> 6, il = i & 63u;
+      u32 qav = 0, qbv = 0, qcv = 0;
+#pragma unroll
+      for (u32 q = 0; q < NQ; q++) {
+        if (NQ == 1 || q == iq) { qav = rdl(qa[q], il); qbv = rdl(qb[q], il); qcv = rdl(qc[q], il); }
+      }
+      const u32 qid = lo16(qav), c = hi16(qav);
       if (type == RKC_EV_RELEASE) {
-        if (lane == i) write_own_record(ST_RELEASED, (i32)t);
-        if (ext() && m_eff(lo16(rdl(qc, i))) == RKC_PROT_OFFLOADED) cold[C_T2] = ufl(cold[C_T2]) - lo16(qbv);
-        // close the gap: lanes >= i take their upper neighbour's claim
-        const bool up = lane >= i;
-        qa = up ? shift_down(qa) : qa; qb = up ? shift_down(qb) : qb; qc = up ? shift_down(qc) : qc;
-        qd = up ? shift_down(qd) : qd; qe = up ? shift_down(qe) : qe; qf = up ? shift_down(qf) : qf;
+#pragma unroll
+        for (u32 q = 0; q < NQ; q++)
+          if ((NQ == 1 || q == iq) && lane == il) write_own_record(q, ST_RELEASED, (i32)t);
+        if (ext() && m_eff(lo16(qcv)) == RKC_PROT_OFFLOADED) cold[C_T2] = ufl(cold[C_T2]) - lo16(qbv);
+        // close the gap: claims above i move down one place (lane 63 of a set takes lane 0 of the
+        // next set, read before that set moves)
+#pragma unroll
+        for (u32 q = 0; q < NQ; q++) {
+          if (q >= iq) {
+            const bool up = q > iq || lane >= il;
+            qa[q] = up ? shift_down(qa[q]) : qa[q]; qb[q] = up ? shift_down(qb[q]) : qb[q];
+            qc[q] = up ? shift_down(qc[q]) : qc[q]; qd[q] = up ? shift_down(qd[q]) : qd[q];
+            qe[q] = up ? shift_down(qe[q]) : qe[q]; qf[q] = up ? shift_down(qf[q]) : qf[q];
+            if (q + 1 < NQ) {
+              qa[q] = wrl(qa[q], rdl(qa[q + 1], 0), 63); qb[q] = wrl(qb[q], rdl(qb[q + 1], 0), 63);
+              qc[q] = wrl(qc[q], rdl(qc[q + 1], 0), 63); qd[q] = wrl(qd[q], rdl(qd[q + 1], 0), 63);
+              qe[q] = wrl(qe[q], rdl(qe[q + 1], 0), 63); qf[q] = wrl(qf[q], rdl(qf[q + 1], 0), 63);
+            }
+          }
+        }
         ncl--;
         o.code = RKC_OC_RELEASED;
         tadd(TW_RELEASED, 1);
       } else {
-        const bool me = lane == i;
-        qc = me ? pk((lo16(qc) & ~7u) | ST_DEMOTED, hi16(qc)) : qc;
-        qe = me ? pk(t, hi16(qe)) : qe;
+#pragma unroll
+        for (u32 q = 0; q < NQ; q++) {
+          const bool me = (NQ == 1 || q == iq) && lane == il;
+          qc[q] = me ? pk((lo16(qc[q]) & ~7u) | ST_DEMOTED, hi16(qc[q])) : qc[q];
+          qe[q] = me ? pk(t, hi16(qe[q])) : qe[q];
+        }
         o.code = RKC_OC_DEMOTED;
         tadd(TW_DEMOTED, 1);
       }
@@ -1038,10 +1157,10 @@ struct Lean {
 };
 
 // Replay of one pool with policy MODE (the descriptor has been checked by the caller).
-template <int NS, int MODE, bool EXT>
+template <int NS, int NQ, int MODE, bool EXT>
 __device__ __forceinline__ void replay_pool(const rkc_lean_args& g, const rkc_pool_desc& d, u32 pool,
                                             unsigned char* lds_raw) {
-  typedef Lean<NS, MODE, EXT> LP;
+  typedef Lean<NS, NQ, MODE, EXT> LP;
   LP P;
   P.lane = __lane_id();
   const i64 ev_off = d.event_offset, slot_off = d.claim_slot_offset;
@@ -1074,7 +1193,8 @@ __device__ __forceinline__ void replay_pool(const rkc_lean_args& g, const rkc_po
   for (u32 c = P.lane; c < nrec; c += 64) {
     P.ch[c] = u32x4{0, 0, 0, pk(NIL, NIL)};
   }
-  P.qa = P.qb = P.qc = P.qd = P.qe = P.qf = 0;
+#pragma unroll
+  for (u32 q = 0; q < NQ; q++) P.qa[q] = P.qb[q] = P.qc[q] = P.qd[q] = P.qe[q] = P.qf[q] = 0;
   P.tv = 0;
   P.F = U; P.A = 0; P.PR = 0; P.peak = 0; P.Eall = 0; P.fbl = 0;
   P.nreq = 0; P.ncl = 0; P.nexp = NEVER;
@@ -1114,7 +1234,9 @@ __device__ __forceinline__ void replay_pool(const rkc_lean_args& g, const rkc_po
   const u32 status = ufl(P.cold[LP::C_STATUS]), queued = ufl(P.cold[LP::C_DQL]);
   const u32 t2peak = ufl(P.cold[LP::C_T2PK]);
   // Final records of the claims still live (each lane writes its own) ...
-  if (P.lane < P.ncl) P.write_own_record(m_state(lo16(P.qc)), -1);
+#pragma unroll
+  for (u32 q = 0; q < NQ; q++)
+    if (P.live(q)) P.write_own_record(q, m_state(lo16(P.qc[q])), -1);
   __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
   // ... then lead_end = min(final leading registered length, L) of every used slot, and blank
   // records for unused slots.
@@ -1229,7 +1351,7 @@ __global__ __launch_bounds__(1024) void rkc_lean_order_identity(i32 n_pools, u32
 
 // One wavefront per pool, in the launch order above; the pool's policy selects its specialized
 // event loop once.
-template <int NS>
+template <int NS, int NQ>
 __global__ __launch_bounds__(64) void rkc_lean(rkc_lean_args g) {
   extern __shared__ __align__(16) unsigned char lds_raw[];
   if ((i32)blockIdx.x >= g.n_pools) return;
@@ -1258,11 +1380,11 @@ __global__ __launch_bounds__(64) void rkc_lean(rkc_lean_args g) {
   }
   const u32 mode = (u32)__builtin_amdgcn_readfirstlane(d.mode & ~RKC_MODE_RELAX);
   const u32 ext = (u32)__builtin_amdgcn_readfirstlane(d.defer_limit) > 0 || (d.mode & RKC_MODE_RELAX);
-  if (mode == RKC_MODE_LRU) replay_pool<NS, RKC_MODE_LRU, false>(g, d, pool, lds_raw);
-  else if (mode == RKC_MODE_SOFT) replay_pool<NS, RKC_MODE_SOFT, false>(g, d, pool, lds_raw);
-  else if (mode == RKC_MODE_NOADMIT) replay_pool<NS, RKC_MODE_NOADMIT, false>(g, d, pool, lds_raw);
-  else if (!ext) replay_pool<NS, RKC_MODE_HARD, false>(g, d, pool, lds_raw);
-  else replay_pool<NS, RKC_MODE_HARD, true>(g, d, pool, lds_raw);
+  if (mode == RKC_MODE_LRU) replay_pool<NS, NQ, RKC_MODE_LRU, false>(g, d, pool, lds_raw);
+  else if (mode == RKC_MODE_SOFT) replay_pool<NS, NQ, RKC_MODE_SOFT, false>(g, d, pool, lds_raw);
+  else if (mode == RKC_MODE_NOADMIT) replay_pool<NS, NQ, RKC_MODE_NOADMIT, false>(g, d, pool, lds_raw);
+  else if (!ext) replay_pool<NS, NQ, RKC_MODE_HARD, false>(g, d, pool, lds_raw);
+  else replay_pool<NS, NQ, RKC_MODE_HARD, true>(g, d, pool, lds_raw);
 }
 
 u64 align_up(u64 v, u64 a) { return (v + a - 1) / a * a; }
@@ -1271,11 +1393,15 @@ u64 align_up(u64 v, u64 a) { return (v + a - 1) / a * a; }
 
 // Layout of the compact kernel for batch b, or false when the batch is outside its limits.
 bool rkc_lean_layout(const rkc_batch* b, rkc_lean_args* g) {
-  if (b->max_usable_blocks > 32767 || b->max_events > 65533 || b->max_chains > 256 ||
-      b->max_live_claims > 64 || b->max_live_requests > 256 || b->max_claim_slots > 65534)
+  // up to 64 live claims with up to 256 chains, or up to 256 live claims (four claim sets) with up
+  // to 64 chains
+  const bool many_claims = b->max_live_claims > 64;
+  if (b->max_usable_blocks > 32767 || b->max_events > 65533 || b->max_chains > (many_claims ? 64 : 256) ||
+      b->max_live_claims > 256 || b->max_live_requests > 256 || b->max_claim_slots > 65534)
     return false;
   const u32 chains = b->max_chains > 0 ? (u32)b->max_chains : 1u;
   const u32 ns = chains <= 64 ? 1u : chains <= 128 ? 2u : 4u;
+  g->nq = many_claims ? 4u : 1u;
   const u32 reqs = b->max_live_requests > 0 ? (u32)b->max_live_requests : 1u;
   g->ns = ns;
   g->node_cap = (u32)b->max_events + 2;
@@ -1315,10 +1441,10 @@ unsigned rkc_lean_uniform_violations(void) {
 }
 #endif
 
-template <int NS>
+template <int NS, int NQ>
 rkc_status launch_ns(const rkc_lean_args* g, hipStream_t s) {
   if (g->lds_bytes > 64 * 1024 &&
-      hipFuncSetAttribute((const void*)rkc_lean<NS>, hipFuncAttributeMaxDynamicSharedMemorySize,
+      hipFuncSetAttribute((const void*)rkc_lean<NS, NQ>, hipFuncAttributeMaxDynamicSharedMemorySize,
                           (int)g->lds_bytes) != hipSuccess)
     return RKC_E_HIP;
   unsigned char* scr = (unsigned char*)g->scratch;
@@ -1335,12 +1461,13 @@ rkc_status launch_ns(const rkc_lean_args* g, hipStream_t s) {
                        (u32*)(scr + g->scr_off_order));
   }
   if (hipGetLastError() != hipSuccess) return RKC_E_HIP;
-  hipLaunchKernelGGL((rkc_lean<NS>), dim3((unsigned)g->n_pools), dim3(64), g->lds_bytes, s, *g);
+  hipLaunchKernelGGL((rkc_lean<NS, NQ>), dim3((unsigned)g->n_pools), dim3(64), g->lds_bytes, s, *g);
   return hipGetLastError() == hipSuccess ? RKC_OK : RKC_E_HIP;
 }
 
 rkc_status rkc_lean_launch(const rkc_lean_args* g, hipStream_t s) {
-  if (g->ns == 1) return launch_ns<1>(g, s);
-  if (g->ns == 2) return launch_ns<2>(g, s);
-  return launch_ns<4>(g, s);
+  if (g->nq == 4) return launch_ns<1, 4>(g, s);
+  if (g->ns == 1) return launch_ns<1, 1>(g, s);
+  if (g->ns == 2) return launch_ns<2, 1>(g, s);
+  return launch_ns<4, 1>(g, s);
 }

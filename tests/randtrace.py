@@ -109,3 +109,54 @@ def random_batch(seed: int, n_pools: int, U_range=(2, 9), n_events=(1, 14), n_ch
             pool["max_live_requests"], pool["max_live_claims"] = caps
         pools.append(pool)
     return tg.from_pools(pools, f"random{seed}")
+
+
+def many_claims_batch(seed: int, n_pools: int, n_events=(600, 1500), claim_cap: int = 256,
+                      n_chains: int = 16, features: bool = True, claim_share: float = 0.50,
+                      release_share: float = 0.05):
+    """Pools that keep up to a few hundred claims live at once (small footprints on a few chains,
+    few releases), with prefills large enough to be refused, relaxed and deferred, demotions,
+    expiry and finishes: the claim tables span several 64-claim sets.  Policies cycle over the
+    four; with features, every other hard-protection pool relaxes (demotable / offloadable claims
+    and a second tier) and defers (RETRY events)."""
+    from paper_2605_24259_amd import tracegen as tg
+    rng = np.random.default_rng(seed)
+    pools = []
+    for i in range(n_pools):
+        mode = i % 4
+        ext = features and mode == 3 and (i // 4) % 2 == 1
+        U = int(rng.integers(500, 4000))
+        ne = int(rng.integers(n_events[0], n_events[1] + 1))
+        evs = []
+        for _ in range(ne):
+            r = rng.random()
+            sel = int(rng.integers(0, 1 << 31))
+            if ext and r < 0.05:
+                evs.append(tg.retry())
+            elif r < claim_share:
+                L = int(rng.integers(1, 24))
+                dur = 0 if rng.random() < 0.6 else int(rng.integers(20, 600))
+                evs.append(tg.claim(L, int(rng.integers(0, n_chains)), int(rng.integers(0, L + 1)),
+                                    hard=int(rng.random() < 0.6), prio=int(rng.integers(0, 4)), dur=dur,
+                                    demotable=int(ext and rng.random() < 0.5),
+                                    best_effort=int(rng.random() < 0.05),
+                                    offloadable=int(ext and rng.random() < 0.4)))
+            elif r < claim_share + 0.18:
+                S = int(rng.integers(1, U // 2 + 2))
+                c = int(rng.integers(0, n_chains))
+                evs.append(tg.prefill(S, c, int(rng.integers(0, min(S, 30) + 1))))
+            elif r < claim_share + 0.28:
+                evs.append(tg.extend(int(rng.integers(1, 60)), sel))
+            elif r < claim_share + 0.38:
+                evs.append(tg.finish(sel))
+            elif r < claim_share + 0.38 + release_share:
+                evs.append(tg.release(sel))
+            else:
+                evs.append(tg.demote(sel))
+        pool = dict(usable_blocks=U, mode=mode | (tg.MODE_RELAX if ext else 0), n_chains=n_chains,
+                    max_live_requests=256, max_live_claims=claim_cap, events=evs)
+        if ext:
+            pool["defer_limit"] = int(rng.integers(1, 4))
+            pool["offload_blocks"] = int(rng.integers(0, U))
+        pools.append(pool)
+    return tg.from_pools(pools, f"many-claims{seed}")

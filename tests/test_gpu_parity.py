@@ -369,6 +369,25 @@ def test_random_deferral_medium(oracle_mod, kernel):
     assert gpu[1][:, 33].sum() > 50
 
 
+@pytest.mark.parametrize("seed,kw", [
+    (201, {}),
+    (202, dict(claim_share=0.30, release_share=0.22, n_events=(1500, 3000))),
+    (203, dict(features=False, claim_cap=130, claim_share=0.35, release_share=0.15)),
+])
+def test_claim_sets(oracle_mod, seed, kw):
+    """The compact kernel with four 64-claim sets (live claims up to 256 on up to 64 chains, as in
+    the nested workload): tables that fill and overflow, releases that close gaps across sets,
+    demotions picked across sets, relaxation and offload picking over every set, deferral; against
+    the oracle and the general kernel on the same inputs."""
+    import paper_2605_24259_amd as rkc
+    trace = randtrace.many_claims_batch(seed, 256, **kw)
+    gpu, ora = _both(oracle_mod, trace)
+    compare_pools(trace, gpu, ora)
+    assert gpu[1][:, 30].max() > min(192, kw.get("claim_cap", 256) - 8)  # claims in the last set
+    gen = gpu_replay(trace, flags=rkc.FLAG_GENERAL_KERNEL)
+    compare_pools(trace, gen, ora)
+
+
 def test_regression_capacity_refusal_record_in_deferring_pools(oracle_mod):
     """Regression guard for a wrong record once produced by builds of the compact kernel: in
     deferring hard-protection pools, capacity refusals came out with b (active live required) equal
