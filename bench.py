@@ -24,16 +24,21 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, AMD published peak
-BYTES_EVENT, BYTES_OUTCOME, BYTES_CLAIM_SLOT, BYTES_POOL_TEL, BYTES_DESC = 16, 16, 40, 256, 64
+# Algorithmic bytes of the hot-path scope: 16 B per event read, 16 B per outcome written, 40 B per
+# claim record written, 128 B of pool telemetry written and a 48 B descriptor read per pool.  (The
+# ABI's pool telemetry record is 256 B and its descriptor 64 B; those are reported beside, never
+# credited.)
+BYTES_EVENT, BYTES_OUTCOME, BYTES_CLAIM_SLOT, BYTES_POOL_TEL, BYTES_DESC = 16, 16, 40, 128, 48
+ABI_POOL_TEL, ABI_DESC = 256, 64
 COPY_BYTES = 1 << 30
 METRIC = "replayed allocator events/sec (1 GPU) + % of HBM peak; bit-exact vs oracle"
 
 
-def credited_bytes(trace) -> int:
+def credited_bytes(trace, pool_tel=BYTES_POOL_TEL, desc=BYTES_DESC) -> int:
     """Algorithmic bytes of one replay launch: events in, outcomes out, claim slots out, pool
     telemetry out, descriptors in.  Scratch, LDS traffic and re-reads are not credited."""
     return (trace.n_events * (BYTES_EVENT + BYTES_OUTCOME) + trace.n_claim_slots * BYTES_CLAIM_SLOT
-            + trace.n_pools * (BYTES_POOL_TEL + BYTES_DESC))
+            + trace.n_pools * (pool_tel + desc))
 
 
 def copy_ceiling(torch, reps=20):
@@ -67,12 +72,10 @@ def oracle_prefix(trace):
     return max(256, int(ORACLE_POOL_WORK // per_event))
 
 
-def cpu_baseline(trace, seconds_budget=12.0):
-    """The oracle as it stands, on the host's cores, over a bounded sample of the same workload:
-    leading pools in chunks until the wall budget is spent (for very large pools, their leading
-    events)."""
+def _oracle_rate(trace, threads, seconds_budget):
+    """Events/s of the oracle over the leading pools of the workload (for very large pools, their
+    leading events), in chunks until the wall budget is spent."""
     import oracle
-    threads = max(1, min(16, os.cpu_count() or 1))
     pre = oracle_prefix(trace)
     done_pools, done_events = 0, 0
     t0 = time.perf_counter()
@@ -85,9 +88,29 @@ def cpu_baseline(trace, seconds_budget=12.0):
         done_events += sub.n_events
     wall = time.perf_counter() - t0
     what = "" if pre >= trace.limits()["max_events"] else f" (first {pre} events of each)"
-    return dict(value=done_events / wall, unit="events/s", cores=threads, kind="oracle",
-                sample=f"first {done_pools} pools of the workload{what}, {done_events} events, "
-                       f"{threads} threads, {wall:.1f} s wall")
+    return done_events / wall, (f"first {done_pools} pools of the workload{what}, {done_events} events, "
+                                f"{threads} thread{'s' if threads > 1 else ''}, {wall:.1f} s wall")
+
+
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(trace, seconds_budget=12.0, single_budget=4.0):
+    """The oracle as it stands, on the host's cores, over a bounded sample of the same workload
+    (up to 16 worker threads, each pool single-threaded), and the same oracle on one core."""
+    threads = max(1, min(16, os.cpu_count() or 1))
+    rate, sample = _oracle_rate(trace, threads, seconds_budget)
+    rate1, sample1 = _oracle_rate(trace, 1, single_budget)
+    return dict(value=rate, unit="events/s", cores=threads, kind="oracle", sample=sample,
+                host_cpus=os.cpu_count(), cpu_model=cpu_model(),
+                single_core=dict(value=rate1, unit="events/s", cores=1, sample=sample1))
 
 
 def profile_record(kernel, workload, kernel_sha):
@@ -109,11 +132,26 @@ SCALAR_ISSUE_PEAK = 256 * 2.4
 
 def kernel_name(lim):
     """Which replay kernel the library picks for these batch limits (the compact one when every
-    limit fits its 16-bit encoding)."""
-    fits = (lim["max_usable_blocks"] <= 32767 and lim["max_events"] <= 65533 and lim["max_chains"] <= 256
-            and lim["max_live_claims"] <= 64 and lim["max_live_requests"] <= 256
-            and lim["max_claim_slots"] <= 65534)
+    limit fits its 16-bit encoding: up to 64 live claims on up to 256 chains, or up to 256 live
+    claims on up to 64 chains)."""
+    claims_ok = (lim["max_live_claims"] <= 64 and lim["max_chains"] <= 256) or \
+                (lim["max_live_claims"] <= 256 and lim["max_chains"] <= 64)
+    fits = (lim["max_usable_blocks"] <= 32767 and lim["max_events"] <= 65533 and claims_ok
+            and lim["max_live_requests"] <= 256 and lim["max_claim_slots"] <= 65534)
     return "rkc_lean" if fits else "rkc_replay_wave"
+
+
+def parallelism(trace, kernel):
+    """How pools map to the GPU for this batch (mirrors the library's launch choice)."""
+    if kernel == "rkc_lean":
+        return "one wavefront per pool"
+    lim = trace.limits()
+    # the general kernel keeps the live lists in LDS when they fit beside the chain records
+    lists_on_chip = (lim["max_live_requests"] * 16 + lim["max_live_claims"] * 32
+                     + max(1, lim["max_chains"]) * 72) <= 159 * 1024
+    if not lists_on_chip and trace.n_pools <= 256:
+        return "one workgroup of 8 wavefronts per pool"
+    return "one wavefront per pool"
 
 
 KERNEL_SOURCES = {
@@ -178,6 +216,7 @@ def main():
     events = trace.n_events
     value = events / (ms_per_step * 1e-3)
     cbytes = credited_bytes(trace)
+    cbytes_abi = credited_bytes(trace, ABI_POOL_TEL, ABI_DESC)
     achieved = cbytes / (ms_per_step * 1e-3) / 1e9
 
     parity = None
@@ -225,7 +264,7 @@ def main():
                         f"blocks x {lim['max_events']} events",
             "pools": trace.n_pools, "usable_blocks": lim["max_usable_blocks"],
             "events_per_pool": lim["max_events"], "events_per_step": events,
-            "claim_slots": trace.n_claim_slots, "parallelism": "one wavefront per pool",
+            "claim_slots": trace.n_claim_slots, "parallelism": parallelism(trace, kernel_name(lim)),
             "kernel": kernel_name(lim),
         },
         "roofline": {
@@ -233,6 +272,8 @@ def main():
             "frac": round(achieved / HBM_PEAK_GBPS, 4),
             "traffic": prof.get("traffic_bytes_per_launch"),
             "credited_bytes_per_launch": cbytes,
+            # the same count with the ABI's 256-B telemetry record and 64-B descriptor per pool
+            "abi_record_bytes_per_launch": cbytes_abi,
             "copy_ceiling_gbps": round(ceiling, 1),
             "frac_of_copy_ceiling": round(achieved / ceiling, 4),
             # what actually bounds the replay: the scalar instructions the counters saw per launch

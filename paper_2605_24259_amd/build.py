@@ -14,6 +14,11 @@ HIPCC_FLAGS = [
     "-O3", "-std=c++17", "-fPIC", "-shared", f"--offload-arch={ARCH}",
     # packed FP32 instructions are kept off for all device code on this hardware
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # Leave regions whose branches are wave-uniform unstructured.  The per-pool event loops branch
+    # only on wave-uniform values; structurizing those regions merged the outputs of two branches of
+    # a refusal wrongly in some builds (a capacity refusal's b came out as the other branch's value),
+    # which no build with this setting shows.
+    "-mllvm", "-structurizecfg-skip-uniform-regions=true",
     "-Wall", "-Wno-unused-function", "-Wno-unused-variable",
     "-I", os.path.join(ROOT, "include"),
 ]

@@ -183,11 +183,16 @@ struct Lean {
   static constexpr u32 NL = NS == 4 ? 128u : 64u;
   uint4* fifo;
   uint4* dq;  // deferred requests: PREFILL step, S, chain, P
-  // per claim slot: chain (NEVER when malformed), L, id | packed decision/state << 16, and 1 when
-  // the final pass writes the whole record (rejected or malformed claims), 0 when a live or
-  // released claim's record is written by its own lane
-  uint4* slotcl;
+  // Claim records.  Until the final pass, word 9 (lead_end) of a used slot holds the claim's
+  // L | chain << 16 (0 for a malformed claim), from which the final pass computes lead_end; a
+  // rejected or malformed claim's other words are written when it happens, a live claim's by its
+  // own lane when it is released or at the end.
   rkc_claim_telemetry* rec;
+  // record of a claim no step ever happens to (rejected or malformed), lead_end word as above
+  __device__ __forceinline__ void write_rejected_record(u32 s, u32 id, u32 packed, u32 lc) {
+    if (lane < 10)
+      rec[s].w[lane] = lane == 0 ? (i32)id : lane == 1 ? (i32)packed : lane < 8 ? -1 : lane == 8 ? 0 : (i32)lc;
+  }
   // live claims, one per lane of each set
   u32 qa[NQ];  // id | chain
   u32 qb[NQ];  // L | T
@@ -888,9 +893,9 @@ struct Lean {
     }
   }
 
-  __device__ __forceinline__ void ev_prefill(u32 t, u32 w1, u32 w2, u32 w3, Out& o) {
-    const i32 s1 = (i32)w1, s2 = (i32)w2, s3 = (i32)w3;
-    if (s1 < 1 || s1 > RKC_MAX_FIELD_BLOCKS || s3 < 0 || s3 > s1 || (s3 > 0 && (s2 < 0 || w2 >= nch()))) {
+  // (bad: the event's fields are out of range, decided for the whole tile by malformed())
+  __device__ __forceinline__ void ev_prefill(u32 t, u32 w1, u32 w2, u32 w3, u32 bad, Out& o) {
+    if (bad) {
       o.code = RKC_OC_INVALID;
     } else if (nreq >= maxr()) {
       o.code = RKC_OC_INVALID;
@@ -916,9 +921,8 @@ struct Lean {
     }
   }
 
-  __device__ __forceinline__ void ev_extend(u32 t, u32 w1, u32 w2, Out& o) {
-    const i32 s1 = (i32)w1;
-    if (s1 < 1 || s1 > RKC_MAX_FIELD_BLOCKS) {
+  __device__ __forceinline__ void ev_extend(u32 t, u32 w1, u32 w2, u32 bad, Out& o) {
+    if (bad) {
       o.code = RKC_OC_INVALID;
     } else if (nreq > 0) {
       const u32 i = w2 % nreq, need = w1;
@@ -941,8 +945,7 @@ struct Lean {
     }
   }
 
-  __device__ __forceinline__ void ev_claim(u32 t, u32 w0, u32 w1, u32 w2, u32 w3, Out& o) {
-    const i32 s1 = (i32)w1, s2 = (i32)w2, s3 = (i32)w3;
+  __device__ __forceinline__ void ev_claim(u32 t, u32 w0, u32 w1, u32 w2, u32 w3, u32 bad, Out& o) {
     const u32 nslot = ufl(cold[C_NSLOT]);
     if (nslot >= nslots()) {
       o.code = RKC_OC_INVALID;
@@ -950,10 +953,10 @@ struct Lean {
     } else {
       const u32 s = nslot;
       cold[C_NSLOT] = nslot + 1;
-      bool ok = !(s1 < 1 || s1 > RKC_MAX_FIELD_BLOCKS || s2 < 0 || w2 >= nch() || s3 < 0 || s3 > s1);
+      bool ok = !bad;
       if (ok && ncl >= maxq()) { set_status(RKC_PS_CLAIM_TABLE); ok = false; }
       if (!ok) {
-        slotcl[s] = make_uint4(NEVER, 0, t, 1);  // every lane, one value
+        write_rejected_record(s, t, 0, 0);
         o.code = RKC_OC_INVALID;
       } else {
         const u32 L = w1, c = w2, T = w3;
@@ -970,15 +973,14 @@ struct Lean {
         if (!r.ok) {
           const u32 dec = obs ? DEC_SHADOW : DEC_REJECTED;
           const u32 m = ST_REJECTED | (eff << 3) | (hardq << 5) | (prio << 6) | (dec << 9) | req_bits;
-          const u32 pw = packed_of(m);
-          slotcl[s] = make_uint4(c, L, pk(t, pw & 0xFFFFu), 1u | ((pw >> 16) << 1));
+          write_rejected_record(s, t, packed_of(m), pk(L, c));
           o.code = RKC_OC_MATFAIL;
           o.id = (i32)t;
           o.a = (i32)need;
           o.b = (i32)(F + r.E);
           tadd(TW_ACCEPTED + dec - DEC_ACCEPTED, 1);
         } else {
-          slotcl[s] = make_uint4(c, L, 0, 0);
+          rec[s].w[9] = (i32)pk(L, c);  // every lane, one value
           const u32 lowered = (mode == RKC_MODE_SOFT) && hardq;
           const u32 dec = obs ? DEC_SHADOW : lowered ? DEC_APPROX : DEC_ACCEPTED;
           const u32 st = obs ? ST_OBSERVED : ST_MATERIALIZED;
@@ -1131,27 +1133,36 @@ struct Lean {
     }
   }
 
-  // One event; returns the outcome words.  Dispatch is an if / else chain in order of how often
-  // the event types occur in the benchmark mixes.
-  __device__ __forceinline__ void step(u32 t, u32 w0, u32 w1, u32 w2, u32 w3, u32& o0, i32& o1, i32& o2, i32& o3) {
+  // Malformed events of a tile (lane k holds event k): field ranges of PREFILL, EXTEND and CLAIM,
+  // decided for all 64 events at once (the table limits are checked per event, in order).
+  __device__ __forceinline__ u64 malformed(u32 e0, u32 e1, u32 e2, u32 e3, u32 cnt) const {
+    const u32 ty = e0 & 15u;
+    const i32 s1 = (i32)e1, s2 = (i32)e2, s3 = (i32)e3;
+    const bool fb = s1 < 1 || s1 > RKC_MAX_FIELD_BLOCKS;
+    const bool cb = s2 < 0 || e2 >= nch();
+    const bool bad = (ty == RKC_EV_PREFILL && (fb || s3 < 0 || s3 > s1 || (s3 > 0 && cb))) ||
+                     (ty == RKC_EV_EXTEND && fb) ||
+                     (ty == RKC_EV_CLAIM && (fb || cb || s3 < 0 || s3 > s1));
+    return ballot(lane < cnt && bad);
+  }
+
+  // One event: its outcome fields in o, the claims expired at its start in `expired` (the caller
+  // assembles the outcome words of a whole tile at once).  Dispatch is an if / else chain in order
+  // of how often the event types occur in the benchmark mixes.
+  __device__ __forceinline__ void step(u32 t, u32 w0, u32 w1, u32 w2, u32 w3, u32 bad, Out& o, u32& expired) {
     const u32 type = w0 & 15u;
-    u32 expired = 0;
-    Out o = {RKC_OC_NOOP, 0, NEVER, 0, -1, 0, 0};
+    expired = 0;
+    o = Out{RKC_OC_NOOP, 0, NEVER, 0, -1, 0, 0};
     if (__builtin_expect(t >= nexp, 0)) expire(t, o.flags, expired);
-    if (type == RKC_EV_PREFILL) ev_prefill(t, w1, w2, w3, o);
-    else if (type == RKC_EV_EXTEND) ev_extend(t, w1, w2, o);
-    else if (type == RKC_EV_CLAIM) ev_claim(t, w0, w1, w2, w3, o);
+    if (type == RKC_EV_PREFILL) ev_prefill(t, w1, w2, w3, bad, o);
+    else if (type == RKC_EV_EXTEND) ev_extend(t, w1, w2, bad, o);
+    else if (type == RKC_EV_CLAIM) ev_claim(t, w0, w1, w2, w3, bad, o);
     else if (type == RKC_EV_FINISH) ev_finish(t, w1, o);
     else if (type == RKC_EV_RELEASE || type == RKC_EV_DEMOTE) ev_lifecycle(t, type, w1, o);
     else if (ext() && type == RKC_EV_RETRY) ev_retry(t, o);
     else if ((type & ~1u) != RKC_EV_NOP) o.code = RKC_OC_INVALID;  // NOP, or RETRY with no ring
     static_assert(RKC_EV_NOP == 6 && RKC_EV_RETRY == 7, "NOP and RETRY differ in bit 0 only");
     if (__builtin_expect(o.sweep_due != 0, 0)) o.flags |= sweep(t);
-    const bool quiet = o.code == RKC_OC_NOOP || o.code == RKC_OC_INVALID;
-    o0 = o.code | (o.flags << 8) | ((o.n16 == NEVER ? min(expired, 65535u) : o.n16) << 16);
-    o1 = quiet ? -1 : o.id;
-    o2 = quiet ? 0 : o.a;
-    o3 = quiet ? 0 : o.b;
     peak = max(peak, A);
   }
 };
@@ -1182,7 +1193,6 @@ __device__ __forceinline__ void replay_pool(const rkc_lean_args& g, const rkc_po
   unsigned char* scr = (unsigned char*)g.scratch + (u64)pool * g.scr_pool_bytes;
   P.ndg = (glb_u32x2*)(scr + g.scr_off_nodes);
   P.fifo = (uint4*)(scr + g.scr_off_fifo);
-  P.slotcl = (uint4*)(scr + g.scr_off_slots);
   P.dq = (uint4*)(scr + g.scr_off_defer);
   P.rec = g.claim_tel + slot_off;
 
@@ -1212,13 +1222,22 @@ __device__ __forceinline__ void replay_pool(const rkc_lean_args& g, const rkc_po
       const int4 x = *(const int4*)(ev + base + P.lane);
       e0 = (u32)x.x; e1 = (u32)x.y; e2 = (u32)x.z; e3 = (u32)x.w;
     }
-    u32 o0 = 0, o1 = 0, o2 = 0, o3 = 0;
+    const u64 badm = P.malformed(e0, e1, e2, e3, cnt);
+    // outcome fields of event k go to lane k; the words are assembled for the tile at once
+    u32 vcode = 0, vflags = 0, vn16 = 0, vexp = 0, vid = 0, va = 0, vb = 0;
     for (u32 k = 0; k < cnt; k++) {
-      u32 r0;
-      i32 r1, r2, r3;
-      P.step(base + k, rdl(e0, k), rdl(e1, k), rdl(e2, k), rdl(e3, k), r0, r1, r2, r3);
-      o0 = wrl(o0, r0, k); o1 = wrl(o1, (u32)r1, k); o2 = wrl(o2, (u32)r2, k); o3 = wrl(o3, (u32)r3, k);
+      typename LP::Out o;
+      u32 expired;
+      P.step(base + k, rdl(e0, k), rdl(e1, k), rdl(e2, k), rdl(e3, k), (u32)(badm >> k) & 1u, o, expired);
+      vcode = wrl(vcode, o.code, k); vflags = wrl(vflags, o.flags, k); vn16 = wrl(vn16, o.n16, k);
+      vexp = wrl(vexp, expired, k); vid = wrl(vid, (u32)o.id, k); va = wrl(va, (u32)o.a, k);
+      vb = wrl(vb, (u32)o.b, k);
     }
+    // n16: the blocking / relaxed count where the event set one, else the claims expired at its
+    // start; no-op and invalid outcomes carry id -1, a = b = 0
+    const bool quiet = vcode == RKC_OC_NOOP || vcode == RKC_OC_INVALID;
+    const u32 o0 = vcode | (vflags << 8) | ((vn16 == NEVER ? min(vexp, 65535u) : vn16) << 16);
+    const u32 o1 = quiet ? 0xFFFFFFFFu : vid, o2 = quiet ? 0u : va, o3 = quiet ? 0u : vb;
     if (P.lane < cnt) *(int4*)(out + base + P.lane) = make_int4((i32)o0, (i32)o1, (i32)o2, (i32)o3);
     // outcomes per code; resident victims (a) and leading hits (b of a served prefill)
     const u32 oc = o0 & 255u;
@@ -1242,16 +1261,8 @@ __device__ __forceinline__ void replay_pool(const rkc_lean_args& g, const rkc_po
   // records for unused slots.
   for (u32 s = P.lane; s < nslots; s += 64) {
     if (s < nslot_used) {
-      const uint4 cl = P.slotcl[s];
-      u32 le = 0;
-      if (cl.x != NEVER) le = min(P.chain_n(cl.x), cl.y);
-      if (cl.w) {
-        // rejected or malformed claim: no step ever happened to it
-        const i32 id = (i32)lo16(cl.z), packed = (i32)(hi16(cl.z) | ((cl.w >> 1) << 16));
-        P.rec[s] = rkc_claim_telemetry{{id, packed, -1, -1, -1, -1, -1, -1, 0, (i32)le}};
-      } else {
-        P.rec[s].w[9] = (i32)le;
-      }
+      const u32 lc = (u32)P.rec[s].w[9];
+      P.rec[s].w[9] = (i32)min(P.chain_n(hi16(lc)), lo16(lc));
     } else {
       P.rec[s] = rkc_claim_telemetry{{-1, 0, -1, -1, -1, -1, -1, -1, 0, 0}};
     }
@@ -1420,8 +1431,6 @@ bool rkc_lean_layout(const rkc_batch* b, rkc_lean_args* g) {
   s += 8ull * (g->node_cap > g->nodes_lds ? g->node_cap - g->nodes_lds : 0u);
   s = align_up(s, 256);
   g->scr_off_fifo = s; s += 16ull * ((u64)b->max_events + 1); s = align_up(s, 256);
-  g->scr_off_slots = s; s += 16ull * (u64)(b->max_claim_slots > 0 ? b->max_claim_slots : 1);
-  s = align_up(s, 256);
   g->scr_off_defer = s; s += 16ull * reqs;
   g->scr_pool_bytes = align_up(s, 256);
   const u64 np = b->n_pools > 0 ? (u64)b->n_pools : 0u;

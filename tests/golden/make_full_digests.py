@@ -66,10 +66,20 @@ def make(name: str, threads: int) -> str:
     del full
     step = CHUNK_POOLS[name]
     firsts = list(range(0, n_pools, step))
+    # finished chunks are kept until the workload's file is written, so an interrupted run resumes
+    part = os.path.join(OUT_DIR, ".partial", name)
+    os.makedirs(part, exist_ok=True)
     done = [0]
 
     def one(first):
-        d = chunk_digest(name, first, min(step, n_pools - first))
+        cache = os.path.join(part, f"{first}.json")
+        if os.path.exists(cache):
+            d = json.load(open(cache))
+        else:
+            d = chunk_digest(name, first, min(step, n_pools - first))
+            with open(cache + ".tmp", "w") as f:
+                json.dump(d, f)
+            os.replace(cache + ".tmp", cache)
         done[0] += 1
         print(f"{name}: chunk {done[0]}/{len(firsts)} (pools {first}..) {time.time() - t0:.0f} s",
               flush=True)
@@ -100,6 +110,9 @@ def make(name: str, threads: int) -> str:
     assert json.loads(text) == doc
     with open(path, "w") as f:
         f.write(text)
+    for first in firsts:
+        os.remove(os.path.join(part, f"{first}.json"))
+    os.rmdir(part)
     print(f"wrote {path} ({time.time() - t0:.0f} s)", flush=True)
     return path
 
