@@ -156,14 +156,15 @@ def parallelism(trace, kernel):
 
 KERNEL_SOURCES = {
     "rkc_lean": ("paper_2605_24259_amd/csrc/rkc_lean.hip", "paper_2605_24259_amd/csrc/rkc_lean.h",
-                 "include/rkc.h"),
-    "rkc_replay_wave": ("paper_2605_24259_amd/csrc/rkc_replay.hip", "include/rkc.h"),
+                 "include/rkc.h", "paper_2605_24259_amd/build.py"),
+    "rkc_replay_wave": ("paper_2605_24259_amd/csrc/rkc_replay.hip", "include/rkc.h",
+                        "paper_2605_24259_amd/build.py"),
 }
 
 
 def kernel_source_sha(kernel="rkc_lean"):
-    """SHA-256 over the sources that define one replay kernel and its launch (the counters
-    describe the build of those sources)."""
+    """SHA-256 over the sources that define one replay kernel and its launch, and the build script
+    that holds its compiler flags (the counters describe the build of those sources)."""
     import hashlib
     h = hashlib.sha256()
     for f in KERNEL_SOURCES[kernel]:

@@ -183,15 +183,14 @@ struct Lean {
   static constexpr u32 NL = NS == 4 ? 128u : 64u;
   uint4* fifo;
   uint4* dq;  // deferred requests: PREFILL step, S, chain, P
-  // Claim records.  Until the final pass, word 9 (lead_end) of a used slot holds the claim's
-  // L | chain << 16 (0 for a malformed claim), from which the final pass computes lead_end; a
-  // rejected or malformed claim's other words are written when it happens, a live claim's by its
-  // own lane when it is released or at the end.
+  // Claim records: a rejected or malformed claim's words 0..8 are written when it happens, a live
+  // claim's by its own lane when it is released or at the end; word 9 (lead_end) of every used slot
+  // by the final pass, from the slot's L | chain << 16 in `slotlc` (0 for a malformed claim).
   rkc_claim_telemetry* rec;
-  // record of a claim no step ever happens to (rejected or malformed), lead_end word as above
-  __device__ __forceinline__ void write_rejected_record(u32 s, u32 id, u32 packed, u32 lc) {
-    if (lane < 10)
-      rec[s].w[lane] = lane == 0 ? (i32)id : lane == 1 ? (i32)packed : lane < 8 ? -1 : lane == 8 ? 0 : (i32)lc;
+  u32* slotlc;
+  // words 0..8 of the record of a claim no step ever happens to (rejected or malformed)
+  __device__ __forceinline__ void write_rejected_record(u32 s, u32 id, u32 packed) {
+    if (lane < 9) rec[s].w[lane] = lane == 0 ? (i32)id : lane == 1 ? (i32)packed : lane < 8 ? -1 : 0;
   }
   // live claims, one per lane of each set
   u32 qa[NQ];  // id | chain
@@ -956,7 +955,8 @@ struct Lean {
       bool ok = !bad;
       if (ok && ncl >= maxq()) { set_status(RKC_PS_CLAIM_TABLE); ok = false; }
       if (!ok) {
-        write_rejected_record(s, t, 0, 0);
+        write_rejected_record(s, t, 0);
+        slotlc[s] = 0;  // every lane, one value
         o.code = RKC_OC_INVALID;
       } else {
         const u32 L = w1, c = w2, T = w3;
@@ -973,14 +973,15 @@ struct Lean {
         if (!r.ok) {
           const u32 dec = obs ? DEC_SHADOW : DEC_REJECTED;
           const u32 m = ST_REJECTED | (eff << 3) | (hardq << 5) | (prio << 6) | (dec << 9) | req_bits;
-          write_rejected_record(s, t, packed_of(m), pk(L, c));
+          write_rejected_record(s, t, packed_of(m));
+          slotlc[s] = pk(L, c);
           o.code = RKC_OC_MATFAIL;
           o.id = (i32)t;
           o.a = (i32)need;
           o.b = (i32)(F + r.E);
           tadd(TW_ACCEPTED + dec - DEC_ACCEPTED, 1);
         } else {
-          rec[s].w[9] = (i32)pk(L, c);  // every lane, one value
+          slotlc[s] = pk(L, c);  // every lane, one value
           const u32 lowered = (mode == RKC_MODE_SOFT) && hardq;
           const u32 dec = obs ? DEC_SHADOW : lowered ? DEC_APPROX : DEC_ACCEPTED;
           const u32 st = obs ? ST_OBSERVED : ST_MATERIALIZED;
@@ -1193,6 +1194,7 @@ __device__ __forceinline__ void replay_pool(const rkc_lean_args& g, const rkc_po
   unsigned char* scr = (unsigned char*)g.scratch + (u64)pool * g.scr_pool_bytes;
   P.ndg = (glb_u32x2*)(scr + g.scr_off_nodes);
   P.fifo = (uint4*)(scr + g.scr_off_fifo);
+  P.slotlc = (u32*)(scr + g.scr_off_slots);
   P.dq = (uint4*)(scr + g.scr_off_defer);
   P.rec = g.claim_tel + slot_off;
 
@@ -1261,7 +1263,7 @@ __device__ __forceinline__ void replay_pool(const rkc_lean_args& g, const rkc_po
   // records for unused slots.
   for (u32 s = P.lane; s < nslots; s += 64) {
     if (s < nslot_used) {
-      const u32 lc = (u32)P.rec[s].w[9];
+      const u32 lc = P.slotlc[s];
       P.rec[s].w[9] = (i32)min(P.chain_n(hi16(lc)), lo16(lc));
     } else {
       P.rec[s] = rkc_claim_telemetry{{-1, 0, -1, -1, -1, -1, -1, -1, 0, 0}};
@@ -1431,6 +1433,8 @@ bool rkc_lean_layout(const rkc_batch* b, rkc_lean_args* g) {
   s += 8ull * (g->node_cap > g->nodes_lds ? g->node_cap - g->nodes_lds : 0u);
   s = align_up(s, 256);
   g->scr_off_fifo = s; s += 16ull * ((u64)b->max_events + 1); s = align_up(s, 256);
+  g->scr_off_slots = s; s += 4ull * (u64)(b->max_claim_slots > 0 ? b->max_claim_slots : 1);
+  s = align_up(s, 256);
   g->scr_off_defer = s; s += 16ull * reqs;
   g->scr_pool_bytes = align_up(s, 256);
   const u64 np = b->n_pools > 0 ? (u64)b->n_pools : 0u;
