@@ -156,3 +156,30 @@ def test_offload_closed_forms(oracle_mod, tg):
     assert not chk.any(), [oracle_mod.check_names(int(c)) for c in chk]
     errs = gf.check(fx, trace, out, ptel, ctel)
     assert not errs, "\n".join(errs)
+
+
+def test_refusal_record_rendering(oracle_mod, tg, tmp_path):
+    """The outcome stream rendered as the §5.4 refusal record (field names of the canonical refusal
+    event): the hard-protection probe gives protected 60, required 70, sum 130, usable 80, shortfall
+    50, blocking claim 0; the other policies refuse nothing."""
+    import json
+    from paper_2605_24259_amd import records
+    trace = tg.probe(80)
+    out, ptel, ctel, chk = oracle_mod.replay(trace.desc, trace.events, trace.n_claim_slots)
+    recs = records.refusal_records(trace.desc, trace.events, out)
+    assert len(recs) == 1
+    r = recs[0]
+    assert r == {"event": "active_request_refused", "pool": 3, "step": 1, "event_type": "prefill",
+                 "refusal": "claim", "blocking_claim_ids": [0], "protected_resident_blocks": 60,
+                 "active_live_blocks_required": 70, "resident_plus_active_blocks": 130,
+                 "usable_blocks": 80, "capacity_shortfall_blocks": 50,
+                 "feasibility": "infeasible_preserve_resident_and_active"}
+    path = tmp_path / "refusals.jsonl"
+    assert records.write_jsonl(path, recs) == 1
+    assert json.loads(open(path).read().strip()) == r
+    # a capacity refusal (U = 69 < 70): no blocking claim, active load alone exceeds the pool
+    trace = tg.probe(69, modes=(3,))
+    out = oracle_mod.replay(trace.desc, trace.events, trace.n_claim_slots)[0]
+    r = records.refusal_records(trace.desc, trace.events, out)[0]
+    assert r["refusal"] == "capacity" and r["blocking_claim_ids"] == []
+    assert r["capacity_shortfall_blocks"] == r["resident_plus_active_blocks"] - 69 > 0
