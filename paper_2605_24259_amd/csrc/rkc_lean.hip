@@ -295,6 +295,13 @@ struct Lean {
     const u32 m = lo16(qc[q]), st = m_state(m);
     return on_chain(c, q) && ((st == ST_MATERIALIZED && m_eff(m) == RKC_PROT_SOFT) || st == ST_DEMOTED);
   }
+  // this lane's claim of set q is a materialized hard claim (hard protection in effect)
+  __device__ __forceinline__ bool hmat(u32 q) const {
+    const u32 m = lo16(qc[q]);
+    return live(q) && m_state(m) == ST_MATERIALIZED && m_eff(m) == RKC_PROT_HARD;
+  }
+  // relaxation order of this lane's claim of set q: priority, then id
+  __device__ __forceinline__ u32 rkey(u32 q) const { return (m_prio(lo16(qc[q])) << 16) | lo16(qa[q]); }
   // soft level of position p of chain c
   __device__ __forceinline__ u32 level_of(u32 c, u32 p) const {
     u32 v = 0;
@@ -730,55 +737,56 @@ struct Lean {
       }
       u64 avail = (u64)F + E;
       if ((u64)need > avail) {
-        u32 m[NQ], c[NQ], L[NQ], key[NQ];
-        bool hm[NQ];
-        u64 left[NQ], S[NQ], O[NQ];  // candidates not visited; picked; picked for offload
-        u32 nleft = 0;
+        // Per lane and claim set q, three bits of `sel`: bit q the claim is a candidate not yet
+        // visited, bit 4 + q picked, bit 8 + q picked for offload (the rest of the picks are
+        // demoted).  The claim fields are read from the claim registers, which stay unchanged
+        // until the picks are applied.
+        u32 sel = 0, nleft = 0;
 #pragma unroll
         for (u32 q = 0; q < NQ; q++) {
-          m[q] = lo16(qc[q]); c[q] = hi16(qa[q]); L[q] = lo16(qb[q]);
-          u32 cov = chain_hold(c[q]);
-          if ((i32)c[q] == hc) cov = max(cov, h);
-          hm[q] = live(q) && m_state(m[q]) == ST_MATERIALIZED && m_eff(m[q]) == RKC_PROT_HARD;
-          key[q] = (m_prio(m[q]) << 16) | lo16(qa[q]);
-          left[q] = ballot(hm[q] && (m[q] & (M_DEMQ | M_OFFQ)) && L[q] > cov);
-          S[q] = 0; O[q] = 0;
-          nleft += (u32)__builtin_popcountll(left[q]);
+          const u32 m = lo16(qc[q]), c = hi16(qa[q]);
+          u32 cov = chain_hold(c);
+          if ((i32)c == hc) cov = max(cov, h);
+          const bool cand = hmat(q) && (m & (M_DEMQ | M_OFFQ)) && lo16(qb[q]) > cov;
+          sel |= cand ? 1u << q : 0u;
+          nleft += (u32)__builtin_popcountll(ballot(cand));
         }
         u32 room = sub0(t2cap(), ufl(cold[C_T2])), moved = 0;
         for (u32 guard = 0; nleft > 0 && (u64)need > avail && guard < 64u * NQ; guard++) {
           u32 kv = NEVER;
 #pragma unroll
-          for (u32 q = 0; q < NQ; q++) kv = min(kv, ((left[q] >> lane) & 1ull) ? key[q] : NEVER);
+          for (u32 q = 0; q < NQ; q++) kv = min(kv, ((sel >> q) & 1u) ? rkey(q) : NEVER);
           const u32 kmin = wmin(kv);
           // the claim with the smallest (priority, id): set lq, lane l (keys are distinct)
           u32 lq = 0, l = 0, ml = 0, Ll = 0, cq = 0;
 #pragma unroll
           for (u32 q = 0; q < NQ; q++) {
-            const u64 b = ballot(((left[q] >> lane) & 1ull) && key[q] == kmin);
+            const u64 b = ballot(((sel >> q) & 1u) && rkey(q) == kmin);
             if (b) {
               lq = q;
               l = (u32)__builtin_ctzll(b);
-              ml = rdl(m[q], l); Ll = rdl(L[q], l); cq = rdl(c[q], l);
-              left[q] &= ~(1ull << l);
+              ml = lo16(rdl(qc[q], l)); Ll = lo16(rdl(qb[q], l)); cq = hi16(rdl(qa[q], l));
             }
           }
+          sel &= lane == l ? ~(1u << lq) : ~0u;
           nleft--;
           const bool off = (ml & M_OFFQ) && Ll <= room;
           if (off || (ml & M_DEMQ)) {
             if (off) { room -= Ll; moved += Ll; }
             const G0 g = rd0(cq);
             const u32 base = (i32)cq == hc ? max(g.hold, h) : g.hold;
-            u32 bv = 0, av = 0;
+            u32 bv = 0;
 #pragma unroll
             for (u32 q = 0; q < NQ; q++) {
-              const bool on = hm[q] && c[q] == cq;
-              bv = max(bv, on && !((S[q] >> lane) & 1ull) ? L[q] : 0u);
-              if (q == lq) {
-                S[q] |= 1ull << l;
-                if (off) O[q] |= 1ull << l;
-              }
-              av = max(av, on && !((S[q] >> lane) & 1ull) ? L[q] : 0u);
+              const bool on = hmat(q) && hi16(qa[q]) == cq;
+              bv = max(bv, on && !((sel >> (4 + q)) & 1u) ? lo16(qb[q]) : 0u);
+            }
+            sel |= lane == l ? (1u << (4 + lq)) | (off ? 1u << (8 + lq) : 0u) : 0u;
+            u32 av = 0;
+#pragma unroll
+            for (u32 q = 0; q < NQ; q++) {
+              const bool on = hmat(q) && hi16(qa[q]) == cq;
+              av = max(av, on && !((sel >> (4 + q)) & 1u) ? lo16(qb[q]) : 0u);
             }
             const u32 before = wmax(bv), after = wmax(av);
             avail += evictable(g.n, base, after) - evictable(g.n, base, before);
@@ -786,14 +794,17 @@ struct Lean {
         }
         if ((u64)need <= avail) {
           u32 no = 0;
+          u64 S[NQ];
 #pragma unroll
           for (u32 q = 0; q < NQ; q++) {
-            const bool o = (O[q] >> lane) & 1ull, d = ((S[q] & ~O[q]) >> lane) & 1ull;
-            qc[q] = d ? pk((m[q] & ~7u) | ST_DEMOTED | M_RELAXED, hi16(qc[q])) : qc[q];
-            qc[q] = o ? pk((m[q] & ~(3u << 3)) | (RKC_PROT_OFFLOADED << 3) | M_RELAXED, hi16(qc[q])) : qc[q];
+            const u32 m = lo16(qc[q]);
+            const bool o = (sel >> (8 + q)) & 1u, d = ((sel >> (4 + q)) & 1u) && !o;
+            qc[q] = d ? pk((m & ~7u) | ST_DEMOTED | M_RELAXED, hi16(qc[q])) : qc[q];
+            qc[q] = o ? pk((m & ~(3u << 3)) | (RKC_PROT_OFFLOADED << 3) | M_RELAXED, hi16(qc[q])) : qc[q];
             qe[q] = d ? pk(t, hi16(qe[q])) : qe[q];
+            S[q] = ballot((sel >> (4 + q)) & 1u);
             k += (u32)__builtin_popcountll(S[q]);
-            no += (u32)__builtin_popcountll(O[q]);
+            no += (u32)__builtin_popcountll(ballot(o));
           }
           recompute_lanes(S);
           tadd(TW_RUNTIME_DEMOTED, k - no);
@@ -1363,9 +1374,11 @@ __global__ __launch_bounds__(1024) void rkc_lean_order_identity(i32 n_pools, u32
 }
 
 // One wavefront per pool, in the launch order above; the pool's policy selects its specialized
-// event loop once.
+// event loop once.  With four claim sets the registers, not LDS, bound residency: the kernel is
+// held to 6 waves per SIMD (80 vector registers; 5 waves and 87 registers otherwise, measured
+// slower: nested 10.8 vs 10.2 ms, 7 and 8 waves 10.7 and 10.6 ms).
 template <int NS, int NQ>
-__global__ __launch_bounds__(64) void rkc_lean(rkc_lean_args g) {
+__global__ __launch_bounds__(64, NQ > 1 ? 6 : 1) void rkc_lean(rkc_lean_args g) {
   extern __shared__ __align__(16) unsigned char lds_raw[];
   if ((i32)blockIdx.x >= g.n_pools) return;
   const u32 pool = ((const u32*)((const unsigned char*)g.scratch + g.scr_off_order))[blockIdx.x];
