@@ -102,6 +102,19 @@ __device__ __forceinline__ u32 ufl(u32 v) {
 __device__ __forceinline__ u32 ufl(u32 v) { return (u32)__builtin_amdgcn_readfirstlane((int)v); }
 #endif
 __device__ __forceinline__ u32 rdl(u32 v, u32 l) { return (u32)__builtin_amdgcn_readlane((int)v, (int)l); }
+// x mod n for wave-uniform x and 1 <= n <= 1024, on the vector unit (the scalar unit is the busier
+// one): x / n from a double-precision reciprocal refined by two Newton steps (relative error below
+// 2^-48, so x / n is off by less than 2^-16 < 1 / n), whose floor is the quotient or, when x is a
+// multiple of n, one less; a single comparison corrects that.
+__device__ __forceinline__ u32 umod(u32 x, u32 n) {
+  const double dn = (double)n;
+  double r = __builtin_amdgcn_rcp(dn);
+  r = __builtin_fma(r, __builtin_fma(-dn, r, 1.0), r);
+  r = __builtin_fma(r, __builtin_fma(-dn, r, 1.0), r);
+  const u32 q = (u32)__builtin_floor((double)x * r);
+  const u32 m = x - q * n;
+  return ufl(m >= n ? m - n : m);
+}
 // a - b, or 0 when b exceeds a
 __device__ __forceinline__ u32 sub0(u32 a, u32 b) { return a > b ? a - b : 0u; }
 // lane l of `old` replaced by the uniform value v
@@ -935,7 +948,7 @@ struct Lean {
     if (bad) {
       o.code = RKC_OC_INVALID;
     } else if (nreq > 0) {
-      const u32 i = w2 % nreq, need = w1;
+      const u32 i = umod(w2, nreq), need = w1;
       G0 g = {0, 0, 0, 0, 0, 0, 0, 0};
       u32 relaxed = 0;
       if (ext()) relaxed = relax(t, need, -1, 0, g);
@@ -1028,7 +1041,7 @@ struct Lean {
 
   __device__ __forceinline__ void ev_finish(u32 t, u32 w1, Out& o) {
     if (nreq > 0) {
-      const u32 i = w1 % nreq;
+      const u32 i = umod(w1, nreq);
       u32x2 e = rq[i];
       e.x = ufl(e.x); e.y = ufl(e.y);
       const u32 rid = lo16(e.x), c = hi16(e.x), R = lo16(e.y), len = hi16(e.y);
@@ -1070,7 +1083,7 @@ struct Lean {
   __device__ __forceinline__ void ev_lifecycle(u32 t, u32 type, u32 w1, Out& o) {
     u32 i = NEVER;
     if (type == RKC_EV_RELEASE) {
-      if (ncl > 0) i = w1 % ncl;
+      if (ncl > 0) i = umod(w1, ncl);
     } else if (softl()) {
       // the (w1 mod count)-th demotable claim in id order (claims sit in id order, set by set)
       u64 cm[NQ];
@@ -1082,7 +1095,7 @@ struct Lean {
         cnt += (u32)__builtin_popcountll(cm[q]);
       }
       if (cnt > 0) {
-        u32 k = w1 % cnt;
+        u32 k = umod(w1, cnt);
 #pragma unroll
         for (u32 q = 0; q < NQ; q++) {
           const u32 pc = (u32)__builtin_popcountll(cm[q]);

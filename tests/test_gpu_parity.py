@@ -388,6 +388,45 @@ def test_claim_sets(oracle_mod, seed, kw):
     compare_pools(trace, gen, ora)
 
 
+def _edge_selectors(n):
+    """u32 selectors at the edges of `sel mod n`: multiples of n (largest one below 2^32
+    included), their neighbours, 0 and 2^32 - 1."""
+    top = (2**32 - 1) // n * n
+    return sorted(x for x in {0, 1, n - 1, n, n + 1, 2 * n, top - n, top - 1, top, 2**32 - 1}
+                  if 0 <= x < 2**32)
+
+
+def test_selector_edges(oracle_mod, tg):
+    """Selector arithmetic (the target is the (sel mod count)-th live request or claim) at the edges
+    of the u32 range and at exact multiples of the count, for every count up to 256 live requests
+    and claims; both kernels against the oracle."""
+    import paper_2605_24259_amd as rkc
+    pools = []
+    for mode in (1, 3):
+        ev = []
+        for p in range(1, 257):
+            ev.append(tg.prefill(1))
+            for sel in _edge_selectors(p)[:: 3 if p > 16 else 1]:
+                ev.append(tg.extend(1, sel))
+        for n in range(256, 0, -1):
+            ev.append(tg.finish(_edge_selectors(n)[n % 10 % len(_edge_selectors(n))]))
+        pools.append(dict(usable_blocks=30000, mode=mode, n_chains=1, max_live_requests=256,
+                          max_live_claims=256, events=ev))
+        ev = []
+        for p in range(1, 257):
+            ev.append(tg.claim(1, 0, 1, hard=1))
+            if p % 7 == 0:
+                ev.append(tg.demote(_edge_selectors(p)[p % 10 % len(_edge_selectors(p))]))
+        for n in range(256, 0, -1):
+            ev.append(tg.release(_edge_selectors(n)[(n // 3) % len(_edge_selectors(n))]))
+        pools.append(dict(usable_blocks=30000, mode=mode, n_chains=1, max_live_requests=256,
+                          max_live_claims=256, events=ev))
+    trace = tg.from_pools(pools, "selector-edges")
+    gpu, ora = _both(oracle_mod, trace)
+    compare_pools(trace, gpu, ora)
+    compare_pools(trace, gpu_replay(trace, flags=rkc.FLAG_GENERAL_KERNEL), ora)
+
+
 def test_regression_capacity_refusal_record_in_deferring_pools(oracle_mod):
     """Regression guard for a wrong record once produced by builds of the compact kernel: in
     deferring hard-protection pools, capacity refusals came out with b (active live required) equal
