@@ -419,7 +419,9 @@ class Pool:
                 code, oid = "demoted", q["id"]
                 a, b = self.prefix_len(q["chain"], q["L"]), q["T"]
                 self.tel[22] += 1
-        if not invalid and unreg:
+        # the predicate sweep runs on every valid step (the oracle restricts it to steps where blocks
+        # left the reuse index; this model does not, so it checks that restriction independently)
+        if not invalid:
             for q in self.claims:
                 if q.get("valid") and q["pred_fail"] < 0 and \
                         q["state"] in ("observed", "materialized", "demoted", "expired") \
