@@ -147,6 +147,11 @@ __device__ __forceinline__ u32 shift_down(u32 v) {
   return (u32)__builtin_amdgcn_update_dpp((int)v, (int)v, 0x130 /* wave_shl:1 */, 0xF, 0xF, false);
 }
 
+// storage of NQ claim sets: one register per set (an array for one set, a vector for four)
+template <int NQ> struct QSets;
+template <> struct QSets<1> { typedef u32 type[1]; };
+template <> struct QSets<4> { typedef u32 type __attribute__((ext_vector_type(4))); };
+
 // chain record: n | hold, prot | bt, nx | covA, stop | sbot (16-bit halves, 16 bytes)
 struct G0 { u32 n, hold, prot, bt, nx, covA, stop, sbot; };
 
@@ -205,13 +210,15 @@ struct Lean {
   __device__ __forceinline__ void write_rejected_record(u32 s, u32 id, u32 packed) {
     if (lane < 9) rec[s].w[lane] = lane == 0 ? (i32)id : lane == 1 ? (i32)packed : lane < 8 ? -1 : 0;
   }
-  // live claims, one per lane of each set
-  u32 qa[NQ];  // id | chain
-  u32 qb[NQ];  // L | T
-  u32 qc[NQ];  // meta | slot
-  u32 qd[NQ];  // duration | blocked count
-  u32 qe[NQ];  // demote step | expire step
-  u32 qf[NQ];  // predicate-failure step | harm step
+  // live claims, one per lane of each set (a vector of NQ registers, so that the sets stay in
+  // registers whatever the compiler does with the loops over them)
+  typedef typename QSets<NQ>::type qv;
+  qv qa;  // id | chain
+  qv qb;  // L | T
+  qv qc;  // meta | slot
+  qv qd;  // duration | blocked count
+  qv qe;  // demote step | expire step
+  qv qf;  // predicate-failure step | harm step
   u32 tv;  // pool telemetry word `lane`
   // scalars
   u32 F, A, PR, peak, Eall, fbl;
@@ -1388,8 +1395,8 @@ __global__ __launch_bounds__(1024) void rkc_lean_order_identity(i32 n_pools, u32
 
 // One wavefront per pool, in the launch order above; the pool's policy selects its specialized
 // event loop once.  With four claim sets the registers, not LDS, bound residency: the kernel is
-// held to 6 waves per SIMD (80 vector registers; 5 waves and 87 registers otherwise, measured
-// slower: nested 10.8 vs 10.2 ms, 7 and 8 waves 10.7 and 10.6 ms).
+// held to 6 waves per SIMD (80 vector registers, a few values spilled to scratch; 5 waves and 93
+// registers otherwise, measured slower: nested 9.9 vs 9.3 ms).
 template <int NS, int NQ>
 __global__ __launch_bounds__(64, NQ > 1 ? 6 : 1) void rkc_lean(rkc_lean_args g) {
   extern __shared__ __align__(16) unsigned char lds_raw[];
