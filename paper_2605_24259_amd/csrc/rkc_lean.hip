@@ -199,16 +199,19 @@ struct Lean {
   // nodes [0, NL) in LDS, the rest in global scratch (a zipf pool of 256 chains peaks at ~80-115
   // live nodes, the 80-block pools at ~35)
   static constexpr u32 NL = NS == 4 ? 128u : 64u;
-  uint4* fifo;
+  u32x2* fifo;  // finished requests' private runs: finish step | low end << 16, top (16-bit fields)
   uint4* dq;  // deferred requests: PREFILL step, S, chain, P
-  // Claim records: a rejected or malformed claim's words 0..8 are written when it happens, a live
-  // claim's by its own lane when it is released or at the end; word 9 (lead_end) of every used slot
-  // by the final pass, from the slot's L | chain << 16 in `slotlc` (0 for a malformed claim).
+  // Claim records.  A live claim's words 0..8 are written by its own lane when it is released or at
+  // the end; everything else by the final pass, from the slot table: per slot (x) L | chain << 16
+  // (0 for a malformed claim), from which lead_end follows, and (y) NEVER for a claim that became
+  // live, else the claim id | its packed word << 16 (a rejected or malformed claim, whose record the
+  // final pass writes whole: those records, most of a pool's, then go out as full consecutive lines
+  // instead of pieces).  The packed word of such a claim never has the relaxed-by-runtime bit (15),
+  // so its bit 16 (offloadable) travels in bit 15.
   rkc_claim_telemetry* rec;
-  u32* slotlc;
-  // words 0..8 of the record of a claim no step ever happens to (rejected or malformed)
-  __device__ __forceinline__ void write_rejected_record(u32 s, u32 id, u32 packed) {
-    if (lane < 9) rec[s].w[lane] = lane == 0 ? (i32)id : lane == 1 ? (i32)packed : lane < 8 ? -1 : 0;
+  u32x2* slot2;
+  __device__ __forceinline__ static u32 pack_rejected(u32 id, u32 packed) {
+    return id | ((packed & 0x7FFFu) | ((packed >> 16) << 15)) << 16;
   }
   // live claims, one per lane of each set (a vector of NQ registers, so that the sets stay in
   // registers whatever the compiler does with the loops over them)
@@ -532,8 +535,9 @@ struct Lean {
   __device__ __forceinline__ void fifo_pop() {
     qh++;
     if (qh != qt) {
-      const uint4 e = fifo[qh];
-      ft = ufl(e.x); flo = ufl(e.y); ftop = ufl(e.z);
+      const u32x2 e = fifo[qh];
+      const u32 x = ufl(e.x);
+      ft = lo16(x); flo = hi16(x); ftop = ufl(e.y);
     }
   }
 
@@ -986,8 +990,7 @@ struct Lean {
       bool ok = !bad;
       if (ok && ncl >= maxq()) { set_status(RKC_PS_CLAIM_TABLE); ok = false; }
       if (!ok) {
-        write_rejected_record(s, t, 0);
-        slotlc[s] = 0;  // every lane, one value
+        slot2[s] = u32x2{0u, pack_rejected(t, 0)};  // every lane, one value
         o.code = RKC_OC_INVALID;
       } else {
         const u32 L = w1, c = w2, T = w3;
@@ -1004,15 +1007,14 @@ struct Lean {
         if (!r.ok) {
           const u32 dec = obs ? DEC_SHADOW : DEC_REJECTED;
           const u32 m = ST_REJECTED | (eff << 3) | (hardq << 5) | (prio << 6) | (dec << 9) | req_bits;
-          write_rejected_record(s, t, packed_of(m));
-          slotlc[s] = pk(L, c);
+          slot2[s] = u32x2{pk(L, c), pack_rejected(t, packed_of(m))};
           o.code = RKC_OC_MATFAIL;
           o.id = (i32)t;
           o.a = (i32)need;
           o.b = (i32)(F + r.E);
           tadd(TW_ACCEPTED + dec - DEC_ACCEPTED, 1);
         } else {
-          slotlc[s] = pk(L, c);  // every lane, one value
+          slot2[s] = u32x2{pk(L, c), NEVER};  // every lane, one value
           const u32 lowered = (mode == RKC_MODE_SOFT) && hardq;
           const u32 dec = obs ? DEC_SHADOW : lowered ? DEC_APPROX : DEC_ACCEPTED;
           const u32 st = obs ? ST_OBSERVED : ST_MATERIALIZED;
@@ -1071,7 +1073,7 @@ struct Lean {
       if (kept > 0) {
         cold_fifo_in();
         if (qh == qt) { ft = t; flo = R; ftop = len; }
-        fifo[qt] = make_uint4(t, R, len, 0);  // every lane, one value
+        fifo[qt] = u32x2{pk(t, R), len};  // every lane, one value
         qt++;
         cold_fifo_out();
       }
@@ -1224,8 +1226,8 @@ __device__ __forceinline__ void replay_pool(const rkc_lean_args& g, const rkc_po
   P.ndl = (lds_u32x2*)(lds + g.off_nodes / 4);
   unsigned char* scr = (unsigned char*)g.scratch + (u64)pool * g.scr_pool_bytes;
   P.ndg = (glb_u32x2*)(scr + g.scr_off_nodes);
-  P.fifo = (uint4*)(scr + g.scr_off_fifo);
-  P.slotlc = (u32*)(scr + g.scr_off_slots);
+  P.fifo = (u32x2*)(scr + g.scr_off_fifo);
+  P.slot2 = (u32x2*)(scr + g.scr_off_slots);
   P.dq = (uint4*)(scr + g.scr_off_defer);
   P.rec = g.claim_tel + slot_off;
 
@@ -1294,8 +1296,15 @@ __device__ __forceinline__ void replay_pool(const rkc_lean_args& g, const rkc_po
   // records for unused slots.
   for (u32 s = P.lane; s < nslots; s += 64) {
     if (s < nslot_used) {
-      const u32 lc = P.slotlc[s];
-      P.rec[s].w[9] = (i32)min(P.chain_n(hi16(lc)), lo16(lc));
+      const u32x2 v = P.slot2[s];
+      const i32 le = (i32)min(P.chain_n(hi16(v.x)), lo16(v.x));
+      if (v.y == NEVER) {
+        P.rec[s].w[9] = le;
+      } else {
+        const u32 pw = hi16(v.y);
+        const i32 packed = (i32)((pw & 0x7FFFu) | ((pw >> 15) << 16));
+        P.rec[s] = rkc_claim_telemetry{{(i32)lo16(v.y), packed, -1, -1, -1, -1, -1, -1, 0, le}};
+      }
     } else {
       P.rec[s] = rkc_claim_telemetry{{-1, 0, -1, -1, -1, -1, -1, -1, 0, 0}};
     }
@@ -1465,8 +1474,8 @@ bool rkc_lean_layout(const rkc_batch* b, rkc_lean_args* g) {
   g->scr_off_nodes = s;
   s += 8ull * (g->node_cap > g->nodes_lds ? g->node_cap - g->nodes_lds : 0u);
   s = align_up(s, 256);
-  g->scr_off_fifo = s; s += 16ull * ((u64)b->max_events + 1); s = align_up(s, 256);
-  g->scr_off_slots = s; s += 4ull * (u64)(b->max_claim_slots > 0 ? b->max_claim_slots : 1);
+  g->scr_off_fifo = s; s += 8ull * ((u64)b->max_events + 1); s = align_up(s, 256);
+  g->scr_off_slots = s; s += 8ull * (u64)(b->max_claim_slots > 0 ? b->max_claim_slots : 1);
   s = align_up(s, 256);
   g->scr_off_defer = s; s += 16ull * reqs;
   g->scr_pool_bytes = align_up(s, 256);
