@@ -193,7 +193,21 @@ struct Lean {
   lds_u32* kk;
   lds_u32* hist;  // outcomes per code (16 counters; entry 15 collects the lanes past the end)
   lds_u32x4* ch;
+  // live requests: entries [0, RQL) in LDS, the rest in global scratch.  With one claim set the
+  // LDS a pool takes sets how many pools share a CU, and a zipf pool that allows 256 live requests
+  // holds ~50 on average and 165 at most, so half of them stay in LDS (18 -> 21 pools per CU); with
+  // four claim sets the registers set it, and all 256 stay in LDS.
+  static constexpr u32 RQL = NQ == 4 ? 256u : 128u;
   lds_u32x2* rq;
+  glb_u32x2* rqg;
+  __device__ __forceinline__ u32x2 rq_ld(u32 j) const {
+    u32x2 v;
+    if (RQL >= 256u || j < RQL) v = rq[j]; else v = rqg[j - RQL];
+    return v;
+  }
+  __device__ __forceinline__ void rq_st(u32 j, u32x2 v) {
+    if (RQL >= 256u || j < RQL) rq[j] = v; else rqg[j - RQL] = v;
+  }
   lds_u32x2* ndl;
   glb_u32x2* ndg;
   // nodes [0, NL) in LDS, the rest in global scratch (a zipf pool of 256 chains peaks at ~80-115
@@ -693,9 +707,9 @@ struct Lean {
     for (u32 base = i; base + 1 < n; base += 64) {
       const u32 j = base + lane;
       const u32 src = min(j + 1, n - 1);
-      const u32x2 v = rq[src];
+      const u32x2 v = rq_ld(src);
       __builtin_amdgcn_wave_barrier();
-      if (j + 1 < n) rq[j] = v;
+      if (j + 1 < n) rq_st(j, v);
       __builtin_amdgcn_wave_barrier();
     }
   }
@@ -706,26 +720,26 @@ struct Lean {
     u32 below = 0;
     for (u32 base = 0; base < n; base += 64) {
       const u32 j = base + lane;
-      below += (u32)(j < n && lo16(rq[min(j, n - 1)].x) < id);
+      below += (u32)(j < n && lo16(rq_ld(min(j, n - 1)).x) < id);
     }
     const u32 k = wsum(below);
     for (u32 top = n; top > k;) {
       const u32 base = top - k > 64 ? top - 64 : k;
       const u32 j = base + lane;
-      const u32x2 v = rq[min(j, top - 1)];
+      const u32x2 v = rq_ld(min(j, top - 1));
       __builtin_amdgcn_wave_barrier();
-      if (j < top) rq[j + 1] = v;
+      if (j < top) rq_st(j + 1, v);
       __builtin_amdgcn_wave_barrier();
       top = base;
     }
-    rq[k] = e;
+    rq_st(k, e);
   }
   // largest R of the live requests on chain c
   __device__ __forceinline__ u32 rq_hold(u32 c, u32 n) {
     u32 hv = 0;
     for (u32 base = 0; base < n; base += 64) {
       const u32 j = base + lane;
-      const u32x2 v = rq[min(j, n - 1)];
+      const u32x2 v = rq_ld(min(j, n - 1));
       hv = max(hv, (j < n && hi16(v.x) == c) ? lo16(v.y) : 0u);
     }
     return wmax(hv);
@@ -907,7 +921,7 @@ struct Lean {
         dq_pop(dh, dl);
         tadd(TW_RETRY_SERVED, 1);
       } else {
-        rq[nreq] = e;
+        rq_st(nreq, e);
       }
       nreq++;
       o.id = (i32)rid;
@@ -968,9 +982,9 @@ struct Lean {
         refusal(need, -1, 0, 0, g, o);
       } else {
         A += need;
-        u32x2 e = rq[i];
+        u32x2 e = rq_ld(i);
         e.x = ufl(e.x); e.y = ufl(e.y);
-        rq[i] = u32x2{e.x, pk(lo16(e.y), hi16(e.y) + need)};
+        rq_st(i, u32x2{e.x, pk(lo16(e.y), hi16(e.y) + need)});
         o.id = (i32)lo16(e.x);
         o.b = (i32)A;
         served(r, o);
@@ -1051,7 +1065,7 @@ struct Lean {
   __device__ __forceinline__ void ev_finish(u32 t, u32 w1, Out& o) {
     if (nreq > 0) {
       const u32 i = umod(w1, nreq);
-      u32x2 e = rq[i];
+      u32x2 e = rq_ld(i);
       e.x = ufl(e.x); e.y = ufl(e.y);
       const u32 rid = lo16(e.x), c = hi16(e.x), R = lo16(e.y), len = hi16(e.y);
       rq_remove(i, nreq);
@@ -1229,6 +1243,7 @@ __device__ __forceinline__ void replay_pool(const rkc_lean_args& g, const rkc_po
   P.fifo = (u32x2*)(scr + g.scr_off_fifo);
   P.slot2 = (u32x2*)(scr + g.scr_off_slots);
   P.dq = (uint4*)(scr + g.scr_off_defer);
+  P.rqg = (glb_u32x2*)(scr + g.scr_off_reqs);
   P.rec = g.claim_tel + slot_off;
 
   for (u32 c = P.lane; c < LP::KC; c += 64) P.kk[c] = KINF;
@@ -1467,7 +1482,8 @@ bool rkc_lean_layout(const rkc_batch* b, rkc_lean_args* g) {
   g->off_cold = take(4ull * 16);
   g->off_hist = take(4ull * 16);
   g->off_chains = take(16ull * chains);
-  g->off_reqs = take(8ull * reqs);
+  const u32 rql = g->nq == 4 ? 256u : 128u;  // LP::RQL
+  g->off_reqs = take(8ull * (reqs < rql ? reqs : rql));
   g->off_nodes = take(8ull * g->nodes_lds);
   g->lds_bytes = (u32)align_up(o, 16);
   u64 s = 0;
@@ -1478,6 +1494,8 @@ bool rkc_lean_layout(const rkc_batch* b, rkc_lean_args* g) {
   g->scr_off_slots = s; s += 8ull * (u64)(b->max_claim_slots > 0 ? b->max_claim_slots : 1);
   s = align_up(s, 256);
   g->scr_off_defer = s; s += 16ull * reqs;
+  s = align_up(s, 256);
+  g->scr_off_reqs = s; s += 8ull * (reqs > rql ? reqs - rql : 0u);
   g->scr_pool_bytes = align_up(s, 256);
   const u64 np = b->n_pools > 0 ? (u64)b->n_pools : 0u;
   const u64 tiles = (np + kOrderTile - 1) / kOrderTile;
