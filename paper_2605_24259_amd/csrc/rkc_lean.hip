@@ -211,8 +211,10 @@ struct Lean {
   lds_u32x2* ndl;
   glb_u32x2* ndg;
   // nodes [0, NL) in LDS, the rest in global scratch (a zipf pool of 256 chains peaks at ~80-115
-  // live nodes, the 80-block pools at ~35)
-  static constexpr u32 NL = NS == 4 ? 128u : 64u;
+  // live nodes, the 80-block pools at ~35).  With 256 chains only 16 stay in LDS: the 896 bytes
+  // this frees bring a pool's LDS to 6,400 B, five of the 1,280-byte units the CU allocates LDS in,
+  // so 25 pools share a CU instead of 21, which outweighs the slower node accesses.
+  static constexpr u32 NL = NS == 4 ? 16u : 64u;
   u32x2* fifo;  // finished requests' private runs: finish step | low end << 16, top (16-bit fields)
   uint4* dq;  // deferred requests: PREFILL step, S, chain, P
   // Claim records.  A live claim's words 0..8 are written by its own lane when it is released or at
@@ -1475,7 +1477,7 @@ bool rkc_lean_layout(const rkc_batch* b, rkc_lean_args* g) {
   const u32 reqs = b->max_live_requests > 0 ? (u32)b->max_live_requests : 1u;
   g->ns = ns;
   g->node_cap = (u32)b->max_events + 2;
-  g->nodes_lds = ns == 4 ? 128u : 64u;  // LP::NL
+  g->nodes_lds = ns == 4 ? 16u : 64u;  // LP::NL
   u64 o = 0;
   auto take = [&](u64 bytes) { o = align_up(o, 16); u64 r = o; o += bytes; return (u32)r; };
   g->off_keys = take(4ull * 64 * ns);
