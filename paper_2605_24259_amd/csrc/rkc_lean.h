@@ -19,7 +19,7 @@ struct rkc_lean_args {
   int32_t n_pools, max_usable, max_events, max_chains, max_reqs, max_claims, max_slots;
   // layout: LDS byte offsets, node split, per-pool scratch regions
   uint32_t ns, nq, node_cap, nodes_lds;  // 64-chain key groups, 64-claim sets, node split
-  uint32_t off_keys, off_hist, off_cold, off_chains, off_reqs, off_nodes, lds_bytes;
+  uint32_t lds_bytes;  // LDS per pool (its regions sit at offsets fixed per kernel instantiation)
   uint64_t scr_pool_bytes, scr_off_nodes, scr_off_fifo, scr_off_slots, scr_off_defer, scr_off_reqs;
   // after the per-pool regions: the launch order (one u32 pool index per workgroup), each pool's
   // loop class (one byte) and per-tile class counts of the ordering passes

@@ -159,6 +159,25 @@ struct AllocRes {
   u32 ok, E, victims, resident, post, unclaimed;
 };
 
+// LDS of one pool (bytes), fixed per instantiation so that every region's address is a constant
+// of the code (no registers hold LDS bases): status block, outcome counters, eviction keys, chain
+// records, the LDS part of the live-request list and of the touch-stack node pool.  NS and NQ
+// bound the chains (64 NS) and the live requests kept in LDS; with one claim set the LDS a pool
+// takes sets how many pools share a CU (the CU allocates LDS in 1,280-byte units), with four the
+// registers set it.
+template <int NS, int NQ>
+struct LdsMap {
+  // live requests in LDS: a zipf pool that allows 256 live requests holds ~50 on average and 165 at
+  // most, so with one claim set half of them stay in LDS and the rest go to global scratch
+  static constexpr u32 RQL = NQ == 4 ? 256u : 128u;
+  // touch-stack nodes in LDS (a zipf pool of 256 chains peaks at ~80-115 live nodes, the 80-block
+  // pools at ~35): with 256 chains only 16, which brings a pool to 6,400 B, five allocation units,
+  // so 25 pools share a CU instead of 21 (more than paying for the slower node accesses)
+  static constexpr u32 NL = NS == 4 ? 16u : 64u;
+  static constexpr u32 COLD = 0, HIST = 64, KEYS = 128, CH = KEYS + 256u * NS, RQ = CH + 1024u * NS,
+                       ND = RQ + 8u * RQL, BYTES = ND + 8u * NL;
+};
+
 // ---- one pool ---------------------------------------------------------------------------------
 // NS: 64-key groups (chains <= 64 NS); NQ: 64-claim sets (live claims <= 64 NQ; claim j sits in lane
 // j mod 64 of set j / 64); MODE: the pool policy, fixed at compile time so that each policy's event
@@ -193,11 +212,8 @@ struct Lean {
   lds_u32* kk;
   lds_u32* hist;  // outcomes per code (16 counters; entry 15 collects the lanes past the end)
   lds_u32x4* ch;
-  // live requests: entries [0, RQL) in LDS, the rest in global scratch.  With one claim set the
-  // LDS a pool takes sets how many pools share a CU, and a zipf pool that allows 256 live requests
-  // holds ~50 on average and 165 at most, so half of them stay in LDS (18 -> 21 pools per CU); with
-  // four claim sets the registers set it, and all 256 stay in LDS.
-  static constexpr u32 RQL = NQ == 4 ? 256u : 128u;
+  // live requests: entries [0, RQL) in LDS, the rest in global scratch
+  static constexpr u32 RQL = LdsMap<NS, NQ>::RQL;
   lds_u32x2* rq;
   glb_u32x2* rqg;
   __device__ __forceinline__ u32x2 rq_ld(u32 j) const {
@@ -210,11 +226,8 @@ struct Lean {
   }
   lds_u32x2* ndl;
   glb_u32x2* ndg;
-  // nodes [0, NL) in LDS, the rest in global scratch (a zipf pool of 256 chains peaks at ~80-115
-  // live nodes, the 80-block pools at ~35).  With 256 chains only 16 stay in LDS: the 896 bytes
-  // this frees bring a pool's LDS to 6,400 B, five of the 1,280-byte units the CU allocates LDS in,
-  // so 25 pools share a CU instead of 21, which outweighs the slower node accesses.
-  static constexpr u32 NL = NS == 4 ? 16u : 64u;
+  // nodes [0, NL) in LDS, the rest in global scratch
+  static constexpr u32 NL = LdsMap<NS, NQ>::NL;
   u32x2* fifo;  // finished requests' private runs: finish step | low end << 16, top (16-bit fields)
   uint4* dq;  // deferred requests: PREFILL step, S, chain, P
   // Claim records.  A live claim's words 0..8 are written by its own lane when it is released or at
@@ -1236,10 +1249,11 @@ __device__ __forceinline__ void replay_pool(const rkc_lean_args& g, const rkc_po
   const u32 U = (u32)d.usable_blocks, nch = (u32)d.n_chains, nslots = (u32)d.n_claim_slots;
 
   lds_u32* lds = (lds_u32*)lds_raw;
-  P.kk = lds + g.off_keys / 4;
-  P.ch = (lds_u32x4*)(lds + g.off_chains / 4);
-  P.rq = (lds_u32x2*)(lds + g.off_reqs / 4);
-  P.ndl = (lds_u32x2*)(lds + g.off_nodes / 4);
+  typedef LdsMap<NS, NQ> M;
+  P.kk = lds + M::KEYS / 4;
+  P.ch = (lds_u32x4*)(lds + M::CH / 4);
+  P.rq = (lds_u32x2*)(lds + M::RQ / 4);
+  P.ndl = (lds_u32x2*)(lds + M::ND / 4);
   unsigned char* scr = (unsigned char*)g.scratch + (u64)pool * g.scr_pool_bytes;
   P.ndg = (glb_u32x2*)(scr + g.scr_off_nodes);
   P.fifo = (u32x2*)(scr + g.scr_off_fifo);
@@ -1249,7 +1263,7 @@ __device__ __forceinline__ void replay_pool(const rkc_lean_args& g, const rkc_po
   P.rec = g.claim_tel + slot_off;
 
   for (u32 c = P.lane; c < LP::KC; c += 64) P.kk[c] = KINF;
-  P.hist = lds + g.off_hist / 4;
+  P.hist = lds + M::HIST / 4;
   if (P.lane < 16) P.hist[P.lane] = 0;
   const u32 nrec = nch > 0 ? nch : 1u;
   for (u32 c = P.lane; c < nrec; c += 64) {
@@ -1260,7 +1274,7 @@ __device__ __forceinline__ void replay_pool(const rkc_lean_args& g, const rkc_po
   P.tv = 0;
   P.F = U; P.A = 0; P.PR = 0; P.peak = 0; P.Eall = 0; P.fbl = 0;
   P.nreq = 0; P.ncl = 0; P.nexp = NEVER;
-  P.cold = lds + g.off_cold / 4;
+  P.cold = lds + M::COLD / 4;
   if (P.lane < LP::C_WORDS) P.cold[P.lane] = P.lane == LP::C_FNODE ? NIL : P.lane == LP::C_DQC ? 1u : 0u;
   __syncthreads();
 
@@ -1477,17 +1491,16 @@ bool rkc_lean_layout(const rkc_batch* b, rkc_lean_args* g) {
   const u32 reqs = b->max_live_requests > 0 ? (u32)b->max_live_requests : 1u;
   g->ns = ns;
   g->node_cap = (u32)b->max_events + 2;
-  g->nodes_lds = ns == 4 ? 16u : 64u;  // LP::NL
-  u64 o = 0;
-  auto take = [&](u64 bytes) { o = align_up(o, 16); u64 r = o; o += bytes; return (u32)r; };
-  g->off_keys = take(4ull * 64 * ns);
-  g->off_cold = take(4ull * 16);
-  g->off_hist = take(4ull * 16);
-  g->off_chains = take(16ull * chains);
-  const u32 rql = g->nq == 4 ? 256u : 128u;  // LP::RQL
-  g->off_reqs = take(8ull * (reqs < rql ? reqs : rql));
-  g->off_nodes = take(8ull * g->nodes_lds);
-  g->lds_bytes = (u32)align_up(o, 16);
+  u32 rql;
+  if (g->nq == 4) {
+    g->lds_bytes = LdsMap<1, 4>::BYTES; g->nodes_lds = LdsMap<1, 4>::NL; rql = LdsMap<1, 4>::RQL;
+  } else if (ns == 1) {
+    g->lds_bytes = LdsMap<1, 1>::BYTES; g->nodes_lds = LdsMap<1, 1>::NL; rql = LdsMap<1, 1>::RQL;
+  } else if (ns == 2) {
+    g->lds_bytes = LdsMap<2, 1>::BYTES; g->nodes_lds = LdsMap<2, 1>::NL; rql = LdsMap<2, 1>::RQL;
+  } else {
+    g->lds_bytes = LdsMap<4, 1>::BYTES; g->nodes_lds = LdsMap<4, 1>::NL; rql = LdsMap<4, 1>::RQL;
+  }
   u64 s = 0;
   g->scr_off_nodes = s;
   s += 8ull * (g->node_cap > g->nodes_lds ? g->node_cap - g->nodes_lds : 0u);
