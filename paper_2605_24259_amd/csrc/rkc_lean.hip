@@ -224,6 +224,22 @@ struct Lean {
   __device__ __forceinline__ void rq_st(u32 j, u32x2 v) {
     if (RQL >= 256u || j < RQL) rq[j] = v; else rqg[j - RQL] = v;
   }
+  // entry j's length grows by k; returns its first word
+  __device__ __forceinline__ u32 rq_grow(u32 j, u32 k) {
+    u32 x;
+    if (RQL >= 256u || j < RQL) {
+      const u32x2 e = rq[j];
+      x = ufl(e.x);
+      const u32 y = ufl(e.y);
+      rq[j] = u32x2{x, pk(lo16(y), hi16(y) + k)};
+    } else {
+      const u32x2 e = rqg[j - RQL];
+      x = ufl(e.x);
+      const u32 y = ufl(e.y);
+      rqg[j - RQL] = u32x2{x, pk(lo16(y), hi16(y) + k)};
+    }
+    return x;
+  }
   lds_u32x2* ndl;
   glb_u32x2* ndg;
   // nodes [0, NL) in LDS, the rest in global scratch
@@ -586,7 +602,8 @@ struct Lean {
         E -= evictable(ghc.n, lo, 0) - evictable(ghc.n, hlo, 0);
       }
       r.E = E;
-      if ((u64)need > (u64)F + E) {
+      // (F + E is at most twice the usable blocks and need at most 2^24: every sum here fits 32 bits)
+      if (need > F + E) {
         r.ok = 0;
       } else {
         u32 K = need - F;
@@ -681,7 +698,7 @@ struct Lean {
       const u32 p = min(ghc.prot, h);
       Pr -= p > ghc.hold ? p - ghc.hold : 0u;
     }
-    const u64 req = (u64)A + Hc + need;
+    const u32 req = A + Hc + need;
     if (Pr > 0 && req <= U()) {
       o.code = RKC_OC_REFUSED_CLAIM;
       u32 mn = NEVER, nb = 0;
@@ -788,8 +805,8 @@ struct Lean {
         const u32 lo = max(ghc.hold, ghc.prot);
         E -= evictable(ghc.n, lo, 0) - evictable(ghc.n, max(lo, h), 0);
       }
-      u64 avail = (u64)F + E;
-      if ((u64)need > avail) {
+      u32 avail = F + E;
+      if (need > avail) {
         // Per lane and claim set q, three bits of `sel`: bit q the claim is a candidate not yet
         // visited, bit 4 + q picked, bit 8 + q picked for offload (the rest of the picks are
         // demoted).  The claim fields are read from the claim registers, which stay unchanged
@@ -805,7 +822,7 @@ struct Lean {
           nleft += (u32)__builtin_popcountll(ballot(cand));
         }
         u32 room = sub0(t2cap(), ufl(cold[C_T2])), moved = 0;
-        for (u32 guard = 0; nleft > 0 && (u64)need > avail && guard < 64u * NQ; guard++) {
+        for (u32 guard = 0; nleft > 0 && need > avail && guard < 64u * NQ; guard++) {
           u32 kv = NEVER;
 #pragma unroll
           for (u32 q = 0; q < NQ; q++) kv = min(kv, ((sel >> q) & 1u) ? rkey(q) : NEVER);
@@ -845,7 +862,7 @@ struct Lean {
             avail += evictable(g.n, base, after) - evictable(g.n, base, before);
           }
         }
-        if ((u64)need <= avail) {
+        if (need <= avail) {
           u32 no = 0;
           u64 S[NQ];
 #pragma unroll
@@ -922,6 +939,7 @@ struct Lean {
       }
     } else {
       A += Hc + need;
+      peak = max(peak, A);
       u32 R = 0;
       if (hc >= 0) {
         const G0 g2 = r.victims ? rd0(cc) : g;  // victims may have shortened this chain above the hits
@@ -997,10 +1015,8 @@ struct Lean {
         refusal(need, -1, 0, 0, g, o);
       } else {
         A += need;
-        u32x2 e = rq_ld(i);
-        e.x = ufl(e.x); e.y = ufl(e.y);
-        rq_st(i, u32x2{e.x, pk(lo16(e.y), hi16(e.y) + need)});
-        o.id = (i32)lo16(e.x);
+        peak = max(peak, A);
+        o.id = (i32)lo16(rq_grow(i, need));
         o.b = (i32)A;
         served(r, o);
         if (relaxed) { o.code = RKC_OC_RELAXED; o.n16 = min(relaxed, 65535u); }
@@ -1226,7 +1242,6 @@ struct Lean {
     else if ((type & ~1u) != RKC_EV_NOP) o.code = RKC_OC_INVALID;  // NOP, or RETRY with no ring
     static_assert(RKC_EV_NOP == 6 && RKC_EV_RETRY == 7, "NOP and RETRY differ in bit 0 only");
     if (__builtin_expect(o.sweep_due != 0, 0)) o.flags |= sweep(t);
-    peak = max(peak, A);
   }
 };
 
