@@ -48,6 +48,7 @@ typedef __attribute__((address_space(3))) u32 lds_u32;
 typedef __attribute__((address_space(3))) u32x2 lds_u32x2;
 typedef __attribute__((address_space(3))) u32x4 lds_u32x4;
 typedef __attribute__((address_space(1))) u32x2 glb_u32x2;
+typedef __attribute__((address_space(1))) u32x4 glb_u32x4;
 
 constexpr u32 NIL = 0xFFFFu;       // 16-bit nil (positions, steps, indices are all below it)
 constexpr u32 KINF = 0xFFFFFFFFu;  // key of a chain with no candidate
@@ -120,6 +121,20 @@ __device__ __forceinline__ u32 sub0(u32 a, u32 b) { return a > b ? a - b : 0u; }
 // lane l of `old` replaced by the uniform value v
 __device__ __forceinline__ u32 wrl(u32 old, u32 v, u32 l) { return __lane_id() == l ? v : old; }
 __device__ __forceinline__ u64 ballot(bool p) { return __ballot(p); }
+// A wave-uniform index moved to a vector register, so that the address arithmetic of an LDS or
+// global access at that index runs on the vector unit: the scalar unit is the busier one, and a
+// global address from a scalar index takes three scalar instructions (64-bit shift and add).
+__device__ __forceinline__ u32 vx(u32 i) {
+  u32 r;
+  asm("v_mov_b32 %0, %1" : "=v"(r) : "s"(ufl(i)));
+  return r;
+}
+// &base[i] for a wave-uniform i, the byte offset formed on the vector unit (a 32-bit offset to a
+// scalar base, which the global instructions take as such)
+template <class T>
+__device__ __forceinline__ T* gat(T* base, u32 i) {
+  return (T*)((__attribute__((address_space(1))) char*)base + (u64)(vx(i) * (u32)sizeof(T)));
+}
 
 // every source lane exists for the permutes used here, so the moved value never needs an old
 // value and the move folds into the consuming min / max / add
@@ -224,19 +239,30 @@ struct Lean {
   __device__ __forceinline__ void rq_st(u32 j, u32x2 v) {
     if (RQL >= 256u || j < RQL) rq[j] = v; else rqg[j - RQL] = v;
   }
-  // entry j's length grows by k; returns its first word
+  // the same for a wave-uniform j (address arithmetic on the vector unit)
+  __device__ __forceinline__ u32x2 rq_get(u32 j) const {
+    u32x2 v;
+    if (RQL >= 256u || j < RQL) v = rq[vx(j)]; else v = *gat(rqg, j - RQL);
+    return u32x2{ufl(v.x), ufl(v.y)};
+  }
+  __device__ __forceinline__ void rq_put(u32 j, u32x2 v) {
+    if (RQL >= 256u || j < RQL) rq[vx(j)] = v; else *gat(rqg, j - RQL) = v;
+  }
+  // entry j's length grows by k (a wave-uniform j); returns its first word
   __device__ __forceinline__ u32 rq_grow(u32 j, u32 k) {
     u32 x;
     if (RQL >= 256u || j < RQL) {
-      const u32x2 e = rq[j];
+      const u32 a = vx(j);
+      const u32x2 e = rq[a];
       x = ufl(e.x);
       const u32 y = ufl(e.y);
-      rq[j] = u32x2{x, pk(lo16(y), hi16(y) + k)};
+      rq[a] = u32x2{x, pk(lo16(y), hi16(y) + k)};
     } else {
-      const u32x2 e = rqg[j - RQL];
+      glb_u32x2* a = gat(rqg, j - RQL);
+      const u32x2 e = *a;
       x = ufl(e.x);
       const u32 y = ufl(e.y);
-      rqg[j - RQL] = u32x2{x, pk(lo16(y), hi16(y) + k)};
+      *a = u32x2{x, pk(lo16(y), hi16(y) + k)};
     }
     return x;
   }
@@ -244,8 +270,8 @@ struct Lean {
   glb_u32x2* ndg;
   // nodes [0, NL) in LDS, the rest in global scratch
   static constexpr u32 NL = LdsMap<NS, NQ>::NL;
-  u32x2* fifo;  // finished requests' private runs: finish step | low end << 16, top (16-bit fields)
-  uint4* dq;  // deferred requests: PREFILL step, S, chain, P
+  glb_u32x2* fifo;  // finished requests' private runs: finish step | low end << 16, top (16-bit fields)
+  glb_u32x4* dq;  // deferred requests: PREFILL step, S, chain, P
   // Claim records.  A live claim's words 0..8 are written by its own lane when it is released or at
   // the end; everything else by the final pass, from the slot table: per slot (x) L | chain << 16
   // (0 for a malformed claim), from which lead_end follows, and (y) NEVER for a claim that became
@@ -254,7 +280,7 @@ struct Lean {
   // instead of pieces).  The packed word of such a claim never has the relaxed-by-runtime bit (15),
   // so its bit 16 (offloadable) travels in bit 15.
   rkc_claim_telemetry* rec;
-  u32x2* slot2;
+  glb_u32x2* slot2;
   __device__ __forceinline__ static u32 pack_rejected(u32 id, u32 packed) {
     return id | ((packed & 0x7FFFu) | ((packed >> 16) << 15)) << 16;
   }
@@ -306,14 +332,14 @@ struct Lean {
 
   // -- chain records --
   __device__ __forceinline__ G0 rd0(u32 c) {
-    const u32x4 v = ch[c];
+    const u32x4 v = ch[vx(c)];
     const u32 a = ufl(v.x), b = ufl(v.y), d = ufl(v.z), e = ufl(v.w);
     return G0{lo16(a), hi16(a), lo16(b), hi16(b), lo16(d), hi16(d), lo16(e), hi16(e)};
   }
   __device__ __forceinline__ void wr0(u32 c, const G0& g) {
     u32x4 v;
     v.x = pk(g.n, g.hold); v.y = pk(g.prot, g.bt); v.z = pk(g.nx, g.covA); v.w = pk(g.stop, g.sbot);
-    ch[c] = v;
+    ch[vx(c)] = v;
   }
   __device__ __forceinline__ u32 chain_n(u32 c) { return lo16(((lds_u32*)(ch + c))[0]); }
   __device__ __forceinline__ u32 chain_hold(u32 c) { return hi16(((lds_u32*)(ch + c))[0]); }
@@ -321,15 +347,15 @@ struct Lean {
   // -- touch-stack nodes: x | t, up | down --
   __device__ __forceinline__ u32x2 nget(u32 i) {
     u32x2 v;
-    if (i < NL) v = ndl[i]; else v = ndg[i - NL];
+    if (i < NL) v = ndl[vx(i)]; else v = *gat(ndg, i - NL);
     v.x = ufl(v.x); v.y = ufl(v.y);
     return v;
   }
   __device__ __forceinline__ void nset(u32 i, u32x2 v) {
-    if (i < NL) ndl[i] = v; else ndg[i - NL] = v;
+    if (i < NL) ndl[vx(i)] = v; else *gat(ndg, i - NL) = v;
   }
   __device__ __forceinline__ void nset_y(u32 i, u32 y) {
-    if (i < NL) ((lds_u32*)(ndl + i))[1] = y; else ((__attribute__((address_space(1))) u32*)(ndg + (i - NL)))[1] = y;
+    if (i < NL) ((lds_u32*)(ndl + vx(i)))[1] = y; else ((__attribute__((address_space(1))) u32*)gat(ndg, i - NL))[1] = y;
   }
   __device__ __forceinline__ u32 nalloc() {
     u32 i;
@@ -462,7 +488,7 @@ struct Lean {
     g.n = nn; g.hold = hh; g.prot = pp;
     cold_nodes_in();
     if (x) touch(g, x, t);
-    kk[c] = top_key(c, g);
+    kk[vx(c)] = top_key(c, g);
     cold_nodes_out();
     wr0(c, g);
   }
@@ -580,7 +606,7 @@ struct Lean {
   __device__ __forceinline__ void fifo_pop() {
     qh++;
     if (qh != qt) {
-      const u32x2 e = fifo[qh];
+      const u32x2 e = *gat(fifo, qh);
       const u32 x = ufl(e.x);
       ft = lo16(x); flo = hi16(x); ftop = ufl(e.y);
     }
@@ -611,7 +637,7 @@ struct Lean {
         cold_fifo_in();
         cold_nodes_in();
         // the hit chain stops being a candidate once only hits remain
-        if (hc >= 0 && ghc.n <= hlo) kk[hc] = KINF;
+        if (hc >= 0 && ghc.n <= hlo) kk[vx(hc)] = KINF;
         for (u32 guard = 0; K > 0; guard++) {
           u32 kmin;
           if (NS == 4) {
@@ -675,7 +701,7 @@ struct Lean {
             K -= m;
             u32 key = top_key(c, g);
             if ((i32)c == hc && nw <= lo) key = KINF;
-            kk[c] = key;
+            kk[vx(c)] = key;
             wr0(c, g);
           } else {
             set_status(0x80000000u);  // cannot happen: feasibility was checked
@@ -764,7 +790,7 @@ struct Lean {
       __builtin_amdgcn_wave_barrier();
       top = base;
     }
-    rq_st(k, e);
+    rq_put(k, e);
   }
   // largest R of the live requests on chain c
   __device__ __forceinline__ u32 rq_hold(u32 c, u32 n) {
@@ -931,7 +957,7 @@ struct Lean {
           const u32 h0 = ufl(hl.x), l0 = ufl(hl.y);
           if (l0 < maxr()) {
             const u32 slot = h0 + l0 >= maxr() ? h0 + l0 - maxr() : h0 + l0;
-            dq[slot] = make_uint4(t, S, cc, P);  // every lane, one value
+            *gat(dq, slot) = u32x4{t, S, cc, P};  // every lane, one value
             cold[C_DQL] = l0 + 1;
             o.code = RKC_OC_DEFERRED;
           }
@@ -954,7 +980,7 @@ struct Lean {
         dq_pop(dh, dl);
         tadd(TW_RETRY_SERVED, 1);
       } else {
-        rq_st(nreq, e);
+        rq_put(nreq, e);
       }
       nreq++;
       o.id = (i32)rid;
@@ -996,7 +1022,7 @@ struct Lean {
         o.code = RKC_OC_INVALID;  // the request stays queued
         set_status(RKC_PS_REQUEST_TABLE);
       } else {
-        const uint4 q = dq[dh];
+        const u32x4 q = *gat(dq, dh);
         admit(t, ufl(q.x), ufl(q.y), ufl(q.z), ufl(q.w), true, dh, dl, o);
       }
     }
@@ -1035,7 +1061,7 @@ struct Lean {
       bool ok = !bad;
       if (ok && ncl >= maxq()) { set_status(RKC_PS_CLAIM_TABLE); ok = false; }
       if (!ok) {
-        slot2[s] = u32x2{0u, pack_rejected(t, 0)};  // every lane, one value
+        *gat(slot2, s) = u32x2{0u, pack_rejected(t, 0)};  // every lane, one value
         o.code = RKC_OC_INVALID;
       } else {
         const u32 L = w1, c = w2, T = w3;
@@ -1052,14 +1078,14 @@ struct Lean {
         if (!r.ok) {
           const u32 dec = obs ? DEC_SHADOW : DEC_REJECTED;
           const u32 m = ST_REJECTED | (eff << 3) | (hardq << 5) | (prio << 6) | (dec << 9) | req_bits;
-          slot2[s] = u32x2{pk(L, c), pack_rejected(t, packed_of(m))};
+          *gat(slot2, s) = u32x2{pk(L, c), pack_rejected(t, packed_of(m))};
           o.code = RKC_OC_MATFAIL;
           o.id = (i32)t;
           o.a = (i32)need;
           o.b = (i32)(F + r.E);
           tadd(TW_ACCEPTED + dec - DEC_ACCEPTED, 1);
         } else {
-          slot2[s] = u32x2{pk(L, c), NEVER};  // every lane, one value
+          *gat(slot2, s) = u32x2{pk(L, c), NEVER};  // every lane, one value
           const u32 lowered = (mode == RKC_MODE_SOFT) && hardq;
           const u32 dec = obs ? DEC_SHADOW : lowered ? DEC_APPROX : DEC_ACCEPTED;
           const u32 st = obs ? ST_OBSERVED : ST_MATERIALIZED;
@@ -1096,8 +1122,7 @@ struct Lean {
   __device__ __forceinline__ void ev_finish(u32 t, u32 w1, Out& o) {
     if (nreq > 0) {
       const u32 i = umod(w1, nreq);
-      u32x2 e = rq_ld(i);
-      e.x = ufl(e.x); e.y = ufl(e.y);
+      const u32x2 e = rq_get(i);
       const u32 rid = lo16(e.x), c = hi16(e.x), R = lo16(e.y), len = hi16(e.y);
       rq_remove(i, nreq);
       nreq--;
@@ -1118,7 +1143,7 @@ struct Lean {
       if (kept > 0) {
         cold_fifo_in();
         if (qh == qt) { ft = t; flo = R; ftop = len; }
-        fifo[qt] = u32x2{pk(t, R), len};  // every lane, one value
+        *gat(fifo, qt) = u32x2{pk(t, R), len};  // every lane, one value
         qt++;
         cold_fifo_out();
       }
@@ -1271,9 +1296,9 @@ __device__ __forceinline__ void replay_pool(const rkc_lean_args& g, const rkc_po
   P.ndl = (lds_u32x2*)(lds + M::ND / 4);
   unsigned char* scr = (unsigned char*)g.scratch + (u64)pool * g.scr_pool_bytes;
   P.ndg = (glb_u32x2*)(scr + g.scr_off_nodes);
-  P.fifo = (u32x2*)(scr + g.scr_off_fifo);
-  P.slot2 = (u32x2*)(scr + g.scr_off_slots);
-  P.dq = (uint4*)(scr + g.scr_off_defer);
+  P.fifo = (glb_u32x2*)(scr + g.scr_off_fifo);
+  P.slot2 = (glb_u32x2*)(scr + g.scr_off_slots);
+  P.dq = (glb_u32x4*)(scr + g.scr_off_defer);
   P.rqg = (glb_u32x2*)(scr + g.scr_off_reqs);
   P.rec = g.claim_tel + slot_off;
 
