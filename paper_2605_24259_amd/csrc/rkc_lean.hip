@@ -1273,7 +1273,7 @@ struct Lean {
 // Replay of one pool with policy MODE (the descriptor has been checked by the caller).
 template <int NS, int NQ, int MODE, bool EXT>
 __device__ __forceinline__ void replay_pool(const rkc_lean_args& g, const rkc_pool_desc& d, u32 pool,
-                                            unsigned char* lds_raw) {
+                                            unsigned char* lds_raw, const rkc_event* __restrict__ evs) {
   typedef Lean<NS, NQ, MODE, EXT> LP;
   LP P;
   P.lane = __lane_id();
@@ -1318,7 +1318,7 @@ __device__ __forceinline__ void replay_pool(const rkc_lean_args& g, const rkc_po
   if (P.lane < LP::C_WORDS) P.cold[P.lane] = P.lane == LP::C_FNODE ? NIL : P.lane == LP::C_DQC ? 1u : 0u;
   __syncthreads();
 
-  const rkc_event* ev = g.events + ev_off;
+  const rkc_event* __restrict__ ev = evs + ev_off;
   rkc_outcome* out = g.outcomes + ev_off;
   const u32 ne = (u32)d.n_events;
   for (u32 base = 0; base < ne; base += 64) {
@@ -1334,7 +1334,11 @@ __device__ __forceinline__ void replay_pool(const rkc_lean_args& g, const rkc_po
     for (u32 k = 0; k < cnt; k++) {
       typename LP::Out o;
       u32 expired;
-      P.step(base + k, rdl(e0, k), rdl(e1, k), rdl(e2, k), rdl(e3, k), (u32)(badm >> k) & 1u, o, expired);
+      // (the event's words straight into scalar registers: a scalar load from the read-only event
+      // array instead of four lane reads of the tile's vector load, which serves the tile-wide
+      // checks)
+      const int4 xe = *(const int4*)(ev + base + k);
+      P.step(base + k, (u32)xe.x, (u32)xe.y, (u32)xe.z, (u32)xe.w, (u32)(badm >> k) & 1u, o, expired);
       vcode = wrl(vcode, o.code, k); vflags = wrl(vflags, o.flags, k); vn16 = wrl(vn16, o.n16, k);
       vexp = wrl(vexp, expired, k); vid = wrl(vid, (u32)o.id, k); va = wrl(va, (u32)o.a, k);
       vb = wrl(vb, (u32)o.b, k);
@@ -1478,7 +1482,9 @@ __global__ __launch_bounds__(1024) void rkc_lean_order_identity(i32 n_pools, u32
 // held to 6 waves per SIMD (80 vector registers, a few values spilled to scratch; 5 waves and 93
 // registers otherwise, measured slower: nested 9.9 vs 9.3 ms).
 template <int NS, int NQ>
-__global__ __launch_bounds__(64, NQ > 1 ? 6 : 1) void rkc_lean(rkc_lean_args g) {
+// (the events come as a separate restrict-qualified argument as well, so that the compiler knows no
+// store of the replay reaches them and may read them through the scalar cache)
+__global__ __launch_bounds__(64, NQ > 1 ? 6 : 1) void rkc_lean(rkc_lean_args g, const rkc_event* __restrict__ evs) {
   extern __shared__ __align__(16) unsigned char lds_raw[];
   if ((i32)blockIdx.x >= g.n_pools) return;
   const u32 pool = ((const u32*)((const unsigned char*)g.scratch + g.scr_off_order))[blockIdx.x];
@@ -1506,11 +1512,11 @@ __global__ __launch_bounds__(64, NQ > 1 ? 6 : 1) void rkc_lean(rkc_lean_args g) 
   }
   const u32 mode = (u32)__builtin_amdgcn_readfirstlane(d.mode & ~RKC_MODE_RELAX);
   const u32 ext = (u32)__builtin_amdgcn_readfirstlane(d.defer_limit) > 0 || (d.mode & RKC_MODE_RELAX);
-  if (mode == RKC_MODE_LRU) replay_pool<NS, NQ, RKC_MODE_LRU, false>(g, d, pool, lds_raw);
-  else if (mode == RKC_MODE_SOFT) replay_pool<NS, NQ, RKC_MODE_SOFT, false>(g, d, pool, lds_raw);
-  else if (mode == RKC_MODE_NOADMIT) replay_pool<NS, NQ, RKC_MODE_NOADMIT, false>(g, d, pool, lds_raw);
-  else if (!ext) replay_pool<NS, NQ, RKC_MODE_HARD, false>(g, d, pool, lds_raw);
-  else replay_pool<NS, NQ, RKC_MODE_HARD, true>(g, d, pool, lds_raw);
+  if (mode == RKC_MODE_LRU) replay_pool<NS, NQ, RKC_MODE_LRU, false>(g, d, pool, lds_raw, evs);
+  else if (mode == RKC_MODE_SOFT) replay_pool<NS, NQ, RKC_MODE_SOFT, false>(g, d, pool, lds_raw, evs);
+  else if (mode == RKC_MODE_NOADMIT) replay_pool<NS, NQ, RKC_MODE_NOADMIT, false>(g, d, pool, lds_raw, evs);
+  else if (!ext) replay_pool<NS, NQ, RKC_MODE_HARD, false>(g, d, pool, lds_raw, evs);
+  else replay_pool<NS, NQ, RKC_MODE_HARD, true>(g, d, pool, lds_raw, evs);
 }
 
 u64 align_up(u64 v, u64 a) { return (v + a - 1) / a * a; }
@@ -1589,7 +1595,7 @@ rkc_status launch_ns(const rkc_lean_args* g, hipStream_t s) {
                        (u32*)(scr + g->scr_off_order));
   }
   if (hipGetLastError() != hipSuccess) return RKC_E_HIP;
-  hipLaunchKernelGGL((rkc_lean<NS, NQ>), dim3((unsigned)g->n_pools), dim3(64), g->lds_bytes, s, *g);
+  hipLaunchKernelGGL((rkc_lean<NS, NQ>), dim3((unsigned)g->n_pools), dim3(64), g->lds_bytes, s, *g, g->events);
   return hipGetLastError() == hipSuccess ? RKC_OK : RKC_E_HIP;
 }
 
