@@ -334,7 +334,9 @@ struct Lean {
   __device__ __forceinline__ G0 rd0(u32 c) {
     const u32x4 v = ch[vx(c)];
     const u32 a = ufl(v.x), b = ufl(v.y), d = ufl(v.z), e = ufl(v.w);
-    return G0{lo16(a), hi16(a), lo16(b), hi16(b), lo16(d), hi16(d), lo16(e), hi16(e)};
+    // (only hard-protection pools ever protect positions: elsewhere the field is 0, and saying so
+    // here lets the compiler drop the protection terms from those pools' loops)
+    return G0{lo16(a), hi16(a), hardm() ? lo16(b) : 0u, hi16(b), lo16(d), hi16(d), lo16(e), hi16(e)};
   }
   __device__ __forceinline__ void wr0(u32 c, const G0& g) {
     u32x4 v;
