@@ -622,7 +622,8 @@ struct Lean {
     if (need <= F) {
       F -= need;
     } else {
-      u32 E = Eall + fbl;
+      // (write no-admit drops finished requests' own blocks: its pools never have private runs)
+      u32 E = noadm() ? Eall : Eall + fbl;
       u32 hlo = 0;  // candidates of chain hc start at hlo
       if (hc >= 0) {
         const u32 lo = max(ghc.hold, ghc.prot);
@@ -636,7 +637,7 @@ struct Lean {
       } else {
         u32 K = need - F;
         F = 0;
-        cold_fifo_in();
+        if (!noadm()) cold_fifo_in();
         cold_nodes_in();
         // the hit chain stops being a candidate once only hits remain
         if (hc >= 0 && ghc.n <= hlo) kk[vx(hc)] = KINF;
@@ -652,7 +653,7 @@ struct Lean {
             kmin = kk[lane];
           }
           const u32 m1 = wmin(kmin);
-          const u32 kf = qh != qt ? (ft << 9) : KINF;
+          const u32 kf = !noadm() && qh != qt ? (ft << 9) : KINF;
           if (kf < m1) {
             // the oldest finished request's private run (level 0)
             const u32 m = min(K, ftop - flo);
@@ -711,7 +712,7 @@ struct Lean {
           }
           if (__builtin_expect(guard > 0x10000u, 0)) { set_status(0x80000000u); K = 0; }
         }
-        cold_fifo_out();
+        if (!noadm()) cold_fifo_out();
         cold_nodes_out();
       }
     }
