@@ -1131,9 +1131,11 @@ struct Lean {
       nreq--;
       u32 turned = 0;
       if (c != NIL) {
-        const u32 hn = rq_hold(c, nreq);
-        turned += R > hn ? R - hn : 0u;
         const G0 g = rd0(c);
+        // the chain's hold is the largest R of its live requests: it can change only when this
+        // request held it (R == hold), and only then are the others scanned
+        const u32 hn = R < g.hold ? g.hold : rq_hold(c, nreq);
+        turned += R > hn ? R - hn : 0u;
         commit(c, g, g.n, hn, g.prot, R, t);
       }
       // write no-admit drops the request's own blocks; otherwise they become a private run
