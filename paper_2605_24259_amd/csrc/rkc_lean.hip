@@ -172,6 +172,7 @@ struct G0 { u32 n, hold, prot, bt, nx, covA, stop, sbot; };
 
 struct AllocRes {
   u32 ok, E, victims, resident, post, unclaimed;
+  u32 hit;  // the allocation took blocks from the hit chain (its record changed)
 };
 
 // LDS of one pool (bytes), fixed per instantiation so that every region's address is a constant
@@ -618,7 +619,7 @@ struct Lean {
   // §5.3 ordinary eviction; hard-protected blocks are never candidates).  hc >= 0 names the chain
   // whose leading h blocks are the event's own hits (not candidates).
   __device__ __forceinline__ AllocRes alloc(u32 need, i32 hc, u32 h, const G0& ghc, u32& sweep_due) {
-    AllocRes r = {1, 0, 0, 0, 0, 0};
+    AllocRes r = {1, 0, 0, 0, 0, 0, 0};
     if (need <= F) {
       F -= need;
     } else {
@@ -668,7 +669,7 @@ struct Lean {
             G0 g = rd0(c);
             const u32 nn = g.n;
             u32 lo = max(g.hold, g.prot);
-            if ((i32)c == hc) lo = max(lo, h);
+            if ((i32)c == hc) { lo = max(lo, h); r.hit = 1; }
             // the top run shares (level, last use): positions below nx were touched later,
             // positions below a higher-level claim's footprint rank higher (only claims within
             // covA matter)
@@ -971,7 +972,7 @@ struct Lean {
       peak = max(peak, A);
       u32 R = 0;
       if (hc >= 0) {
-        const G0 g2 = r.victims ? rd0(cc) : g;  // victims may have shortened this chain above the hits
+        const G0 g2 = r.hit ? rd0(cc) : g;  // victims may have shortened this chain above the hits
         R = noadm() ? h : P;
         const u32 nn = (!noadm() && P > g2.n) ? P : g2.n;
         commit(cc, g2, nn, max(g2.hold, R), g2.prot, R, t);
@@ -1108,7 +1109,7 @@ struct Lean {
             }
           }
           if (dur_eff > 0) nexp = min(nexp, t + dur_eff);
-          G0 g2 = r.victims ? rd0(c) : g;
+          G0 g2 = r.hit ? rd0(c) : g;
           g2.covA = max(g2.covA, L);
           // a materialized hard claim in a hard-protection pool protects [0, L)
           const u32 pp = eff == RKC_PROT_HARD ? max(g2.prot, L) : g2.prot;
