@@ -1342,8 +1342,8 @@ __device__ __forceinline__ void replay_pool(const rkc_lean_args& g, const rkc_po
       u32 expired;
       // (the event's words straight into scalar registers: a scalar load from the read-only event
       // array instead of four lane reads of the tile's vector load, which serves the tile-wide
-      // checks)
-      const int4 xe = *(const int4*)(ev + base + k);
+      // checks; a 32-bit byte offset to the tile's base keeps the address a single shift)
+      const int4 xe = *(const int4*)((const char*)(ev + base) + (k << 4));
       P.step(base + k, (u32)xe.x, (u32)xe.y, (u32)xe.z, (u32)xe.w, (u32)(badm >> k) & 1u, o, expired);
       vcode = wrl(vcode, o.code, k); vflags = wrl(vflags, o.flags, k); vn16 = wrl(vn16, o.n16, k);
       vexp = wrl(vexp, expired, k); vid = wrl(vid, (u32)o.id, k); va = wrl(va, (u32)o.a, k);
