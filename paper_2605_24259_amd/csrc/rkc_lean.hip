@@ -1262,7 +1262,11 @@ struct Lean {
   __device__ __forceinline__ void step(u32 t, u32 w0, u32 w1, u32 w2, u32 w3, u32 bad, Out& o, u32& expired) {
     const u32 type = w0 & 15u;
     expired = 0;
-    o = Out{RKC_OC_NOOP, 0, NEVER, 0, -1, 0, 0};
+    // (every outcome that is not quiet sets id, a and b; a quiet one gets id -1 and a = b = 0 when
+    // the tile's outcome words are assembled, so they start unspecified here and no path pays for
+    // materializing them)
+    const i32 any = __builtin_nondeterministic_value(0);
+    o = Out{RKC_OC_NOOP, 0, NEVER, 0, any, any, any};
     if (__builtin_expect(t >= nexp, 0)) expire(t, o.flags, expired);
     if (type == RKC_EV_PREFILL) ev_prefill(t, w1, w2, w3, bad, o);
     else if (type == RKC_EV_EXTEND) ev_extend(t, w1, w2, bad, o);
