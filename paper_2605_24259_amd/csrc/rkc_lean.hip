@@ -309,7 +309,7 @@ struct Lean {
   enum : u32 { C_QH = 0, C_QT, C_FT, C_FLO, C_FTOP, C_FNODE, C_BUMP, C_NSLOT, C_VIC, C_POST, C_STATUS,
                C_DQC, C_DQH, C_DQL, C_T2, C_T2PK, C_WORDS };
   static_assert(C_QH % 4 == 0 && C_VIC % 2 == 0 && C_DQH % 2 == 0 && C_WORDS <= 16, "cold block layout");
-  u32 fnode, bump;              // valid between cold_nodes_in() and cold_nodes_out()
+  u32 fnode, bump;              // valid between cold_nodes_in() and cold_nodes_out() (touches)
   u32 qh, qt, ft, flo, ftop;    // valid between cold_fifo_in() and cold_fifo_out()
   __device__ __forceinline__ void cold_nodes_in() { fnode = ufl(cold[C_FNODE]); bump = ufl(cold[C_BUMP]); }
   __device__ __forceinline__ void cold_nodes_out() { cold[C_FNODE] = fnode; cold[C_BUMP] = bump; }
@@ -422,6 +422,8 @@ struct Lean {
     u32 key = KINF;
     if (g.n > max(g.hold, g.prot)) {
       if (g.nx >= g.n) {
+        // (rare: the node free list is read and written here, not kept in registers around it)
+        u32 fn = ufl(cold[C_FNODE]);
         u32 b = g.sbot;
         u32x2 nb = nget(b);
         u32 up = lo16(nb.y), nxv = 0;
@@ -431,8 +433,8 @@ struct Lean {
           nxv = lo16(nu.x);
           if (nxv >= g.n) {
             // node b leaves the stack: free it; up becomes the bottom (its down link is cut)
-            nset_y(b, pk(NIL, fnode));
-            fnode = b;
+            nset_y(b, pk(NIL, fn));
+            fn = b;
             b = up;
             nb = nu;
             up = lo16(nb.y);
@@ -443,6 +445,7 @@ struct Lean {
           }
         }
         nset_y(b, pk(up, NIL));
+        cold[C_FNODE] = fn;
         g.sbot = b;
         g.bt = hi16(nb.x);
         g.nx = nxv;
@@ -489,10 +492,12 @@ struct Lean {
     Eall += evictable(nn, hh, pp) - evictable(g.n, g.hold, g.prot);
     PR += protd(hh, pp) - protd(g.hold, g.prot);
     g.n = nn; g.hold = hh; g.prot = pp;
-    cold_nodes_in();
-    if (x) touch(g, x, t);
+    if (x) {
+      cold_nodes_in();
+      touch(g, x, t);
+      cold_nodes_out();
+    }
     kk[vx(c)] = top_key(c, g);
-    cold_nodes_out();
     wr0(c, g);
   }
 
@@ -639,7 +644,6 @@ struct Lean {
         u32 K = need - F;
         F = 0;
         if (!noadm()) cold_fifo_in();
-        cold_nodes_in();
         // the hit chain stops being a candidate once only hits remain
         if (hc >= 0 && ghc.n <= hlo) kk[vx(hc)] = KINF;
         for (u32 guard = 0; K > 0; guard++) {
@@ -684,12 +688,16 @@ struct Lean {
               bool due = false;
 #pragma unroll
               for (u32 q = 0; q < NQ; q++) {
-                const u32 st = m_state(lo16(qc[q]));
+                // (the barrier keeps the per-lane claim tests here, where they are needed, instead of
+                // ahead of the eviction loop, where every evicting allocation would pay for them)
+                u32 mc = lo16(qc[q]);
+                asm volatile("" : "+v"(mc));
+                const u32 st = m_state(mc);
                 const bool on = on_chain(c, q);
-                const bool off = m_eff(lo16(qc[q])) == RKC_PROT_OFFLOADED;
+                const bool off = m_eff(mc) == RKC_PROT_OFFLOADED;
                 cv = max(cv, (on && !off && (st == ST_OBSERVED || st == ST_MATERIALIZED || st == ST_HARMED)) ? lo16(qb[q]) : 0u);
                 // a claim whose predicate still holds needs more than nw leading blocks
-                due = due || (on && !off && m_pend(lo16(qc[q])) && hi16(qb[q]) > nw);
+                due = due || (on && !off && m_pend(mc) && hi16(qb[q]) > nw);
               }
               const u32 covS = wmax(cv);
               rs = min(nn, g.covA) - nw;
@@ -714,7 +722,6 @@ struct Lean {
           if (__builtin_expect(guard > 0x10000u, 0)) { set_status(0x80000000u); K = 0; }
         }
         if (!noadm()) cold_fifo_out();
-        cold_nodes_out();
       }
     }
     return r;
