@@ -300,25 +300,26 @@ struct Lean {
   u32 nreq, ncl, nexp;
   // Scalars that only a few paths touch live in LDS (`cold`), so that the registers carried around
   // the event loop are the hot counters only: node free list and bump allocator, the FIFO of
-  // private runs (head, tail, front run), claim slots used, victim counters, the status word, and
+  // private runs (head, tail, the front run's eviction key, or KINF when there is none, and its
+  // bounds), claim slots used, victim counters, the status word, and
   // the deferral ring (head, length, DEFERRED outcomes of the head entry; every entry behind the
   // head has had exactly one).
   lds_u32* cold;
   // (QH..FLO is one 16-byte group, VIC, POST and DQH, DQL 8-byte groups: keep their word offsets
   // aligned)
-  enum : u32 { C_QH = 0, C_QT, C_FT, C_FLO, C_FTOP, C_FNODE, C_BUMP, C_NSLOT, C_VIC, C_POST, C_STATUS,
+  enum : u32 { C_QH = 0, C_QT, C_FKEY, C_FLO, C_FTOP, C_FNODE, C_BUMP, C_NSLOT, C_VIC, C_POST, C_STATUS,
                C_DQC, C_DQH, C_DQL, C_T2, C_T2PK, C_WORDS };
   static_assert(C_QH % 4 == 0 && C_VIC % 2 == 0 && C_DQH % 2 == 0 && C_WORDS <= 16, "cold block layout");
   u32 fnode, bump;              // valid between cold_nodes_in() and cold_nodes_out() (touches)
-  u32 qh, qt, ft, flo, ftop;    // valid between cold_fifo_in() and cold_fifo_out()
+  u32 qh, qt, fk, flo, ftop;    // valid between cold_fifo_in() and cold_fifo_out()
   __device__ __forceinline__ void cold_nodes_in() { fnode = ufl(cold[C_FNODE]); bump = ufl(cold[C_BUMP]); }
   __device__ __forceinline__ void cold_nodes_out() { cold[C_FNODE] = fnode; cold[C_BUMP] = bump; }
   __device__ __forceinline__ void cold_fifo_in() {
-    const u32x4 v = *(lds_u32x4*)(cold + C_QH);  // QH, QT, FT, FLO
-    qh = ufl(v.x); qt = ufl(v.y); ft = ufl(v.z); flo = ufl(v.w); ftop = ufl(cold[C_FTOP]);
+    const u32x4 v = *(lds_u32x4*)(cold + C_QH);  // QH, QT, FKEY, FLO
+    qh = ufl(v.x); qt = ufl(v.y); fk = ufl(v.z); flo = ufl(v.w); ftop = ufl(cold[C_FTOP]);
   }
   __device__ __forceinline__ void cold_fifo_out() {
-    *(lds_u32x4*)(cold + C_QH) = u32x4{qh, qt, ft, flo};
+    *(lds_u32x4*)(cold + C_QH) = u32x4{qh, qt, fk, flo};
     cold[C_FTOP] = ftop;
   }
   __device__ __forceinline__ void set_status(u32 bits) { cold[C_STATUS] = ufl(cold[C_STATUS]) | bits; }
@@ -613,10 +614,11 @@ struct Lean {
 
   __device__ __forceinline__ void fifo_pop() {
     qh++;
+    fk = KINF;
     if (qh != qt) {
       const u32x2 e = *gat(fifo, qh);
       const u32 x = ufl(e.x);
-      ft = lo16(x); flo = hi16(x); ftop = ufl(e.y);
+      fk = lo16(x) << 9; flo = hi16(x); ftop = ufl(e.y);
     }
   }
 
@@ -643,7 +645,8 @@ struct Lean {
       } else {
         u32 K = need - F;
         F = 0;
-        if (!noadm()) cold_fifo_in();
+        // the front private run's key (the rest of the FIFO state is read when a run is taken)
+        u32 kf = noadm() ? KINF : ufl(cold[C_FKEY]);
         // the hit chain stops being a candidate once only hits remain
         if (hc >= 0 && ghc.n <= hlo) kk[vx(hc)] = KINF;
         for (u32 guard = 0; K > 0; guard++) {
@@ -658,9 +661,9 @@ struct Lean {
             kmin = kk[lane];
           }
           const u32 m1 = wmin(kmin);
-          const u32 kf = !noadm() && qh != qt ? (ft << 9) : KINF;
           if (kf < m1) {
             // the oldest finished request's private run (level 0)
+            cold_fifo_in();
             const u32 m = min(K, ftop - flo);
             ftop -= m;
             fbl -= m;
@@ -668,6 +671,8 @@ struct Lean {
             r.unclaimed += m;
             K -= m;
             if (ftop == flo) fifo_pop();
+            cold_fifo_out();
+            kf = fk;
           } else if (m1 != KINF) {
             const u32 c = (m1 & 511u) - 1u;
             G0 g = rd0(c);
@@ -721,7 +726,6 @@ struct Lean {
           }
           if (__builtin_expect(guard > 0x10000u, 0)) { set_status(0x80000000u); K = 0; }
         }
-        if (!noadm()) cold_fifo_out();
       }
     }
     return r;
@@ -1155,7 +1159,7 @@ struct Lean {
       fbl += kept;
       if (kept > 0) {
         cold_fifo_in();
-        if (qh == qt) { ft = t; flo = R; ftop = len; }
+        if (qh == qt) { fk = t << 9; flo = R; ftop = len; }
         *gat(fifo, qt) = u32x2{pk(t, R), len};  // every lane, one value
         qt++;
         cold_fifo_out();
@@ -1332,7 +1336,8 @@ __device__ __forceinline__ void replay_pool(const rkc_lean_args& g, const rkc_po
   P.F = U; P.A = 0; P.PR = 0; P.peak = 0; P.Eall = 0; P.fbl = 0;
   P.nreq = 0; P.ncl = 0; P.nexp = NEVER;
   P.cold = lds + M::COLD / 4;
-  if (P.lane < LP::C_WORDS) P.cold[P.lane] = P.lane == LP::C_FNODE ? NIL : P.lane == LP::C_DQC ? 1u : 0u;
+  if (P.lane < LP::C_WORDS)
+    P.cold[P.lane] = P.lane == LP::C_FNODE ? NIL : P.lane == LP::C_DQC ? 1u : P.lane == LP::C_FKEY ? KINF : 0u;
   __syncthreads();
 
   const rkc_event* __restrict__ ev = evs + ev_off;
