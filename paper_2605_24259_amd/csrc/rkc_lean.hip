@@ -298,18 +298,18 @@ struct Lean {
   // scalars
   u32 F, A, PR, peak, Eall, fbl;
   u32 nreq, ncl, nexp;
+  u32 vic, post;  // victims, post-release losses (pool telemetry words 10 and 12)
   // Scalars that only a few paths touch live in LDS (`cold`), so that the registers carried around
   // the event loop are the hot counters only: node free list and bump allocator, the FIFO of
   // private runs (head, tail, the front run's eviction key, or KINF when there is none, and its
-  // bounds), claim slots used, victim counters, the status word, and
+  // bounds), claim slots used, the status word, and
   // the deferral ring (head, length, DEFERRED outcomes of the head entry; every entry behind the
   // head has had exactly one).
   lds_u32* cold;
-  // (QH..FLO is one 16-byte group, VIC, POST and DQH, DQL 8-byte groups: keep their word offsets
-  // aligned)
-  enum : u32 { C_QH = 0, C_QT, C_FKEY, C_FLO, C_FTOP, C_FNODE, C_BUMP, C_NSLOT, C_VIC, C_POST, C_STATUS,
+  // (QH..FLO is one 16-byte group, DQH, DQL an 8-byte group: keep their word offsets aligned)
+  enum : u32 { C_QH = 0, C_QT, C_FKEY, C_FLO, C_FTOP, C_FNODE, C_BUMP, C_NSLOT, C_STATUS,
                C_DQC, C_DQH, C_DQL, C_T2, C_T2PK, C_WORDS };
-  static_assert(C_QH % 4 == 0 && C_VIC % 2 == 0 && C_DQH % 2 == 0 && C_WORDS <= 16, "cold block layout");
+  static_assert(C_QH % 4 == 0 && C_DQH % 2 == 0 && C_WORDS <= 16, "cold block layout");
   u32 fnode, bump;              // valid between cold_nodes_in() and cold_nodes_out() (touches)
   u32 qh, qt, fk, flo, ftop;    // valid between cold_fifo_in() and cold_fifo_out()
   __device__ __forceinline__ void cold_nodes_in() { fnode = ufl(cold[C_FNODE]); bump = ufl(cold[C_BUMP]); }
@@ -769,10 +769,8 @@ struct Lean {
     o.code = r.resident ? RKC_OC_EVICT_RESIDENT : RKC_OC_ADMIT;
     o.a = (i32)r.resident;
     o.flags |= (r.post ? (u32)RKC_FL_POST_RELEASE_LOSS : 0u) | (r.unclaimed ? (u32)RKC_FL_EVICT_UNCLAIMED : 0u);
-    if (r.victims) {
-      const u32x2 vp = *(lds_u32x2*)(cold + C_VIC);
-      *(lds_u32x2*)(cold + C_VIC) = u32x2{ufl(vp.x) + r.victims, ufl(vp.y) + r.post};
-    }
+    vic += r.victims;
+    post += r.post;
   }
 
   // Remove request entry i from the compact list of n entries (n <= 256).
@@ -1334,7 +1332,7 @@ __device__ __forceinline__ void replay_pool(const rkc_lean_args& g, const rkc_po
   for (u32 q = 0; q < NQ; q++) P.qa[q] = P.qb[q] = P.qc[q] = P.qd[q] = P.qe[q] = P.qf[q] = 0;
   P.tv = 0;
   P.F = U; P.A = 0; P.PR = 0; P.peak = 0; P.Eall = 0; P.fbl = 0;
-  P.nreq = 0; P.ncl = 0; P.nexp = NEVER;
+  P.nreq = 0; P.ncl = 0; P.nexp = NEVER; P.vic = 0; P.post = 0;
   P.cold = lds + M::COLD / 4;
   if (P.lane < LP::C_WORDS)
     P.cold[P.lane] = P.lane == LP::C_FNODE ? NIL : P.lane == LP::C_DQC ? 1u : P.lane == LP::C_FKEY ? KINF : 0u;
@@ -1381,7 +1379,7 @@ __device__ __forceinline__ void replay_pool(const rkc_lean_args& g, const rkc_po
   }
 
   const u32 nslot_used = ufl(P.cold[LP::C_NSLOT]);
-  const u32 vic = ufl(P.cold[LP::C_VIC]), post = ufl(P.cold[LP::C_POST]);
+  const u32 vic = P.vic, post = P.post;
   const u32 status = ufl(P.cold[LP::C_STATUS]), queued = ufl(P.cold[LP::C_DQL]);
   const u32 t2peak = ufl(P.cold[LP::C_T2PK]);
   // Final records of the claims still live (each lane writes its own) ...
