@@ -299,17 +299,18 @@ struct Lean {
   u32 F, A, PR, peak, Eall, fbl;
   u32 nreq, ncl, nexp;
   u32 vic, post;  // victims, post-release losses (pool telemetry words 10 and 12)
+  u32 nslot;      // claim slots used
   // Scalars that only a few paths touch live in LDS (`cold`), so that the registers carried around
   // the event loop are the hot counters only: node free list and bump allocator, the FIFO of
   // private runs (head, tail, the front run's eviction key, or KINF when there is none, and its
-  // bounds), claim slots used, the status word, and
+  // bounds), the status word, and
   // the deferral ring (head, length, DEFERRED outcomes of the head entry; every entry behind the
   // head has had exactly one).
   lds_u32* cold;
   // (QH..FLO is one 16-byte group, DQH, DQL an 8-byte group: keep their word offsets aligned)
-  enum : u32 { C_QH = 0, C_QT, C_FKEY, C_FLO, C_FTOP, C_FNODE, C_BUMP, C_NSLOT, C_STATUS,
-               C_DQC, C_DQH, C_DQL, C_T2, C_T2PK, C_WORDS };
-  static_assert(C_QH % 4 == 0 && C_DQH % 2 == 0 && C_WORDS <= 16, "cold block layout");
+  enum : u32 { C_QH = 0, C_QT, C_FKEY, C_FLO, C_FTOP, C_FNODE, C_BUMP, C_STATUS,
+               C_DQH, C_DQL, C_DQC, C_T2, C_T2PK, C_WORDS };
+  static_assert(C_QH % 4 == 0 && C_DQH % 2 == 0 && C_DQL == C_DQH + 1 && C_WORDS <= 16, "cold block layout");
   u32 fnode, bump;              // valid between cold_nodes_in() and cold_nodes_out() (touches)
   u32 qh, qt, fk, flo, ftop;    // valid between cold_fifo_in() and cold_fifo_out()
   __device__ __forceinline__ void cold_nodes_in() { fnode = ufl(cold[C_FNODE]); bump = ufl(cold[C_BUMP]); }
@@ -1064,13 +1065,11 @@ struct Lean {
   }
 
   __device__ __forceinline__ void ev_claim(u32 t, u32 w0, u32 w1, u32 w2, u32 w3, u32 bad, Out& o) {
-    const u32 nslot = ufl(cold[C_NSLOT]);
     if (nslot >= nslots()) {
       o.code = RKC_OC_INVALID;
       set_status(RKC_PS_SLOT_TABLE);
     } else {
-      const u32 s = nslot;
-      cold[C_NSLOT] = nslot + 1;
+      const u32 s = nslot++;
       bool ok = !bad;
       if (ok && ncl >= maxq()) { set_status(RKC_PS_CLAIM_TABLE); ok = false; }
       if (!ok) {
@@ -1332,7 +1331,7 @@ __device__ __forceinline__ void replay_pool(const rkc_lean_args& g, const rkc_po
   for (u32 q = 0; q < NQ; q++) P.qa[q] = P.qb[q] = P.qc[q] = P.qd[q] = P.qe[q] = P.qf[q] = 0;
   P.tv = 0;
   P.F = U; P.A = 0; P.PR = 0; P.peak = 0; P.Eall = 0; P.fbl = 0;
-  P.nreq = 0; P.ncl = 0; P.nexp = NEVER; P.vic = 0; P.post = 0;
+  P.nreq = 0; P.ncl = 0; P.nexp = NEVER; P.vic = 0; P.post = 0; P.nslot = 0;
   P.cold = lds + M::COLD / 4;
   if (P.lane < LP::C_WORDS)
     P.cold[P.lane] = P.lane == LP::C_FNODE ? NIL : P.lane == LP::C_DQC ? 1u : P.lane == LP::C_FKEY ? KINF : 0u;
@@ -1378,7 +1377,7 @@ __device__ __forceinline__ void replay_pool(const rkc_lean_args& g, const rkc_po
     P.tadd(TW_HITS, wsum(srv && (ty == RKC_EV_PREFILL || (LP::ext() && ty == RKC_EV_RETRY)) ? o3 : 0u));
   }
 
-  const u32 nslot_used = ufl(P.cold[LP::C_NSLOT]);
+  const u32 nslot_used = P.nslot;
   const u32 vic = P.vic, post = P.post;
   const u32 status = ufl(P.cold[LP::C_STATUS]), queued = ufl(P.cold[LP::C_DQL]);
   const u32 t2peak = ufl(P.cold[LP::C_T2PK]);
