@@ -224,6 +224,8 @@ struct Lean {
   // only hard protection refuses on behalf of claims, so only hard-protection pools can defer or
   // relax
   __device__ __forceinline__ static constexpr bool ext() { return MODE == RKC_MODE_HARD && EXT; }
+  // meta m says offloaded to the second tier (only relaxing pools offload)
+  __device__ __forceinline__ static bool offl(u32 m) { return ext() && m_eff(m) == RKC_PROT_OFFLOADED; }
   // memory
   lds_u32* kk;
   lds_u32* hist;  // outcomes per code (16 counters; entry 15 collects the lanes past the end)
@@ -512,7 +514,7 @@ struct Lean {
       const u32 L = lo16(qb[q]), m = lo16(qc[q]);
       const bool on = on_chain(c, q);
       pv = max(pv, (on && hardm() && m_state(m) == ST_MATERIALIZED && m_eff(m) == RKC_PROT_HARD) ? L : 0u);
-      cv = max(cv, on && m_eff(m) != RKC_PROT_OFFLOADED ? L : 0u);
+      cv = max(cv, on && !offl(m) ? L : 0u);
     }
     const u32 pp = wmax(pv);
     G0 g = rd0(c);
@@ -594,7 +596,7 @@ struct Lean {
     for (u32 q = 0; q < NQ; q++) {
       const u32 m = lo16(qc[q]), T = hi16(qb[q]), c = hi16(qa[q]);
       const u32 nc = chain_n(c);
-      const bool fail = live(q) && m_pend(m) && nc < T && m_eff(m) != RKC_PROT_OFFLOADED;
+      const bool fail = live(q) && m_pend(m) && nc < T && !offl(m);
       const bool harm = fail && m_state(m) == ST_MATERIALIZED;
       const u32 m2 = (m & ~(1u << 8) & ~(harm ? 7u : 0u)) | (harm ? ST_HARMED : 0u);
       qc[q] = fail ? pk(m2, hi16(qc[q])) : qc[q];
@@ -700,7 +702,7 @@ struct Lean {
                 asm volatile("" : "+v"(mc));
                 const u32 st = m_state(mc);
                 const bool on = on_chain(c, q);
-                const bool off = m_eff(mc) == RKC_PROT_OFFLOADED;
+                const bool off = offl(mc);
                 cv = max(cv, (on && !off && (st == ST_OBSERVED || st == ST_MATERIALIZED || st == ST_HARMED)) ? lo16(qb[q]) : 0u);
                 // a claim whose predicate still holds needs more than nw leading blocks
                 due = due || (on && !off && m_pend(mc) && hi16(qb[q]) > nw);
@@ -1184,7 +1186,7 @@ struct Lean {
 #pragma unroll
       for (u32 q = 0; q < NQ; q++) {
         const u32 m = lo16(qc[q]);
-        cm[q] = ballot(live(q) && m_state(m) == ST_MATERIALIZED && m_hard(m) && m_eff(m) != RKC_PROT_OFFLOADED);
+        cm[q] = ballot(live(q) && m_state(m) == ST_MATERIALIZED && m_hard(m) && !offl(m));
         cnt += (u32)__builtin_popcountll(cm[q]);
       }
       if (cnt > 0) {
@@ -1275,7 +1277,9 @@ struct Lean {
     // materializing them)
     const i32 any = __builtin_nondeterministic_value(0);
     o = Out{RKC_OC_NOOP, 0, NEVER, 0, any, any, any};
-    if (__builtin_expect(t >= nexp, 0)) expire(t, o.flags, expired);
+    // (claims in native and write no-admit pools are only observed, and observed claims never
+    // expire: those loops carry no expiry)
+    if (!shadm() && __builtin_expect(t >= nexp, 0)) expire(t, o.flags, expired);
     if (type == RKC_EV_PREFILL) ev_prefill(t, w1, w2, w3, bad, o);
     else if (type == RKC_EV_EXTEND) ev_extend(t, w1, w2, bad, o);
     else if (type == RKC_EV_CLAIM) ev_claim(t, w0, w1, w2, w3, bad, o);
