@@ -698,14 +698,17 @@ struct Lean {
               for (u32 q = 0; q < NQ; q++) {
                 // (the barrier keeps the per-lane claim tests here, where they are needed, instead of
                 // ahead of the eviction loop, where every evicting allocation would pay for them)
+                // (bitwise tests, so that no lane-dependent branch is formed)
                 u32 mc = lo16(qc[q]);
                 asm volatile("" : "+v"(mc));
                 const u32 st = m_state(mc);
-                const bool on = on_chain(c, q);
-                const bool off = offl(mc);
-                cv = max(cv, (on && !off && (st == ST_OBSERVED || st == ST_MATERIALIZED || st == ST_HARMED)) ? lo16(qb[q]) : 0u);
+                const bool on = live(q) & (hi16(qa[q]) == c) & !offl(mc);
+                // observed (1), materialized (2) or harmed (6)
+                const bool res = ((0x46u >> st) & 1u) != 0;
+                static_assert(ST_OBSERVED == 1 && ST_MATERIALIZED == 2 && ST_HARMED == 6, "state codes");
+                cv = max(cv, (on & res) ? lo16(qb[q]) : 0u);
                 // a claim whose predicate still holds needs more than nw leading blocks
-                due = due || (on && !off && m_pend(mc) && hi16(qb[q]) > nw);
+                due = due | (on & (m_pend(mc) != 0) & (hi16(qb[q]) > nw));
               }
               const u32 covS = wmax(cv);
               rs = min(nn, g.covA) - nw;
