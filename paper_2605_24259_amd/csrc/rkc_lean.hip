@@ -234,13 +234,17 @@ struct Lean {
   static constexpr u32 RQL = LdsMap<NS, NQ>::RQL;
   lds_u32x2* rq;
   glb_u32x2* rqg;
+  // (per-lane j; L: the caller knows every index it uses lies in LDS, so no lane-dependent branch
+  // between LDS and scratch is formed)
+  template <bool L>
   __device__ __forceinline__ u32x2 rq_ld(u32 j) const {
     u32x2 v;
-    if (RQL >= 256u || j < RQL) v = rq[j]; else v = rqg[j - RQL];
+    if (L || RQL >= 256u || j < RQL) v = rq[j]; else v = rqg[j - RQL];
     return v;
   }
+  template <bool L>
   __device__ __forceinline__ void rq_st(u32 j, u32x2 v) {
-    if (RQL >= 256u || j < RQL) rq[j] = v; else rqg[j - RQL] = v;
+    if (L || RQL >= 256u || j < RQL) rq[j] = v; else rqg[j - RQL] = v;
   }
   // the same for a wave-uniform j (address arithmetic on the vector unit)
   __device__ __forceinline__ u32x2 rq_get(u32 j) const {
@@ -780,46 +784,58 @@ struct Lean {
   }
 
   // Remove request entry i from the compact list of n entries (n <= 256).
-  __device__ __forceinline__ void rq_remove(u32 i, u32 n) {
+  template <bool L>
+  __device__ __forceinline__ void rq_remove_(u32 i, u32 n) {
     for (u32 base = i; base + 1 < n; base += 64) {
       const u32 j = base + lane;
       const u32 src = min(j + 1, n - 1);
-      const u32x2 v = rq_ld(src);
+      const u32x2 v = rq_ld<L>(src);
       __builtin_amdgcn_wave_barrier();
-      if (j + 1 < n) rq_st(j, v);
+      if (j + 1 < n) rq_st<L>(j, v);
       __builtin_amdgcn_wave_barrier();
     }
   }
+  __device__ __forceinline__ void rq_remove(u32 i, u32 n) {
+    if (n <= RQL) rq_remove_<true>(i, n); else rq_remove_<false>(i, n);
+  }
   // Insert entry e at its id-ordered place in the compact list of n entries (n below the
   // capacity): entries with larger ids move up one place, highest chunk first.
-  __device__ __forceinline__ void rq_insert(u32x2 e, u32 n) {
+  template <bool L>
+  __device__ __forceinline__ void rq_insert_(u32x2 e, u32 n) {
     const u32 id = lo16(e.x);
     u32 below = 0;
     for (u32 base = 0; base < n; base += 64) {
       const u32 j = base + lane;
-      below += (u32)(j < n && lo16(rq_ld(min(j, n - 1)).x) < id);
+      below += (u32)(j < n && lo16(rq_ld<L>(min(j, n - 1)).x) < id);
     }
     const u32 k = wsum(below);
     for (u32 top = n; top > k;) {
       const u32 base = top - k > 64 ? top - 64 : k;
       const u32 j = base + lane;
-      const u32x2 v = rq_ld(min(j, top - 1));
+      const u32x2 v = rq_ld<L>(min(j, top - 1));
       __builtin_amdgcn_wave_barrier();
-      if (j < top) rq_st(j + 1, v);
+      if (j < top) rq_st<L>(j + 1, v);
       __builtin_amdgcn_wave_barrier();
       top = base;
     }
     rq_put(k, e);
   }
+  __device__ __forceinline__ void rq_insert(u32x2 e, u32 n) {
+    if (n + 1 <= RQL) rq_insert_<true>(e, n); else rq_insert_<false>(e, n);
+  }
   // largest R of the live requests on chain c
-  __device__ __forceinline__ u32 rq_hold(u32 c, u32 n) {
+  template <bool L>
+  __device__ __forceinline__ u32 rq_hold_(u32 c, u32 n) {
     u32 hv = 0;
     for (u32 base = 0; base < n; base += 64) {
       const u32 j = base + lane;
-      const u32x2 v = rq_ld(min(j, n - 1));
+      const u32x2 v = rq_ld<L>(min(j, n - 1));
       hv = max(hv, (j < n && hi16(v.x) == c) ? lo16(v.y) : 0u);
     }
     return wmax(hv);
+  }
+  __device__ __forceinline__ u32 rq_hold(u32 c, u32 n) {
+    return n <= RQL ? rq_hold_<true>(c, n) : rq_hold_<false>(c, n);
   }
 
   // ---- event handlers: each fills the outcome fields; no early exits (see top_key) ----
