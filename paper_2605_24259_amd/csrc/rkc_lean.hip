@@ -520,7 +520,7 @@ struct Lean {
       pv = max(pv, (on && hardm() && m_state(m) == ST_MATERIALIZED && m_eff(m) == RKC_PROT_HARD) ? L : 0u);
       cv = max(cv, on && !offl(m) ? L : 0u);
     }
-    const u32 pp = wmax(pv);
+    const u32 pp = hardm() ? wmax(pv) : 0u;  // (0 outside hard protection, known as such)
     G0 g = rd0(c);
     g.covA = wmax(cv);
     commit(c, g, g.n, g.hold, pp, 0, 0);
