@@ -643,7 +643,7 @@ struct Lean {
       if (hc >= 0) {
         const u32 lo = max(ghc.hold, ghc.prot);
         hlo = max(lo, h);
-        E -= evictable(ghc.n, lo, 0) - evictable(ghc.n, hlo, 0);
+        E -= sub0(min(ghc.n, hlo), lo);  // = evictable(n, lo) - evictable(n, hlo), hlo >= lo
       }
       r.E = E;
       // (F + E is at most twice the usable blocks and need at most 2^24: every sum here fits 32 bits)
@@ -864,7 +864,7 @@ struct Lean {
       u32 E = Eall + fbl;
       if (hc >= 0) {
         const u32 lo = max(ghc.hold, ghc.prot);
-        E -= evictable(ghc.n, lo, 0) - evictable(ghc.n, max(lo, h), 0);
+        E -= sub0(min(ghc.n, max(lo, h)), lo);
       }
       u32 avail = F + E;
       if (need > avail) {
