@@ -26,9 +26,10 @@
 //
 // Live claims sit one per lane in six VGPRs (16-bit halves), so expiry, attribution, predicate
 // sweeps and claim maxima are single vector passes with DPP reductions.  Live requests are a
-// compact id-ordered list in LDS (8 bytes each).  Touch-stack nodes use LDS first, then global
-// scratch; finished requests' private runs form a FIFO in global scratch, and so do the deferred
-// requests of hard-protection pools that defer (a ring of live-request-capacity entries).
+// compact id-ordered list (8 bytes each) in LDS, past its first 128 entries in global scratch
+// (one claim set).  Touch-stack nodes use LDS first, then global scratch; finished requests'
+// private runs form a FIFO in global scratch, and so do the deferred requests of
+// hard-protection pools that defer (a ring of live-request-capacity entries).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 

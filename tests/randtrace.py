@@ -160,3 +160,52 @@ def many_claims_batch(seed: int, n_pools: int, n_events=(600, 1500), claim_cap: 
             pool["offload_blocks"] = int(rng.integers(0, U))
         pools.append(pool)
     return tg.from_pools(pools, f"many-claims{seed}")
+
+
+def many_requests_batch(seed: int, n_pools: int, n_events=(700, 1200), n_chains: int = 200,
+                        req_cap: int = 256):
+    """Pools whose live-request lists grow past a few hundred entries (small served prefills, few
+    finishes at first), with extends and finishes picking anywhere in the list, claims, and in every
+    other hard-protection pool deferral with RETRY events (retried requests enter the list in id
+    order); the request table fills and overflows.  Policies cycle over the four."""
+    from paper_2605_24259_amd import tracegen as tg
+    rng = np.random.default_rng(seed)
+    pools = []
+    for i in range(n_pools):
+        mode = i % 4
+        ext = mode == 3 and (i // 4) % 2 == 1
+        U = int(rng.integers(600, 3000))
+        ne = int(rng.integers(n_events[0], n_events[1] + 1))
+        evs = []
+        for k in range(ne):
+            r = rng.random()
+            sel = int(rng.integers(0, 1 << 32))
+            # the list grows first, then shrinks
+            pre, fin = (0.50, 0.04) if k < ne // 2 else (0.20, 0.34)
+            if ext and r < 0.06:
+                evs.append(tg.retry())
+            elif r < pre:
+                S = int(rng.integers(1, 9))
+                if rng.random() < 0.3:
+                    evs.append(tg.prefill(S, -1, 0))
+                else:
+                    evs.append(tg.prefill(S, int(rng.integers(0, n_chains)), int(rng.integers(0, S + 1))))
+            elif r < pre + 0.12:
+                evs.append(tg.extend(int(rng.integers(1, 5)), sel))
+            elif r < pre + 0.12 + fin:
+                evs.append(tg.finish(sel))
+            elif r < pre + 0.12 + fin + 0.08:
+                L = int(rng.integers(1, 40))
+                evs.append(tg.claim(L, int(rng.integers(0, n_chains)), int(rng.integers(0, L + 1)),
+                                    hard=int(rng.random() < 0.6), prio=int(rng.integers(0, 4)),
+                                    dur=0 if rng.random() < 0.6 else int(rng.integers(20, 400))))
+            elif r < pre + 0.12 + fin + 0.10:
+                evs.append(tg.release(sel))
+            else:
+                evs.append(tg.nop())
+        pool = dict(usable_blocks=U, mode=mode, n_chains=n_chains, max_live_requests=req_cap,
+                    max_live_claims=64, events=evs)
+        if ext:
+            pool["defer_limit"] = int(rng.integers(1, 4))
+        pools.append(pool)
+    return tg.from_pools(pools, f"manyreq{seed}")

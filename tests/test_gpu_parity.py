@@ -388,6 +388,23 @@ def test_claim_sets(oracle_mod, seed, kw):
     compare_pools(trace, gen, ora)
 
 
+@pytest.mark.parametrize("seed", [5, 6])
+def test_request_list_past_lds(oracle_mod, seed):
+    """Live-request lists of up to 256 entries, of which the compact kernel keeps the first 128 in
+    LDS and the rest in global scratch: lists that grow past that split, fill the table and shrink
+    back below it, with extends and finishes picking anywhere in them and retried requests entering
+    in id order; against the oracle and the general kernel on the same inputs."""
+    import paper_2605_24259_amd as rkc
+    trace = randtrace.many_requests_batch(seed, 256)
+    gpu, ora = _both(oracle_mod, trace)
+    compare_pools(trace, gpu, ora)
+    live = ora[1][:, 29]
+    assert (live > 128).any() and (live < 128).any()
+    assert (ora[1][:, 31] & 1).any()  # RKC_PS_REQUEST_TABLE: some lists reached the capacity
+    gen = gpu_replay(trace, flags=rkc.FLAG_GENERAL_KERNEL)
+    compare_pools(trace, gen, ora)
+
+
 def _edge_selectors(n):
     """u32 selectors at the edges of `sel mod n`: multiples of n (largest one below 2^32
     included), their neighbours, 0 and 2^32 - 1."""
