@@ -587,7 +587,8 @@ struct Pool {
     }
     const i32 E = candidates(hc, h);
     r.E = E;
-    if ((i64)need > (i64)F + E) {
+    // (usable blocks are at most 2^22 and a request at most 2^24: these sums fit 32 bits)
+    if (need > F + E) {
       r.ok = 0;
       return r;
     }
@@ -698,7 +699,7 @@ struct Pool {
       const uint4 g0 = cg((u32)hc, 0);
       Pr -= max(0, (i32)min(g0.z, h) - (i32)g0.y);
     }
-    const i64 req = (i64)A + Hc + need;
+    const i32 req = A + Hc + need;
     if (Pr > 0 && req <= U) {
       code = RKC_OC_REFUSED_CLAIM;
       post(J_ATTRIB, (u32)hc, h, ncl);
@@ -1050,10 +1051,10 @@ struct Pool {
   __device__ __forceinline__ u32 relax(u32 t, i32 need, i32 hc, u32 h) {
     u32 k = 0;
     if (relax_on && need > F) {
-      i64 avail = (i64)F + candidates(hc, h);
-      if ((i64)need > avail) {
+      i32 avail = F + candidates(hc, h);
+      if (need > avail) {
         u32 room = t2cap > t2used ? t2cap - t2used : 0u, moved = 0, no = 0, lo = 0;
-        for (u32 guard = 0; (i64)need > avail && guard <= ncl; guard++) {
+        for (u32 guard = 0; need > avail && guard <= ncl; guard++) {
           u32 best = 0xFFFFFFFFu, bi = 0;
           for (u32 i = lane; i < ncl; i += 64) {
             const u32 m = cla(CL_META)[i];
@@ -1086,7 +1087,7 @@ struct Pool {
           if (off) { room -= L; moved += L; no++; }
           k++;
         }
-        const bool fits = (i64)need <= avail;
+        const bool fits = need <= avail;
         if (k) {
           __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");  // the marks reach the scan
           for (u32 i = lane; i < ncl; i += 64) {
