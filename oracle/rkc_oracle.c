@@ -24,6 +24,13 @@
  *
  * Readings of the paper used where it is silent are listed in the design notes; each is marked
  * "reading" where it is applied.
+ *
+ * Parity unpinned (the paper fixes no value that could catch a mistake in these; the brute-force
+ * model shares the reading, so agreement with it checks the code, not the reading):
+ *   - the victim key order (level, last use, position descending): the paper prints only the
+ *     counts of its probe (50 evicted, 10 remain);
+ *   - the offload and restore accounting (pool words 38-41): the paper fixes only the precondition
+ *     of offloading (§3.1 offloadable; §3.5 offload resident).
  */
 #include <stdint.h>
 #include <stdlib.h>
