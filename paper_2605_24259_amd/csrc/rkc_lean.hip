@@ -697,23 +697,22 @@ struct Lean {
             u32 rs = 0, sc = 0;
             if (g.covA > nw) {
               // victims inside live claims: resident; inside only demoted / expired ones: post-release
-              u32 cv = 0;
-              bool due = false;
+              u32 cv = 0, due = 0;
 #pragma unroll
               for (u32 q = 0; q < NQ; q++) {
                 // (the barrier keeps the per-lane claim tests here, where they are needed, instead of
-                // ahead of the eviction loop, where every evicting allocation would pay for them)
-                // (bitwise tests, so that no lane-dependent branch is formed)
+                // ahead of the eviction loop, where every evicting allocation would pay for them;
+                // the tests are 0/1 words combined bitwise, so that no lane-dependent branch forms)
                 u32 mc = lo16(qc[q]);
                 asm volatile("" : "+v"(mc));
                 const u32 st = m_state(mc);
-                const bool on = live(q) & (hi16(qa[q]) == c) & !offl(mc);
+                const u32 on = (u32)live(q) & (u32)(hi16(qa[q]) == c) & (u32)!offl(mc);
                 // observed (1), materialized (2) or harmed (6)
-                const bool res = ((0x46u >> st) & 1u) != 0;
+                const u32 res = (0x46u >> st) & 1u;
                 static_assert(ST_OBSERVED == 1 && ST_MATERIALIZED == 2 && ST_HARMED == 6, "state codes");
                 cv = max(cv, (on & res) ? lo16(qb[q]) : 0u);
                 // a claim whose predicate still holds needs more than nw leading blocks
-                due = due | (on & (m_pend(mc) != 0) & (hi16(qb[q]) > nw));
+                due |= on & (u32)(m_pend(mc) != 0) & (u32)(hi16(qb[q]) > nw);
               }
               const u32 covS = wmax(cv);
               rs = min(nn, g.covA) - nw;
