@@ -2,8 +2,9 @@
 //
 // Same contract, same outputs, as the general kernel in rkc_replay.hip; this variant serves the
 // batches whose limits allow a tighter encoding:
-//   usable blocks <= 32,767, events per pool <= 65,533, shared chains <= 256,
-//   live claims <= 64, live requests <= 256, claim slots <= 65,534.
+//   usable blocks <= 32,767, events per pool <= 65,533, live requests <= 256,
+//   claim slots <= 65,534, and live claims <= 64 with shared chains <= 256 or live claims <= 256
+//   (four 64-claim sets) with shared chains <= 64.
 // One 64-lane wavefront replays one pool.  The per-event state machine runs on the scalar unit:
 // every branch is on a wave-uniform value, so no exec-mask juggling happens on the event path.
 //
@@ -310,9 +311,8 @@ struct Lean {
   // Scalars that only a few paths touch live in LDS (`cold`), so that the registers carried around
   // the event loop are the hot counters only: node free list and bump allocator, the FIFO of
   // private runs (head, tail, the front run's eviction key, or KINF when there is none, and its
-  // bounds), the status word, and
-  // the deferral ring (head, length, DEFERRED outcomes of the head entry; every entry behind the
-  // head has had exactly one).
+  // bounds), the status word, the deferral ring (head, length, DEFERRED outcomes of the head
+  // entry; every entry behind the head has had exactly one), and the second tier's use and peak.
   lds_u32* cold;
   // (QH..FLO is one 16-byte group, DQH, DQL an 8-byte group: keep their word offsets aligned)
   enum : u32 { C_QH = 0, C_QT, C_FKEY, C_FLO, C_FTOP, C_FNODE, C_BUMP, C_STATUS,
