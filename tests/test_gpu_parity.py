@@ -74,6 +74,17 @@ def test_random_medium(oracle_mod, seed):
     compare_pools(trace, gpu, ora)
 
 
+@pytest.mark.parametrize("n_chains", [64, 65, 128, 129, 256])
+def test_chain_groups(oracle_mod, n_chains):
+    """Pools with many shared chains at the edges of the compact kernel's key groups (64 chains per
+    lane-wide group: one, two or four groups), so every key group and chain record is in use."""
+    trace = randtrace.random_batch(50 + n_chains, 300, U_range=(40, 400), n_events=(100, 500),
+                                   n_chains=n_chains, p_malformed=0.01, tight_every=9, caps=(256, 64))
+    assert trace.limits()["max_chains"] == n_chains
+    gpu, ora = _both(oracle_mod, trace)
+    compare_pools(trace, gpu, ora)
+
+
 def test_edge_cases(oracle_mod, tg):
     """Empty pools, one-block pools, no chains, a maximal pool size, a pool whose events all fail."""
     pools = [
