@@ -461,7 +461,8 @@ struct Lean {
       }
       // no claim reaches the top position unless covA >= n
       const u32 lvl = (softl() && g.covA >= g.n) ? level_of(c, g.n - 1) : 0u;
-      key = (lvl << 25) | (g.bt << 9) | (c + 1);
+      // (formed on the vector unit, where the key is stored from)
+      key = (lvl << 25) | (vx(g.bt) << 9) | (c + 1);
     }
     return key;
   }
@@ -1272,9 +1273,10 @@ struct Lean {
     }
   }
 
-  // Malformed events of a tile (lane k holds event k): field ranges of PREFILL, EXTEND and CLAIM,
-  // decided for all 64 events at once (the table limits are checked per event, in order).
-  __device__ __forceinline__ u64 malformed(u32 e0, u32 e1, u32 e2, u32 e3, u32 cnt) const {
+  // Malformed events of a tile (lane k holds event k, and its flag): field ranges of PREFILL,
+  // EXTEND and CLAIM, decided for all 64 events at once (the table limits are checked per event,
+  // in order).
+  __device__ __forceinline__ u32 malformed(u32 e0, u32 e1, u32 e2, u32 e3) const {
     const u32 ty = e0 & 15u;
     const i32 s1 = (i32)e1, s2 = (i32)e2, s3 = (i32)e3;
     const bool fb = s1 < 1 || s1 > RKC_MAX_FIELD_BLOCKS;
@@ -1282,7 +1284,7 @@ struct Lean {
     const bool bad = (ty == RKC_EV_PREFILL && (fb || s3 < 0 || s3 > s1 || (s3 > 0 && cb))) ||
                      (ty == RKC_EV_EXTEND && fb) ||
                      (ty == RKC_EV_CLAIM && (fb || cb || s3 < 0 || s3 > s1));
-    return ballot(lane < cnt && bad);
+    return (u32)bad;
   }
 
   // One event: its outcome fields in o, the claims expired at its start in `expired` (the caller
@@ -1370,7 +1372,7 @@ __device__ __forceinline__ void replay_pool(const rkc_lean_args& g, const rkc_po
       const int4 x = *(const int4*)(ev + base + P.lane);
       e0 = (u32)x.x; e1 = (u32)x.y; e2 = (u32)x.z; e3 = (u32)x.w;
     }
-    const u64 badm = P.malformed(e0, e1, e2, e3, cnt);
+    const u32 badv = P.malformed(e0, e1, e2, e3);
     // outcome fields of event k go to lane k; the words are assembled for the tile at once
     u32 vcode = 0, vflags = 0, vn16 = 0, vexp = 0, vid = 0, va = 0, vb = 0;
     for (u32 k = 0; k < cnt; k++) {
@@ -1378,9 +1380,11 @@ __device__ __forceinline__ void replay_pool(const rkc_lean_args& g, const rkc_po
       u32 expired;
       // (the event's words straight into scalar registers: a scalar load from the read-only event
       // array instead of four lane reads of the tile's vector load, which serves the tile-wide
-      // checks; a 32-bit byte offset to the tile's base keeps the address a single shift)
+      // checks; a 32-bit byte offset to the tile's base keeps the address a single shift; the
+      // event's malformed flag is read from its lane, one vector instruction in place of a 64-bit
+      // scalar shift and a mask)
       const int4 xe = *(const int4*)((const char*)(ev + base) + (k << 4));
-      P.step(base + k, (u32)xe.x, (u32)xe.y, (u32)xe.z, (u32)xe.w, (u32)(badm >> k) & 1u, o, expired);
+      P.step(base + k, (u32)xe.x, (u32)xe.y, (u32)xe.z, (u32)xe.w, rdl(badv, k), o, expired);
       vcode = wrl(vcode, o.code, k); vflags = wrl(vflags, o.flags, k); vn16 = wrl(vn16, o.n16, k);
       vexp = wrl(vexp, expired, k); vid = wrl(vid, (u32)o.id, k); va = wrl(va, (u32)o.a, k);
       vb = wrl(vb, (u32)o.b, k);
