@@ -173,7 +173,7 @@ template <> struct QSets<4> { typedef u32 type __attribute__((ext_vector_type(4)
 struct G0 { u32 n, hold, prot, bt, nx, covA, stop, sbot; };
 
 struct AllocRes {
-  u32 ok, E, victims, resident, post, unclaimed;
+  u32 ok, E, resident, post, unclaimed;
   u32 hit;  // the allocation took blocks from the hit chain (its record changed)
 };
 
@@ -304,8 +304,11 @@ struct Lean {
   qv qf;  // predicate-failure step | harm step
   u32 tv;  // pool telemetry word `lane`
   // scalars
-  u32 F, A, PR, peak, Eall, fbl;
+  // E: the evictable blocks, those of chains above their hold and protection plus the private runs
+  // of finished requests (write no-admit pools never keep private runs)
+  u32 F, A, PR, peak, E;
   u32 nreq, ncl, nexp;
+  u32 sweep_due;  // a victim fell inside a claim whose predicate held: sweep at the end of the step
   u32 vic, post;  // victims, post-release losses (pool telemetry words 10 and 12)
   u32 nslot;      // claim slots used
   // Scalars that only a few paths touch live in LDS (`cold`), so that the registers carried around
@@ -383,7 +386,7 @@ struct Lean {
     return i;
   }
 
-  // -- chain counters: Eall (evictable shared blocks) and PR (protected cached blocks) --
+  // -- chain counters: E (evictable blocks) and PR (protected cached blocks) --
   __device__ __forceinline__ static u32 evictable(u32 n, u32 hold, u32 prot) {
     const u32 lo = max(hold, prot);
     return n > lo ? n - lo : 0u;
@@ -427,10 +430,12 @@ struct Lean {
   // Key of chain c's top run; advances a stale stack bottom (the node above it reaches n).
   // (Control flow on the event path is written without early exits: the compiler's structurizer
   // turns every break / early return into flow blocks with register copies paid by every event.)
-  __device__ __forceinline__ u32 top_key(u32 c, G0& g) {
+  // (moved: set when the stack bottom advanced, i.e. the record's bottom fields changed)
+  __device__ __forceinline__ u32 top_key(u32 c, G0& g, bool& moved) {
     u32 key = KINF;
     if (g.n > max(g.hold, g.prot)) {
       if (g.nx >= g.n) {
+        moved = true;
         // (rare: the node free list is read and written here, not kept in registers around it)
         u32 fn = ufl(cold[C_FNODE]);
         u32 b = g.sbot;
@@ -496,10 +501,10 @@ struct Lean {
     g.stop = nw;
   }
 
-  // Apply new (n, hold, prot) to chain c (keeping Eall and PR exact), optionally touch [0, x)
+  // Apply new (n, hold, prot) to chain c (keeping E and PR exact), optionally touch [0, x)
   // at t, refresh the key and store the record.
   __device__ __forceinline__ void commit(u32 c, G0 g, u32 nn, u32 hh, u32 pp, u32 x, u32 t) {
-    Eall += evictable(nn, hh, pp) - evictable(g.n, g.hold, g.prot);
+    E += evictable(nn, hh, pp) - evictable(g.n, g.hold, g.prot);
     PR += protd(hh, pp) - protd(g.hold, g.prot);
     g.n = nn; g.hold = hh; g.prot = pp;
     if (x) {
@@ -507,7 +512,8 @@ struct Lean {
       touch(g, x, t);
       cold_nodes_out();
     }
-    kk[vx(c)] = top_key(c, g);
+    bool moved = false;
+    kk[vx(c)] = top_key(c, g, moved);
     wr0(c, g);
   }
 
@@ -634,26 +640,29 @@ struct Lean {
   // ALLOC: FREE blocks first, then the (need - F) smallest-key candidates (§3.1 soft priority;
   // §5.3 ordinary eviction; hard-protected blocks are never candidates).  hc >= 0 names the chain
   // whose leading h blocks are the event's own hits (not candidates).
-  __device__ __forceinline__ AllocRes alloc(u32 need, i32 hc, u32 h, const G0& ghc, u32& sweep_due) {
-    AllocRes r = {1, 0, 0, 0, 0, 0, 0};
+  __device__ __forceinline__ AllocRes alloc(u32 need, i32 hc, u32 h, const G0& ghc) {
+    AllocRes r = {1, 0, 0, 0, 0, 0};
     if (need <= F) {
       F -= need;
     } else {
-      // (write no-admit drops finished requests' own blocks: its pools never have private runs)
-      u32 E = noadm() ? Eall : Eall + fbl;
+      u32 Ec = E;
       u32 hlo = 0;  // candidates of chain hc start at hlo
       if (hc >= 0) {
         const u32 lo = max(ghc.hold, ghc.prot);
         hlo = max(lo, h);
-        E -= sub0(min(ghc.n, hlo), lo);  // = evictable(n, lo) - evictable(n, hlo), hlo >= lo
+        Ec -= sub0(min(ghc.n, hlo), lo);  // = evictable(n, lo) - evictable(n, hlo), hlo >= lo
       }
-      r.E = E;
-      // (F + E is at most twice the usable blocks and need at most 2^24: every sum here fits 32 bits)
-      if (need > F + E) {
+      r.E = Ec;
+      // (F + Ec is at most twice the usable blocks and need at most 2^24: every sum here fits 32 bits)
+      if (need > F + Ec) {
         r.ok = 0;
       } else {
         u32 K = need - F;
         F = 0;
+        // (every block taken below is a victim, so the victims are K; those inside no live claim
+        // are the victims less the resident ones; a feasible allocation is always served)
+        const u32 K0 = K;
+        vic += K;
         // the front private run's key (the rest of the FIFO state is read when a run is taken)
         u32 kf = noadm() ? KINF : ufl(cold[C_FKEY]);
         // the hit chain stops being a candidate once only hits remain
@@ -675,9 +684,7 @@ struct Lean {
             cold_fifo_in();
             const u32 m = min(K, ftop - flo);
             ftop -= m;
-            fbl -= m;
-            r.victims += m;
-            r.unclaimed += m;
+            E -= m;
             K -= m;
             if (ftop == flo) fifo_pop();
             cold_fifo_out();
@@ -720,23 +727,25 @@ struct Lean {
               sc = min(nn, covS) > nw ? min(nn, covS) - nw : 0u;
               if (ballot(due)) sweep_due = 1;
             }
-            r.victims += m;
             r.resident += rs;
             r.post += rs - sc;
-            r.unclaimed += m - rs;
-            Eall -= m;
+            E -= m;
             g.n = nw;
             K -= m;
-            u32 key = top_key(c, g);
+            bool moved = false;
+            u32 key = top_key(c, g, moved);
             if ((i32)c == hc && nw <= lo) key = KINF;
             kk[vx(c)] = key;
-            wr0(c, g);
+            // (only n changed unless the stack bottom advanced)
+            if (moved) wr0(c, g);
+            else ((lds_u32*)(ch + vx(c)))[0] = pk(g.n, g.hold);
           } else {
             set_status(0x80000000u);  // cannot happen: feasibility was checked
             K = 0;
           }
           if (__builtin_expect(guard > 0x10000u, 0)) { set_status(0x80000000u); K = 0; }
         }
+        r.unclaimed = K0 - r.resident;
       }
     }
     return r;
@@ -780,7 +789,6 @@ struct Lean {
     o.code = r.resident ? RKC_OC_EVICT_RESIDENT : RKC_OC_ADMIT;
     o.a = (i32)r.resident;
     o.flags |= (r.post ? (u32)RKC_FL_POST_RELEASE_LOSS : 0u) | (r.unclaimed ? (u32)RKC_FL_EVICT_UNCLAIMED : 0u);
-    vic += r.victims;
     post += r.post;
   }
 
@@ -841,7 +849,7 @@ struct Lean {
 
   // ---- event handlers: each fills the outcome fields; no early exits (see top_key) ----
   struct Out {
-    u32 code, flags, n16, sweep_due;
+    u32 code, flags, n16;
     i32 id, a, b;
   };
 
@@ -862,12 +870,12 @@ struct Lean {
   __device__ __forceinline__ u32 relax(u32 t, u32 need, i32 hc, u32 h, G0& ghc) {
     u32 k = 0;
     if (relax_on() && need > F) {
-      u32 E = Eall + fbl;
+      u32 Ec = E;
       if (hc >= 0) {
         const u32 lo = max(ghc.hold, ghc.prot);
-        E -= sub0(min(ghc.n, max(lo, h)), lo);
+        Ec -= sub0(min(ghc.n, max(lo, h)), lo);
       }
-      u32 avail = F + E;
+      u32 avail = F + Ec;
       if (need > avail) {
         // Per lane and claim set q, three bits of `sel`: bit q the claim is a candidate not yet
         // visited, bit 4 + q picked, bit 8 + q picked for offload (the rest of the picks are
@@ -974,7 +982,7 @@ struct Lean {
     const u32 need = S - h;
     u32 relaxed = 0;
     if (ext()) relaxed = relax(t, need, hc, h, g);
-    const AllocRes r = alloc(need, hc, h, g, o.sweep_due);
+    const AllocRes r = alloc(need, hc, h, g);
     if (!r.ok) {
       refusal(need, hc, h, Hc, g, o);
       if (ext()) {
@@ -1001,7 +1009,6 @@ struct Lean {
       }
     } else {
       A += Hc + need;
-      peak = max(peak, A);
       u32 R = 0;
       if (hc >= 0) {
         const G0 g2 = r.hit ? rd0(cc) : g;  // victims may have shortened this chain above the hits
@@ -1072,12 +1079,11 @@ struct Lean {
       G0 g = {0, 0, 0, 0, 0, 0, 0, 0};
       u32 relaxed = 0;
       if (ext()) relaxed = relax(t, need, -1, 0, g);
-      const AllocRes r = alloc(need, -1, 0, g, o.sweep_due);
+      const AllocRes r = alloc(need, -1, 0, g);
       if (!r.ok) {
         refusal(need, -1, 0, 0, g, o);
       } else {
         A += need;
-        peak = max(peak, A);
         o.id = (i32)lo16(rq_grow(i, need));
         o.b = (i32)A;
         served(r, o);
@@ -1106,7 +1112,7 @@ struct Lean {
         const bool obs = shadm() || beq;
         const G0 g = rd0(c);
         const u32 h = min(L, g.n), need = L - h;
-        const AllocRes r = alloc(need, (i32)c, h, g, o.sweep_due);
+        const AllocRes r = alloc(need, (i32)c, h, g);
         const u32 eff = beq ? RKC_PROT_NONE : hardm() ? (hardq ? RKC_PROT_HARD : RKC_PROT_SOFT)
                       : (mode == RKC_MODE_SOFT ? RKC_PROT_SOFT : RKC_PROT_NONE);
         if (!r.ok) {
@@ -1175,7 +1181,7 @@ struct Lean {
       const u32 kept = own - dropped;
       turned += kept;
       F += dropped;
-      fbl += kept;
+      E += kept;
       if (kept > 0) {
         cold_fifo_in();
         if (qh == qt) { fk = t << 9; flo = R; ftop = len; }
@@ -1183,6 +1189,8 @@ struct Lean {
         qt++;
         cold_fifo_out();
       }
+      // (A only falls here: its peak is taken before each fall and once at the end)
+      peak = max(peak, A);
       A -= turned + dropped;
       o.code = RKC_OC_FINISHED;
       o.id = (i32)rid;
@@ -1287,20 +1295,24 @@ struct Lean {
     return (u32)bad;
   }
 
-  // One event: its outcome fields in o, the claims expired at its start in `expired` (the caller
-  // assembles the outcome words of a whole tile at once).  Dispatch is an if / else chain in order
-  // of how often the event types occur in the benchmark mixes.
-  __device__ __forceinline__ void step(u32 t, u32 w0, u32 w1, u32 w2, u32 w3, u32 bad, Out& o, u32& expired) {
+  // One event: its outcome fields in o (the caller assembles the outcome words of a whole tile at
+  // once).  Dispatch is an if / else chain in order of how often the event types occur in the
+  // benchmark mixes.
+  __device__ __forceinline__ void step(u32 t, u32 w0, u32 w1, u32 w2, u32 w3, u32 bad, Out& o) {
     const u32 type = w0 & 15u;
-    expired = 0;
     // (every outcome that is not quiet sets id, a and b; a quiet one gets id -1 and a = b = 0 when
     // the tile's outcome words are assembled, so they start unspecified here and no path pays for
     // materializing them)
     const i32 any = __builtin_nondeterministic_value(0);
-    o = Out{RKC_OC_NOOP, 0, NEVER, 0, any, any, any};
+    o = Out{RKC_OC_NOOP, 0, 0, any, any, any};
     // (claims in native and write no-admit pools are only observed, and observed claims never
     // expire: those loops carry no expiry)
-    if (!shadm() && __builtin_expect(t >= nexp, 0)) expire(t, o.flags, expired);
+    if (!shadm() && __builtin_expect(t >= nexp, 0)) {
+      u32 expired;
+      expire(t, o.flags, expired);
+      // n16 is the claims expired at the start of the step unless the event sets it
+      o.n16 = min(expired, 65535u);
+    }
     if (type == RKC_EV_PREFILL) ev_prefill(t, w1, w2, w3, bad, o);
     else if (type == RKC_EV_EXTEND) ev_extend(t, w1, w2, bad, o);
     else if (type == RKC_EV_CLAIM) ev_claim(t, w0, w1, w2, w3, bad, o);
@@ -1309,7 +1321,10 @@ struct Lean {
     else if (ext() && type == RKC_EV_RETRY) ev_retry(t, o);
     else if ((type & ~1u) != RKC_EV_NOP) o.code = RKC_OC_INVALID;  // NOP, or RETRY with no ring
     static_assert(RKC_EV_NOP == 6 && RKC_EV_RETRY == 7, "NOP and RETRY differ in bit 0 only");
-    if (__builtin_expect(o.sweep_due != 0, 0)) o.flags |= sweep(t);
+    if (__builtin_expect(sweep_due != 0, 0)) {
+      sweep_due = 0;
+      o.flags |= sweep(t);
+    }
   }
 };
 
@@ -1355,8 +1370,8 @@ __device__ __forceinline__ void replay_pool(const rkc_lean_args& g, const rkc_po
 #pragma unroll
   for (u32 q = 0; q < NQ; q++) P.qa[q] = P.qb[q] = P.qc[q] = P.qd[q] = P.qe[q] = P.qf[q] = 0;
   P.tv = 0;
-  P.F = U; P.A = 0; P.PR = 0; P.peak = 0; P.Eall = 0; P.fbl = 0;
-  P.nreq = 0; P.ncl = 0; P.nexp = NEVER; P.vic = 0; P.post = 0; P.nslot = 0;
+  P.F = U; P.A = 0; P.PR = 0; P.peak = 0; P.E = 0;
+  P.nreq = 0; P.ncl = 0; P.nexp = NEVER; P.sweep_due = 0; P.vic = 0; P.post = 0; P.nslot = 0;
   P.cold = lds + M::COLD / 4;
   if (P.lane < LP::C_WORDS)
     P.cold[P.lane] = P.lane == LP::C_FNODE ? NIL : P.lane == LP::C_DQC ? 1u : P.lane == LP::C_FKEY ? KINF : 0u;
@@ -1374,25 +1389,22 @@ __device__ __forceinline__ void replay_pool(const rkc_lean_args& g, const rkc_po
     }
     const u32 badv = P.malformed(e0, e1, e2, e3);
     // outcome fields of event k go to lane k; the words are assembled for the tile at once
-    u32 vcode = 0, vflags = 0, vn16 = 0, vexp = 0, vid = 0, va = 0, vb = 0;
+    u32 vcode = 0, vflags = 0, vn16 = 0, vid = 0, va = 0, vb = 0;
     for (u32 k = 0; k < cnt; k++) {
       typename LP::Out o;
-      u32 expired;
       // (the event's words straight into scalar registers: a scalar load from the read-only event
       // array instead of four lane reads of the tile's vector load, which serves the tile-wide
       // checks; a 32-bit byte offset to the tile's base keeps the address a single shift; the
       // event's malformed flag is read from its lane, one vector instruction in place of a 64-bit
       // scalar shift and a mask)
       const int4 xe = *(const int4*)((const char*)(ev + base) + (k << 4));
-      P.step(base + k, (u32)xe.x, (u32)xe.y, (u32)xe.z, (u32)xe.w, rdl(badv, k), o, expired);
+      P.step(base + k, (u32)xe.x, (u32)xe.y, (u32)xe.z, (u32)xe.w, rdl(badv, k), o);
       vcode = wrl(vcode, o.code, k); vflags = wrl(vflags, o.flags, k); vn16 = wrl(vn16, o.n16, k);
-      vexp = wrl(vexp, expired, k); vid = wrl(vid, (u32)o.id, k); va = wrl(va, (u32)o.a, k);
-      vb = wrl(vb, (u32)o.b, k);
+      vid = wrl(vid, (u32)o.id, k); va = wrl(va, (u32)o.a, k); vb = wrl(vb, (u32)o.b, k);
     }
-    // n16: the blocking / relaxed count where the event set one, else the claims expired at its
-    // start; no-op and invalid outcomes carry id -1, a = b = 0
+    // no-op and invalid outcomes carry id -1, a = b = 0
     const bool quiet = vcode == RKC_OC_NOOP || vcode == RKC_OC_INVALID;
-    const u32 o0 = vcode | (vflags << 8) | ((vn16 == NEVER ? min(vexp, 65535u) : vn16) << 16);
+    const u32 o0 = vcode | (vflags << 8) | (vn16 << 16);
     const u32 o1 = quiet ? 0xFFFFFFFFu : vid, o2 = quiet ? 0u : va, o3 = quiet ? 0u : vb;
     if (P.lane < cnt) *(int4*)(out + base + P.lane) = make_int4((i32)o0, (i32)o1, (i32)o2, (i32)o3);
     // outcomes per code; resident victims (a) and leading hits (b of a served prefill)
@@ -1440,7 +1452,7 @@ __device__ __forceinline__ void replay_pool(const rkc_lean_args& g, const rkc_po
     if (w == 41) v = (i32)t2peak;
     if (w == TW_VICTIMS) v = (i32)vic;
     else if (w == TW_POST) v = (i32)post;
-    else if (w == 24) v = (i32)P.peak;
+    else if (w == 24) v = (i32)max(P.peak, P.A);
     else if (w == 25) v = (i32)P.A;
     else if (w == 26) v = (i32)(U - P.F - P.A);
     else if (w == 27) v = (i32)P.F;
