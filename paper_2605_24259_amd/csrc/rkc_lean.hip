@@ -186,12 +186,14 @@ struct AllocRes {
 template <int NS, int NQ>
 struct LdsMap {
   // live requests in LDS: a zipf pool that allows 256 live requests holds ~50 on average and 165 at
-  // most, so with one claim set half of them stay in LDS and the rest go to global scratch
-  static constexpr u32 RQL = NQ == 4 ? 256u : 128u;
+  // most, so with one claim set the first 128 (96 with 256 chains) stay in LDS and the rest go to
+  // global scratch
+  static constexpr u32 RQL = NQ == 4 ? 256u : NS == 4 ? 96u : 128u;
   // touch-stack nodes in LDS (a zipf pool of 256 chains peaks at ~80-115 live nodes, the 80-block
-  // pools at ~35): with 256 chains only 16, which brings a pool to 6,400 B, five allocation units,
-  // so 25 pools share a CU instead of 21 (more than paying for the slower node accesses)
-  static constexpr u32 NL = NS == 4 ? 16u : 64u;
+  // pools at ~35): with 256 chains 48, which brings a pool to 6,400 B, five allocation units, so 25
+  // pools share a CU instead of 21 (more than paying for the slower node accesses); of those five
+  // units, 96 requests and 48 nodes measured faster than 128 and 16 or 64 and 80
+  static constexpr u32 NL = NS == 4 ? 48u : 64u;
   static constexpr u32 COLD = 0, HIST = 64, KEYS = 128, CH = KEYS + 256u * NS, RQ = CH + 1024u * NS,
                        ND = RQ + 8u * RQL, BYTES = ND + 8u * NL;
 };
@@ -474,21 +476,26 @@ struct Lean {
 
   // Record a touch of positions [0, x) of chain c at step t (x > 0).
   __device__ __forceinline__ void touch(G0& g, u32 x, u32 t) {
-    u32 tp = g.stop, tpd = NIL;
+    u32 tp = g.stop, tpd = NIL, reuse = NIL;
     bool go = tp != NIL;
     for (u32 guard = 0; go && guard < 0x10000u; guard++) {
       const u32x2 nt = nget(tp);
       tpd = hi16(nt.y);
       if (lo16(nt.x) <= x) {
-        nset_y(tp, pk(NIL, fnode));
-        fnode = tp;
+        // the node leaves the stack; the last one to leave becomes the new node, the others go to
+        // the free list
+        if (reuse != NIL) {
+          nset_y(reuse, pk(NIL, fnode));
+          fnode = reuse;
+        }
+        reuse = tp;
         tp = tpd;
         go = tp != NIL;
       } else {
         go = false;
       }
     }
-    const u32 nw = nalloc();
+    const u32 nw = reuse != NIL ? reuse : nalloc();
     nset(nw, u32x2{pk(x, t), pk(NIL, tp)});
     if (tp != NIL) {
       nset_y(tp, pk(nw, tpd));
@@ -734,7 +741,9 @@ struct Lean {
             K -= m;
             bool moved = false;
             u32 key = top_key(c, g, moved);
-            if ((i32)c == hc && nw <= lo) key = KINF;
+            // (the hit chain stops being a candidate once only hits remain; any other chain's key
+            // is already KINF when nw <= lo)
+            if (nw <= lo) key = KINF;
             kk[vx(c)] = key;
             // (only n changed unless the stack bottom advanced)
             if (moved) wr0(c, g);
