@@ -314,7 +314,7 @@ struct Lean {
   u32 vic, post;  // victims, post-release losses (pool telemetry words 10 and 12)
   u32 nslot;      // claim slots used
   // Scalars that only a few paths touch live in LDS (`cold`), so that the registers carried around
-  // the event loop are the hot counters only: node free list and bump allocator, the FIFO of
+  // the event loop are the hot counters only: node free-list head and bump allocator, the FIFO of
   // private runs (head, tail, the front run's eviction key, or KINF when there is none, and its
   // bounds), the status word, the deferral ring (head, length, DEFERRED outcomes of the head
   // entry; every entry behind the head has had exactly one), and the second tier's use and peak.
@@ -323,10 +323,7 @@ struct Lean {
   enum : u32 { C_QH = 0, C_QT, C_FKEY, C_FLO, C_FTOP, C_FNODE, C_BUMP, C_STATUS,
                C_DQH, C_DQL, C_DQC, C_T2, C_T2PK, C_WORDS };
   static_assert(C_QH % 4 == 0 && C_DQH % 2 == 0 && C_DQL == C_DQH + 1 && C_WORDS <= 16, "cold block layout");
-  u32 fnode, bump;              // valid between cold_nodes_in() and cold_nodes_out() (touches)
   u32 qh, qt, fk, flo, ftop;    // valid between cold_fifo_in() and cold_fifo_out()
-  __device__ __forceinline__ void cold_nodes_in() { fnode = ufl(cold[C_FNODE]); bump = ufl(cold[C_BUMP]); }
-  __device__ __forceinline__ void cold_nodes_out() { cold[C_FNODE] = fnode; cold[C_BUMP] = bump; }
   __device__ __forceinline__ void cold_fifo_in() {
     const u32x4 v = *(lds_u32x4*)(cold + C_QH);  // QH, QT, FKEY, FLO
     qh = ufl(v.x); qt = ufl(v.y); fk = ufl(v.z); flo = ufl(v.w); ftop = ufl(cold[C_FTOP]);
@@ -374,16 +371,23 @@ struct Lean {
   __device__ __forceinline__ void nset_y(u32 i, u32 y) {
     if (i < NL) ((lds_u32*)(ndl + vx(i)))[1] = y; else ((__attribute__((address_space(1))) u32*)gat(ndg, i - NL))[1] = y;
   }
+  // (the free list head and the bump pointer are read and written in the cold block where they
+  // are needed: a touch that reuses a popped node needs neither)
   __device__ __forceinline__ u32 nalloc() {
     u32 i;
-    if (fnode != NIL) {
-      i = fnode;
-      fnode = hi16(nget(i).y);
-    } else if (bump < ncap()) {
-      i = bump++;
+    const u32 fn = ufl(cold[C_FNODE]);
+    if (fn != NIL) {
+      i = fn;
+      cold[C_FNODE] = hi16(nget(i).y);
     } else {
-      set_status(0x80000000u);  // cannot happen: one node per touch, at most node cap - 2 touches
-      i = 0;
+      const u32 b = ufl(cold[C_BUMP]);
+      if (b < ncap()) {
+        i = b;
+        cold[C_BUMP] = b + 1;
+      } else {
+        set_status(0x80000000u);  // cannot happen: one node per touch, at most node cap - 2 touches
+        i = 0;
+      }
     }
     return i;
   }
@@ -485,8 +489,8 @@ struct Lean {
         // the node leaves the stack; the last one to leave becomes the new node, the others go to
         // the free list
         if (reuse != NIL) {
-          nset_y(reuse, pk(NIL, fnode));
-          fnode = reuse;
+          nset_y(reuse, pk(NIL, ufl(cold[C_FNODE])));
+          cold[C_FNODE] = reuse;
         }
         reuse = tp;
         tp = tpd;
@@ -514,11 +518,7 @@ struct Lean {
     E += evictable(nn, hh, pp) - evictable(g.n, g.hold, g.prot);
     PR += protd(hh, pp) - protd(g.hold, g.prot);
     g.n = nn; g.hold = hh; g.prot = pp;
-    if (x) {
-      cold_nodes_in();
-      touch(g, x, t);
-      cold_nodes_out();
-    }
+    if (x) touch(g, x, t);
     bool moved = false;
     kk[vx(c)] = top_key(c, g, moved);
     wr0(c, g);
