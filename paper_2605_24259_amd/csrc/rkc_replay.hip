@@ -474,14 +474,16 @@ struct Pool {
   // Record a touch of positions [0, x) of chain c at step t.
   __device__ __forceinline__ void touch(u32 c, u32 x, u32 t) {
     if (x == 0) return;
-    u32 tp = cfn(c, CF_STOP);
+    u32 tp = cfn(c, CF_STOP), reuse = NIL;
     const u32 sb = cfn(c, CF_SBOT);
     for (u32 guard = 0; guard < node_cap && tp != NIL && nget_x(tp) <= x; guard++) {
       const u32 d = nget_w(tp);
-      node_free(tp);
+      // the last node to leave the stack becomes the new one, the others go to the free list
+      if (reuse != NIL) node_free(reuse);
+      reuse = tp;
       tp = d;
     }
-    const u32 nw = node_alloc();
+    const u32 nw = reuse != NIL ? reuse : node_alloc();
     nset(nw, make_uint4(x, t, NIL, tp));
     if (tp != NIL) {
       nset_z(tp, nw);
